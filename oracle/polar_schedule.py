@@ -13,15 +13,16 @@ This module derives that schedule in float64 with the Remez exchange
 algorithm.  The HIP library carries its own table, produced by an independent
 generator; a test compares the two.
 
-Once E drops below ``CONTACT_SWITCH`` the interval is so narrow that the
-minimax problem is ill-conditioned; from there on the schedule uses the
-odd quintic with third-order contact at 1, fixed by p(1) = 1, p'(1) = 0,
-p''(1) = 0, i.e. (a, b, c) = (15/8, -10/8, 3/8), whose error on [1-E, 1+E]
-is O(E^3).
+Once the interval [l, u] is narrower than ``CONTACT_SWITCH`` (half-width
+below 0.05) the minimax problem becomes ill-conditioned (the optimal error
+is O(width^3) and the coefficients lose digits); from there on the schedule
+uses the odd quintic with third-order contact at 1, fixed by p(1) = 1,
+p'(1) = 0, p''(1) = 0, i.e. (a, b, c) = (15/8, -10/8, 3/8), which is
+monotone and maps [1 - w, 1 + w] to within O(w^3) of 1.
 """
 import numpy as np
 
-CONTACT_SWITCH = 1e-6
+CONTACT_SWITCH = 0.1
 
 
 def _poly(coef, x):
@@ -83,7 +84,7 @@ def greedy_schedule(lo, steps, hi=1.0):
     l, u = float(lo), float(hi)
     for _ in range(steps):
         intervals.append((l, u))
-        if u - l < 2.0 * CONTACT_SWITCH:
+        if u - l < CONTACT_SWITCH:
             a, b, c = 15.0 / 8.0, -10.0 / 8.0, 3.0 / 8.0
             coefs.append((a, b, c))
             # image of [l, u] under the contact polynomial
