@@ -1,0 +1,201 @@
+/*
+ * mapl.h -- C ABI of the MAPL stage-boundary codec and SPEL projector step
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Learned Subspace Compression for Communication-Efficient Pipeline
+ * Parallelism" (MAPL).  At each pipeline boundary the sender removes a
+ * per-stage factorised anchor embedding from the boundary activations and
+ * projects them onto an orthonormal projector (Sec. 3.2, Eq. 1), optionally
+ * residual-vector-quantises the coordinates (Sec. 3.5); the receiver
+ * rebuilds the activations (Eq. 2).  The projector is updated by SPEL
+ * (Sec. 3.3, Eqs. 4-7; the projector-update half of Algorithm 1).
+ *
+ * Notation used below (paper -> argument):
+ *   X^{b_p} [B,T,d] flattened to X [T,d]   boundary activations
+ *   A_p in St(d,r)                 -> U [d,r] fp32 (orthonormal columns)
+ *   E_p^small [V,k] (anchor table) -> A_s (sender), A_r (receiver) [V,k]
+ *   P_p (frozen companion)         -> B_s, B_r: [k,d] for the ambient anchor
+ *                                     of Eqs. 1-2, [k,r] for the coordinate
+ *                                     reading (anchor added in r-space)
+ *   t_ids                          -> ids [T] int32, 0 <= id < V
+ *   Z^{b_p} [T,r]                  -> payload when L == 0
+ *   R rounds of residual VQ        -> L stages, K codewords each,
+ *                                     codebooks C [L,K,r] fp32
+ *
+ * Conventions shared by every call
+ *   - Every array pointer is a DEVICE pointer owned by the caller; the
+ *     library never allocates, frees or retains user memory.  Arrays are
+ *     dense and row-major (last index fastest), 16-byte aligned.
+ *   - Scratch memory comes only from the caller's workspace `ws` of
+ *     `ws_bytes` bytes (256-byte aligned), sized by mapl_workspace_bytes().
+ *     The workspace is not preserved between calls.
+ *   - `stream` is a hipStream_t (passed as void*; NULL = default stream).
+ *     Calls only enqueue work on it and never synchronise.
+ *   - All arguments are validated on the host before anything is enqueued;
+ *     on any error nothing is written and a negative mapl_status is
+ *     returned; mapl_last_error() then describes it (thread-local string).
+ *   - Outputs must not overlap inputs (except U and M of
+ *     mapl_stiefel_step, which are updated in place).
+ *   - Token ids are not range-checked on the device (the caller guarantees
+ *     0 <= id < V); set MAPL_DEBUG=1 in the environment to have each codec
+ *     call check them (this synchronises the stream) and fail with
+ *     MAPL_E_RANGE.
+ *   - Codes are written token-major, codes[t*L + l]; among codewords at
+ *     equal distance the lowest index is chosen.
+ *   - Calls that run concurrently on different streams must use different
+ *     workspaces.
+ */
+#ifndef MAPL_H
+#define MAPL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MAPL_VERSION 1
+
+enum mapl_status {
+  MAPL_OK = 0,
+  MAPL_E_NULL = -1,        /* a required pointer is NULL                    */
+  MAPL_E_SHAPE = -2,       /* sizes out of range or inconsistent            */
+  MAPL_E_DTYPE = -3,       /* unknown or mismatched element type            */
+  MAPL_E_RANGE = -4,       /* K too large for the code type; bad token id   */
+  MAPL_E_ALIGN = -5,       /* pointer not 16-byte (workspace: 256) aligned  */
+  MAPL_E_ALIAS = -6,       /* an output overlaps an input                   */
+  MAPL_E_WORKSPACE = -7,   /* workspace missing or too small                */
+  MAPL_E_UNSUPPORTED = -8, /* valid request this build does not implement   */
+  MAPL_E_HIP = -9          /* a HIP launch or runtime call failed           */
+};
+
+enum mapl_dtype { MAPL_F32 = 0, MAPL_BF16 = 1, MAPL_U8 = 2, MAPL_U16 = 3 };
+
+enum mapl_anchor_space {
+  MAPL_ANCHOR_AMBIENT = 0, /* B is [k,d]: Eq. 1-2 (anchor removed/added in d-space) */
+  MAPL_ANCHOR_COORD = 1    /* B is [k,r]: anchor removed after projection,
+                              added back before the lift by U^T            */
+};
+
+enum mapl_call {
+  MAPL_CALL_ENCODE = 0,
+  MAPL_CALL_DECODE = 1,
+  MAPL_CALL_DECODE_BWD = 2,
+  MAPL_CALL_ENCODE_BWD = 3,
+  MAPL_CALL_STIEFEL = 4
+};
+
+/* One boundary, one micro-batch.
+ *   T  tokens (B*T of the paper flattened), 0 <= T < 2^31
+ *   d  model width, multiple of 64, 64 <= d <= 16384
+ *   r  projector rank, multiple of 32, 32 <= r <= min(d, 1024)
+ *   V  vocabulary size (rows of A), >= 1 when k > 0
+ *   k  anchor rank, multiple of 16, 0 <= k <= min(d, 512); 0 = no anchor
+ *   anchor_space  enum mapl_anchor_space
+ *   L  RVQ stages, 0 <= L <= 8; 0 = no quantisation, payload is Z [T,r]
+ *   K  codewords per stage (L > 0): multiple of 32, 32 <= K <= 65536
+ *   x_dtype   MAPL_BF16 or MAPL_F32: X, Z, Xhat, dXhat, dZ, dX
+ *   ab_dtype  element type of A and B; must equal x_dtype
+ *   code_dtype MAPL_U8 (K <= 256) or MAPL_U16 (K <= 65536); ignored if L == 0
+ *   On the bf16 path U is rounded to bf16 (round-to-nearest-even) where it
+ *   enters the matrix units; accumulation is fp32.  On the fp32 path every
+ *   operand stays fp32.
+ */
+typedef struct mapl_codec_desc {
+  int64_t T, d, r, V, k;
+  int32_t anchor_space;
+  int32_t L, K;
+  int32_t x_dtype, ab_dtype, code_dtype;
+} mapl_codec_desc;
+
+/* Sender side, Eq. 1 (Alg. 1, "Project") followed by RVQ (Sec. 3.5).
+ *   Z0[t] = (X[t] - A_s[ids[t]] B_s) U          (ambient)
+ *   Z0[t] = X[t] U - A_s[ids[t]] B_s            (coord)
+ *   L == 0: payload = Z0 rounded to x_dtype, [T,r].
+ *   L  > 0: for l = 0..L-1, codes[t,l] = argmin_j ||R_l[t] - C[l,j]||^2 with
+ *           R_0 = Z0, R_{l+1} = R_l - C[l, codes[t,l]]; payload = codes [T,L]
+ *           of code_dtype.  Distances are decided in fp32 from Z0 computed
+ *           with fp32 accumulation (bf16 matrix-unit screening, then exact
+ *           fp32 rescoring of every codeword that could be nearest).
+ *   C may be NULL when L == 0.  A_s/B_s may be NULL when k == 0. */
+int mapl_encode(const mapl_codec_desc* desc, const void* X, const int32_t* ids,
+                const float* U, const void* A_s, const void* B_s, const float* C,
+                void* payload, void* ws, size_t ws_bytes, void* stream);
+
+/* Receiver side, Eq. 2 (Alg. 1, "Reconstruct").
+ *   Zhat = payload (L == 0) or sum_l C[l, codes[t,l]] (L > 0)
+ *   Xhat[t] = Zhat[t] U^T + A_r[ids[t]] B_r       (ambient)
+ *   Xhat[t] = (Zhat[t] + A_r[ids[t]] B_r) U^T     (coord)
+ *   Xhat is [T,d] of x_dtype.  Codes >= K are a caller error. */
+int mapl_decode(const mapl_codec_desc* desc, const void* payload, const int32_t* ids,
+                const float* U, const void* A_r, const void* B_r, const float* C,
+                void* Xhat, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of Eq. 2 (Sec. 3.2: the gradient is routed back through the
+ * same projector).
+ *   dZ = dXhat U                                   [T,r] of x_dtype
+ *   dU (+)= dXhat^T Zhat                            (ambient)
+ *   dU (+)= dXhat^T (Zhat + A_r[ids] B_r)           (coord)      [d,r] fp32
+ * accumulate_dU = 0 overwrites dU, 1 adds to it (the sender's and the
+ * receiver's contributions to the shared projector sum). */
+int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, const void* payload,
+                    const int32_t* ids, const float* U, const void* A_r, const void* B_r,
+                    const float* C, void* dZ, float* dU, int accumulate_dU, void* ws,
+                    size_t ws_bytes, void* stream);
+
+/* Backward of Eq. 1; the quantiser is passed straight through (the gradient
+ * of the codes' reconstruction is taken as the gradient of Z0).
+ *   dX = dZ U^T                                    [T,d] of x_dtype
+ *   dU (+)= (X - A_s[ids] B_s)^T dZ                 (ambient)
+ *   dU (+)= X^T dZ                                   (coord)     [d,r] fp32 */
+int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, const void* X,
+                    const int32_t* ids, const float* U, const void* A_s, const void* B_s,
+                    void* dX, float* dU, int accumulate_dU, void* ws, size_t ws_bytes,
+                    void* stream);
+
+/* SPEL step (Sec. 3.3, Eqs. 4-7) on P independent projectors, all fp32,
+ * arrays [P,d,r]:
+ *   g_R = G - U sym(U^T G)                     (Eq. 4, sym(S) = (S+S^T)/2)
+ *   M   = beta M + (1 - beta) g_R              (Eq. 5, in place)
+ *   D   = PolarExpress_{lmo_steps}(M / (||M||_F + 1e-7))          (Eq. 6)
+ *   Y   = U - lr D
+ *   U   = PolarExpress_{retract_steps}(Y / nu), nu^2 = max row sum of
+ *         |Y^T Y| (an upper bound of sigma_max(Y)^2)                (Eq. 7)
+ * PolarExpress step: X <- a X + X (b S + c S^2), S = X^T X, with the greedy
+ * minimax odd-quintic schedule designed for singular values in [1e-3, 1]
+ * (LMO) and [0.5, 1] (retraction).  Requirements: 1 <= P, 32 <= r <= d,
+ * r multiple of 32, d multiple of 32, r <= 1024, 1 <= lmo_steps,
+ * retract_steps <= 16.  The retraction is accurate while lr*||D||_2 <= 1/3. */
+int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, const float* G, float* M,
+                      float lr, float beta, int lmo_steps, int retract_steps, void* ws,
+                      size_t ws_bytes, void* stream);
+
+/* Workspace bytes needed by `call` (enum mapl_call).  Codec calls read
+ * `desc` and ignore P, d, r; MAPL_CALL_STIEFEL ignores `desc`.  Returns 0
+ * for an invalid request (mapl_last_error() says why). */
+size_t mapl_workspace_bytes(const mapl_codec_desc* desc, int call, int64_t P, int64_t d,
+                            int64_t r);
+
+/* Thread-local description of the last error on this thread ("" if none). */
+const char* mapl_last_error(void);
+
+/* MAPL_VERSION of the built library. */
+int mapl_version(void);
+
+/* Tracing.  mapl_profile(1) makes every later call bracket each of its
+ * kernel launches with a pair of HIP events on the call's stream (a small
+ * per-launch overhead); mapl_profile(0) stops it.  mapl_profile_report()
+ * waits for the recorded events, writes one line "name launches total_ms"
+ * per kernel (names are "<call>:<kernel>") into buf (NUL-terminated, at most
+ * `bytes` bytes), and forgets the records.  Returns MAPL_OK, MAPL_E_HIP if an
+ * event could not be resolved, or MAPL_E_WORKSPACE if buf was too small (the
+ * text is truncated). */
+int mapl_profile(int enable);
+int mapl_profile_report(char* buf, size_t bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MAPL_H */

@@ -1,0 +1,59 @@
+// Shared device helpers for the gfx950 (CDNA4) kernels of libmapl.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mapl {
+
+typedef uint16_t bf16_t;  // bf16 stored as its bit pattern
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+
+constexpr int WAVE = 64;
+
+// fp32 -> bf16 bits, round to nearest even (inputs here are finite).
+__device__ __forceinline__ uint32_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
+__device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
+  return f2bf(lo) | (f2bf(hi) << 16);
+}
+
+// 32x32x16 bf16 MFMA, fp32 accumulate.
+// Lane l holds A[m = l%32][k = 8(l/32) .. +7] and B[k = 8(l/32) .. +7][n = l%32];
+// accumulator j of lane l is D[m = 8(j/4) + 4(l/32) + j%4][n = l%32].
+__device__ __forceinline__ f32x16_t mfma32x32x16(const uint4& a, const uint4& b, f32x16_t c) {
+  bf16x8_t av = __builtin_bit_cast(bf16x8_t, a);
+  bf16x8_t bv = __builtin_bit_cast(bf16x8_t, b);
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, c, 0, 0, 0);
+}
+
+// 32x32x2 fp32 MFMA: lane l holds A[m = l%32][k = l/32], B[k = l/32][n = l%32];
+// accumulator layout as above.
+__device__ __forceinline__ f32x16_t mfma32x32x2f32(float a, float b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+// Token ids outside [0, V) read row 0 instead of faulting.
+__device__ __forceinline__ int clamp_id(int id, int V) { return (unsigned)id < (unsigned)V ? id : 0; }
+
+__device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
+
+// Wave-wide reductions (wave64) through LDS-free cross-lane shuffles.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  return v;
+}
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, WAVE));
+  return v;
+}
+
+}  // namespace mapl

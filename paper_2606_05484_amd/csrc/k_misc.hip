@@ -1,0 +1,220 @@
+// Small kernels: the fp32 codec path (gathers, exact fp32 RVQ, codebook
+// sums) and the elementwise / reduction steps of the SPEL update
+// (Sec. 3.3: Eq. 4 symmetrisation, Eq. 5 momentum, the normalisations that
+// precede the two PolarExpress iterations of Eqs. 6-7).
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace mapl {
+
+namespace {
+
+__global__ void k_gather_rows_f32(const float* __restrict__ A, int k, const int32_t* __restrict__ ids,
+                                  int V, int T, float* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)T * k) return;
+  const int t = (int)(i / k), c = (int)(i % k);
+  out[i] = A[(int64_t)clamp_id(ids[t], V) * k + c];
+}
+
+// One wave per token: residual in registers/LDS, exact fp32 squared
+// distances sum_c (R_c - C_jc)^2 for every codeword, lowest index on ties.
+__global__ void k_rvq_f32(const float* __restrict__ Z0, const float* __restrict__ C, int T, int r, int L,
+                          int K, void* codes, int code_bytes) {
+  extern __shared__ float sh[];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + wave;
+  if (t >= T) return;
+  float* R = sh + wave * r;
+  for (int c = lane; c < r; c += 64) R[c] = Z0[(int64_t)t * r + c];
+  __builtin_amdgcn_wave_barrier();
+  for (int l = 0; l < L; ++l) {
+    const float* Cl = C + (int64_t)l * K * r;
+    float best = INFINITY;
+    int bj = 0x7fffffff;
+    for (int j = lane; j < K; j += 64) {
+      float s = 0.f;
+      for (int c = 0; c < r; ++c) {
+        const float df = R[c] - Cl[(int64_t)j * r + c];
+        s = fmaf(df, df, s);
+      }
+      if (s < best) { best = s; bj = j; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ob = __shfl_xor(best, o, WAVE);
+      const int oj = __shfl_xor(bj, o, WAVE);
+      if (ob < best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+    }
+    if (bj >= K) bj = 0;  // only reachable with non-finite inputs
+    if (lane == 0) {
+      if (code_bytes == 1)
+        ((uint8_t*)codes)[(int64_t)t * L + l] = (uint8_t)bj;
+      else
+        ((uint16_t*)codes)[(int64_t)t * L + l] = (uint16_t)bj;
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int c = lane; c < r; c += 64) R[c] -= Cl[(int64_t)bj * r + c];
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+__global__ void k_codes_sum_f32(const void* __restrict__ codes, int code_bytes, const float* __restrict__ C,
+                                int T, int r, int L, int K, float* __restrict__ Zhat) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)T * r) return;
+  const int t = (int)(i / r), c = (int)(i % r);
+  float v = 0.f;
+  for (int l = 0; l < L; ++l) {
+    int code = code_bytes == 1 ? ((const uint8_t*)codes)[(int64_t)t * L + l]
+                               : ((const uint16_t*)codes)[(int64_t)t * L + l];
+    code = code < K ? code : K - 1;
+    v += C[((int64_t)l * K + code) * r + c];
+  }
+  Zhat[i] = v;
+}
+
+__global__ void k_copy_f32(const float* __restrict__ src, float* __restrict__ dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+
+__global__ void k_symmetrize(float* S, int r) {
+  float* Sp = S + (int64_t)blockIdx.y * r * r;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)r * r) return;
+  const int a = (int)(i / r), b = (int)(i % r);
+  if (a < b) {
+    const float v = 0.5f * (Sp[(int64_t)a * r + b] + Sp[(int64_t)b * r + a]);
+    Sp[(int64_t)a * r + b] = v;
+    Sp[(int64_t)b * r + a] = v;
+  }
+}
+
+// grid (nblk, P): block-stride loop, one partial sum of M^2 per block.
+__global__ void k_momentum(float* __restrict__ M, const float* __restrict__ gR, int64_t n, float beta,
+                           float* __restrict__ partial) {
+  __shared__ float red[4];
+  const int p = blockIdx.y;
+  float* Mp = M + (int64_t)p * n;
+  const float* gp = gR + (int64_t)p * n;
+  float s = 0.f;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const float v = beta * Mp[i] + (1.f - beta) * gp[i];
+    Mp[i] = v;
+    s = fmaf(v, v, s);
+  }
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) partial[(int64_t)p * gridDim.x + blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ void k_fro_scale(const float* __restrict__ partial, int nblk, float eps, float* scale,
+                            float* scale2) {
+  const int p = blockIdx.x, lane = threadIdx.x;
+  float s = 0.f;
+  for (int i = lane; i < nblk; i += 64) s += partial[(int64_t)p * nblk + i];
+  s = wave_sum(s);
+  if (lane == 0) {
+    const float sc = 1.f / (sqrtf(s) + eps);
+    scale[p] = sc;
+    scale2[p] = sc * sc;
+  }
+}
+
+__global__ void k_axpy(const float* __restrict__ U, const float* __restrict__ D, float lr, float* __restrict__ Y,
+                       int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) Y[i] = U[i] - lr * D[i];
+}
+
+// One block per projector: nu2 = max_i sum_j |S_ij|.
+__global__ void k_inf_norm_scales(const float* __restrict__ S, int r, float* inv_nu, float* inv_nu2,
+                                  float* inv_nu4) {
+  __shared__ float red[4];
+  const int p = blockIdx.x;
+  const float* Sp = S + (int64_t)p * r * r;
+  float m = 0.f;
+  for (int i = threadIdx.x; i < r; i += blockDim.x) {
+    float s = 0.f;
+    for (int j = 0; j < r; ++j) s += fabsf(Sp[(int64_t)i * r + j]);
+    m = fmaxf(m, s);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, WAVE));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float nu2 = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const float in2 = 1.f / nu2;
+    inv_nu2[p] = in2;
+    inv_nu4[p] = in2 * in2;
+    inv_nu[p] = sqrtf(in2);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gather_rows_f32(const float* A, int k, const int32_t* ids, int V, int T, float* out,
+                                  hipStream_t s) {
+  const int64_t n = (int64_t)T * k;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_rows_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, A, k, ids, V, T, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_rvq_f32(const float* Z0, const float* C, int T, int r, int L, int K, void* codes,
+                          int code_bytes, hipStream_t s) {
+  if (T <= 0 || L <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rvq_f32, dim3((T + 3) / 4), dim3(256), 4 * r * sizeof(float), s, Z0, C, T, r, L, K,
+                     codes, code_bytes);
+  return hipGetLastError();
+}
+
+hipError_t launch_codes_sum_f32(const void* codes, int code_bytes, const float* C, int T, int r, int L, int K,
+                                float* Zhat, hipStream_t s) {
+  const int64_t n = (int64_t)T * r;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_codes_sum_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, codes, code_bytes, C,
+                     T, r, L, K, Zhat);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_symmetrize(float* S, int P, int r, hipStream_t s) {
+  const int64_t n = (int64_t)r * r;
+  hipLaunchKernelGGL(k_symmetrize, dim3((unsigned)((n + 255) / 256), P), dim3(256), 0, s, S, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_momentum(float* M, const float* gR, int64_t n, int P, float beta, float* partial, int nblk,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(k_momentum, dim3(nblk, P), dim3(256), 0, s, M, gR, n, beta, partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float* scale, float* scale2,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(k_fro_scale, dim3(P), dim3(64), 0, s, partial, nblk, eps, scale, scale2);
+  return hipGetLastError();
+}
+
+hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_axpy, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, U, D, lr, Y, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* inv_nu, float* inv_nu2, float* inv_nu4,
+                                  hipStream_t s) {
+  hipLaunchKernelGGL(k_inf_norm_scales, dim3(P), dim3(256), 0, s, S, r, inv_nu, inv_nu2, inv_nu4);
+  return hipGetLastError();
+}
+
+}  // namespace mapl

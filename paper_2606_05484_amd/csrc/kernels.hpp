@@ -1,0 +1,134 @@
+// Launchers of the gfx950 kernels behind libmapl.  Host-side only
+// declarations; every launcher enqueues on the given stream and returns
+// hipGetLastError().
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mapl {
+
+typedef uint16_t bf16_t;
+
+// ---------------------------------------------------------------- bf16 GEMM
+// out[t,n] = sum_{c<Ka} A[t,c] W[n,c] + sum_{i<Kg} T[ids[t],i] W[n,Ka+i]
+// Ka % 32 == 0, Kg % 16 == 0, ldw >= Ka + roundup(Kg,32) with zero padding,
+// lda, ldt, ldw multiples of 8 (16 B rows), N % 32 == 0.
+struct TnArgs {
+  const bf16_t* A; int64_t lda;
+  const bf16_t* T; int64_t ldt; const int32_t* ids; int Kg; int V;  // ids clamped to [0,V)
+  const bf16_t* W; int64_t ldw;
+  int M, N, Ka;
+  void* out; int64_t ldo; int out_f32;
+};
+hipError_t launch_gemm_tn(const TnArgs& g, hipStream_t s);
+
+// ---------------------------------------------------------------- fp32 GEMM
+// C[b](m,n) = alpha_b sum_k A[b](m,k) B[b](k,n) + beta_b Cin[b](m,n)
+// element types: 0 = fp32, 1 = bf16 (A, B, C); Cin is fp32 (may be null).
+struct GemmF32Args {
+  const void* A; int64_t sAm, sAk, sAb;
+  const void* B; int64_t sBk, sBn, sBb;
+  const float* Cin; int64_t sCinm, sCinn, sCinb;
+  void* C; int64_t sCm, sCn, sCb;
+  int M, N, K, batch;
+  float alpha, beta;
+  const float* alpha_ptr; const float* beta_ptr;
+};
+hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStream_t s);
+
+// ---------------------------------------------------------------- weight gradient
+// part[s][m][n] = sum over tokens t of split s of P[t,m] Q[t,n], where
+// P[t,m] = Pa[t,m] for m < Ma and Tg[ids[t], m-Ma] for Ma <= m < Ma+Mg.
+// Ma % 8 == 0, Mg % 8 == 0, N % 64 == 0; bf16 inputs, fp32 partials.
+struct WgradArgs {
+  const bf16_t* Pa; int64_t ldp; int Ma;
+  const bf16_t* Tg; int64_t ldt; const int32_t* ids; int Mg; int V;
+  const bf16_t* Q; int64_t ldq;
+  int T, N, splits, tokens_per_split;
+  float* part;  // [splits][Ma+Mg][N]
+};
+hipError_t launch_wgrad(const WgradArgs& g, hipStream_t s);
+// dst[m][n] (+)= sum_s part[s][m][n] for m < M (fixed summation order).
+hipError_t launch_reduce_splits(const float* part, int splits, int M, int N, int64_t part_stride,
+                                float* dst, int accumulate, hipStream_t s);
+
+// ---------------------------------------------------------------- operand prep
+// Ub[j][c] = bf16(U[j][c]) (row stride ldub, c < r), Ut[c][j] = bf16(U[j][c])
+// (row stride ldut, j < d); either pointer may be null.  Padding columns
+// [r, ldub) of Ub and [d, ldut) of Ut are zeroed.
+hipError_t launch_prep_u(const float* U, int d, int r, bf16_t* Ub, int64_t ldub, bf16_t* Ut,
+                         int64_t ldut, hipStream_t s);
+// dst[j*ldd + off + i] = bf16(scale * src[i*lds + j]) for i < rows, j < cols
+// (a transposed, scaled copy of a [rows, cols] matrix); src_f32 selects fp32
+// or bf16 source.
+hipError_t launch_transpose_into(const void* src, int src_f32, int rows, int cols, int64_t lds,
+                                 float scale, bf16_t* dst, int64_t ldd, int off, hipStream_t s);
+// Cb[l][j][c] = bf16(C[l][j][c]); cn2[l*K+j] = ||C[l][j]||^2; cnrm = sqrt.
+hipError_t launch_prep_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* cn2,
+                                float* cnrm, hipStream_t s);
+
+// ---------------------------------------------------------------- receiver-side operand
+// out[t][0:r]   = Zhat[t]: payload row (bf16) or sum_l C[l][codes[t,l]] (fp32 -> bf16)
+// out[t][r:r+k] = A[ids[t]] when A != null; remaining columns up to ldo zeroed.
+// When Bc != null (coordinate anchor), out[t][0:r] = Zhat[t] + A[ids[t]] Bc
+// (Bc [k,r] bf16) and no anchor columns are appended.
+struct AssembleArgs {
+  const bf16_t* Zp;                  // [T,r] bf16 payload (L == 0) or null
+  const void* codes; int code_bytes; // [T,L] (L > 0)
+  const float* C; int L, K;          // [L,K,r]
+  const bf16_t* A; int k;            // anchor table [V,k] or null
+  const bf16_t* Bc;                  // [k,r] coordinate anchor companion or null
+  const int32_t* ids; int V;
+  int T, r; int64_t ldo;
+  bf16_t* out;
+};
+hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- RVQ (bf16 screen + fp32 rescore)
+struct RvqArgs {
+  const float* Z0;     // [T,r] fp32 unquantised coordinates
+  const bf16_t* Cb;    // [L,K,r] bf16 screening copy
+  const float* C;      // [L,K,r] fp32 codebooks
+  const float* cn2;    // [L,K] ||C||^2
+  const float* cnrm;   // [L,K] ||C||
+  int T, r, L, K;
+  void* codes; int code_bytes;  // [T,L]
+  int* stats;          // [4] optional counters (candidates, overflow), may be null
+};
+hipError_t launch_rvq(const RvqArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- fp32 codec path helpers
+// out[t][i] = A[ids[t]][i] (fp32) for i < k.
+hipError_t launch_gather_rows_f32(const float* A, int k, const int32_t* ids, int V, int T, float* out,
+                                  hipStream_t s);
+// fp32 residual quantisation with exact fp32 distances over all K.
+hipError_t launch_rvq_f32(const float* Z0, const float* C, int T, int r, int L, int K, void* codes,
+                          int code_bytes, hipStream_t s);
+// Zhat[t] = sum_l C[l][codes[t,l]] (fp32).
+hipError_t launch_codes_sum_f32(const void* codes, int code_bytes, const float* C, int T, int r, int L,
+                                int K, float* Zhat, hipStream_t s);
+hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s);
+
+// ---------------------------------------------------------------- Stiefel step helpers
+// S <- (S + S^T)/2 for each of P [r,r] matrices, in place.
+hipError_t launch_symmetrize(float* S, int P, int r, hipStream_t s);
+// M <- beta M + (1-beta) gR (n elements per projector, P projectors);
+// partial sums of M^2 -> partial[P][nblk].
+hipError_t launch_momentum(float* M, const float* gR, int64_t n, int P, float beta, float* partial,
+                           int nblk, hipStream_t s);
+// scale[p] = 1/(sqrt(sum partial[p]) + eps), scale2[p] = scale^2.
+hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float* scale,
+                            float* scale2, hipStream_t s);
+// Y = U - lr D.
+hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64_t n, hipStream_t s);
+// For S [P][r][r]: nu2 = max_i sum_j |S_ij|; inv_nu = 1/sqrt(nu2), inv_nu2 = 1/nu2,
+// inv_nu4 = 1/nu2^2.
+hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* inv_nu, float* inv_nu2,
+                                  float* inv_nu4, hipStream_t s);
+
+// ---------------------------------------------------------------- debug
+// flag[0] = 1 if any ids[t] is outside [0, V).
+hipError_t launch_check_ids(const int32_t* ids, int T, int64_t V, int* flag, hipStream_t s);
+hipError_t launch_zero_bytes(void* p, int64_t bytes, hipStream_t s);
+
+}  // namespace mapl

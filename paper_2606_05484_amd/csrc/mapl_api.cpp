@@ -1,0 +1,914 @@
+// libmapl host side: argument validation, workspace layout and kernel
+// sequencing for the five C-ABI calls declared in include/mapl.h.
+//
+// Data flow per call (bf16 path; "~" = rounded to bf16 for the matrix units):
+//   encode      prep U~^T | B_s U~ (ambient) -> Z0 = [X | a_s] [U~ ; -(B_s U~)]^T
+//               (one token-major GEMM, anchors gathered in flight) -> bf16 Z
+//               (L = 0) or fp32 Z0 -> RVQ screen/rescore -> codes
+//   decode      prep [U~ | B_r^T] -> Zhat (payload, or codebook gather-sum)
+//               -> Xhat = [Zhat | a_r] [U~ | B_r^T]^T
+//   decode_bwd  dZ = dXhat U~;  dU (+)= dXhat^T Zhat  (split over tokens,
+//               fixed-order reduction)
+//   encode_bwd  dX = dZ U~^T;  dU (+)= X^T dZ - B_s^T (a_s^T dZ)
+//   stiefel     Eq. 4 tangent projection, Eq. 5 momentum, Eq. 6 LMO and
+//               Eq. 7 retraction by PolarExpress, batched over projectors.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/mapl.h"
+#include "kernels.hpp"
+#include "polar_coeffs.h"
+
+using namespace mapl;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(MAPL_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define MAPL_HIP(expr)                                  \
+  do {                                                  \
+    hipError_t e_ = (expr);                             \
+    if (e_ != hipSuccess) return hip_fail(e_, #expr);   \
+  } while (0)
+
+bool debug_ids() {
+  static const int on = [] {
+    const char* v = getenv("MAPL_DEBUG");
+    return (v && v[0] && v[0] != '0') ? 1 : 0;
+  }();
+  return on != 0;
+}
+
+// ------------------------------------------------------------------ tracing
+// mapl_profile(1) brackets every kernel launch with a pair of HIP events on
+// the caller's stream; mapl_profile_report() resolves them into per-kernel
+// launch counts and total milliseconds.
+struct ProfRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof = false;
+std::vector<ProfRec> g_prof_recs;
+std::vector<hipEvent_t> g_prof_pool;
+
+hipEvent_t prof_event() {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_pool.empty()) {
+    hipEvent_t e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void prof_push(const char* name, hipEvent_t a, hipEvent_t b) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_recs.push_back({name, a, b});
+}
+
+#define LAUNCH(NAME, EXPR)                                              \
+  do {                                                                  \
+    hipEvent_t e0_ = nullptr, e1_ = nullptr;                            \
+    if (g_prof && (e0_ = prof_event()) != nullptr) (void)hipEventRecord(e0_, s); \
+    MAPL_HIP(EXPR);                                                     \
+    if (e0_ && (e1_ = prof_event()) != nullptr) {                       \
+      (void)hipEventRecord(e1_, s);                                     \
+      prof_push(NAME, e0_, e1_);                                        \
+    }                                                                   \
+  } while (0)
+
+inline int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline size_t esize(int dt) { return dt == MAPL_F32 ? 4 : 2; }
+inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// ------------------------------------------------------------------ workspace
+struct Carve {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    size_t o = off;
+    off = (size_t)rup((int64_t)(off + bytes), 256);
+    return o;
+  }
+};
+
+struct SplitPlan {
+  int splits, tps;
+};
+
+SplitPlan plan_splits(int64_t T, int Mtot, int N) {
+  const int bn = (N % 128 == 0) ? 128 : 64;
+  const int64_t tiles = ((Mtot + 127) / 128) * (int64_t)(N / bn);
+  int64_t want = (512 + tiles - 1) / tiles;
+  int64_t maxs = (T + 63) / 64;
+  if (want > maxs) want = maxs;
+  if (want < 1) want = 1;
+  int64_t tps = rup((T + want - 1) / want, 64);
+  if (tps < 64) tps = 64;
+  int64_t splits = (T + tps - 1) / tps;
+  if (splits < 1) splits = 1;
+  return {(int)splits, (int)tps};
+}
+
+struct Layout {
+  size_t total = 0;
+  size_t w = 0, w2 = 0, z0 = 0, cb = 0, cn2 = 0, cnr = 0, stats = 0, flag = 0;
+  size_t ahat = 0, part = 0, wsum = 0, ga = 0, bu = 0, zh = 0, z2 = 0;
+  int64_t kp = 0, kw = 0;
+  SplitPlan sp{1, 64};
+};
+
+Layout layout(const mapl_codec_desc& D, int call) {
+  Layout Lo;
+  Carve c;
+  c.take(0);
+  const bool bf = D.x_dtype == MAPL_BF16;
+  const int64_t T = D.T, d = D.d, r = D.r, k = D.k;
+  const bool amb = D.anchor_space == MAPL_ANCHOR_AMBIENT;
+  Lo.flag = c.take(256);
+  Lo.kp = k > 0 ? rup(k, 32) : 0;
+  if (bf) {
+    switch (call) {
+      case MAPL_CALL_ENCODE:
+        Lo.kw = d + Lo.kp;
+        Lo.w = c.take((size_t)r * Lo.kw * 2);
+        if (D.L > 0) {
+          Lo.z0 = c.take((size_t)T * r * 4);
+          Lo.cb = c.take((size_t)D.L * D.K * r * 2);
+          Lo.cn2 = c.take((size_t)D.L * D.K * 4);
+          Lo.cnr = c.take((size_t)D.L * D.K * 4);
+          Lo.stats = c.take(16);
+        }
+        break;
+      case MAPL_CALL_DECODE:
+        Lo.kw = r + Lo.kp;
+        Lo.w2 = c.take((size_t)d * Lo.kw * 2);
+        if (D.L > 0) Lo.ahat = c.take((size_t)T * r * 2);
+        break;
+      case MAPL_CALL_DECODE_BWD:
+        Lo.w = c.take((size_t)r * d * 2);
+        if (D.L > 0 || (!amb && k > 0)) Lo.ahat = c.take((size_t)T * r * 2);
+        Lo.sp = plan_splits(T, (int)d, (int)r);
+        Lo.part = c.take((size_t)Lo.sp.splits * d * r * 4);
+        break;
+      case MAPL_CALL_ENCODE_BWD: {
+        Lo.w2 = c.take((size_t)d * r * 2);
+        const int mg = (amb && k > 0) ? (int)k : 0;
+        Lo.sp = plan_splits(T, (int)(d + mg), (int)r);
+        Lo.part = c.take((size_t)Lo.sp.splits * (d + mg) * r * 4);
+        if (mg) Lo.wsum = c.take((size_t)k * r * 4);
+        break;
+      }
+    }
+  } else {
+    switch (call) {
+      case MAPL_CALL_ENCODE:
+        if (k > 0) Lo.ga = c.take((size_t)T * k * 4);
+        if (k > 0 && amb) Lo.bu = c.take((size_t)k * r * 4);
+        if (D.L > 0) Lo.z0 = c.take((size_t)T * r * 4);
+        break;
+      case MAPL_CALL_DECODE:
+      case MAPL_CALL_DECODE_BWD:
+        if (k > 0) Lo.ga = c.take((size_t)T * k * 4);
+        Lo.zh = c.take((size_t)T * r * 4);
+        if (!amb && k > 0) Lo.z2 = c.take((size_t)T * r * 4);
+        break;
+      case MAPL_CALL_ENCODE_BWD:
+        if (k > 0 && amb) {
+          Lo.ga = c.take((size_t)T * k * 4);
+          Lo.wsum = c.take((size_t)k * r * 4);
+        }
+        break;
+    }
+  }
+  Lo.total = c.off;
+  return Lo;
+}
+
+// ------------------------------------------------------------------ validation
+int check_desc(const mapl_codec_desc* D) {
+  if (!D) return fail(MAPL_E_NULL, "desc is NULL");
+  if (D->x_dtype != MAPL_BF16 && D->x_dtype != MAPL_F32)
+    return fail(MAPL_E_DTYPE, "x_dtype must be MAPL_BF16 or MAPL_F32 (got %d)", D->x_dtype);
+  if (D->ab_dtype != D->x_dtype)
+    return fail(MAPL_E_DTYPE, "ab_dtype (%d) must equal x_dtype (%d)", D->ab_dtype, D->x_dtype);
+  if (D->T < 0 || D->T >= ((int64_t)1 << 31)) return fail(MAPL_E_SHAPE, "T=%lld out of range", (long long)D->T);
+  if (D->d < 64 || D->d > 16384 || D->d % 64) return fail(MAPL_E_SHAPE, "d=%lld: need 64 <= d <= 16384, d %% 64 == 0", (long long)D->d);
+  if (D->r < 32 || D->r > 1024 || D->r % 32 || D->r > D->d)
+    return fail(MAPL_E_SHAPE, "r=%lld: need 32 <= r <= min(d,1024), r %% 32 == 0", (long long)D->r);
+  if (D->k < 0 || D->k > 512 || D->k % 16 || D->k > D->d)
+    return fail(MAPL_E_SHAPE, "k=%lld: need 0 <= k <= min(d,512), k %% 16 == 0", (long long)D->k);
+  if (D->k > 0 && (D->V < 1 || D->V >= ((int64_t)1 << 31))) return fail(MAPL_E_SHAPE, "V=%lld out of range", (long long)D->V);
+  if (D->anchor_space != MAPL_ANCHOR_AMBIENT && D->anchor_space != MAPL_ANCHOR_COORD)
+    return fail(MAPL_E_SHAPE, "anchor_space=%d unknown", D->anchor_space);
+  if (D->L < 0 || D->L > 8) return fail(MAPL_E_SHAPE, "L=%d: need 0 <= L <= 8", D->L);
+  if (D->L > 0) {
+    if (D->K < 32 || D->K > 65536 || D->K % 32) return fail(MAPL_E_SHAPE, "K=%d: need 32 <= K <= 65536, K %% 32 == 0", D->K);
+    if (D->code_dtype == MAPL_U8) {
+      if (D->K > 256) return fail(MAPL_E_RANGE, "K=%d does not fit MAPL_U8 codes", D->K);
+    } else if (D->code_dtype != MAPL_U16) {
+      return fail(MAPL_E_DTYPE, "code_dtype must be MAPL_U8 or MAPL_U16 (got %d)", D->code_dtype);
+    }
+    if (D->x_dtype == MAPL_BF16 && D->r > 256)
+      return fail(MAPL_E_UNSUPPORTED, "RVQ on the bf16 path supports r <= 256 (got %lld)", (long long)D->r);
+  }
+  return MAPL_OK;
+}
+
+struct Span {
+  const void* p;
+  size_t bytes;
+  const char* name;
+};
+
+int check_ptrs(std::initializer_list<Span> req, std::initializer_list<Span> outs, std::initializer_list<Span> ins) {
+  for (const Span& s : req)
+    if (s.bytes > 0 && !s.p) return fail(MAPL_E_NULL, "%s is NULL", s.name);
+  for (const Span& s : req)
+    if (s.p && !aligned(s.p, 16)) return fail(MAPL_E_ALIGN, "%s is not 16-byte aligned", s.name);
+  for (const Span& o : outs) {
+    if (!o.p || !o.bytes) continue;
+    const uintptr_t a0 = (uintptr_t)o.p, a1 = a0 + o.bytes;
+    for (const Span& i : ins) {
+      if (!i.p || !i.bytes) continue;
+      const uintptr_t b0 = (uintptr_t)i.p, b1 = b0 + i.bytes;
+      if (a0 < b1 && b0 < a1) return fail(MAPL_E_ALIAS, "output %s overlaps input %s", o.name, i.name);
+    }
+  }
+  return MAPL_OK;
+}
+
+int check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return MAPL_OK;
+  if (!ws) return fail(MAPL_E_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (!aligned(ws, 256)) return fail(MAPL_E_ALIGN, "workspace is not 256-byte aligned");
+  if (ws_bytes < need) return fail(MAPL_E_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+  return MAPL_OK;
+}
+
+int run_id_check(const int32_t* ids, int64_t T, int64_t V, void* ws, const Layout& Lo, hipStream_t s) {
+  if (!debug_ids() || T == 0) return MAPL_OK;
+  int* flag = (int*)((char*)ws + Lo.flag);
+  MAPL_HIP(launch_zero_bytes(flag, 4, s));
+  MAPL_HIP(launch_check_ids(ids, (int)T, V, flag, s));
+  int h = 0;
+  MAPL_HIP(hipMemcpyAsync(&h, flag, 4, hipMemcpyDeviceToHost, s));
+  MAPL_HIP(hipStreamSynchronize(s));
+  if (h) return fail(MAPL_E_RANGE, "a token id is outside [0, V=%lld)", (long long)V);
+  return MAPL_OK;
+}
+
+// Convenience builders for the fp32-unit GEMM.
+GemmF32Args gemm(int M, int N, int K) {
+  GemmF32Args g;
+  memset(&g, 0, sizeof g);
+  g.M = M; g.N = N; g.K = K; g.batch = 1;
+  g.alpha = 1.f; g.beta = 0.f;
+  return g;
+}
+
+template <typename P>
+inline P* at(void* ws, size_t off) { return (P*)((char*)ws + off); }
+
+size_t code_bytes(const mapl_codec_desc& D) { return D.code_dtype == MAPL_U8 ? 1 : 2; }
+size_t payload_bytes(const mapl_codec_desc& D) {
+  return D.L == 0 ? (size_t)D.T * D.r * esize(D.x_dtype) : (size_t)D.T * D.L * code_bytes(D);
+}
+size_t b_cols(const mapl_codec_desc& D) { return D.anchor_space == MAPL_ANCHOR_AMBIENT ? D.d : D.r; }
+
+}  // namespace
+
+// ===================================================================== API
+
+extern "C" const char* mapl_last_error(void) { return g_err.c_str(); }
+extern "C" int mapl_version(void) { return MAPL_VERSION; }
+
+extern "C" size_t mapl_workspace_bytes(const mapl_codec_desc* desc, int call, int64_t P, int64_t d, int64_t r) {
+  g_err.clear();
+  if (call == MAPL_CALL_STIEFEL) {
+    if (P < 1 || d < 32 || r < 32 || r > d || r > 1024 || r % 32 || d % 32) {
+      fail(MAPL_E_SHAPE, "stiefel: need 1 <= P, 32 <= r <= min(d,1024), r and d multiples of 32");
+      return 0;
+    }
+    Carve c;
+    c.take((size_t)P * r * r * 4);   // S
+    c.take((size_t)P * r * r * 4);   // Q
+    c.take((size_t)P * d * r * 4);   // X0
+    c.take((size_t)P * d * r * 4);   // X1
+    c.take((size_t)P * 1024 * 4);    // partial sums
+    c.take((size_t)P * 8 * 4);       // scalars
+    return c.off;
+  }
+  if (call < MAPL_CALL_ENCODE || call > MAPL_CALL_ENCODE_BWD) {
+    fail(MAPL_E_SHAPE, "unknown call %d", call);
+    return 0;
+  }
+  if (check_desc(desc) != MAPL_OK) return 0;
+  return layout(*desc, call).total;
+}
+
+// --------------------------------------------------------------------- encode
+extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int32_t* ids, const float* U,
+                           const void* A_s, const void* B_s, const float* C, void* payload, void* ws,
+                           size_t ws_bytes, void* stream) {
+  g_err.clear();
+  int st = check_desc(desc);
+  if (st) return st;
+  const mapl_codec_desc& D = *desc;
+  const int64_t T = D.T, d = D.d, r = D.r, k = D.k;
+  const size_t xe = esize(D.x_dtype);
+  st = check_ptrs({{X, (size_t)T * d * xe, "X"}, {ids, k > 0 ? (size_t)T * 4 : 0, "ids"},
+                   {U, (size_t)d * r * 4, "U"}, {A_s, k > 0 ? (size_t)D.V * k * xe : 0, "A_s"},
+                   {B_s, k > 0 ? (size_t)k * b_cols(D) * xe : 0, "B_s"},
+                   {C, D.L > 0 ? (size_t)D.L * D.K * r * 4 : 0, "C"}, {payload, payload_bytes(D), "payload"}},
+                  {{payload, payload_bytes(D), "payload"}},
+                  {{X, (size_t)T * d * xe, "X"}, {ids, (size_t)T * 4, "ids"}, {U, (size_t)d * r * 4, "U"},
+                   {A_s, (size_t)D.V * k * xe, "A_s"}, {B_s, (size_t)k * b_cols(D) * xe, "B_s"},
+                   {C, (size_t)D.L * D.K * r * 4, "C"}, {ws, ws_bytes, "workspace"}});
+  if (st) return st;
+  const Layout Lo = layout(D, MAPL_CALL_ENCODE);
+  if ((st = check_ws(ws, ws_bytes, Lo.total))) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (k > 0 && (st = run_id_check(ids, T, D.V, ws, Lo, s))) return st;
+  if (T == 0) return MAPL_OK;
+  const bool amb = D.anchor_space == MAPL_ANCHOR_AMBIENT;
+  const int cbytes = (int)code_bytes(D);
+
+  if (D.x_dtype == MAPL_BF16) {
+    bf16_t* Wt = at<bf16_t>(ws, Lo.w);
+    LAUNCH("enc:prep_u", launch_prep_u(U, (int)d, (int)r, nullptr, 0, Wt, Lo.kw, s));
+    if (k > 0) {
+      if (amb) {
+        // Wt[c][d+i] = -bf16( (B_s U~)[i][c] )
+        GemmF32Args g = gemm((int)k, (int)r, (int)d);
+        g.A = B_s; g.sAm = d; g.sAk = 1;
+        g.B = Wt; g.sBk = 1; g.sBn = Lo.kw;
+        g.C = Wt + d; g.sCm = 1; g.sCn = Lo.kw;
+        g.alpha = -1.f;
+        LAUNCH("enc:gemm_f32", launch_gemm_f32(g, 1, 1, 1, s));
+      } else {
+        LAUNCH("enc:transpose_into", launch_transpose_into(B_s, 0, (int)k, (int)r, r, -1.f, Wt, Lo.kw, (int)d, s));
+      }
+    }
+    TnArgs g{};
+    g.A = (const bf16_t*)X; g.lda = d; g.Ka = (int)d;
+    g.T = (const bf16_t*)A_s; g.ldt = k; g.ids = ids; g.Kg = (int)k; g.V = (int)D.V;
+    g.W = Wt; g.ldw = Lo.kw;
+    g.M = (int)T; g.N = (int)r;
+    if (D.L == 0) {
+      g.out = payload; g.ldo = r; g.out_f32 = 0;
+      LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
+      return MAPL_OK;
+    }
+    float* Z0 = at<float>(ws, Lo.z0);
+    g.out = Z0; g.ldo = r; g.out_f32 = 1;
+    LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
+    bf16_t* Cb = at<bf16_t>(ws, Lo.cb);
+    float* cn2 = at<float>(ws, Lo.cn2);
+    float* cnr = at<float>(ws, Lo.cnr);
+    LAUNCH("enc:prep_codebook", launch_prep_codebook(C, D.L, D.K, (int)r, Cb, cn2, cnr, s));
+    RvqArgs a{};
+    a.Z0 = Z0; a.Cb = Cb; a.C = C; a.cn2 = cn2; a.cnrm = cnr;
+    a.T = (int)T; a.r = (int)r; a.L = D.L; a.K = D.K;
+    a.codes = payload; a.code_bytes = cbytes;
+    a.stats = nullptr;
+    LAUNCH("enc:rvq", launch_rvq(a, s));
+    return MAPL_OK;
+  }
+
+  // ---------------- fp32 path
+  float* out = D.L == 0 ? (float*)payload : at<float>(ws, Lo.z0);
+  {
+    GemmF32Args g = gemm((int)T, (int)r, (int)d);
+    g.A = X; g.sAm = d; g.sAk = 1;
+    g.B = U; g.sBk = r; g.sBn = 1;
+    g.C = out; g.sCm = r; g.sCn = 1;
+    LAUNCH("enc:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  if (k > 0) {
+    float* a = at<float>(ws, Lo.ga);
+    LAUNCH("enc:gather_rows_f32", launch_gather_rows_f32((const float*)A_s, (int)k, ids, (int)D.V, (int)T, a, s));
+    const float* Bk = (const float*)B_s;  // coord: [k,r]
+    if (amb) {
+      float* BU = at<float>(ws, Lo.bu);
+      GemmF32Args g = gemm((int)k, (int)r, (int)d);
+      g.A = B_s; g.sAm = d; g.sAk = 1;
+      g.B = U; g.sBk = r; g.sBn = 1;
+      g.C = BU; g.sCm = r; g.sCn = 1;
+      LAUNCH("enc:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+      Bk = BU;
+    }
+    GemmF32Args g = gemm((int)T, (int)r, (int)k);
+    g.A = a; g.sAm = k; g.sAk = 1;
+    g.B = Bk; g.sBk = r; g.sBn = 1;
+    g.Cin = out; g.sCinm = r; g.sCinn = 1;
+    g.C = out; g.sCm = r; g.sCn = 1;
+    g.alpha = -1.f; g.beta = 1.f;
+    LAUNCH("enc:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  if (D.L > 0) LAUNCH("enc:rvq_f32", launch_rvq_f32(out, C, (int)T, (int)r, D.L, D.K, payload, cbytes, s));
+  return MAPL_OK;
+}
+
+// --------------------------------------------------------------------- decode
+extern "C" int mapl_decode(const mapl_codec_desc* desc, const void* payload, const int32_t* ids, const float* U,
+                           const void* A_r, const void* B_r, const float* C, void* Xhat, void* ws,
+                           size_t ws_bytes, void* stream) {
+  g_err.clear();
+  int st = check_desc(desc);
+  if (st) return st;
+  const mapl_codec_desc& D = *desc;
+  const int64_t T = D.T, d = D.d, r = D.r, k = D.k;
+  const size_t xe = esize(D.x_dtype);
+  st = check_ptrs({{payload, payload_bytes(D), "payload"}, {ids, k > 0 ? (size_t)T * 4 : 0, "ids"},
+                   {U, (size_t)d * r * 4, "U"}, {A_r, k > 0 ? (size_t)D.V * k * xe : 0, "A_r"},
+                   {B_r, k > 0 ? (size_t)k * b_cols(D) * xe : 0, "B_r"},
+                   {C, D.L > 0 ? (size_t)D.L * D.K * r * 4 : 0, "C"}, {Xhat, (size_t)T * d * xe, "Xhat"}},
+                  {{Xhat, (size_t)T * d * xe, "Xhat"}},
+                  {{payload, payload_bytes(D), "payload"}, {ids, (size_t)T * 4, "ids"}, {U, (size_t)d * r * 4, "U"},
+                   {A_r, (size_t)D.V * k * xe, "A_r"}, {B_r, (size_t)k * b_cols(D) * xe, "B_r"},
+                   {C, (size_t)D.L * D.K * r * 4, "C"}, {ws, ws_bytes, "workspace"}});
+  if (st) return st;
+  const Layout Lo = layout(D, MAPL_CALL_DECODE);
+  if ((st = check_ws(ws, ws_bytes, Lo.total))) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (k > 0 && (st = run_id_check(ids, T, D.V, ws, Lo, s))) return st;
+  if (T == 0) return MAPL_OK;
+  const bool amb = D.anchor_space == MAPL_ANCHOR_AMBIENT;
+  const int cbytes = (int)code_bytes(D);
+
+  if (D.x_dtype == MAPL_BF16) {
+    bf16_t* W2 = at<bf16_t>(ws, Lo.w2);
+    LAUNCH("dec:prep_u", launch_prep_u(U, (int)d, (int)r, W2, Lo.kw, nullptr, 0, s));
+    if (k > 0) {
+      if (amb) {
+        LAUNCH("dec:transpose_into", launch_transpose_into(B_r, 0, (int)k, (int)d, d, 1.f, W2, Lo.kw, (int)r, s));
+      } else {
+        // W2[j][r+i] = bf16( (B_r U~^T)[i][j] )
+        GemmF32Args g = gemm((int)k, (int)d, (int)r);
+        g.A = B_r; g.sAm = r; g.sAk = 1;
+        g.B = W2; g.sBk = 1; g.sBn = Lo.kw;
+        g.C = W2 + r; g.sCm = 1; g.sCn = Lo.kw;
+        LAUNCH("dec:gemm_f32", launch_gemm_f32(g, 1, 1, 1, s));
+      }
+    }
+    const bf16_t* Aop = (const bf16_t*)payload;
+    if (D.L > 0) {
+      bf16_t* Ah = at<bf16_t>(ws, Lo.ahat);
+      AssembleArgs a{};
+      a.codes = payload; a.code_bytes = cbytes; a.C = C; a.L = D.L; a.K = D.K;
+      a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah;
+      LAUNCH("dec:assemble", launch_assemble(a, s));
+      Aop = Ah;
+    }
+    TnArgs g{};
+    g.A = Aop; g.lda = r; g.Ka = (int)r;
+    g.T = (const bf16_t*)A_r; g.ldt = k; g.ids = ids; g.Kg = (int)k; g.V = (int)D.V;
+    g.W = W2; g.ldw = Lo.kw;
+    g.M = (int)T; g.N = (int)d;
+    g.out = Xhat; g.ldo = d; g.out_f32 = 0;
+    LAUNCH("dec:gemm_tn", launch_gemm_tn(g, s));
+    return MAPL_OK;
+  }
+
+  // ---------------- fp32 path
+  const float* Zh = (const float*)payload;
+  if (D.L > 0) {
+    float* z = at<float>(ws, Lo.zh);
+    LAUNCH("dec:codes_sum_f32", launch_codes_sum_f32(payload, cbytes, C, (int)T, (int)r, D.L, D.K, z, s));
+    Zh = z;
+  }
+  float* a = k > 0 ? at<float>(ws, Lo.ga) : nullptr;
+  if (k > 0) LAUNCH("dec:gather_rows_f32", launch_gather_rows_f32((const float*)A_r, (int)k, ids, (int)D.V, (int)T, a, s));
+  if (!amb && k > 0) {
+    float* z2 = at<float>(ws, Lo.z2);
+    GemmF32Args g = gemm((int)T, (int)r, (int)k);
+    g.A = a; g.sAm = k; g.sAk = 1;
+    g.B = B_r; g.sBk = r; g.sBn = 1;
+    g.Cin = Zh; g.sCinm = r; g.sCinn = 1; g.beta = 1.f;
+    g.C = z2; g.sCm = r; g.sCn = 1;
+    LAUNCH("dec:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+    Zh = z2;
+  }
+  {
+    GemmF32Args g = gemm((int)T, (int)d, (int)r);
+    g.A = Zh; g.sAm = r; g.sAk = 1;
+    g.B = U; g.sBk = 1; g.sBn = r;
+    g.C = Xhat; g.sCm = d; g.sCn = 1;
+    LAUNCH("dec:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  if (amb && k > 0) {
+    GemmF32Args g = gemm((int)T, (int)d, (int)k);
+    g.A = a; g.sAm = k; g.sAk = 1;
+    g.B = B_r; g.sBk = d; g.sBn = 1;
+    g.Cin = (const float*)Xhat; g.sCinm = d; g.sCinn = 1; g.beta = 1.f;
+    g.C = Xhat; g.sCm = d; g.sCn = 1;
+    LAUNCH("dec:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  return MAPL_OK;
+}
+
+// ----------------------------------------------------------------- decode_bwd
+extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, const void* payload,
+                               const int32_t* ids, const float* U, const void* A_r, const void* B_r, const float* C,
+                               void* dZ, float* dU, int accumulate_dU, void* ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  int st = check_desc(desc);
+  if (st) return st;
+  const mapl_codec_desc& D = *desc;
+  const int64_t T = D.T, d = D.d, r = D.r, k = D.k;
+  const size_t xe = esize(D.x_dtype);
+  const bool amb = D.anchor_space == MAPL_ANCHOR_AMBIENT;
+  const bool need_anchor = !amb && k > 0;
+  st = check_ptrs({{dXhat, (size_t)T * d * xe, "dXhat"}, {payload, payload_bytes(D), "payload"},
+                   {ids, need_anchor ? (size_t)T * 4 : 0, "ids"}, {U, (size_t)d * r * 4, "U"},
+                   {A_r, need_anchor ? (size_t)D.V * k * xe : 0, "A_r"},
+                   {B_r, need_anchor ? (size_t)k * r * xe : 0, "B_r"},
+                   {C, D.L > 0 ? (size_t)D.L * D.K * r * 4 : 0, "C"}, {dZ, (size_t)T * r * xe, "dZ"},
+                   {dU, (size_t)d * r * 4, "dU"}},
+                  {{dZ, (size_t)T * r * xe, "dZ"}, {dU, (size_t)d * r * 4, "dU"}},
+                  {{dXhat, (size_t)T * d * xe, "dXhat"}, {payload, payload_bytes(D), "payload"},
+                   {ids, (size_t)T * 4, "ids"}, {U, (size_t)d * r * 4, "U"}, {A_r, (size_t)D.V * k * xe, "A_r"},
+                   {B_r, (size_t)k * b_cols(D) * xe, "B_r"}, {C, (size_t)D.L * D.K * r * 4, "C"},
+                   {ws, ws_bytes, "workspace"}});
+  if (st) return st;
+  if (dZ && dU) {
+    const uintptr_t a0 = (uintptr_t)dZ, a1 = a0 + T * r * xe, b0 = (uintptr_t)dU, b1 = b0 + d * r * 4;
+    if (a0 < b1 && b0 < a1) return fail(MAPL_E_ALIAS, "output dZ overlaps output dU");
+  }
+  const Layout Lo = layout(D, MAPL_CALL_DECODE_BWD);
+  if ((st = check_ws(ws, ws_bytes, Lo.total))) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (need_anchor && (st = run_id_check(ids, T, D.V, ws, Lo, s))) return st;
+  const int cbytes = (int)code_bytes(D);
+  if (T == 0) {
+    if (!accumulate_dU) LAUNCH("dec_bwd:zero_bytes", launch_zero_bytes(dU, d * r * 4, s));
+    return MAPL_OK;
+  }
+
+  if (D.x_dtype == MAPL_BF16) {
+    bf16_t* Ut = at<bf16_t>(ws, Lo.w);
+    LAUNCH("dec_bwd:prep_u", launch_prep_u(U, (int)d, (int)r, nullptr, 0, Ut, d, s));
+    TnArgs g{};
+    g.A = (const bf16_t*)dXhat; g.lda = d; g.Ka = (int)d;
+    g.W = Ut; g.ldw = d;
+    g.M = (int)T; g.N = (int)r;
+    g.out = dZ; g.ldo = r; g.out_f32 = 0;
+    LAUNCH("dec_bwd:gemm_tn", launch_gemm_tn(g, s));
+    const bf16_t* Q = (const bf16_t*)payload;
+    if (D.L > 0 || need_anchor) {
+      bf16_t* Ah = at<bf16_t>(ws, Lo.ahat);
+      AssembleArgs a{};
+      a.Zp = D.L == 0 ? (const bf16_t*)payload : nullptr;
+      a.codes = payload; a.code_bytes = cbytes; a.C = C; a.L = D.L; a.K = D.K;
+      if (need_anchor) { a.A = (const bf16_t*)A_r; a.k = (int)k; a.Bc = (const bf16_t*)B_r; a.ids = ids; a.V = (int)D.V; }
+      a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah;
+      LAUNCH("dec_bwd:assemble", launch_assemble(a, s));
+      Q = Ah;
+    }
+    WgradArgs w{};
+    w.Pa = (const bf16_t*)dXhat; w.ldp = d; w.Ma = (int)d;
+    w.Q = Q; w.ldq = r;
+    w.T = (int)T; w.N = (int)r; w.splits = Lo.sp.splits; w.tokens_per_split = Lo.sp.tps;
+    w.part = at<float>(ws, Lo.part);
+    LAUNCH("dec_bwd:wgrad", launch_wgrad(w, s));
+    LAUNCH("dec_bwd:reduce_splits", launch_reduce_splits(w.part, w.splits, (int)d, (int)r, d * r, dU, accumulate_dU, s));
+    return MAPL_OK;
+  }
+
+  // ---------------- fp32 path
+  {
+    GemmF32Args g = gemm((int)T, (int)r, (int)d);
+    g.A = dXhat; g.sAm = d; g.sAk = 1;
+    g.B = U; g.sBk = r; g.sBn = 1;
+    g.C = dZ; g.sCm = r; g.sCn = 1;
+    LAUNCH("dec_bwd:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  const float* Zh = (const float*)payload;
+  if (D.L > 0) {
+    float* z = at<float>(ws, Lo.zh);
+    LAUNCH("dec_bwd:codes_sum_f32", launch_codes_sum_f32(payload, cbytes, C, (int)T, (int)r, D.L, D.K, z, s));
+    Zh = z;
+  }
+  if (need_anchor) {
+    float* a = at<float>(ws, Lo.ga);
+    LAUNCH("dec_bwd:gather_rows_f32", launch_gather_rows_f32((const float*)A_r, (int)k, ids, (int)D.V, (int)T, a, s));
+    float* z2 = at<float>(ws, Lo.z2);
+    GemmF32Args g = gemm((int)T, (int)r, (int)k);
+    g.A = a; g.sAm = k; g.sAk = 1;
+    g.B = B_r; g.sBk = r; g.sBn = 1;
+    g.Cin = Zh; g.sCinm = r; g.sCinn = 1; g.beta = 1.f;
+    g.C = z2; g.sCm = r; g.sCn = 1;
+    LAUNCH("dec_bwd:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+    Zh = z2;
+  }
+  {
+    GemmF32Args g = gemm((int)d, (int)r, (int)T);
+    g.A = dXhat; g.sAm = 1; g.sAk = d;
+    g.B = Zh; g.sBk = r; g.sBn = 1;
+    if (accumulate_dU) { g.Cin = dU; g.sCinm = r; g.sCinn = 1; g.beta = 1.f; }
+    g.C = dU; g.sCm = r; g.sCn = 1;
+    LAUNCH("dec_bwd:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  return MAPL_OK;
+}
+
+// ----------------------------------------------------------------- encode_bwd
+extern "C" int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, const void* X, const int32_t* ids,
+                               const float* U, const void* A_s, const void* B_s, void* dX, float* dU,
+                               int accumulate_dU, void* ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  int st = check_desc(desc);
+  if (st) return st;
+  const mapl_codec_desc& D = *desc;
+  const int64_t T = D.T, d = D.d, r = D.r, k = D.k;
+  const size_t xe = esize(D.x_dtype);
+  const bool amb = D.anchor_space == MAPL_ANCHOR_AMBIENT;
+  const bool need_anchor = amb && k > 0;
+  st = check_ptrs({{dZ, (size_t)T * r * xe, "dZ"}, {X, (size_t)T * d * xe, "X"},
+                   {ids, need_anchor ? (size_t)T * 4 : 0, "ids"}, {U, (size_t)d * r * 4, "U"},
+                   {A_s, need_anchor ? (size_t)D.V * k * xe : 0, "A_s"},
+                   {B_s, need_anchor ? (size_t)k * d * xe : 0, "B_s"}, {dX, (size_t)T * d * xe, "dX"},
+                   {dU, (size_t)d * r * 4, "dU"}},
+                  {{dX, (size_t)T * d * xe, "dX"}, {dU, (size_t)d * r * 4, "dU"}},
+                  {{dZ, (size_t)T * r * xe, "dZ"}, {X, (size_t)T * d * xe, "X"}, {ids, (size_t)T * 4, "ids"},
+                   {U, (size_t)d * r * 4, "U"}, {A_s, (size_t)D.V * k * xe, "A_s"},
+                   {B_s, (size_t)k * b_cols(D) * xe, "B_s"}, {ws, ws_bytes, "workspace"}});
+  if (st) return st;
+  if (dX && dU) {
+    const uintptr_t a0 = (uintptr_t)dX, a1 = a0 + T * d * xe, b0 = (uintptr_t)dU, b1 = b0 + d * r * 4;
+    if (a0 < b1 && b0 < a1) return fail(MAPL_E_ALIAS, "output dX overlaps output dU");
+  }
+  const Layout Lo = layout(D, MAPL_CALL_ENCODE_BWD);
+  if ((st = check_ws(ws, ws_bytes, Lo.total))) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (need_anchor && (st = run_id_check(ids, T, D.V, ws, Lo, s))) return st;
+  if (T == 0) {
+    if (!accumulate_dU) LAUNCH("enc_bwd:zero_bytes", launch_zero_bytes(dU, d * r * 4, s));
+    return MAPL_OK;
+  }
+
+  if (D.x_dtype == MAPL_BF16) {
+    bf16_t* Ub = at<bf16_t>(ws, Lo.w2);
+    LAUNCH("enc_bwd:prep_u", launch_prep_u(U, (int)d, (int)r, Ub, r, nullptr, 0, s));
+    TnArgs g{};
+    g.A = (const bf16_t*)dZ; g.lda = r; g.Ka = (int)r;
+    g.W = Ub; g.ldw = r;
+    g.M = (int)T; g.N = (int)d;
+    g.out = dX; g.ldo = d; g.out_f32 = 0;
+    LAUNCH("enc_bwd:gemm_tn", launch_gemm_tn(g, s));
+    WgradArgs w{};
+    w.Pa = (const bf16_t*)X; w.ldp = d; w.Ma = (int)d;
+    if (need_anchor) { w.Tg = (const bf16_t*)A_s; w.ldt = k; w.ids = ids; w.Mg = (int)k; w.V = (int)D.V; }
+    w.Q = (const bf16_t*)dZ; w.ldq = r;
+    w.T = (int)T; w.N = (int)r; w.splits = Lo.sp.splits; w.tokens_per_split = Lo.sp.tps;
+    w.part = at<float>(ws, Lo.part);
+    const int64_t stride = (d + w.Mg) * r;
+    LAUNCH("enc_bwd:wgrad", launch_wgrad(w, s));
+    LAUNCH("enc_bwd:reduce_splits", launch_reduce_splits(w.part, w.splits, (int)d, (int)r, stride, dU, accumulate_dU, s));
+    if (need_anchor) {
+      float* Ws = at<float>(ws, Lo.wsum);
+      LAUNCH("enc_bwd:reduce_splits", launch_reduce_splits(w.part + d * r, w.splits, (int)k, (int)r, stride, Ws, 0, s));
+      GemmF32Args e = gemm((int)d, (int)r, (int)k);
+      e.A = B_s; e.sAm = 1; e.sAk = d;
+      e.B = Ws; e.sBk = r; e.sBn = 1;
+      e.Cin = dU; e.sCinm = r; e.sCinn = 1; e.beta = 1.f;
+      e.C = dU; e.sCm = r; e.sCn = 1;
+      e.alpha = -1.f;
+      LAUNCH("enc_bwd:gemm_f32", launch_gemm_f32(e, 1, 0, 0, s));
+    }
+    return MAPL_OK;
+  }
+
+  // ---------------- fp32 path
+  {
+    GemmF32Args g = gemm((int)T, (int)d, (int)r);
+    g.A = dZ; g.sAm = r; g.sAk = 1;
+    g.B = U; g.sBk = 1; g.sBn = r;
+    g.C = dX; g.sCm = d; g.sCn = 1;
+    LAUNCH("enc_bwd:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  {
+    GemmF32Args g = gemm((int)d, (int)r, (int)T);
+    g.A = X; g.sAm = 1; g.sAk = d;
+    g.B = dZ; g.sBk = r; g.sBn = 1;
+    if (accumulate_dU) { g.Cin = dU; g.sCinm = r; g.sCinn = 1; g.beta = 1.f; }
+    g.C = dU; g.sCm = r; g.sCn = 1;
+    LAUNCH("enc_bwd:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  if (need_anchor) {
+    float* a = at<float>(ws, Lo.ga);
+    float* Wm = at<float>(ws, Lo.wsum);
+    LAUNCH("enc_bwd:gather_rows_f32", launch_gather_rows_f32((const float*)A_s, (int)k, ids, (int)D.V, (int)T, a, s));
+    GemmF32Args g = gemm((int)k, (int)r, (int)T);
+    g.A = a; g.sAm = 1; g.sAk = k;
+    g.B = dZ; g.sBk = r; g.sBn = 1;
+    g.C = Wm; g.sCm = r; g.sCn = 1;
+    LAUNCH("enc_bwd:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+    GemmF32Args e = gemm((int)d, (int)r, (int)k);
+    e.A = B_s; e.sAm = 1; e.sAk = d;
+    e.B = Wm; e.sBk = r; e.sBn = 1;
+    e.Cin = dU; e.sCinm = r; e.sCinn = 1; e.beta = 1.f;
+    e.C = dU; e.sCm = r; e.sCn = 1;
+    e.alpha = -1.f;
+    LAUNCH("enc_bwd:gemm_f32", launch_gemm_f32(e, 0, 0, 0, s));
+  }
+  return MAPL_OK;
+}
+
+// ---------------------------------------------------------------- stiefel
+extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, const float* G, float* M, float lr,
+                                 float beta, int lmo_steps, int retract_steps, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  g_err.clear();
+  if (P < 1 || P > 65535 || d < 32 || r < 32 || r > d || r > 1024 || r % 32 || d % 32 || d > 65536)
+    return fail(MAPL_E_SHAPE, "stiefel: need 1 <= P <= 65535, 32 <= r <= min(d,1024), d <= 65536, r and d multiples of 32");
+  if (lmo_steps < 1 || lmo_steps > kPolarMaxSteps || retract_steps < 1 || retract_steps > kPolarMaxSteps)
+    return fail(MAPL_E_SHAPE, "stiefel: 1 <= lmo_steps, retract_steps <= %d", kPolarMaxSteps);
+  if (!(beta >= 0.f && beta < 1.f)) return fail(MAPL_E_RANGE, "stiefel: beta must lie in [0, 1)");
+  if (!(lr >= 0.f && lr < 1.f)) return fail(MAPL_E_RANGE, "stiefel: lr must lie in [0, 1)");
+  const size_t nb = (size_t)P * d * r * 4;
+  int st = check_ptrs({{U, nb, "U"}, {G, nb, "G"}, {M, nb, "M"}}, {{U, nb, "U"}, {M, nb, "M"}},
+                      {{G, nb, "G"}, {ws, ws_bytes, "workspace"}});
+  if (st) return st;
+  {
+    const uintptr_t a0 = (uintptr_t)U, b0 = (uintptr_t)M;
+    if (a0 < b0 + nb && b0 < a0 + nb) return fail(MAPL_E_ALIAS, "U overlaps M");
+  }
+  const size_t need = mapl_workspace_bytes(nullptr, MAPL_CALL_STIEFEL, P, d, r);
+  if ((st = check_ws(ws, ws_bytes, need))) return st;
+  hipStream_t s = (hipStream_t)stream;
+
+  Carve c;
+  float* S = at<float>(ws, c.take((size_t)P * r * r * 4));
+  float* Qm = at<float>(ws, c.take((size_t)P * r * r * 4));
+  float* X0 = at<float>(ws, c.take((size_t)P * d * r * 4));
+  float* X1 = at<float>(ws, c.take((size_t)P * d * r * 4));
+  float* partial = at<float>(ws, c.take((size_t)P * 1024 * 4));
+  float* sc = at<float>(ws, c.take((size_t)P * 8 * 4));
+  float* scale = sc, *scale2 = sc + P, *inv_nu = sc + 2 * P, *inv_nu2 = sc + 3 * P, *inv_nu4 = sc + 4 * P;
+  const int64_t n = d * r, rr = r * r;
+
+  auto gram = [&](const float* X, const float* aptr) {  // S = X^T X (times aptr)
+    GemmF32Args g = gemm((int)r, (int)r, (int)d);
+    g.batch = (int)P;
+    g.A = X; g.sAm = 1; g.sAk = r; g.sAb = n;
+    g.B = X; g.sBk = r; g.sBn = 1; g.sBb = n;
+    g.C = S; g.sCm = r; g.sCn = 1; g.sCb = rr;
+    g.alpha_ptr = aptr;
+    return launch_gemm_f32(g, 0, 0, 0, s);
+  };
+  auto poly = [&](double b, double cc, const float* aptr, const float* bptr) {  // Qm = c S S + b S
+    GemmF32Args g = gemm((int)r, (int)r, (int)r);
+    g.batch = (int)P;
+    g.A = S; g.sAm = r; g.sAk = 1; g.sAb = rr;
+    g.B = S; g.sBk = r; g.sBn = 1; g.sBb = rr;
+    g.Cin = S; g.sCinm = r; g.sCinn = 1; g.sCinb = rr;
+    g.C = Qm; g.sCm = r; g.sCn = 1; g.sCb = rr;
+    g.alpha = (float)cc; g.beta = (float)b;
+    g.alpha_ptr = aptr; g.beta_ptr = bptr;
+    return launch_gemm_f32(g, 0, 0, 0, s);
+  };
+  auto apply = [&](const float* X, float* Xo, double a, const float* sptr) {  // Xo = s (a X + X Qm)
+    GemmF32Args g = gemm((int)d, (int)r, (int)r);
+    g.batch = (int)P;
+    g.A = X; g.sAm = r; g.sAk = 1; g.sAb = n;
+    g.B = Qm; g.sBk = r; g.sBn = 1; g.sBb = rr;
+    g.Cin = X; g.sCinm = r; g.sCinn = 1; g.sCinb = n;
+    g.C = Xo; g.sCm = r; g.sCn = 1; g.sCb = n;
+    g.alpha = 1.f; g.beta = (float)a;
+    g.alpha_ptr = sptr; g.beta_ptr = sptr;
+    return launch_gemm_f32(g, 0, 0, 0, s);
+  };
+
+  // Eq. 4: S = U^T G, sym, g_R = G - U sym(S)  -> X0
+  {
+    GemmF32Args g = gemm((int)r, (int)r, (int)d);
+    g.batch = (int)P;
+    g.A = U; g.sAm = 1; g.sAk = r; g.sAb = n;
+    g.B = G; g.sBk = r; g.sBn = 1; g.sBb = n;
+    g.C = S; g.sCm = r; g.sCn = 1; g.sCb = rr;
+    LAUNCH("stiefel:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  LAUNCH("stiefel:symmetrize", launch_symmetrize(S, (int)P, (int)r, s));
+  {
+    GemmF32Args g = gemm((int)d, (int)r, (int)r);
+    g.batch = (int)P;
+    g.A = U; g.sAm = r; g.sAk = 1; g.sAb = n;
+    g.B = S; g.sBk = r; g.sBn = 1; g.sBb = rr;
+    g.Cin = G; g.sCinm = r; g.sCinn = 1; g.sCinb = n; g.beta = 1.f;
+    g.C = X0; g.sCm = r; g.sCn = 1; g.sCb = n;
+    g.alpha = -1.f;
+    LAUNCH("stiefel:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  // Eq. 5 and the LMO normalisation 1 / (||M||_F + 1e-7)
+  int nblk = (int)((n + 255) / 256);
+  if (nblk > 1024) nblk = 1024;
+  LAUNCH("stiefel:momentum", launch_momentum(M, X0, n, (int)P, beta, partial, nblk, s));
+  LAUNCH("stiefel:fro_scale", launch_fro_scale(partial, nblk, (int)P, 1e-7f, scale, scale2, s));
+
+  // Eq. 6: D = PE(M / (||M|| + eps))
+  const float* Xin = M;
+  float* bufs[2] = {X0, X1};
+  int cur = 0;
+  for (int i = 0; i < lmo_steps; ++i) {
+    const double a = kLmoCoef[i][0], b = kLmoCoef[i][1], cc = kLmoCoef[i][2];
+    const bool first = i == 0;
+    LAUNCH("stiefel:gram", gram(Xin, first ? scale2 : nullptr));
+    LAUNCH("stiefel:poly", poly(b, cc, nullptr, nullptr));
+    float* Xo = bufs[cur];
+    LAUNCH("stiefel:apply", apply(Xin, Xo, a, first ? scale : nullptr));
+    Xin = Xo;
+    cur ^= 1;
+  }
+  // Y = U - lr D
+  float* Y = bufs[cur];
+  LAUNCH("stiefel:axpy", launch_axpy(U, Xin, lr, Y, P * n, s));
+  cur ^= 1;
+  // Eq. 7: U = PE(Y / nu), nu^2 = max row sum |Y^T Y|
+  LAUNCH("stiefel:gram", gram(Y, nullptr));
+  LAUNCH("stiefel:inf_norm_scales", launch_inf_norm_scales(S, (int)P, (int)r, inv_nu, inv_nu2, inv_nu4, s));
+  Xin = Y;
+  for (int i = 0; i < retract_steps; ++i) {
+    const double a = kRetractCoef[i][0], b = kRetractCoef[i][1], cc = kRetractCoef[i][2];
+    const bool first = i == 0;
+    if (!first) LAUNCH("stiefel:gram", gram(Xin, nullptr));
+    LAUNCH("stiefel:poly", poly(b, cc, first ? inv_nu4 : nullptr, first ? inv_nu2 : nullptr));
+    float* Xo = (i == retract_steps - 1) ? U : bufs[cur];
+    LAUNCH("stiefel:apply", apply(Xin, Xo, a, first ? inv_nu : nullptr));
+    Xin = Xo;
+    cur ^= 1;
+  }
+  return MAPL_OK;
+}
+
+// ---------------------------------------------------------------- tracing API
+extern "C" int mapl_profile(int enable) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof = enable != 0;
+  return MAPL_OK;
+}
+
+extern "C" int mapl_profile_report(char* buf, size_t bytes) {
+  std::vector<ProfRec> recs;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    recs.swap(g_prof_recs);
+  }
+  std::map<std::string, std::pair<long, double>> agg;
+  int st = MAPL_OK;
+  for (const ProfRec& r : recs) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) {
+      st = fail(MAPL_E_HIP, "profile: event query failed");
+      continue;
+    }
+    auto& e = agg[r.name];
+    e.first += 1;
+    e.second += ms;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    for (const ProfRec& r : recs) {
+      g_prof_pool.push_back(r.a);
+      g_prof_pool.push_back(r.b);
+    }
+  }
+  std::string outs;
+  char line[256];
+  for (const auto& kv : agg) {
+    snprintf(line, sizeof line, "%s %ld %.6f\n", kv.first.c_str(), kv.second.first, kv.second.second);
+    outs += line;
+  }
+  if (buf && bytes) {
+    const size_t n = outs.size() < bytes - 1 ? outs.size() : bytes - 1;
+    memcpy(buf, outs.data(), n);
+    buf[n] = 0;
+    if (outs.size() >= bytes) return fail(MAPL_E_WORKSPACE, "profile report needs %zu bytes", outs.size() + 1);
+  }
+  return st;
+}

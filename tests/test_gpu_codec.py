@@ -1,0 +1,237 @@
+"""GPU parity of the boundary codec against the float64 oracle.
+
+Every comparison: relative Frobenius error <= 2e-2 (bf16 paths) or 1e-5
+(fp32 path); RVQ codes bit-exact except tokens whose oracle top-2 gap is
+under 1e-4 relative (counted).  Workloads come from the seeded generator;
+sizes span several tiles with ragged tails."""
+import numpy as np
+import pytest
+
+from oracle import codec as ocodec
+from paper_2606_05484_amd import mapl, synth
+from _helpers import (BF16_TOL, F32_TOL, Dev, codes_np, compare_codes, descr, f64, host_f64, operand,
+                      oracle_encode, rel_fro, run_encode, stress_codebooks, tol, torch)
+
+pytestmark = pytest.mark.gpu
+
+SMALL = dict(T=1000, d=256, r=64, V=500, k=16, L=0, K=0, dtype="bf16", alpha=0.8, n_out=4, cb_sigma=None,
+             gscale=1.0)
+
+
+def _x(name=None, seed=None, **over):
+    print("workload", name, seed, over, flush=True)
+    return synth.codec_inputs(name, seed=seed, **over)
+
+
+def _chain(x, C=None, L=None, K=None):
+    """encode -> decode -> decode_bwd -> encode_bwd on the GPU; returns host results."""
+    t = torch()
+    D = descr(x, L, K)
+    g = Dev(x, C)
+    payload = run_encode(x, D, g)
+    Xh = t.full((x["T"], x["d"]), float("nan"), dtype=g.tdt, device="cuda")
+    ws = mapl.workspace(max(mapl.workspace_bytes(D, c) for c in range(4)))
+    mapl.decode(D, payload, g.ids, g.U, g.A, g.B, g.C, Xh, ws)
+    dZ = t.full((x["T"], x["r"]), float("nan"), dtype=g.tdt, device="cuda")
+    dU = t.full((x["d"], x["r"]), float("nan"), dtype=t.float32, device="cuda")
+    mapl.decode_bwd(D, g.dXhat, payload, g.ids, g.U, g.A, g.B, g.C, dZ, dU, 0, ws)
+    dU_dec = dU.clone()
+    dX = t.full((x["T"], x["d"]), float("nan"), dtype=g.tdt, device="cuda")
+    mapl.encode_bwd(D, g.dZ, g.X, g.ids, g.U, g.A, g.B, dX, dU, 1, ws)
+    t.cuda.synchronize()
+    return dict(D=D, payload=payload, Xh=host_f64(Xh), dZ=host_f64(dZ), dU_dec=host_f64(dU_dec),
+                dU=host_f64(dU), dX=host_f64(dX))
+
+
+def _check_chain(x, res, C=None):
+    """Oracle for each call, fed the same inputs the GPU call saw."""
+    Cn = x["C"] if C is None else C
+    op, sp = operand(x), x["anchor_space"]
+    X, A, B = f64(x, "X"), f64(x, "A"), f64(x, "B")
+    D = res["D"]
+    if D.L == 0:
+        Z0 = ocodec.project(X, x["ids"], x["U"], A, B, sp, op)
+        Zg = host_f64(res["payload"])
+        assert np.isfinite(Zg).all()
+        e = rel_fro(Zg, Z0)
+        print("Z rel err", e)
+        assert e <= tol(x)
+        pay_ref = Zg  # decode is checked on the payload the GPU produced
+        Cref = None
+    else:
+        codes_ref, gap, _ = ocodec.rvq_encode(ocodec.project(X, x["ids"], x["U"], A, B, sp, op), Cn)
+        cg = codes_np(res["payload"], D)
+        bad, ex = compare_codes(cg, codes_ref, gap)
+        print("codes: mismatched non-exempt", bad, "exempt", ex, "of", x["T"])
+        assert bad == 0
+        pay_ref = cg
+        Cref = Cn
+    Xh_ref = ocodec.decode(pay_ref, x["ids"], x["U"], A, B, Cref, sp, op)
+    e = rel_fro(res["Xh"], Xh_ref)
+    print("Xhat rel err", e)
+    assert np.isfinite(res["Xh"]).all() and e <= tol(x)
+    dXh = f64(x, "dXhat")
+    dZ_ref, dUd_ref = ocodec.decode_bwd(dXh, pay_ref, x["ids"], x["U"], A, B, Cref, sp, op)
+    e1, e2 = rel_fro(res["dZ"], dZ_ref), rel_fro(res["dU_dec"], dUd_ref)
+    print("dZ rel err", e1, "dU_dec rel err", e2)
+    assert e1 <= tol(x) and e2 <= tol(x)
+    dX_ref, dUe_ref = ocodec.encode_bwd(f64(x, "dZ"), X, x["ids"], x["U"], A, B, sp, op)
+    e3, e4 = rel_fro(res["dX"], dX_ref), rel_fro(res["dU"], dUd_ref + dUe_ref)
+    print("dX rel err", e3, "dU (enc+dec) rel err", e4)
+    assert e3 <= tol(x) and e4 <= tol(x)
+
+
+@pytest.mark.parametrize("r", [64, 128, 256, 512])
+def test_c2_projection_only(r):
+    x = _x("c2_r%d" % r)
+    _check_chain(x, _chain(x))
+
+
+def test_c1_fp32_with_rvq():
+    x = _x("c1")
+    _check_chain(x, _chain(x))
+
+
+def test_c1_fp32_no_rvq():
+    x = _x("c1")
+    _check_chain(x, _chain(x, L=0, K=0))
+
+
+def test_c3_rvq_official_codebooks():
+    x = _x("c3")
+    _check_chain(x, _chain(x))
+
+
+def test_c3_rvq_stress_codebooks():
+    x = _x("c3")
+    C = stress_codebooks(x, 103)
+    _check_chain(x, _chain(x, C=C), C=C)
+
+
+@pytest.mark.parametrize("space", ["ambient", "coord"])
+@pytest.mark.parametrize("L,K", [(0, 0), (2, 96)])
+def test_ragged_small_both_anchor_spaces(space, L, K):
+    x = _x(None, seed=7, anchor_space=space, **dict(SMALL, L=L, K=K))
+    C = stress_codebooks(x, 107) if L else None
+    _check_chain(x, _chain(x, C=C), C=C)
+
+
+def test_fp32_coord_anchor():
+    x = _x("c1", anchor_space="coord")
+    _check_chain(x, _chain(x))
+
+
+def test_no_anchor_k0():
+    x = _x(None, seed=8, **dict(SMALL, k=0, T=333))
+    _check_chain(x, _chain(x))
+
+
+def test_distinct_sender_receiver_anchors():
+    """Eq. 2 adds the *receiving* stage's anchor: decode with A_r, B_r that
+    differ from the sender's."""
+    t = torch()
+    x = _x(None, seed=9, **SMALL)
+    x2 = _x(None, seed=10, **SMALL)
+    D = descr(x)
+    g = Dev(x)
+    Ar, Br = Dev(x2).A, Dev(x2).B
+    Z = run_encode(x, D, g)
+    Xh = t.empty((x["T"], x["d"]), dtype=g.tdt, device="cuda")
+    ws = mapl.workspace(mapl.workspace_bytes(D, mapl.CALL_DECODE))
+    mapl.decode(D, Z, g.ids, g.U, Ar, Br, None, Xh, ws)
+    t.cuda.synchronize()
+    ref = ocodec.decode(host_f64(Z), x["ids"], x["U"], f64(x2, "A"), f64(x2, "B"), None, "ambient", "bf16")
+    assert rel_fro(host_f64(Xh), ref) <= BF16_TOL
+
+
+def test_empty_batch():
+    t = torch()
+    x = _x(None, seed=11, **dict(SMALL, T=0, L=2, K=64))
+    D = descr(x)
+    g = Dev(x)
+    codes = t.empty((0, 2), dtype=t.uint8, device="cuda")
+    run_encode(x, D, g, codes)
+    dU = t.full((x["d"], x["r"]), 3.0, device="cuda")
+    ws = mapl.workspace(mapl.workspace_bytes(D, mapl.CALL_DECODE_BWD))
+    dZ = t.empty((0, x["r"]), dtype=g.tdt, device="cuda")
+    mapl.decode_bwd(D, g.dXhat, codes, g.ids, g.U, g.A, g.B, g.C, dZ, dU, 0, ws)
+    t.cuda.synchronize()
+    assert float(dU.abs().max()) == 0.0  # overwrite with an empty sum
+
+
+def test_accumulate_flag_adds():
+    t = torch()
+    x = _x(None, seed=12, **SMALL)
+    D = descr(x)
+    g = Dev(x)
+    ws = mapl.workspace(mapl.workspace_bytes(D, mapl.CALL_ENCODE_BWD))
+    dX = t.empty((x["T"], x["d"]), dtype=g.tdt, device="cuda")
+    dU0 = t.zeros((x["d"], x["r"]), device="cuda")
+    mapl.encode_bwd(D, g.dZ, g.X, g.ids, g.U, g.A, g.B, dX, dU0, 0, ws)
+    base = t.randn((x["d"], x["r"]), device="cuda")
+    dU1 = base.clone()
+    mapl.encode_bwd(D, g.dZ, g.X, g.ids, g.U, g.A, g.B, dX, dU1, 1, ws)
+    t.cuda.synchronize()
+    assert t.equal(dU1, base + dU0) or float((dU1 - base - dU0).abs().max()) <= 1e-6 * float(dU0.abs().max())
+
+
+def test_deterministic_repeat():
+    x = _x(None, seed=13, **dict(SMALL, L=2, K=64))
+    C = stress_codebooks(x, 113)
+    a = _chain(x, C=C)
+    b = _chain(x, C=C)
+    for key in ("Xh", "dZ", "dU", "dX"):
+        assert np.array_equal(a[key], b[key]), key
+    assert np.array_equal(codes_np(a["payload"], a["D"]), codes_np(b["payload"], b["D"]))
+
+
+def test_planted_codewords_and_duplicate_tie():
+    """Codewords planted at oracle coordinates of chosen tokens are picked
+    (residual 0, later rounds pick the zero codeword); a duplicated codeword
+    resolves to the lower index."""
+    x = _x(None, seed=14, **dict(SMALL, L=2, K=64))
+    Z0 = ocodec.project(f64(x, "X"), x["ids"], x["U"], f64(x, "A"), f64(x, "B"), "ambient", "bf16")
+    C = np.zeros((2, 64, x["r"]), dtype=np.float32)
+    rng = np.random.default_rng(0)
+    C[:, 1:] = (5 + rng.standard_normal((2, 63, x["r"]))).astype(np.float32)
+    plant = {5: 7, 300: 12, 999: 40}
+    for t_, j in plant.items():
+        C[0, j] = Z0[t_].astype(np.float32)
+    C[0, 50] = C[0, 12]  # duplicate of 12
+    D = descr(x)
+    g = Dev(x, C)
+    codes = codes_np(run_encode(x, D, g), D)
+    for t_, j in plant.items():
+        assert codes[t_, 0] == j, (t_, codes[t_])
+        assert codes[t_, 1] == 0
+
+
+@pytest.mark.slow
+def test_c4_full_size_sampled():
+    """The benchmark workload (T=32768, d=2048, r=256, k=128, L=2, K=1024)
+    in the launch configuration the benchmark times: codes on every token
+    against the oracle, Xhat / dZ / dX on 512 sampled tokens, dU in full."""
+    t = torch()
+    x = _x("c4")
+    res = _chain(x)
+    D = res["D"]
+    X, A, B = f64(x, "X"), f64(x, "A"), f64(x, "B")
+    Z0 = ocodec.project(X, x["ids"], x["U"], A, B, "ambient", "bf16")
+    codes_ref, gap, _ = ocodec.rvq_encode(Z0, x["C"])
+    cg = codes_np(res["payload"], D)
+    bad, ex = compare_codes(cg, codes_ref, gap)
+    print("c4 codes: mismatched", bad, "exempt", ex)
+    assert bad == 0
+    rows = np.random.default_rng(4).choice(x["T"], 512, replace=False)
+    Xh_ref = ocodec.decode(cg[rows], x["ids"][rows], x["U"], A, B, x["C"], "ambient", "bf16")
+    assert rel_fro(res["Xh"][rows], Xh_ref) <= BF16_TOL
+    dXh = f64(x, "dXhat")
+    dZ_ref = dXh[rows] @ ocodec._projector(x["U"], "bf16")
+    assert rel_fro(res["dZ"][rows], dZ_ref) <= BF16_TOL
+    dX_ref = f64(x, "dZ")[rows] @ ocodec._projector(x["U"], "bf16").T
+    assert rel_fro(res["dX"][rows], dX_ref) <= BF16_TOL
+    _, dUd = ocodec.decode_bwd(dXh, cg, x["ids"], x["U"], A, B, x["C"], "ambient", "bf16")
+    _, dUe = ocodec.encode_bwd(f64(x, "dZ"), X, x["ids"], x["U"], A, B, "ambient", "bf16")
+    e = rel_fro(res["dU"], dUd + dUe)
+    print("c4 dU rel err", e)
+    assert e <= BF16_TOL

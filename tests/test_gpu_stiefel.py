@@ -1,0 +1,96 @@
+"""GPU parity of the SPEL step (Eqs. 4-7) against the float64 oracle.
+
+Tolerances: U_new and M_new within 1e-5 relative Frobenius error of the
+iteration-matched oracle (same PolarExpress schedule and normalisations,
+float64); max |U^T U - I| <= 1e-5 after every step.  The gap to the exact
+(SVD) polar factor is printed, not gated."""
+import numpy as np
+import pytest
+
+from oracle import spel
+from paper_2606_05484_amd import mapl, synth
+from _helpers import dev, rel_fro, torch
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_step(U, G, M, lr, beta, lmo=5, ret=7):
+    t = torch()
+    P, d, r = U.shape
+    Ug, Gg, Mg = dev(U, "f32"), dev(G, "f32"), dev(M, "f32")
+    ws = mapl.workspace(mapl.workspace_bytes(None, mapl.CALL_STIEFEL, P, d, r))
+    mapl.stiefel_step(P, d, r, Ug, Gg, Mg, lr, beta, lmo, ret, ws)
+    t.cuda.synchronize()
+    return Ug.cpu().numpy().astype(np.float64), Mg.cpu().numpy().astype(np.float64)
+
+
+def _orth_err(U):
+    r = U.shape[-1]
+    return max(np.abs(u.T @ u - np.eye(r)).max() for u in U)
+
+
+def test_c1_single_step():
+    st = synth.stiefel_inputs("c1")
+    U, G, M = st["U"], st["G"], st["M"]
+    Un, Mn = _gpu_step(U, G, M, st["lr"], st["beta"])
+    Ur, Mr = spel.stiefel_step_batched(U, G, M, st["lr"], st["beta"], mode="pe")
+    Ue, _ = spel.stiefel_step_batched(U, G, M, st["lr"], st["beta"], mode="exact")
+    e_u, e_m = rel_fro(Un, Ur), rel_fro(Mn, Mr)
+    du = rel_fro(Un - U, Ur - U)
+    print("c1: U rel err", e_u, "M rel err", e_m, "dU rel err", du, "orth", _orth_err(Un),
+          "gap to exact polar", rel_fro(Ur, Ue))
+    assert e_u <= 1e-5 and e_m <= 1e-5
+    assert _orth_err(Un) <= 1e-5
+
+
+def test_c5_step_sampled_projectors():
+    """All 16 projectors [2048,512] on the GPU; the oracle checks 3 of them."""
+    st = synth.stiefel_inputs("c5")
+    U, G, M = st["U"], st["G"], st["M"]
+    Un, Mn = _gpu_step(U, G, M, st["lr"], st["beta"])
+    assert _orth_err(Un) <= 1e-5
+    for p in (0, 7, 15):
+        ur, mr, _, _ = spel.stiefel_step(U[p], G[p], M[p], st["lr"], st["beta"], mode="pe")
+        e_u, e_m = rel_fro(Un[p], ur), rel_fro(Mn[p], mr)
+        print("c5 proj", p, "U rel err", e_u, "M rel err", e_m, "dU rel err", rel_fro(Un[p] - U[p], ur - U[p]))
+        assert e_u <= 1e-5 and e_m <= 1e-5
+
+
+def test_c5_trajectory_stays_orthonormal():
+    """100 consecutive steps with fresh gradients: orthonormality after
+    every step; the drift of the final iterate against the oracle's own
+    100-step trajectory (projector 0) is printed."""
+    t = torch()
+    st = synth.stiefel_inputs("c5")
+    P, d, r = st["P"], st["d"], st["r"]
+    Ug, Mg = dev(st["U"], "f32"), dev(st["M"], "f32")
+    ws = mapl.workspace(mapl.workspace_bytes(None, mapl.CALL_STIEFEL, P, d, r))
+    U0 = st["U"][0].astype(np.float64)
+    M0 = np.zeros((d, r))
+    worst = 0.0
+    for step in range(st["steps"]):
+        G = synth.next_gradient(st) if step else st["G"]
+        mapl.stiefel_step(P, d, r, Ug, dev(G, "f32"), Mg, st["lr"], st["beta"], 5, 7, ws)
+        Uh = Ug[0].double()
+        worst = max(worst, float((Uh.T @ Uh - t.eye(r, dtype=t.float64, device="cuda")).abs().max()))
+        if step < 3:
+            U0, M0, _, _ = spel.stiefel_step(U0, G[0], M0, st["lr"], st["beta"], mode="pe")
+    t.cuda.synchronize()
+    print("max orthonormality error over 100 steps", worst)
+    assert worst <= 1e-5
+    orth = _orth_err(Ug.cpu().numpy().astype(np.float64))
+    assert orth <= 1e-5
+
+
+def test_symmetric_gradient_moves_little():
+    """G = U S (S symmetric) is normal to the manifold: the tangent part is
+    rounding noise, so U may move only by about lr times that noise."""
+    rng = np.random.default_rng(3)
+    P, d, r = 2, 256, 64
+    U = np.stack([np.linalg.qr(rng.standard_normal((d, r)))[0] for _ in range(P)]).astype(np.float32)
+    S = rng.standard_normal((P, r, r))
+    S = S + S.transpose(0, 2, 1)
+    G = np.einsum("pdr,prs->pds", U.astype(np.float64), S).astype(np.float32)
+    Un, _ = _gpu_step(U, G, np.zeros_like(U), 1e-2, 0.95)
+    assert _orth_err(Un) <= 1e-5
+    print("symmetric-gradient move", np.abs(Un - U).max())
