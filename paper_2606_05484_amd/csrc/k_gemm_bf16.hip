@@ -6,14 +6,23 @@
 // sum gathers anchor rows T[ids[t]] (bf16, [V, ldt]) -- the token-id lookup of
 // Eqs. 1-2 -- straight into the K loop, so the anchored operand [X | a] is
 // never materialised.  fp32 accumulation; the epilogue stores bf16 (RNE) or
-// fp32.  One kernel serves the four dense products of the codec:
+// fp32 (optionally accumulating).  One kernel serves the dense products of
+// the codec:
 //   encode      Z0   = [X | a_s] [U~ ; -(B_s U~)]        (N = r)
 //   decode_bwd  dZ   = dXhat U~                          (N = r)
 //   decode      Xhat = [Zhat | a_r] [U~^T ; B_r]         (N = d)
 //   encode_bwd  dX   = dZ U~^T                           (N = d)
-// Tiles: BM tokens x BN outputs per workgroup of 4 waves (WM x WN), K staged
-// through LDS 32 at a time, double-buffered, with a register prefetch of
-// the next stage while the matrix units work on the current one.
+// and, with split-K over grid z, the small per-call operand products.
+//
+// Pipeline: a workgroup of 4 waves owns BM = 128 tokens and walks a run of
+// BN-wide output tiles; K is staged 64 at a time through three LDS stages
+// filled by buffer_load ... lds (direct-to-LDS, no register staging), two
+// stages in flight while the matrix units consume the third.  Each stage
+// lives in its own __shared__ array so the compiler's wait counting stays
+// per-stage.  LDS rows are 128 B with the 16 B chunks XOR-swizzled by
+// (row & 7), which keeps both the lane-linear DMA writes and the 32-row
+// fragment reads free of bank conflicts.  Buffer resources bound every
+// operand: lanes past the last token row, past Kg or past ldw read zeros.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -21,76 +30,107 @@ namespace mapl {
 
 namespace {
 
-constexpr int TB_BK = 32;
-constexpr int TB_LDK = TB_BK + 8;  // +16 B per row: conflict-free 16 B fragment reads
-constexpr int TB_THREADS = 256;
+typedef __attribute__((address_space(3))) void* lds_ptr;
 
-template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(TB_THREADS) void k_gemm_tn(TnArgs g) {
-  static_assert(WM * WN == 4, "4 waves");
-  constexpr int FM = BM / (32 * WM), FN = BN / (32 * WN);
-  static_assert(FM >= 1 && FN >= 1, "tile");
-  constexpr int ACH = BM * TB_BK / 8 / TB_THREADS;  // 16 B chunks per thread
-  constexpr int BCH = BN * TB_BK / 8 / TB_THREADS;
-  constexpr int ACH1 = ACH > 0 ? ACH : 1;
-  constexpr int BCH1 = BCH > 0 ? BCH : 1;
+constexpr int GM = 128, GK = 64, GTHREADS = 256;
+constexpr uint32_t OOB = 0x80000000u;  // any offset >= num_records reads zero
 
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM][TB_LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t Ws[2][BN][TB_LDK];
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint64_t bytes) {
+  const uint32_t n = bytes > 0x7fffffffull ? 0x7fffffffu : (uint32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, n, 0x00020000);
+}
+
+template <int BN>
+struct TnSmem {
+  bf16_t a[GM * GK];
+  bf16_t w[BN * GK];
+};
+
+// NS pipeline stages (2 or 3), one __shared__ array each.
+template <int BN, int NS>
+__global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_wg) {
+#if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature (launch stub)
+  static_assert(NS == 2 || NS == 3, "stages");
+  constexpr int FM = 2, FN = BN / 64;           // 2 x 2 waves, wave tile 64 x BN/2
+  constexpr int ABLK = GM / 8 / 4;              // A: 1 KiB blocks (8 rows) per wave per stage
+  constexpr int WBLK = BN / 8 / 4;              // W: 1 KiB blocks per wave per stage
+  constexpr int LOADS = ABLK + WBLK;            // buffer_load...lds per wave per stage
+  __shared__ __attribute__((aligned(1024))) TnSmem<BN> S0;
+  __shared__ __attribute__((aligned(1024))) TnSmem<BN> S1;
+  __shared__ __attribute__((aligned(1024))) TnSmem<NS == 3 ? BN : 64> S2;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-  const int ka_steps = g.Ka / TB_BK;
-  const int kg_steps = (g.Kg + TB_BK - 1) / TB_BK;
-  const int nsteps = ka_steps + kg_steps;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.x * GM;
+  const int nt0 = blockIdx.y * ntiles_per_wg;
+  const int ntiles = min(ntiles_per_wg, g.N / BN - nt0);
+  const int kz = g.kz > 0 ? g.kz : g.Ka;
+  const int kbase = g.kz > 0 ? blockIdx.z * g.kz : 0;
+  const int ka_steps = (kz + GK - 1) / GK;
+  const int kg_steps = (g.Kg + GK - 1) / GK;
+  const int KS = ka_steps + kg_steps;
+  const int KSP = (KS + NS - 1) / NS * NS;      // padded: stage buffers repeat every tile
+  const int total = ntiles * KSP;
 
-  uint4 ra[ACH1], rw[BCH1];
+  // Buffer resources: A rows of this workgroup, the anchor table, W.
+  const int mrows = min(GM, g.M - m0);
+  const __amdgpu_buffer_rsrc_t ra = rsrc(g.A + (int64_t)m0 * g.lda, (uint64_t)(mrows > 0 ? mrows : 0) * g.lda * 2);
+  const __amdgpu_buffer_rsrc_t rt = rsrc(g.T, g.T ? (uint64_t)g.V * g.ldt * 2 : 0);
+  const __amdgpu_buffer_rsrc_t rw = rsrc(g.W, (uint64_t)g.N * g.ldw * 2);
 
-  auto load_stage = [&](int s) {
-    const bool gathered = s >= ka_steps;
-    const int kc = gathered ? (s - ka_steps) * TB_BK : s * TB_BK;
+  // Per-lane DMA geometry: lane i of block b fills row 8b + i/8, physical
+  // chunk i%8.  Since 8b + i/8 = i/8 (mod 8), every block of this lane holds
+  // the same logical chunk lch = (i%8) ^ (i/8).  All offsets are 32-bit byte
+  // offsets from the resource bases (validated on the host).
+  const int lrow = lane >> 3;
+  const uint32_t lch = (uint32_t)((lane & 7) ^ lrow);
+  uint32_t a_off[ABLK], t_off[ABLK], w_off[WBLK];
 #pragma unroll
-    for (int i = 0; i < ACH1; ++i) {
-      int c = tid + i * TB_THREADS;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (ACH > 0 || c < BM * TB_BK / 8) {
-        int row = c >> 2, col = (c & 3) * 8;
-        int t = m0 + row;
-        if (t < g.M) {
-          if (!gathered) {
-            v = *(const uint4*)(g.A + (int64_t)t * g.lda + kc + col);
-          } else if (kc + col < g.Kg) {
-            int id = clamp_id(g.ids[t], g.V);
-            v = *(const uint4*)(g.T + (int64_t)id * g.ldt + kc + col);
-          }
-        }
-      }
-      ra[i] = v;
-    }
-    const int kw = s * TB_BK;
+  for (int j = 0; j < ABLK; ++j) {
+    const int row = 8 * (wave * ABLK + j) + lrow;
+    a_off[j] = (uint32_t)row * (uint32_t)g.lda * 2u + 16u * lch;
+    const bool has = g.Kg > 0 && m0 + row < g.M;
+    t_off[j] = has ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + 16u * lch : OOB;
+  }
 #pragma unroll
-    for (int i = 0; i < BCH1; ++i) {
-      int c = tid + i * TB_THREADS;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (BCH > 0 || c < BN * TB_BK / 8) {
-        int row = c >> 2, col = (c & 3) * 8;
-        v = *(const uint4*)(g.W + (int64_t)(n0 + row) * g.ldw + kw + col);
-      }
-      rw[i] = v;
-    }
-  };
-  auto store_stage = [&](int buf) {
+  for (int j = 0; j < WBLK; ++j) {
+    const int row = 8 * (wave * WBLK + j) + lrow;
+    w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lch;
+  }
+
+  // Every stage issues exactly LOADS loads per wave (padding steps read
+  // zeros), so the wait count below is exact.  Straight-line code: validity
+  // is a select on the offset, never a branch around a load.
+  auto issue = [&](int step, bf16_t* sa, bf16_t* sw) {
+    const int nt = nt0 + step / KSP, ks = step % KSP;
+    const bool pad = ks >= KS;
+    const bool gathered = ks >= ka_steps;
+    const int kc = gathered ? (ks - ka_steps) * GK : ks * GK;
+    const int col = kc + 8 * (int)lch;  // this lane's first column in the stage
+    if (!gathered || pad) {
+      const bool ok = !pad && col < kz;
+      const uint32_t add = (uint32_t)(kbase + kc) * 2u;
 #pragma unroll
-    for (int i = 0; i < ACH1; ++i) {
-      int c = tid + i * TB_THREADS;
-      if (ACH > 0 || c < BM * TB_BK / 8) *(uint4*)&As[buf][c >> 2][(c & 3) * 8] = ra[i];
-    }
+      for (int j = 0; j < ABLK; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(sa + (wave * ABLK + j) * 512), 16,
+                                                 ok ? a_off[j] + add : OOB, 0, 0, 0);
+    } else {
+      const bool ok = col < g.Kg;
+      const uint32_t add = (uint32_t)kc * 2u;
 #pragma unroll
-    for (int i = 0; i < BCH1; ++i) {
-      int c = tid + i * TB_THREADS;
-      if (BCH > 0 || c < BN * TB_BK / 8) *(uint4*)&Ws[buf][c >> 2][(c & 3) * 8] = rw[i];
+      for (int j = 0; j < ABLK; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, (lds_ptr)(sa + (wave * ABLK + j) * 512), 16,
+                                                 (ok && t_off[j] != OOB) ? t_off[j] + add : OOB, 0, 0, 0);
     }
+    const int wcol0 = gathered ? g.Ka + kc : kbase + kc;
+    const int wlim = pad ? 0 : gathered ? g.Ka + g.Kg : kbase + kz;
+    const int wc = wcol0 + 8 * (int)lch;
+    const bool wok = wc < wlim && wc < g.ldw;
+    const uint32_t wadd = (uint32_t)nt * BN * (uint32_t)g.ldw * 2u + (uint32_t)wcol0 * 2u;
+#pragma unroll
+    for (int j = 0; j < WBLK; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(sw + (wave * WBLK + j) * 512), 16,
+                                               wok ? w_off[j] + wadd : OOB, 0, 0, 0);
   };
 
   f32x16_t acc[FM][FN];
@@ -99,75 +139,113 @@ __global__ __launch_bounds__(TB_THREADS) void k_gemm_tn(TnArgs g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
 
-  if (nsteps > 0) {
-    load_stage(0);
-    store_stage(0);
-  }
-  __syncthreads();
-  for (int s = 0; s < nsteps; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nsteps) load_stage(s + 1);
+  auto compute = [&](const bf16_t* sa, const bf16_t* sw) {
 #pragma unroll
-    for (int kk = 0; kk < TB_BK; kk += 16) {
+    for (int kk = 0; kk < GK / 16; ++kk) {
+      const int lch = 2 * kk + (lane >> 5);
       uint4 af[FM], wf[FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-        af[i] = *(const uint4*)&As[buf][wm * (BM / WM) + i * 32 + (lane & 31)][kk + 8 * (lane >> 5)];
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * 64 + i * 32 + (lane & 31);
+        af[i] = *(const uint4*)(sa + row * GK + 8 * (lch ^ (row & 7)));
+      }
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        wf[j] = *(const uint4*)&Ws[buf][wn * (BN / WN) + j * 32 + (lane & 31)][kk + 8 * (lane >> 5)];
+      for (int j = 0; j < FN; ++j) {
+        const int row = wn * (BN / 2) + j * 32 + (lane & 31);
+        wf[j] = *(const uint4*)(sw + row * GK + 8 * (lch ^ (row & 7)));
+      }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(af[i], wf[j], acc[i][j]);
     }
-    if (s + 1 < nsteps) store_stage(buf ^ 1);
-    __syncthreads();
-  }
+  };
 
-  // Epilogue: lane holds column n = lane%32 of each 32x32 fragment.
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * (BN / WN) + j * 32 + (lane & 31);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int t = m0 + wm * (BM / WM) + i * 32 + acc_row(e, lane);
-        if (t < g.M) {
-          float v = acc[i][j][e];
-          if (g.out_f32)
-            ((float*)g.out)[(int64_t)t * g.ldo + n] = v;
-          else
-            ((bf16_t*)g.out)[(int64_t)t * g.ldo + n] = (bf16_t)f2bf(v);
-        }
+  // One pipeline step: stage s (in buffer `cur`) is consumed; stage s + NS - 1
+  // is issued into `nxt` (the buffer consumed at step s - 1).
+  auto step = [&](int s, int ks, const bf16_t* ca, const bf16_t* cw, bf16_t* na, bf16_t* nw) {
+    if (s + 1 < total)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS * (NS - 2)) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    if (s + NS - 1 < total) issue(s + NS - 1, na, nw);
+    if (ks < KS) compute(ca, cw);
+  };
+
+  issue(0, S0.a, S0.w);
+  if (NS == 3 && total > 1) issue(1, S1.a, S1.w);
+  char* obase = (char*)g.out + (g.kz > 0 ? (int64_t)blockIdx.z * g.out_z * 4 : 0);
+  for (int tile = 0; tile < ntiles; ++tile) {
+    for (int ks = 0; ks < KSP; ks += NS) {
+      const int s = tile * KSP + ks;
+      if constexpr (NS == 3) {
+        step(s, ks, S0.a, S0.w, S2.a, S2.w);
+        step(s + 1, ks + 1, S1.a, S1.w, S0.a, S0.w);
+        step(s + 2, ks + 2, S2.a, S2.w, S1.a, S1.w);
+      } else {
+        step(s, ks, S0.a, S0.w, S1.a, S1.w);
+        step(s + 1, ks + 1, S1.a, S1.w, S0.a, S0.w);
       }
     }
+    // epilogue: lane holds column n = lane%32 of each 32x32 fragment
+    const int nt = nt0 + tile;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int n = nt * BN + wn * (BN / 2) + j * 32 + (lane & 31);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int t = m0 + wm * 64 + i * 32 + acc_row(e, lane);
+          if (t < g.M) {
+            const float v = acc[i][j][e];
+            if (g.out_f32) {
+              float* o = (float*)obase + (int64_t)t * g.ldo + n;
+              *o = g.out_accum ? *o + v : v;
+            } else {
+              ((bf16_t*)obase)[(int64_t)t * g.ldo + n] = (bf16_t)f2bf(v);
+            }
+          }
+        }
+        acc[i][j] = f32x16_t{};
+      }
+  }
+#endif
 }
 
-template <int BM, int BN, int WM, int WN>
-hipError_t launch_tn(const TnArgs& g, hipStream_t s) {
-  dim3 grid((g.M + BM - 1) / BM, g.N / BN);
-  hipLaunchKernelGGL((k_gemm_tn<BM, BN, WM, WN>), grid, dim3(TB_THREADS), 0, s, g);
+
+template <int BN, int NS>
+hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
+  const int mt = (g.M + GM - 1) / GM;
+  const int nt = g.N / BN;
+  const int zs = g.kz > 0 ? g.Ka / g.kz : 1;
+  // enough workgroups to cover the chip once; each walks a run of N tiles
+  int per = 1;
+  while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) * zs >= 256) per *= 2;
+  dim3 grid(mt, (nt + per - 1) / per, zs);
+  hipLaunchKernelGGL((k_gemm_tn<BN, NS>), grid, dim3(GTHREADS), 0, s, g, per);
   return hipGetLastError();
+}
+
+template <int BN>
+hipError_t launch_ns(const TnArgs& g, hipStream_t s) {
+  // deep pipeline for long K streamed from HBM; double buffering when K is
+  // short and the run over N tiles keeps the stages flowing
+  const int kz = g.kz > 0 ? g.kz : g.Ka;
+  const int ks = (kz + GK - 1) / GK + (g.Kg + GK - 1) / GK;
+  return ks >= 12 ? launch_bn<BN, 3>(g, s) : launch_bn<BN, 2>(g, s);
 }
 
 }  // namespace
 
-// Tile choice: cover N with as few column tiles as possible (each A row is
-// then streamed from HBM once) and shrink BM when the token count alone
-// would leave compute units idle.
 hipError_t launch_gemm_tn(const TnArgs& g, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
-  const int BN = g.N % 256 == 0 ? 256 : g.N % 128 == 0 ? 128 : g.N % 64 == 0 ? 64 : g.N % 32 == 0 ? 32 : 0;
-  if (BN == 0) return hipErrorInvalidValue;
-  const bool small = (int64_t)((g.M + 127) / 128) * (g.N / BN) < 256;
-  switch (BN) {
-    case 256: return small ? launch_tn<64, 256, 2, 2>(g, s) : launch_tn<128, 256, 2, 2>(g, s);
-    case 128: return small ? launch_tn<64, 128, 2, 2>(g, s) : launch_tn<128, 128, 2, 2>(g, s);
-    case 64: return small ? launch_tn<64, 64, 2, 2>(g, s) : launch_tn<128, 64, 2, 2>(g, s);
-    default: return launch_tn<128, 32, 4, 1>(g, s);
-  }
+  if (g.kz > 0 && (g.kz % GK != 0 || g.Ka % g.kz != 0 || g.Kg != 0)) return hipErrorInvalidValue;
+  if (g.N % 256 == 0) return launch_ns<256>(g, s);
+  if (g.N % 128 == 0) return launch_ns<128>(g, s);
+  if (g.N % 64 == 0) return launch_ns<64>(g, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace mapl

@@ -149,7 +149,36 @@ __global__ void k_reduce_splits(const float* __restrict__ part, int splits, int6
   ((float4*)dst)[i] = v;
 }
 
+__global__ void k_reduce_splits_t_bf16(const float* __restrict__ part, int splits, int M, int N,
+                                       int64_t stride, float scale, bf16_t* __restrict__ dst, int64_t ldd,
+                                       int off) {
+  __shared__ float tile[32][33];
+  const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int y = ty; y < 32; y += 8) {
+    const int m = m0 + y, n = n0 + tx;
+    float v = 0.f;
+    if (m < M && n < N)
+      for (int s = 0; s < splits; ++s) v += part[s * stride + (int64_t)m * N + n];
+    tile[y][tx] = v;
+  }
+  __syncthreads();
+  for (int y = ty; y < 32; y += 8) {
+    const int n = n0 + y, m = m0 + tx;
+    if (n < N && m < M) dst[(int64_t)n * ldd + off + m] = (bf16_t)f2bf(scale * tile[tx][y]);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_reduce_splits_t_bf16(const float* part, int splits, int M, int N, int64_t part_stride,
+                                       float scale, bf16_t* dst, int64_t ldd, int off, hipStream_t s) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  dim3 grid((N + 31) / 32, (M + 31) / 32);
+  hipLaunchKernelGGL(k_reduce_splits_t_bf16, grid, dim3(256), 0, s, part, splits, M, N, part_stride, scale, dst,
+                     ldd, off);
+  return hipGetLastError();
+}
 
 hipError_t launch_wgrad(const WgradArgs& g, hipStream_t s) {
   const int Mtot = g.Ma + g.Mg;

@@ -13,12 +13,16 @@ typedef uint16_t bf16_t;
 // out[t,n] = sum_{c<Ka} A[t,c] W[n,c] + sum_{i<Kg} T[ids[t],i] W[n,Ka+i]
 // Ka % 32 == 0, Kg % 16 == 0, ldw >= Ka + roundup(Kg,32) with zero padding,
 // lda, ldt, ldw multiples of 8 (16 B rows), N % 32 == 0.
+// Split-K: with kz > 0 (and Kg == 0) grid z-slice s covers columns
+// [s*kz, (s+1)*kz) of A and W and writes its own fp32 partial at out + s*out_z.
+// out_accum (fp32 output only) adds to the existing output instead of storing.
 struct TnArgs {
   const bf16_t* A; int64_t lda;
   const bf16_t* T; int64_t ldt; const int32_t* ids; int Kg; int V;  // ids clamped to [0,V)
   const bf16_t* W; int64_t ldw;
   int M, N, Ka;
   void* out; int64_t ldo; int out_f32;
+  int kz; int64_t out_z; int out_accum;
 };
 hipError_t launch_gemm_tn(const TnArgs& g, hipStream_t s);
 
@@ -48,6 +52,9 @@ struct WgradArgs {
   float* part;  // [splits][Ma+Mg][N]
 };
 hipError_t launch_wgrad(const WgradArgs& g, hipStream_t s);
+// dst[n*ldd + off + m] = bf16(scale * sum_s part[s][m][n]) (transposed, fixed order).
+hipError_t launch_reduce_splits_t_bf16(const float* part, int splits, int M, int N, int64_t part_stride,
+                                       float scale, bf16_t* dst, int64_t ldd, int off, hipStream_t s);
 // dst[m][n] (+)= sum_s part[s][m][n] for m < M (fixed summation order).
 hipError_t launch_reduce_splits(const float* part, int splits, int M, int N, int64_t part_stride,
                                 float* dst, int accumulate, hipStream_t s);

@@ -137,10 +137,13 @@ SplitPlan plan_splits(int64_t T, int Mtot, int N) {
 struct Layout {
   size_t total = 0;
   size_t w = 0, w2 = 0, z0 = 0, cb = 0, cn2 = 0, cnr = 0, stats = 0, flag = 0;
-  size_t ahat = 0, part = 0, wsum = 0, ga = 0, bu = 0, zh = 0, z2 = 0;
+  size_t ahat = 0, part = 0, wsum = 0, ga = 0, bu = 0, zh = 0, z2 = 0, bt = 0, wt = 0;
   int64_t kp = 0, kw = 0;
   SplitPlan sp{1, 64};
 };
+
+// K slice of the split-K anchor-factor product B_s U~ (columns of d per slice).
+inline int64_t bu_kz(int64_t d) { return d % 128 == 0 ? 128 : 64; }
 
 Layout layout(const mapl_codec_desc& D, int call) {
   Layout Lo;
@@ -156,6 +159,7 @@ Layout layout(const mapl_codec_desc& D, int call) {
       case MAPL_CALL_ENCODE:
         Lo.kw = d + Lo.kp;
         Lo.w = c.take((size_t)r * Lo.kw * 2);
+        if (k > 0 && amb) Lo.bu = c.take((size_t)(d / bu_kz(d)) * k * r * 4);
         if (D.L > 0) {
           Lo.z0 = c.take((size_t)T * r * 4);
           Lo.cb = c.take((size_t)D.L * D.K * r * 2);
@@ -168,6 +172,7 @@ Layout layout(const mapl_codec_desc& D, int call) {
         Lo.kw = r + Lo.kp;
         Lo.w2 = c.take((size_t)d * Lo.kw * 2);
         if (D.L > 0) Lo.ahat = c.take((size_t)T * r * 2);
+        if (k > 0 && !amb) Lo.bu = c.take((size_t)k * d * 4);
         break;
       case MAPL_CALL_DECODE_BWD:
         Lo.w = c.take((size_t)r * d * 2);
@@ -180,7 +185,10 @@ Layout layout(const mapl_codec_desc& D, int call) {
         const int mg = (amb && k > 0) ? (int)k : 0;
         Lo.sp = plan_splits(T, (int)(d + mg), (int)r);
         Lo.part = c.take((size_t)Lo.sp.splits * (d + mg) * r * 4);
-        if (mg) Lo.wsum = c.take((size_t)k * r * 4);
+        if (mg) {
+          Lo.bt = c.take((size_t)d * Lo.kp * 2);  // B_s^T, zero-padded to kp columns
+          Lo.wt = c.take((size_t)r * Lo.kp * 2);  // -(a_s^T dZ)^T
+        }
         break;
       }
     }
@@ -363,13 +371,17 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
     LAUNCH("enc:prep_u", launch_prep_u(U, (int)d, (int)r, nullptr, 0, Wt, Lo.kw, s));
     if (k > 0) {
       if (amb) {
-        // Wt[c][d+i] = -bf16( (B_s U~)[i][c] )
-        GemmF32Args g = gemm((int)k, (int)r, (int)d);
-        g.A = B_s; g.sAm = d; g.sAk = 1;
-        g.B = Wt; g.sBk = 1; g.sBn = Lo.kw;
-        g.C = Wt + d; g.sCm = 1; g.sCn = Lo.kw;
-        g.alpha = -1.f;
-        LAUNCH("enc:gemm_f32", launch_gemm_f32(g, 1, 1, 1, s));
+        // Wt[c][d+i] = -bf16( (B_s U~)[i][c] ): split-K over d, fixed-order reduce
+        const int kz = (int)bu_kz(d), S = (int)(d / kz);
+        float* part = at<float>(ws, Lo.bu);
+        TnArgs b{};
+        b.A = (const bf16_t*)B_s; b.lda = d; b.Ka = (int)d; b.kz = kz; b.out_z = k * r;
+        b.W = Wt; b.ldw = Lo.kw;
+        b.M = (int)k; b.N = (int)r;
+        b.out = part; b.ldo = r; b.out_f32 = 1;
+        LAUNCH("enc:bu_gemm", launch_gemm_tn(b, s));
+        LAUNCH("enc:bu_reduce", launch_reduce_splits_t_bf16(part, S, (int)k, (int)r, k * r, -1.f, Wt, Lo.kw,
+                                                             (int)d, s));
       } else {
         LAUNCH("enc:transpose_into", launch_transpose_into(B_s, 0, (int)k, (int)r, r, -1.f, Wt, Lo.kw, (int)d, s));
       }
@@ -469,11 +481,15 @@ extern "C" int mapl_decode(const mapl_codec_desc* desc, const void* payload, con
         LAUNCH("dec:transpose_into", launch_transpose_into(B_r, 0, (int)k, (int)d, d, 1.f, W2, Lo.kw, (int)r, s));
       } else {
         // W2[j][r+i] = bf16( (B_r U~^T)[i][j] )
-        GemmF32Args g = gemm((int)k, (int)d, (int)r);
-        g.A = B_r; g.sAm = r; g.sAk = 1;
-        g.B = W2; g.sBk = 1; g.sBn = Lo.kw;
-        g.C = W2 + r; g.sCm = 1; g.sCn = Lo.kw;
-        LAUNCH("dec:gemm_f32", launch_gemm_f32(g, 1, 1, 1, s));
+        float* part = at<float>(ws, Lo.bu);
+        TnArgs b{};
+        b.A = (const bf16_t*)B_r; b.lda = r; b.Ka = (int)r;
+        b.W = W2; b.ldw = Lo.kw;
+        b.M = (int)k; b.N = (int)d;
+        b.out = part; b.ldo = d; b.out_f32 = 1;
+        LAUNCH("dec:bu_gemm", launch_gemm_tn(b, s));
+        LAUNCH("dec:bu_reduce", launch_reduce_splits_t_bf16(part, 1, (int)k, (int)d, k * d, 1.f, W2, Lo.kw,
+                                                             (int)r, s));
       }
     }
     const bf16_t* Aop = (const bf16_t*)payload;
@@ -691,15 +707,23 @@ extern "C" int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, cons
     LAUNCH("enc_bwd:wgrad", launch_wgrad(w, s));
     LAUNCH("enc_bwd:reduce_splits", launch_reduce_splits(w.part, w.splits, (int)d, (int)r, stride, dU, accumulate_dU, s));
     if (need_anchor) {
-      float* Ws = at<float>(ws, Lo.wsum);
-      LAUNCH("enc_bwd:reduce_splits", launch_reduce_splits(w.part + d * r, w.splits, (int)k, (int)r, stride, Ws, 0, s));
-      GemmF32Args e = gemm((int)d, (int)r, (int)k);
-      e.A = B_s; e.sAm = 1; e.sAk = d;
-      e.B = Ws; e.sBk = r; e.sBn = 1;
-      e.Cin = dU; e.sCinm = r; e.sCinn = 1; e.beta = 1.f;
-      e.C = dU; e.sCm = r; e.sCn = 1;
-      e.alpha = -1.f;
-      LAUNCH("enc_bwd:gemm_f32", launch_gemm_f32(e, 1, 0, 0, s));
+      // dU -= B_s^T (a_s^T dZ) as one more accumulating token-major GEMM:
+      // A = B_s^T [d,kp], W = -(a_s^T dZ)^T [r,kp] (bf16, padding zeroed)
+      bf16_t* Bt = at<bf16_t>(ws, Lo.bt);
+      bf16_t* Wn = at<bf16_t>(ws, Lo.wt);
+      if (Lo.kp != k) {
+        LAUNCH("enc_bwd:zero", launch_zero_bytes(Bt, d * Lo.kp * 2, s));
+        LAUNCH("enc_bwd:zero", launch_zero_bytes(Wn, r * Lo.kp * 2, s));
+      }
+      LAUNCH("enc_bwd:transpose_into", launch_transpose_into(B_s, 0, (int)k, (int)d, d, 1.f, Bt, Lo.kp, 0, s));
+      LAUNCH("enc_bwd:anchor_reduce", launch_reduce_splits_t_bf16(w.part + d * r, w.splits, (int)k, (int)r, stride,
+                                                                 -1.f, Wn, Lo.kp, 0, s));
+      TnArgs e{};
+      e.A = Bt; e.lda = Lo.kp; e.Ka = (int)Lo.kp;
+      e.W = Wn; e.ldw = Lo.kp;
+      e.M = (int)d; e.N = (int)r;
+      e.out = dU; e.ldo = r; e.out_f32 = 1; e.out_accum = 1;
+      LAUNCH("enc_bwd:anchor_gemm", launch_gemm_tn(e, s));
     }
     return MAPL_OK;
   }
