@@ -44,6 +44,16 @@ __device__ __forceinline__ int clamp_id(int id, int V) { return (unsigned)id < (
 
 __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
 
+// Screening margin of the RVQ kernel for residual width R:
+//   |s~_j - s_j| <= k1 ||R|| ||C_j|| + k2 ||C_j||^2, with
+//   k1 = 2 (2^-7 (bf16 rounding of both operands) + R 2^-24 (fp32
+//   accumulation)) plus the rounding of the fused add and of the fp32 norms,
+//   and k2 covering the fp32 norm ||C_j||^2; both inflated.
+__host__ __device__ constexpr float rvq_margin_k1(int R) {
+  return 0.015625f * 1.0078125f + 8.0f * R / 16777216.0f + 1.0f / 1048576.0f;
+}
+__host__ __device__ constexpr float rvq_margin_k2(int R) { return 4.0f * (R + 2) / 16777216.0f; }
+
 // Wave-wide reductions (wave64) through LDS-free cross-lane shuffles.
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

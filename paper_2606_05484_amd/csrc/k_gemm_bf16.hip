@@ -190,26 +190,56 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
     }
     // epilogue: lane holds column n = lane%32 of each 32x32 fragment
     const int nt = nt0 + tile;
+    if (g.out_f32) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int n = nt * BN + wn * (BN / 2) + j * 32 + (lane & 31);
+        for (int j = 0; j < FN; ++j) {
+          const int n = nt * BN + wn * (BN / 2) + j * 32 + (lane & 31);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int t = m0 + wm * 64 + i * 32 + acc_row(e, lane);
-          if (t < g.M) {
-            const float v = acc[i][j][e];
-            if (g.out_f32) {
+          for (int e = 0; e < 16; ++e) {
+            const int t = m0 + wm * 64 + i * 32 + acc_row(e, lane);
+            if (t < g.M) {
               float* o = (float*)obase + (int64_t)t * g.ldo + n;
-              *o = g.out_accum ? *o + v : v;
-            } else {
-              ((bf16_t*)obase)[(int64_t)t * g.ldo + n] = (bf16_t)f2bf(v);
+              *o = g.out_accum ? *o + acc[i][j][e] : acc[i][j][e];
             }
           }
+          acc[i][j] = f32x16_t{};
         }
-        acc[i][j] = f32x16_t{};
+    } else {
+      // bf16 output staged through the stage buffer consumed last (no DMA
+      // targets it until the next tile's first step): each wave writes its
+      // 64 x 64-column slices there, then stores 16 B row segments.
+      __builtin_amdgcn_s_barrier();  // every wave is done reading that buffer
+      constexpr int HALVES = FN >= 2 ? FN / 2 : 1;
+      constexpr int FJ = FN >= 2 ? 2 : 1;  // fragments per half
+      constexpr int COLS = FJ * 32, CPR = COLS / 8;  // staged columns, 16 B chunks per row
+      static_assert(4 * 64 * COLS <= GM * GK + BN * GK, "staging fits the stage buffer");
+      bf16_t* stg = S2.a + wave * (64 * COLS);
+#pragma unroll
+      for (int h = 0; h < HALVES; ++h) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int jj = 0; jj < FJ; ++jj)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              stg[(i * 32 + acc_row(e, lane)) * COLS + jj * 32 + (lane & 31)] = (bf16_t)f2bf(acc[i][h * FJ + jj][e]);
+#pragma unroll
+        for (int q = 0; q < CPR; ++q) {
+          const int c = lane + 64 * q;
+          const int row = c / CPR, ch = c % CPR;
+          const int t = m0 + wm * 64 + row;
+          const uint4 v = *(const uint4*)(stg + row * COLS + ch * 8);
+          if (t < g.M)
+            *(uint4*)((bf16_t*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + h * COLS + ch * 8) = v;
+        }
       }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
+    }
   }
 #endif
 }
@@ -230,11 +260,9 @@ hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
 
 template <int BN>
 hipError_t launch_ns(const TnArgs& g, hipStream_t s) {
-  // deep pipeline for long K streamed from HBM; double buffering when K is
-  // short and the run over N tiles keeps the stages flowing
-  const int kz = g.kz > 0 ? g.kz : g.Ka;
-  const int ks = (kz + GK - 1) / GK + (g.Kg + GK - 1) / GK;
-  return ks >= 12 ? launch_bn<BN, 3>(g, s) : launch_bn<BN, 2>(g, s);
+  // three stages throughout; short K pads its step count to a multiple of
+  // three (padding steps only rotate the pipeline)
+  return launch_bn<BN, 3>(g, s);
 }
 
 }  // namespace

@@ -57,57 +57,92 @@ __global__ void k_transpose_into(const void* __restrict__ src, int src_f32, int 
   }
 }
 
-// One wave per codeword: bf16 copy and fp32 norms.
-__global__ void k_prep_codebook(const float* __restrict__ C, int LK, int r, bf16_t* __restrict__ Cb,
-                                float* __restrict__ cn2, float* __restrict__ cnrm) {
+// One wave per (stage, codeword slot of a 64-codeword chunk): bf16 copy and
+// the fp32 screen constants, laid out per chunk as [n2 | ||C|| | k2 n2] x 64.
+__global__ void k_prep_codebook(const float* __restrict__ C, int L, int K, int r, bf16_t* __restrict__ Cb,
+                                float* __restrict__ meta) {
+  const int nch = (K + 63) / 64;
   const int w = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (w >= LK) return;
-  const float* row = C + (int64_t)w * r;
+  if (w >= L * nch * 64) return;
+  const int l = w / (nch * 64), slot = w % (nch * 64);
+  const int j = slot;  // codeword index within stage l
   float s = 0.f;
-  for (int c = lane; c < r; c += 64) {
-    const float v = row[c];
-    s += v * v;
-    Cb[(int64_t)w * r + c] = (bf16_t)f2bf(v);
+  if (j < K) {
+    const float* row = C + ((int64_t)l * K + j) * r;
+    for (int c = lane; c < r; c += 64) {
+      const float v = row[c];
+      s += v * v;
+      Cb[((int64_t)l * K + j) * r + c] = (bf16_t)f2bf(v);
+    }
   }
   s = wave_sum(s);
   if (lane == 0) {
-    cn2[w] = s;
-    cnrm[w] = sqrtf(s);
+    float* m = meta + ((int64_t)l * nch + j / 64) * 192 + (j % 64);
+    m[0] = s;
+    m[64] = sqrtf(s);
+    m[128] = rvq_margin_k2(r) * s;
   }
 }
 
-// One wave per token row.
+// One thread per (token, 8 columns): 16 B stores, independent gathers.
+// Requires r % 8 == 0 and, for the anchor columns, k % 8 == 0.
 __global__ void k_assemble(AssembleArgs a) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (t >= a.T) return;
-  bf16_t* out = a.out + (int64_t)t * a.ldo;
-  const int id = (a.A != nullptr) ? clamp_id(a.ids[t], a.V) : 0;
-  for (int c = lane; c < a.r; c += 64) {
-    float v;
+  const int per_row = a.ldo / 8;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (int64_t)a.T * per_row) return;
+  const int t = (int)(e / per_row), c0 = (int)(e % per_row) * 8;
+  bf16_t* out = a.out + (int64_t)t * a.ldo + c0;
+  const bool anchor_cols = a.A != nullptr && a.Bc == nullptr;
+  float v[8];
+  if (c0 < a.r) {
     if (a.L == 0) {
-      v = bf2f(a.Zp[(int64_t)t * a.r + c]);
+      const uint4 z = *(const uint4*)(a.Zp + (int64_t)t * a.r + c0);
+      const uint32_t w[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { v[2 * q] = bf2f(w[q] & 0xFFFFu); v[2 * q + 1] = bf2f(w[q] >> 16); }
     } else {
-      v = 0.f;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = 0.f;
       for (int l = 0; l < a.L; ++l) {
         int code = a.code_bytes == 1 ? ((const uint8_t*)a.codes)[(int64_t)t * a.L + l]
                                      : ((const uint16_t*)a.codes)[(int64_t)t * a.L + l];
         code = code < a.K ? code : a.K - 1;
-        v += a.C[((int64_t)l * a.K + code) * a.r + c];
+        const float4* cw = (const float4*)(a.C + ((int64_t)l * a.K + code) * a.r + c0);
+        const float4 p = cw[0], q4 = cw[1];
+        v[0] += p.x; v[1] += p.y; v[2] += p.z; v[3] += p.w;
+        v[4] += q4.x; v[5] += q4.y; v[6] += q4.z; v[7] += q4.w;
       }
     }
     if (a.Bc != nullptr) {
-      const bf16_t* arow = a.A + (int64_t)id * a.k;
-      for (int i = 0; i < a.k; ++i) v += bf2f(arow[i]) * bf2f(a.Bc[(int64_t)i * a.r + c]);
+      const bf16_t* arow = a.A + (int64_t)clamp_id(a.ids[t], a.V) * a.k;
+      for (int i = 0; i < a.k; ++i) {
+        const float ai = bf2f(arow[i]);
+        const uint4 b = *(const uint4*)(a.Bc + (int64_t)i * a.r + c0);
+        const uint32_t w[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          v[2 * q] = fmaf(ai, bf2f(w[q] & 0xFFFFu), v[2 * q]);
+          v[2 * q + 1] = fmaf(ai, bf2f(w[q] >> 16), v[2 * q + 1]);
+        }
+      }
     }
-    out[c] = (bf16_t)f2bf(v);
+    *(uint4*)out = make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7]));
+  } else if (anchor_cols && c0 < a.r + a.k) {
+    const bf16_t* arow = a.A + (int64_t)clamp_id(a.ids[t], a.V) * a.k;
+    *(uint4*)out = *(const uint4*)(arow + (c0 - a.r));
+  } else {
+    *(uint4*)out = make_uint4(0, 0, 0, 0);
   }
-  int col = a.r;
-  if (a.A != nullptr && a.Bc == nullptr) {
-    const bf16_t* arow = a.A + (int64_t)id * a.k;
-    for (int i = lane; i < a.k; i += 64) out[a.r + i] = arow[i];
-    col += a.k;
-  }
-  for (int c = col + lane; c < a.ldo; c += 64) out[c] = 0;
+}
+
+// One thread per 8 columns of a gathered row (16 B copies).
+__global__ void k_gather_rows_bf16(const bf16_t* __restrict__ A, int k, const int32_t* __restrict__ ids, int V,
+                                   int T, bf16_t* __restrict__ out) {
+  const int cpr = k / 8;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (int64_t)T * cpr) return;
+  const int t = (int)(e / cpr), c = (int)(e % cpr) * 8;
+  *(uint4*)(out + (int64_t)t * k + c) = *(const uint4*)(A + (int64_t)clamp_id(ids[t], V) * k + c);
 }
 
 __global__ void k_check_ids(const int32_t* __restrict__ ids, int T, int64_t V, int* flag) {
@@ -140,17 +175,27 @@ hipError_t launch_transpose_into(const void* src, int src_f32, int rows, int col
   return hipGetLastError();
 }
 
-hipError_t launch_prep_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* cn2, float* cnrm,
-                                hipStream_t s) {
-  const int LK = L * K;
-  if (LK <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_prep_codebook, dim3((LK + 3) / 4), dim3(256), 0, s, C, LK, r, Cb, cn2, cnrm);
+hipError_t launch_prep_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* meta, hipStream_t s) {
+  const int64_t slots = (int64_t)L * ((K + 63) / 64) * 64;
+  if (slots <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_prep_codebook, dim3((unsigned)((slots + 3) / 4)), dim3(256), 0, s, C, L, K, r, Cb, meta);
   return hipGetLastError();
 }
 
 hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_assemble, dim3((a.T + 3) / 4), dim3(256), 0, s, a);
+  if (a.r % 8 || a.ldo % 8 || (a.A != nullptr && a.k % 8)) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)a.T * (a.ldo / 8);
+  hipLaunchKernelGGL(k_assemble, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows_bf16(const bf16_t* A, int k, const int32_t* ids, int V, int T, bf16_t* out,
+                                   hipStream_t s) {
+  if (k % 8) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)T * (k / 8);
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_rows_bf16, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, A, k, ids, V, T, out);
   return hipGetLastError();
 }
 

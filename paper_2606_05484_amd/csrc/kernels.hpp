@@ -42,19 +42,29 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
 
 // ---------------------------------------------------------------- weight gradient
 // part[s][m][n] = sum over tokens t of split s of P[t,m] Q[t,n], where
-// P[t,m] = Pa[t,m] for m < Ma and Tg[ids[t], m-Ma] for Ma <= m < Ma+Mg.
-// Ma % 8 == 0, Mg % 8 == 0, N % 64 == 0; bf16 inputs, fp32 partials.
+// P[t,m] = Pa[t,m] for m < Ma and Tg[t, m-Mao] for Mao <= m < Mao+Mg, with
+// Mao = wgrad_row_offset(Ma) (Ma rounded up to a 128-row tile; rows in
+// [Ma, Mao) are written as zeros).  Tg is token-major [T, Mg].
+// Ma, Mg, ldp, ldq multiples of 8, N % 64 == 0; bf16 inputs, fp32 partials.
 struct WgradArgs {
   const bf16_t* Pa; int64_t ldp; int Ma;
-  const bf16_t* Tg; int64_t ldt; const int32_t* ids; int Mg; int V;
+  const bf16_t* Tg; int Mg;
   const bf16_t* Q; int64_t ldq;
   int T, N, splits, tokens_per_split;
-  float* part;  // [splits][Ma+Mg][N]
+  float* part;  // [splits][Mao+Mg][N]
 };
 hipError_t launch_wgrad(const WgradArgs& g, hipStream_t s);
+int wgrad_row_offset(int Ma);
+// out[t][i] = A[ids[t]][i] (bf16) for i < k.
+hipError_t launch_gather_rows_bf16(const bf16_t* A, int k, const int32_t* ids, int V, int T, bf16_t* out,
+                                   hipStream_t s);
 // dst[n*ldd + off + m] = bf16(scale * sum_s part[s][m][n]) (transposed, fixed order).
 hipError_t launch_reduce_splits_t_bf16(const float* part, int splits, int M, int N, int64_t part_stride,
                                        float scale, bf16_t* dst, int64_t ldd, int off, hipStream_t s);
+// dU[i][c] (+)= sum_s part[s][i][c] - sum_j B[j][i] Wa[j][c] (fixed order; B bf16
+// [k,d], Wa fp32 [k,r]; Wa == null skips the correction).  r % 4 == 0.
+hipError_t launch_reduce_dU(const float* part, int splits, int64_t part_stride, int d, int r, float* dU,
+                            int accumulate, const bf16_t* B, const float* Wa, int k, hipStream_t s);
 // dst[m][n] (+)= sum_s part[s][m][n] for m < M (fixed summation order).
 hipError_t launch_reduce_splits(const float* part, int splits, int M, int N, int64_t part_stride,
                                 float* dst, int accumulate, hipStream_t s);
@@ -70,9 +80,10 @@ hipError_t launch_prep_u(const float* U, int d, int r, bf16_t* Ub, int64_t ldub,
 // or bf16 source.
 hipError_t launch_transpose_into(const void* src, int src_f32, int rows, int cols, int64_t lds,
                                  float scale, bf16_t* dst, int64_t ldd, int off, hipStream_t s);
-// Cb[l][j][c] = bf16(C[l][j][c]); cn2[l*K+j] = ||C[l][j]||^2; cnrm = sqrt.
-hipError_t launch_prep_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* cn2,
-                                float* cnrm, hipStream_t s);
+// Cb[l][j][c] = bf16(C[l][j][c]); meta: per 64-codeword chunk, the arrays
+// ||C_j||^2, ||C_j|| and rvq_margin_k2(r) ||C_j||^2 (zero past K).
+hipError_t launch_prep_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* meta, hipStream_t s);
+inline int64_t rvq_meta_floats(int L, int K) { return (int64_t)L * ((K + 63) / 64) * 192; }
 
 // ---------------------------------------------------------------- receiver-side operand
 // out[t][0:r]   = Zhat[t]: payload row (bf16) or sum_l C[l][codes[t,l]] (fp32 -> bf16)
@@ -92,12 +103,12 @@ struct AssembleArgs {
 hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- RVQ (bf16 screen + fp32 rescore)
+// r in {32, 64, 128, 256}.
 struct RvqArgs {
   const float* Z0;     // [T,r] fp32 unquantised coordinates
   const bf16_t* Cb;    // [L,K,r] bf16 screening copy
   const float* C;      // [L,K,r] fp32 codebooks
-  const float* cn2;    // [L,K] ||C||^2
-  const float* cnrm;   // [L,K] ||C||
+  const float* meta;   // [L][ceil(K/64)][3][64]: ||C||^2, ||C||, k2 ||C||^2 (rvq_meta_floats)
   int T, r, L, K;
   void* codes; int code_bytes;  // [T,L]
   int* stats;          // [4] optional counters (candidates, overflow), may be null

@@ -120,10 +120,15 @@ struct SplitPlan {
   int splits, tps;
 };
 
-SplitPlan plan_splits(int64_t T, int Mtot, int N) {
-  const int bn = (N % 128 == 0) ? 128 : 64;
-  const int64_t tiles = ((Mtot + 127) / 128) * (int64_t)(N / bn);
-  int64_t want = (512 + tiles - 1) / tiles;
+// Token splits of the weight-gradient kernel: one workgroup per compute
+// unit (it holds 144 KiB of LDS), splits a multiple of 8 when that keeps
+// the grid a multiple of the 8 XCDs.
+SplitPlan plan_splits(int64_t T, int Ma, int Mg, int N) {
+  const int bn = (N % 256 == 0) ? 256 : (N % 128 == 0) ? 128 : 64;
+  const int64_t mt = wgrad_row_offset(Ma) / 128 + (Mg + 127) / 128;
+  const int64_t tiles = mt * (int64_t)(N / bn);
+  int64_t want = (256 + tiles - 1) / tiles;
+  if (want > 1 && (want * tiles) % 8) want = (want + 7) / 8 * 8;
   int64_t maxs = (T + 63) / 64;
   if (want > maxs) want = maxs;
   if (want < 1) want = 1;
@@ -163,8 +168,7 @@ Layout layout(const mapl_codec_desc& D, int call) {
         if (D.L > 0) {
           Lo.z0 = c.take((size_t)T * r * 4);
           Lo.cb = c.take((size_t)D.L * D.K * r * 2);
-          Lo.cn2 = c.take((size_t)D.L * D.K * 4);
-          Lo.cnr = c.take((size_t)D.L * D.K * 4);
+          Lo.cn2 = c.take((size_t)rvq_meta_floats(D.L, D.K) * 4);
           Lo.stats = c.take(16);
         }
         break;
@@ -177,17 +181,17 @@ Layout layout(const mapl_codec_desc& D, int call) {
       case MAPL_CALL_DECODE_BWD:
         Lo.w = c.take((size_t)r * d * 2);
         if (D.L > 0 || (!amb && k > 0)) Lo.ahat = c.take((size_t)T * r * 2);
-        Lo.sp = plan_splits(T, (int)d, (int)r);
-        Lo.part = c.take((size_t)Lo.sp.splits * d * r * 4);
+        Lo.sp = plan_splits(T, (int)d, 0, (int)r);
+        Lo.part = c.take((size_t)Lo.sp.splits * wgrad_row_offset((int)d) * r * 4);
         break;
       case MAPL_CALL_ENCODE_BWD: {
         Lo.w2 = c.take((size_t)d * r * 2);
         const int mg = (amb && k > 0) ? (int)k : 0;
-        Lo.sp = plan_splits(T, (int)(d + mg), (int)r);
-        Lo.part = c.take((size_t)Lo.sp.splits * (d + mg) * r * 4);
+        Lo.sp = plan_splits(T, (int)d, mg, (int)r);
+        Lo.part = c.take((size_t)Lo.sp.splits * (wgrad_row_offset((int)d) + mg) * r * 4);
         if (mg) {
-          Lo.bt = c.take((size_t)d * Lo.kp * 2);  // B_s^T, zero-padded to kp columns
-          Lo.wt = c.take((size_t)r * Lo.kp * 2);  // -(a_s^T dZ)^T
+          Lo.wsum = c.take((size_t)k * r * 4);   // a_s^T dZ
+          Lo.ga = c.take((size_t)T * k * 2);     // a_s = A_s[ids], token-major bf16
         }
         break;
       }
@@ -230,7 +234,8 @@ int check_desc(const mapl_codec_desc* D) {
     return fail(MAPL_E_SHAPE, "r=%lld: need 32 <= r <= min(d,1024), r %% 32 == 0", (long long)D->r);
   if (D->k < 0 || D->k > 512 || D->k % 16 || D->k > D->d)
     return fail(MAPL_E_SHAPE, "k=%lld: need 0 <= k <= min(d,512), k %% 16 == 0", (long long)D->k);
-  if (D->k > 0 && (D->V < 1 || D->V >= ((int64_t)1 << 31))) return fail(MAPL_E_SHAPE, "V=%lld out of range", (long long)D->V);
+  if (D->k > 0 && (D->V < 1 || D->V * D->k * (D->x_dtype == MAPL_F32 ? 4 : 2) >= ((int64_t)1 << 31)))
+    return fail(MAPL_E_SHAPE, "V=%lld: need V >= 1 and an anchor table under 2 GiB", (long long)D->V);
   if (D->anchor_space != MAPL_ANCHOR_AMBIENT && D->anchor_space != MAPL_ANCHOR_COORD)
     return fail(MAPL_E_SHAPE, "anchor_space=%d unknown", D->anchor_space);
   if (D->L < 0 || D->L > 8) return fail(MAPL_E_SHAPE, "L=%d: need 0 <= L <= 8", D->L);
@@ -241,8 +246,8 @@ int check_desc(const mapl_codec_desc* D) {
     } else if (D->code_dtype != MAPL_U16) {
       return fail(MAPL_E_DTYPE, "code_dtype must be MAPL_U8 or MAPL_U16 (got %d)", D->code_dtype);
     }
-    if (D->x_dtype == MAPL_BF16 && D->r > 256)
-      return fail(MAPL_E_UNSUPPORTED, "RVQ on the bf16 path supports r <= 256 (got %lld)", (long long)D->r);
+    if (D->x_dtype == MAPL_BF16 && D->r != 32 && D->r != 64 && D->r != 128 && D->r != 256)
+      return fail(MAPL_E_UNSUPPORTED, "RVQ on the bf16 path supports r in {32, 64, 128, 256} (got %lld)", (long long)D->r);
   }
   return MAPL_OK;
 }
@@ -400,11 +405,10 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
     g.out = Z0; g.ldo = r; g.out_f32 = 1;
     LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
     bf16_t* Cb = at<bf16_t>(ws, Lo.cb);
-    float* cn2 = at<float>(ws, Lo.cn2);
-    float* cnr = at<float>(ws, Lo.cnr);
-    LAUNCH("enc:prep_codebook", launch_prep_codebook(C, D.L, D.K, (int)r, Cb, cn2, cnr, s));
+    float* meta = at<float>(ws, Lo.cn2);
+    LAUNCH("enc:prep_codebook", launch_prep_codebook(C, D.L, D.K, (int)r, Cb, meta, s));
     RvqArgs a{};
-    a.Z0 = Z0; a.Cb = Cb; a.C = C; a.cn2 = cn2; a.cnrm = cnr;
+    a.Z0 = Z0; a.Cb = Cb; a.C = C; a.meta = meta;
     a.T = (int)T; a.r = (int)r; a.L = D.L; a.K = D.K;
     a.codes = payload; a.code_bytes = cbytes;
     a.stats = nullptr;
@@ -612,7 +616,8 @@ extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, c
     w.T = (int)T; w.N = (int)r; w.splits = Lo.sp.splits; w.tokens_per_split = Lo.sp.tps;
     w.part = at<float>(ws, Lo.part);
     LAUNCH("dec_bwd:wgrad", launch_wgrad(w, s));
-    LAUNCH("dec_bwd:reduce_splits", launch_reduce_splits(w.part, w.splits, (int)d, (int)r, d * r, dU, accumulate_dU, s));
+    LAUNCH("dec_bwd:reduce", launch_reduce_splits(w.part, w.splits, (int)d, (int)r,
+                                                  (int64_t)wgrad_row_offset((int)d) * r, dU, accumulate_dU, s));
     return MAPL_OK;
   }
 
@@ -699,31 +704,24 @@ extern "C" int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, cons
     LAUNCH("enc_bwd:gemm_tn", launch_gemm_tn(g, s));
     WgradArgs w{};
     w.Pa = (const bf16_t*)X; w.ldp = d; w.Ma = (int)d;
-    if (need_anchor) { w.Tg = (const bf16_t*)A_s; w.ldt = k; w.ids = ids; w.Mg = (int)k; w.V = (int)D.V; }
+    if (need_anchor) {
+      bf16_t* ga = at<bf16_t>(ws, Lo.ga);
+      LAUNCH("enc_bwd:gather", launch_gather_rows_bf16((const bf16_t*)A_s, (int)k, ids, (int)D.V, (int)T, ga, s));
+      w.Tg = ga; w.Mg = (int)k;
+    }
     w.Q = (const bf16_t*)dZ; w.ldq = r;
     w.T = (int)T; w.N = (int)r; w.splits = Lo.sp.splits; w.tokens_per_split = Lo.sp.tps;
     w.part = at<float>(ws, Lo.part);
-    const int64_t stride = (d + w.Mg) * r;
+    const int64_t mao = wgrad_row_offset((int)d);
+    const int64_t stride = (mao + w.Mg) * r;
     LAUNCH("enc_bwd:wgrad", launch_wgrad(w, s));
-    LAUNCH("enc_bwd:reduce_splits", launch_reduce_splits(w.part, w.splits, (int)d, (int)r, stride, dU, accumulate_dU, s));
+    LAUNCH("enc_bwd:reduce", launch_reduce_splits(w.part, w.splits, (int)d, (int)r, stride, dU, accumulate_dU, s));
     if (need_anchor) {
-      // dU -= B_s^T (a_s^T dZ) as one more accumulating token-major GEMM:
-      // A = B_s^T [d,kp], W = -(a_s^T dZ)^T [r,kp] (bf16, padding zeroed)
-      bf16_t* Bt = at<bf16_t>(ws, Lo.bt);
-      bf16_t* Wn = at<bf16_t>(ws, Lo.wt);
-      if (Lo.kp != k) {
-        LAUNCH("enc_bwd:zero", launch_zero_bytes(Bt, d * Lo.kp * 2, s));
-        LAUNCH("enc_bwd:zero", launch_zero_bytes(Wn, r * Lo.kp * 2, s));
-      }
-      LAUNCH("enc_bwd:transpose_into", launch_transpose_into(B_s, 0, (int)k, (int)d, d, 1.f, Bt, Lo.kp, 0, s));
-      LAUNCH("enc_bwd:anchor_reduce", launch_reduce_splits_t_bf16(w.part + d * r, w.splits, (int)k, (int)r, stride,
-                                                                 -1.f, Wn, Lo.kp, 0, s));
-      TnArgs e{};
-      e.A = Bt; e.lda = Lo.kp; e.Ka = (int)Lo.kp;
-      e.W = Wn; e.ldw = Lo.kp;
-      e.M = (int)d; e.N = (int)r;
-      e.out = dU; e.ldo = r; e.out_f32 = 1; e.out_accum = 1;
-      LAUNCH("enc_bwd:anchor_gemm", launch_gemm_tn(e, s));
+      // dU -= B_s^T (a_s^T dZ), a_s^T dZ summed from the anchor rows of the partials
+      float* Wa = at<float>(ws, Lo.wsum);
+      LAUNCH("enc_bwd:anchor_reduce", launch_reduce_splits(w.part + mao * r, w.splits, (int)k, (int)r, stride, Wa, 0, s));
+      LAUNCH("enc_bwd:anchor_corr", launch_reduce_dU(w.part, 0, stride, (int)d, (int)r, dU, 1, (const bf16_t*)B_s, Wa,
+                                                     (int)k, s));
     }
     return MAPL_OK;
   }
