@@ -20,8 +20,14 @@
 // stages in flight while the matrix units consume the third.  Each stage
 // lives in its own __shared__ array so the compiler's wait counting stays
 // per-stage.  LDS rows are 128 B with the 16 B chunks XOR-swizzled by
-// (row & 7), which keeps both the lane-linear DMA writes and the 32-row
-// fragment reads free of bank conflicts.  Buffer resources bound every
+// ((row >> 1) & 7): 16 consecutive rows reading one logical chunk then hit
+// 16 distinct 16 B bank groups of the 64-bank LDS (rows alternate between
+// the two halves of the bank space), and the lane-linear DMA writes are
+// conflict-free by construction.  The matrix units are fed W as the first
+// operand and the tokens as the second, so each lane ends up holding four
+// consecutive output columns of one token: fp32 results leave as 16 B
+// stores, bf16 results are paired across lane halves (v_permlane32_swap) into
+// 16 B row segments and staged through LDS into full 128 B row writes.  Buffer resources bound every
 // operand: lanes past the last token row, past Kg or past ldw read zeros.
 #include "common.hpp"
 #include "kernels.hpp"
@@ -79,23 +85,24 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
   const __amdgpu_buffer_rsrc_t rw = rsrc(g.W, (uint64_t)g.N * g.ldw * 2);
 
   // Per-lane DMA geometry: lane i of block b fills row 8b + i/8, physical
-  // chunk i%8.  Since 8b + i/8 = i/8 (mod 8), every block of this lane holds
-  // the same logical chunk lch = (i%8) ^ (i/8).  All offsets are 32-bit byte
-  // offsets from the resource bases (validated on the host).
+  // chunk i%8, so it loads logical chunk (i%8) ^ ((row >> 1) & 7), which
+  // depends only on the parity of b.  All offsets are 32-bit byte offsets
+  // from the resource bases (validated on the host).
   const int lrow = lane >> 3;
-  const uint32_t lch = (uint32_t)((lane & 7) ^ lrow);
+  const uint32_t lchp[2] = {(uint32_t)((lane & 7) ^ (lane >> 4)), (uint32_t)((lane & 7) ^ (4 + (lane >> 4)))};
   uint32_t a_off[ABLK], t_off[ABLK], w_off[WBLK];
 #pragma unroll
   for (int j = 0; j < ABLK; ++j) {
     const int row = 8 * (wave * ABLK + j) + lrow;
-    a_off[j] = (uint32_t)row * (uint32_t)g.lda * 2u + 16u * lch;
+    const uint32_t lc = lchp[j & 1];
+    a_off[j] = (uint32_t)row * (uint32_t)g.lda * 2u + 16u * lc;
     const bool has = g.Kg > 0 && m0 + row < g.M;
-    t_off[j] = has ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + 16u * lch : OOB;
+    t_off[j] = has ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + 16u * lc : OOB;
   }
 #pragma unroll
   for (int j = 0; j < WBLK; ++j) {
     const int row = 8 * (wave * WBLK + j) + lrow;
-    w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lch;
+    w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lchp[j & 1];
   }
 
   // Every stage issues exactly LOADS loads per wave (padding steps read
@@ -106,31 +113,33 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
     const bool pad = ks >= KS;
     const bool gathered = ks >= ka_steps;
     const int kc = gathered ? (ks - ka_steps) * GK : ks * GK;
-    const int col = kc + 8 * (int)lch;  // this lane's first column in the stage
+    // this lane's first column in the stage, per block parity
+    const int col0 = kc + 8 * (int)lchp[0], col1 = kc + 8 * (int)lchp[1];
     if (!gathered || pad) {
-      const bool ok = !pad && col < kz;
+      const bool ok0 = !pad && col0 < kz, ok1 = !pad && col1 < kz;
       const uint32_t add = (uint32_t)(kbase + kc) * 2u;
 #pragma unroll
       for (int j = 0; j < ABLK; ++j)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(sa + (wave * ABLK + j) * 512), 16,
-                                                 ok ? a_off[j] + add : OOB, 0, 0, 0);
+                                                 ((j & 1) ? ok1 : ok0) ? a_off[j] + add : OOB, 0, 0, 0);
     } else {
-      const bool ok = col < g.Kg;
+      const bool ok0 = col0 < g.Kg, ok1 = col1 < g.Kg;
       const uint32_t add = (uint32_t)kc * 2u;
 #pragma unroll
       for (int j = 0; j < ABLK; ++j)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, (lds_ptr)(sa + (wave * ABLK + j) * 512), 16,
-                                                 (ok && t_off[j] != OOB) ? t_off[j] + add : OOB, 0, 0, 0);
+                                                 (((j & 1) ? ok1 : ok0) && t_off[j] != OOB) ? t_off[j] + add : OOB,
+                                                 0, 0, 0);
     }
     const int wcol0 = gathered ? g.Ka + kc : kbase + kc;
     const int wlim = pad ? 0 : gathered ? g.Ka + g.Kg : kbase + kz;
-    const int wc = wcol0 + 8 * (int)lch;
-    const bool wok = wc < wlim && wc < g.ldw;
+    const int wc0 = wcol0 + 8 * (int)lchp[0], wc1 = wcol0 + 8 * (int)lchp[1];
+    const bool wok0 = wc0 < wlim && wc0 < g.ldw, wok1 = wc1 < wlim && wc1 < g.ldw;
     const uint32_t wadd = (uint32_t)nt * BN * (uint32_t)g.ldw * 2u + (uint32_t)wcol0 * 2u;
 #pragma unroll
     for (int j = 0; j < WBLK; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(sw + (wave * WBLK + j) * 512), 16,
-                                               wok ? w_off[j] + wadd : OOB, 0, 0, 0);
+                                               ((j & 1) ? wok1 : wok0) ? w_off[j] + wadd : OOB, 0, 0, 0);
   };
 
   f32x16_t acc[FM][FN];
@@ -139,6 +148,8 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
 
+  // acc[i][j] is the transposed 32 x 32 block: rows = output columns
+  // (W fragment j), columns = tokens (A fragment i).
   auto compute = [&](const bf16_t* sa, const bf16_t* sw) {
 #pragma unroll
     for (int kk = 0; kk < GK / 16; ++kk) {
@@ -147,17 +158,17 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int row = wm * 64 + i * 32 + (lane & 31);
-        af[i] = *(const uint4*)(sa + row * GK + 8 * (lch ^ (row & 7)));
+        af[i] = *(const uint4*)(sa + row * GK + 8 * (lch ^ ((row >> 1) & 7)));
       }
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int row = wn * (BN / 2) + j * 32 + (lane & 31);
-        wf[j] = *(const uint4*)(sw + row * GK + 8 * (lch ^ (row & 7)));
+        wf[j] = *(const uint4*)(sw + row * GK + 8 * (lch ^ ((row >> 1) & 7)));
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(af[i], wf[j], acc[i][j]);
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(wf[j], af[i], acc[i][j]);
     }
   };
 
@@ -188,28 +199,37 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
         step(s + 1, ks + 1, S1.a, S1.w, S0.a, S0.w);
       }
     }
-    // epilogue: lane holds column n = lane%32 of each 32x32 fragment
+    // epilogue: lane l holds token (l % 32) of fragment i and, for g = 0..3,
+    // output columns 8g + 4(l / 32) + 0..3 of fragment j
     const int nt = nt0 + tile;
+    const int half = lane >> 5;
     if (g.out_f32) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FM; ++i) {
+        const int t = m0 + wm * 64 + i * 32 + (lane & 31);
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          const int n = nt * BN + wn * (BN / 2) + j * 32 + (lane & 31);
+          if (t < g.M) {
+            float* o = (float*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + j * 32 + 4 * half;
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int t = m0 + wm * 64 + i * 32 + acc_row(e, lane);
-            if (t < g.M) {
-              float* o = (float*)obase + (int64_t)t * g.ldo + n;
-              *o = g.out_accum ? *o + acc[i][j][e] : acc[i][j][e];
+            for (int q = 0; q < 4; ++q) {
+              float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+              if (g.out_accum) {
+                const float4 p = *(const float4*)(o + 8 * q);
+                v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+              }
+              *(float4*)(o + 8 * q) = v;
             }
           }
           acc[i][j] = f32x16_t{};
         }
+      }
     } else {
-      // bf16 output staged through the stage buffer consumed last (no DMA
-      // targets it until the next tile's first step): each wave writes its
-      // 64 x 64-column slices there, then stores 16 B row segments.
+      // bf16: after the cross-half swap lane (t, h) holds the 16 B segment
+      // of token t covering columns 8(2q + h) .. +7 of fragment j (q = 0, 1).
+      // Segments are staged through the stage buffer consumed last (no DMA
+      // targets it before the next tile's first step), 128 B rows with
+      // chunks swizzled by ((row >> 1) & 7), then stored as full rows.
       __builtin_amdgcn_s_barrier();  // every wave is done reading that buffer
       constexpr int HALVES = FN >= 2 ? FN / 2 : 1;
       constexpr int FJ = FN >= 2 ? 2 : 1;  // fragments per half
@@ -221,16 +241,34 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
-          for (int jj = 0; jj < FJ; ++jj)
+          for (int jj = 0; jj < FJ; ++jj) {
+            const f32x16_t& c = acc[i][h * FJ + jj];
+            uint32_t p[8];
 #pragma unroll
-            for (int e = 0; e < 16; ++e)
-              stg[(i * 32 + acc_row(e, lane)) * COLS + jj * 32 + (lane & 31)] = (bf16_t)f2bf(acc[i][h * FJ + jj][e]);
+            for (int e = 0; e < 8; ++e) p[e] = pack_bf2(c[2 * e], c[2 * e + 1]);
+            // p[2g], p[2g+1]: columns 8g + 4h + 0..3; swap groups (0,1) and (2,3)
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+              for (int w = 0; w < 2; ++w) {
+                const auto sw2 = __builtin_amdgcn_permlane32_swap(p[4 * q + w], p[4 * q + 2 + w], false, false);
+                p[4 * q + w] = sw2[0];
+                p[4 * q + 2 + w] = sw2[1];
+              }
+            const int row = i * 32 + (lane & 31);
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+              const int ch = jj * 4 + 2 * q + half;
+              *(uint4*)(stg + row * COLS + 8 * (ch ^ ((row >> 1) & (CPR - 1)))) =
+                  make_uint4(p[4 * q], p[4 * q + 1], p[4 * q + 2], p[4 * q + 3]);
+            }
+          }
 #pragma unroll
         for (int q = 0; q < CPR; ++q) {
           const int c = lane + 64 * q;
           const int row = c / CPR, ch = c % CPR;
           const int t = m0 + wm * 64 + row;
-          const uint4 v = *(const uint4*)(stg + row * COLS + ch * 8);
+          const uint4 v = *(const uint4*)(stg + row * COLS + 8 * (ch ^ ((row >> 1) & (CPR - 1))));
           if (t < g.M)
             *(uint4*)((bf16_t*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + h * COLS + ch * 8) = v;
         }

@@ -258,60 +258,106 @@ __global__ void k_reduce_splits_t_bf16(const float* __restrict__ part, int split
   dst[(int64_t)n * ldd + off + m] = (bf16_t)f2bf(scale * v);
 }
 
-// dU[i][c] (+)= sum_s part[s][i][c] - sum_j B[j][i] Wa[j][c]   (Wa may be null)
-// One 64 x 64 tile of dU per block; B (bf16 [k,d]) and Wa (fp32 [k,r]) are
-// staged through LDS in 32-row slices.
+// dU (+)= sum_s part[s][i][c] - sum_j B[j][i] Wa[j][c]: the split-K reduction
+// of the weight gradient fused with the ambient-anchor correction
+// -B_s^T (a_s^T dZ) of the encoder backward.  B is bf16 [k, d], Wa fp32
+// [k, r] (already reduced).  A workgroup owns 32 rows x 64 columns of dU;
+// thread (ty, tx) owns row ty and columns 8tx .. 8tx+7.  All loads of a
+// chunk are issued before any LDS store so their latencies overlap.
+constexpr int RD_I = 32, RD_C = 64, RD_KC = 128;
+
 __global__ __launch_bounds__(256) void k_reduce_dU(const float* __restrict__ part, int splits, int64_t stride,
                                                    int d, int r, float* __restrict__ dU, int accumulate,
                                                    const bf16_t* __restrict__ B, const float* __restrict__ Wa,
                                                    int k) {
-  __shared__ float Bs[32][64 + 1];
-  __shared__ float Ws[32][64 + 1];
-  const int i0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;  // 16 x 16 threads, 4 x 4 outputs each
-  float acc[4][4];
+  __shared__ float Bs[RD_KC][RD_I + 1];
+  __shared__ __attribute__((aligned(16))) float Ws[RD_KC][RD_C];
+  const int i0 = blockIdx.y * RD_I, c0 = blockIdx.x * RD_C;
+  const int tid = threadIdx.x, ty = tid >> 3, tx = tid & 7;
+  const int i = i0 + ty, c = c0 + 8 * tx;
+  const bool own = i < d && c < r;  // r % 32 == 0: c < r implies c + 7 < r
+  const int64_t o = (int64_t)i * r + c;
+  float v[8];
+  if (own && accumulate) {
+    const float4 p0 = *(const float4*)(dU + o), p1 = *(const float4*)(dU + o + 4);
+    v[0] = p0.x; v[1] = p0.y; v[2] = p0.z; v[3] = p0.w; v[4] = p1.x; v[5] = p1.y; v[6] = p1.z; v[7] = p1.w;
+  } else {
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+    for (int e = 0; e < 8; ++e) v[e] = 0.f;
+  }
+  if (own) {
+    int s = 0;
+    for (; s + 4 <= splits; s += 4) {
+      float4 q[8];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = 0.f;
-  if (Wa != nullptr) {
-    for (int j0 = 0; j0 < k; j0 += 32) {
-      for (int e = threadIdx.x; e < 32 * 64; e += 256) {
-        const int jj = e / 64, q = e % 64;
-        const int j = j0 + jj;
-        Bs[jj][q] = (j < k && i0 + q < d) ? bf2f(B[(int64_t)j * d + i0 + q]) : 0.f;
-        Ws[jj][q] = (j < k && c0 + q < r) ? Wa[(int64_t)j * r + c0 + q] : 0.f;
+      for (int u = 0; u < 4; ++u) {
+        q[2 * u] = *(const float4*)(part + (s + u) * stride + o);
+        q[2 * u + 1] = *(const float4*)(part + (s + u) * stride + o + 4);
       }
-      __syncthreads();
-#pragma unroll 4
-      for (int jj = 0; jj < 32; ++jj) {
-        float bv[4], wv[4];
 #pragma unroll
-        for (int a = 0; a < 4; ++a) bv[a] = Bs[jj][ty * 4 + a];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) wv[b] = Ws[jj][tx * 4 + b];
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-#pragma unroll
-          for (int b = 0; b < 4; ++b) acc[a][b] = fmaf(bv[a], wv[b], acc[a][b]);
+      for (int u = 0; u < 4; ++u) {
+        v[0] += q[2 * u].x; v[1] += q[2 * u].y; v[2] += q[2 * u].z; v[3] += q[2 * u].w;
+        v[4] += q[2 * u + 1].x; v[5] += q[2 * u + 1].y; v[6] += q[2 * u + 1].z; v[7] += q[2 * u + 1].w;
       }
-      __syncthreads();
+    }
+    for (; s < splits; ++s) {
+      const float4 p0 = *(const float4*)(part + s * stride + o), p1 = *(const float4*)(part + s * stride + o + 4);
+      v[0] += p0.x; v[1] += p0.y; v[2] += p0.z; v[3] += p0.w; v[4] += p1.x; v[5] += p1.y; v[6] += p1.z; v[7] += p1.w;
     }
   }
+  if (Wa != nullptr && k > 0) {
+    float acc[8];
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const int i = i0 + ty * 4 + a;
-    if (i >= d) continue;
-    const int c = c0 + tx * 4;
-    if (c >= r) continue;
-    const int64_t o = (int64_t)i * r + c;
-    float4 v = accumulate ? *(const float4*)(dU + o) : make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s = 0; s < splits; ++s) {
-      const float4 p = *(const float4*)(part + s * stride + o);
-      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+    for (int j0 = 0; j0 < k; j0 += RD_KC) {
+      const int kc = min(RD_KC, k - j0);
+      // B rows j0.., columns i0 .. i0+31: 4 x 16 B per row, 2 per thread;
+      // Wa rows j0.., columns c0 .. c0+63: 16 float4 per row, 8 per thread
+      uint4 bq[2];
+      float4 wq[8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int e = tid + 256 * u, jj = e >> 2, q = (e & 3) * 8;
+        bq[u] = jj < kc ? *(const uint4*)(B + (int64_t)(j0 + jj) * d + i0 + q) : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = tid + 256 * u, jj = e >> 4, q = (e & 15) * 4;
+        wq[u] = (jj < kc && c0 + q < r) ? *(const float4*)(Wa + (int64_t)(j0 + jj) * r + c0 + q)
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      __syncthreads();  // the previous chunk's readers are done
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int e = tid + 256 * u, jj = e >> 2, q = (e & 3) * 8;
+        const uint32_t w4[4] = {bq[u].x, bq[u].y, bq[u].z, bq[u].w};
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          Bs[jj][q + 2 * h] = bf2f(w4[h] & 0xFFFFu);
+          Bs[jj][q + 2 * h + 1] = bf2f(w4[h] >> 16);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = tid + 256 * u, jj = e >> 4, q = (e & 15) * 4;
+        *(float4*)&Ws[jj][q] = wq[u];
+      }
+      __syncthreads();
+      for (int jj = 0; jj < kc; ++jj) {
+        const float b = Bs[jj][ty];
+        const float4 w0 = *(const float4*)&Ws[jj][8 * tx], w1 = *(const float4*)&Ws[jj][8 * tx + 4];
+        acc[0] = fmaf(b, w0.x, acc[0]); acc[1] = fmaf(b, w0.y, acc[1]);
+        acc[2] = fmaf(b, w0.z, acc[2]); acc[3] = fmaf(b, w0.w, acc[3]);
+        acc[4] = fmaf(b, w1.x, acc[4]); acc[5] = fmaf(b, w1.y, acc[5]);
+        acc[6] = fmaf(b, w1.z, acc[6]); acc[7] = fmaf(b, w1.w, acc[7]);
+      }
     }
-    v.x -= acc[a][0]; v.y -= acc[a][1]; v.z -= acc[a][2]; v.w -= acc[a][3];
-    *(float4*)(dU + o) = v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] -= acc[e];
+  }
+  if (own) {
+    *(float4*)(dU + o) = make_float4(v[0], v[1], v[2], v[3]);
+    *(float4*)(dU + o + 4) = make_float4(v[4], v[5], v[6], v[7]);
   }
 }
 
@@ -328,7 +374,8 @@ hipError_t launch_reduce_splits_t_bf16(const float* part, int splits, int M, int
 
 hipError_t launch_reduce_dU(const float* part, int splits, int64_t part_stride, int d, int r, float* dU,
                             int accumulate, const bf16_t* B, const float* Wa, int k, hipStream_t s) {
-  dim3 grid((r + 63) / 64, (d + 63) / 64);
+  if (d % RD_I || r % 32 || (uintptr_t)B % 16) return hipErrorInvalidValue;
+  dim3 grid((r + RD_C - 1) / RD_C, d / RD_I);
   hipLaunchKernelGGL(k_reduce_dU, grid, dim3(256), 0, s, part, splits, part_stride, d, r, dU, accumulate, B, Wa, k);
   return hipGetLastError();
 }

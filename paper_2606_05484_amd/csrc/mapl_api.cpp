@@ -127,8 +127,9 @@ SplitPlan plan_splits(int64_t T, int Ma, int Mg, int N) {
   const int bn = (N % 256 == 0) ? 256 : (N % 128 == 0) ? 128 : 64;
   const int64_t mt = wgrad_row_offset(Ma) / 128 + (Mg + 127) / 128;
   const int64_t tiles = mt * (int64_t)(N / bn);
-  int64_t want = (256 + tiles - 1) / tiles;
-  if (want > 1 && (want * tiles) % 8) want = (want + 7) / 8 * 8;
+  // one workgroup per CU (the kernel's LDS footprint) and a single wave of
+  // workgroups: at most 256 in total
+  int64_t want = tiles >= 256 ? 1 : 256 / tiles;
   int64_t maxs = (T + 63) / 64;
   if (want > maxs) want = maxs;
   if (want < 1) want = 1;
@@ -715,13 +716,15 @@ extern "C" int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, cons
     const int64_t mao = wgrad_row_offset((int)d);
     const int64_t stride = (mao + w.Mg) * r;
     LAUNCH("enc_bwd:wgrad", launch_wgrad(w, s));
-    LAUNCH("enc_bwd:reduce", launch_reduce_splits(w.part, w.splits, (int)d, (int)r, stride, dU, accumulate_dU, s));
     if (need_anchor) {
-      // dU -= B_s^T (a_s^T dZ), a_s^T dZ summed from the anchor rows of the partials
+      // dU = sum of the partials - B_s^T (a_s^T dZ); a_s^T dZ is summed first
+      // from the anchor rows of the partials
       float* Wa = at<float>(ws, Lo.wsum);
       LAUNCH("enc_bwd:anchor_reduce", launch_reduce_splits(w.part + mao * r, w.splits, (int)k, (int)r, stride, Wa, 0, s));
-      LAUNCH("enc_bwd:anchor_corr", launch_reduce_dU(w.part, 0, stride, (int)d, (int)r, dU, 1, (const bf16_t*)B_s, Wa,
-                                                     (int)k, s));
+      LAUNCH("enc_bwd:reduce_corr", launch_reduce_dU(w.part, w.splits, stride, (int)d, (int)r, dU, accumulate_dU,
+                                                     (const bf16_t*)B_s, Wa, (int)k, s));
+    } else {
+      LAUNCH("enc_bwd:reduce", launch_reduce_splits(w.part, w.splits, (int)d, (int)r, stride, dU, accumulate_dU, s));
     }
     return MAPL_OK;
   }
