@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace mapl {
 
 typedef uint16_t bf16_t;  // bf16 stored as its bit pattern
@@ -44,15 +46,19 @@ __device__ __forceinline__ int clamp_id(int id, int V) { return (unsigned)id < (
 
 __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
 
-// Screening margin of the RVQ kernel for residual width R:
-//   |s~_j - s_j| <= k1 ||R|| ||C_j|| + k2 ||C_j||^2, with
-//   k1 = 2 (2^-7 (bf16 rounding of both operands) + R 2^-24 (fp32
-//   accumulation)) plus the rounding of the fused add and of the fp32 norms,
-//   and k2 covering the fp32 norm ||C_j||^2; both inflated.
+// Screening margin of the RVQ kernel for residual width R: with the
+// accumulator started at ||C_j||^2 and bf16 operands,
+//   |s~_j - s_j| <= k1 ||R|| ||C_j|| + k2 ||C_j||^2, where
+//   k1 = 2 (2 * 2^-8 + 2^-16)  (bf16 rounding of both operands, doubled)
+//      + 8 R 2^-24             (fp32 accumulation of 2R~.C~, any order,
+//                               relative error up to 2 u per addition)
+//      + 2^-20 + 2^-17         (norm rounding; the 4-bit index tag)
+//   k2 = 4 (R + 4) 2^-24 + 2^-18 (accumulation and fp32 rounding of
+//                               ||C_j||^2; the index tag)
 __host__ __device__ constexpr float rvq_margin_k1(int R) {
-  return 0.015625f * 1.0078125f + 8.0f * R / 16777216.0f + 1.0f / 1048576.0f;
+  return 0.015625f * 1.0078125f + 8.0f * R / 16777216.0f + 1.0f / 1048576.0f + 1.0f / 131072.0f;
 }
-__host__ __device__ constexpr float rvq_margin_k2(int R) { return 4.0f * (R + 2) / 16777216.0f; }
+__host__ __device__ constexpr float rvq_margin_k2(int R) { return 4.0f * (R + 4) / 16777216.0f + 1.0f / 262144.0f; }
 
 // Wave-wide reductions (wave64) through LDS-free cross-lane shuffles.
 __device__ __forceinline__ float wave_sum(float v) {
@@ -65,5 +71,83 @@ __device__ __forceinline__ float wave_min(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, WAVE));
   return v;
 }
+
+// ---- LDS access through inline asm
+// The pipelined kernels fill LDS with buffer_load ... lds (direct-to-LDS)
+// while reading earlier stages.  The compiler cannot prove that an ordinary
+// LDS read does not alias a DMA still in flight and drains every
+// outstanding DMA (s_waitcnt vmcnt(0)) before it, which serialises the
+// pipeline.  Reads issued as inline asm are invisible to that analysis; the
+// kernels order them with explicit s_waitcnt vmcnt + barriers (stage ready)
+// and lds_wait() (data returned), whose in/out operands keep every use of
+// the loaded registers after the wait.
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+template <int OFF = 0>
+__device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset is 16 bits");
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF) : "memory");
+  return r;
+}
+
+template <int OFF = 0>
+__device__ __forceinline__ void lds_write_b128(uint32_t addr, u32x4 v) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset is 16 bits");
+  asm volatile("ds_write_b128 %0, %1 offset:%2" ::"v"(addr), "v"(v), "i"(OFF) : "memory");
+}
+
+// Wait until every LDS access of this wave has completed; the listed
+// registers become defined only after the wait.
+template <int N>
+__device__ __forceinline__ void lds_wait(u32x4 (&v)[N]) {
+  static_assert(N >= 1 && N <= 8, "lds_wait takes 1..8 registers per call");
+  if constexpr (N == 1) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0])::"memory");
+  if constexpr (N == 2) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1])::"memory");
+  if constexpr (N == 3) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2])::"memory");
+  if constexpr (N == 4)
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3])::"memory");
+  if constexpr (N == 5)
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4])::"memory");
+  if constexpr (N == 6)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5])::"memory");
+  if constexpr (N == 7)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6])::"memory");
+  if constexpr (N == 8)
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),
+                   "+v"(v[7])::"memory");
+}
+
+// Wait until every LDS access of this wave has completed; pair with
+// reg_pin() on the registers loaded before it.
+__device__ __forceinline__ void lds_wait0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Pins registers after an earlier lds_wait0() / lds_wait() (no instruction
+// emitted): both are volatile asm, so their order is kept, and every later
+// use of the registers depends on the pin.
+template <int N>
+__device__ __forceinline__ void reg_pin(u32x4 (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I = B .. E-1.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+__device__ __forceinline__ uint4 as_uint4(u32x4 v) { return make_uint4(v.x, v.y, v.z, v.w); }
+__device__ __forceinline__ u32x4 as_u32x4(uint4 v) { return u32x4{v.x, v.y, v.z, v.w}; }
 
 }  // namespace mapl

@@ -149,26 +149,40 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
 
   // acc[i][j] is the transposed 32 x 32 block: rows = output columns
-  // (W fragment j), columns = tokens (A fragment i).
+  // (W fragment j), columns = tokens (A fragment i).  Fragment reads are
+  // inline asm (see lds_read_b128), double-buffered in registers: the reads
+  // of k-step kk + 1 are in flight while the matrix units work on kk.  The
+  // lane's row is lane % 32 (+ multiples of 16, which keep the swizzle), its
+  // logical chunk 2 kk + lane / 32.
+  const int half = lane >> 5;
+  uint32_t koff[GK / 16];
+#pragma unroll
+  for (int kk = 0; kk < GK / 16; ++kk)
+    koff[kk] = (uint32_t)((lane & 31) * (GK * 2) + 16 * ((2 * kk + half) ^ (((lane & 31) >> 1) & 7)));
   auto compute = [&](const bf16_t* sa, const bf16_t* sw) {
+    const uint32_t ba = lds_addr(sa) + wm * 64 * (GK * 2), bw = lds_addr(sw) + wn * (BN / 2) * (GK * 2);
+    u32x4 fr[2][FM + FN];
+    auto load = [&](int kk, u32x4 (&f)[FM + FN]) {
+      static_for<0, FM>([&](auto ic) {
+        constexpr int I = decltype(ic)::value;
+        f[I] = lds_read_b128<I * 32 * GK * 2>(ba + koff[kk]);
+      });
+      static_for<0, FN>([&](auto jc) {
+        constexpr int J = decltype(jc)::value;
+        f[FM + J] = lds_read_b128<J * 32 * GK * 2>(bw + koff[kk]);
+      });
+    };
+    load(0, fr[0]);
+    lds_wait(fr[0]);
 #pragma unroll
     for (int kk = 0; kk < GK / 16; ++kk) {
-      const int lch = 2 * kk + (lane >> 5);
-      uint4 af[FM], wf[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int row = wm * 64 + i * 32 + (lane & 31);
-        af[i] = *(const uint4*)(sa + row * GK + 8 * (lch ^ ((row >> 1) & 7)));
-      }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int row = wn * (BN / 2) + j * 32 + (lane & 31);
-        wf[j] = *(const uint4*)(sw + row * GK + 8 * (lch ^ ((row >> 1) & 7)));
-      }
+      const int cb = kk & 1;
+      if (kk + 1 < GK / 16) load(kk + 1, fr[cb ^ 1]);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(wf[j], af[i], acc[i][j]);
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(as_uint4(fr[cb][FM + j]), as_uint4(fr[cb][i]), acc[i][j]);
+      if (kk + 1 < GK / 16) lds_wait(fr[cb ^ 1]);
     }
   };
 
@@ -202,7 +216,6 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
     // epilogue: lane l holds token (l % 32) of fragment i and, for g = 0..3,
     // output columns 8g + 4(l / 32) + 0..3 of fragment j
     const int nt = nt0 + tile;
-    const int half = lane >> 5;
     if (g.out_f32) {
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
@@ -235,7 +248,7 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
       constexpr int FJ = FN >= 2 ? 2 : 1;  // fragments per half
       constexpr int COLS = FJ * 32, CPR = COLS / 8;  // staged columns, 16 B chunks per row
       static_assert(4 * 64 * COLS <= GM * GK + BN * GK, "staging fits the stage buffer");
-      bf16_t* stg = S2.a + wave * (64 * COLS);
+      const uint32_t stg = lds_addr(S2.a) + wave * (64 * COLS * 2);
 #pragma unroll
       for (int h = 0; h < HALVES; ++h) {
 #pragma unroll
@@ -259,18 +272,25 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #pragma unroll
             for (int q = 0; q < 2; ++q) {
               const int ch = jj * 4 + 2 * q + half;
-              *(uint4*)(stg + row * COLS + 8 * (ch ^ ((row >> 1) & (CPR - 1)))) =
-                  make_uint4(p[4 * q], p[4 * q + 1], p[4 * q + 2], p[4 * q + 3]);
+              lds_write_b128(stg + row * COLS * 2 + 16 * (ch ^ ((row >> 1) & (CPR - 1))),
+                             u32x4{p[4 * q], p[4 * q + 1], p[4 * q + 2], p[4 * q + 3]});
             }
           }
+        u32x4 v[CPR];
+#pragma unroll
+        for (int q = 0; q < CPR; ++q) {
+          const int c = lane + 64 * q;
+          const int row = c / CPR, ch = c % CPR;
+          v[q] = lds_read_b128(stg + row * COLS * 2 + 16 * (ch ^ ((row >> 1) & (CPR - 1))));
+        }
+        lds_wait(v);
 #pragma unroll
         for (int q = 0; q < CPR; ++q) {
           const int c = lane + 64 * q;
           const int row = c / CPR, ch = c % CPR;
           const int t = m0 + wm * 64 + row;
-          const uint4 v = *(const uint4*)(stg + row * COLS + 8 * (ch ^ ((row >> 1) & (CPR - 1))));
           if (t < g.M)
-            *(uint4*)((bf16_t*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + h * COLS + ch * 8) = v;
+            *(uint4*)((bf16_t*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + h * COLS + ch * 8) = as_uint4(v[q]);
         }
       }
 #pragma unroll

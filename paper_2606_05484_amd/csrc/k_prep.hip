@@ -58,7 +58,7 @@ __global__ void k_transpose_into(const void* __restrict__ src, int src_f32, int 
 }
 
 // One wave per (stage, codeword slot of a 64-codeword chunk): bf16 copy and
-// the fp32 screen constants, laid out per chunk as [n2 | ||C|| | k2 n2] x 64.
+// the fp32 squared norm, laid out per chunk as 64 consecutive floats.
 __global__ void k_prep_codebook(const float* __restrict__ C, int L, int K, int r, bf16_t* __restrict__ Cb,
                                 float* __restrict__ meta) {
   const int nch = (K + 63) / 64;
@@ -76,12 +76,7 @@ __global__ void k_prep_codebook(const float* __restrict__ C, int L, int K, int r
     }
   }
   s = wave_sum(s);
-  if (lane == 0) {
-    float* m = meta + ((int64_t)l * nch + j / 64) * 192 + (j % 64);
-    m[0] = s;
-    m[64] = sqrtf(s);
-    m[128] = rvq_margin_k2(r) * s;
-  }
+  if (lane == 0) meta[((int64_t)l * nch + j / 64) * 64 + (j % 64)] = s;
 }
 
 // One thread per (token, 8 columns): 16 B stores, independent gathers.

@@ -3,17 +3,21 @@
 // current residual R_l and subtracts it.  Ties go to the lowest index.
 //
 // Decision procedure (exact with respect to the fp32 residual):
-//   screen  s~_j = ||C_j||^2 - 2 R~ . C~_j on the bf16 matrix units, with
-//           R~ = bf16(R), C~ = bf16(C), fp32 accumulation.  The true
-//           s_j = ||C_j||^2 - 2 R.C_j obeys |s~_j - s_j| <= delta_j with
-//           delta_j = kappa ||R|| ||C_j|| + kappa2 ||C_j||^2 (bf16 rounding of
-//           both operands, fp32 accumulation and the final fused add; the
-//           constants carry a safety factor, see rvq_margin()).
-//   bound   U* = min_j (s~_j + delta_j) >= min_j s_j; the nearest codeword is
-//           among {j : s~_j - delta_j <= U*}.
-//   pass 1  tracks U*, the smallest and second-smallest lower bound; if the
-//           second-smallest exceeds U* the candidate set is a single
-//           codeword and the decision is final.
+//   screen  s~_j = ||C_j||^2 - 2 R~ . C~_j on the bf16 matrix units with
+//           R~ = bf16(R), C~ = bf16(C): the accumulator starts at ||C_j||^2
+//           (fp32) and the second operand is bf16(-2R) = -2 R~ exactly.  The
+//           true s_j = ||C_j||^2 - 2 R.C_j differs from s~_j by at most
+//           Delta = k1 ||R|| max_j||C_j|| + k2 max_j||C_j||^2 (bf16 rounding
+//           of both operands, fp32 accumulation and norms, the index tag
+//           below; constants inflated, see rvq_margin_k1/k2), one margin per
+//           token and round.
+//   tag     the low 4 mantissa bits of s~_j are replaced by the codeword's
+//           slot among the 16 scores a lane sees per tile, so a plain float
+//           min also yields the position; the tile is tracked separately.
+//   pass 1  per lane: smallest tagged score m1 (and its tile) and the
+//           second smallest m2 (v_med3); the nearest codeword lies in
+//           {j : s~_j <= m1 + 2 Delta}; if m2 exceeds that bound the set
+//           is a single codeword and the decision is final.
 //   pass 2  (only when a token of the workgroup is ambiguous) re-screens
 //           and lists every candidate; the candidates are rescored exactly
 //           in fp32 as sum_c (R_c - C_jc)^2.
@@ -21,14 +25,14 @@
 // already chosen, so screening and rescoring see the same R.
 //
 // Layout: a workgroup of 4 waves owns 128 tokens, 32 per wave.  A wave keeps
-// its tokens' bf16 residual as the B operand of v_mfma_f32_32x32x16_bf16 in
+// its tokens' bf16(-2R) as the B operand of v_mfma_f32_32x32x16_bf16 in
 // registers (tokens along N); 64-codeword chunks of C~ stream through three
 // LDS stages filled by buffer_load ... lds (direct-to-LDS, one __shared__
 // array per stage) as the A operand (codewords along M), together with the
-// chunk's per-codeword screen constants (||C||^2, ||C||, kappa2 ||C||^2).
-// Each lane thus sees the scores of ONE token for 16 codewords per tile and
-// tracks its bounds in registers; only the two lane halves that share a
-// token merge at the end of a pass.
+// chunk's ||C_j||^2 (a wave-private copy, the accumulator's initial value).
+// Each lane thus sees the scores of ONE token for 16 codewords per tile;
+// the fold of one tile into (m1, m2) overlaps the matrix products of the
+// next.  The two lane halves that share a token merge at the end of a pass.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -45,23 +49,40 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rq_rsrc(const void* base, uint
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, n, 0x00020000);
 }
 
+// Codeword rows are stored 2R + 16 bytes apart, so the 16 rows that read one
+// 16 B column chunk of a fragment start 4 banks apart: conflict-free reads
+// whose addresses differ per k-step by an immediate offset only.
+template <int R>
+constexpr int rq_row_bytes() { return 2 * R + 16; }
+template <int R>
+constexpr int rq_blocks() {  // 1 KiB DMA blocks per wave covering the 64 padded rows
+  return (RQ_CW * rq_row_bytes<R>() + 4 * 1024 - 1) / (4 * 1024);
+}
+
 template <int R>
 struct RqStage {
-  bf16_t c[RQ_CW * R];   // codewords, 2R bytes per row, 16 B chunks XOR-swizzled by row
-  float meta[4][256];    // per wave: [n2 | cnr | n2k] x 64 codewords (wave-private copy)
+  bf16_t c[4 * rq_blocks<R>() * 512];  // 64 codeword rows of 2R + 16 bytes (+ tail)
+  float n2[4][256];      // per wave: ||C_j||^2 of the chunk's 64 codewords (wave-private
+                         // copy; the DMA writes 16 B for each of the 64 lanes)
 };
 
 __device__ __forceinline__ int load_code(const void* codes, int cb, int64_t idx) {
   return cb == 1 ? ((const uint8_t*)codes)[idx] : ((const uint16_t*)codes)[idx];
 }
 
+// Row of a 32-codeword tile held by accumulator slot e of a lane in `half`.
+__device__ __forceinline__ int rq_row(int e, int half) { return 8 * (e >> 2) + 4 * half + (e & 3); }
+
+__device__ __forceinline__ float rq_tag(float s, int e) {
+  return __uint_as_float((__float_as_uint(s) & ~15u) | (uint32_t)e);
+}
+
 template <int R>
-__global__ __launch_bounds__(RQ_THREADS) void k_rvq(RvqArgs a) {
+__global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_rvq(RvqArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature (launch stub)
   constexpr int NK16 = R / 16;
   constexpr int CPR = R / 8;                       // 16 B chunks per codeword row
-  constexpr int CBLK = RQ_CW * CPR / 64 / 4;       // 1 KiB DMA blocks per wave per stage
-  constexpr int LOADS = CBLK + 1;                  // + the wave's meta copy
+  constexpr int LOADS = rq_blocks<R>() + 1;        // DMA blocks per wave per stage + the norms
   __shared__ __attribute__((aligned(1024))) RqStage<R> S0;
   __shared__ __attribute__((aligned(1024))) RqStage<R> S1;
   __shared__ __attribute__((aligned(1024))) RqStage<R> S2;
@@ -69,6 +90,7 @@ __global__ __launch_bounds__(RQ_THREADS) void k_rvq(RvqArgs a) {
   __shared__ int cand_cnt[RQ_TOK];
   __shared__ uint16_t cand[RQ_TOK][RQ_CAP];
   __shared__ int amb_s[RQ_TOK];
+  __shared__ float red_s[4];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
   const int tl = wave * 32 + (lane & 31);  // token within the workgroup
@@ -77,147 +99,209 @@ __global__ __launch_bounds__(RQ_THREADS) void k_rvq(RvqArgs a) {
   const int nchunks = (a.K + RQ_CW - 1) / RQ_CW;
   const int total = (nchunks + 2) / 3 * 3;       // padded: stage buffers repeat every pass
 
-  // DMA geometry (codeword chunk): lane i of block b writes row b*rpb + i/CPR,
-  // physical chunk i%CPR holding logical chunk (i%CPR) ^ (row & 15 & (CPR-1)):
-  // 16 consecutive rows read one logical chunk from 16 different bank groups.
-  constexpr int RPB = 64 / CPR;
+  // DMA geometry: LDS byte 1024 b + 16 i of a stage (lane i of block b)
+  // holds 16 B column chunk `ch` of codeword row `row` of the chunk, or a
+  // padding slot (zeros).  Per lane the global offset is fixed up to the
+  // chunk's base, so it is computed once.
+  constexpr int RB = rq_row_bytes<R>();
+  constexpr int CBLK = rq_blocks<R>();
   uint32_t c_off[CBLK];
 #pragma unroll
   for (int jb = 0; jb < CBLK; ++jb) {
-    const int b = wave * CBLK + jb;
-    const int row = b * RPB + lane / CPR;
-    const int lch = (lane % CPR) ^ (row & 15 & (CPR - 1));
-    c_off[jb] = (uint32_t)row * (uint32_t)(R * 2) + (uint32_t)lch * 16u;
+    const int byte = (wave * CBLK + jb) * 1024 + lane * 16;
+    const int row = byte / RB, ch = (byte % RB) / 16;
+    c_off[jb] = (row < RQ_CW && ch < CPR) ? (uint32_t)row * (uint32_t)(R * 2) + (uint32_t)ch * 16u : RQ_OOB;
+  }
+
+  // fp32 residual of the lane's token, columns 16 s + 8 (lane / 32) + 0..7:
+  // R_0 = Z0, R_{l+1} = R_l - C_l[code_l] (the same operation sequence as
+  // rebuilding it from Z0 and the codes)
+  float res[NK16][8];
+#pragma unroll
+  for (int s = 0; s < NK16; ++s) {
+    float4 z0 = make_float4(0.f, 0.f, 0.f, 0.f), z1 = z0;
+    if (valid) {
+      const float4* zp = (const float4*)(a.Z0 + (int64_t)t * R + 16 * s + 8 * half);
+      z0 = zp[0];
+      z1 = zp[1];
+    }
+    res[s][0] = z0.x; res[s][1] = z0.y; res[s][2] = z0.z; res[s][3] = z0.w;
+    res[s][4] = z1.x; res[s][5] = z1.y; res[s][6] = z1.z; res[s][7] = z1.w;
   }
 
   for (int l = 0; l < a.L; ++l) {
     const __amdgpu_buffer_rsrc_t rc = rq_rsrc(a.Cb + (int64_t)l * a.K * R, (uint64_t)a.K * R * 2);
-    const __amdgpu_buffer_rsrc_t rm = rq_rsrc(a.meta + (int64_t)l * nchunks * 192, (uint64_t)nchunks * 192 * 4);
+    const float* n2g = a.meta + (int64_t)l * nchunks * 64;
+    const __amdgpu_buffer_rsrc_t rm = rq_rsrc(n2g, (uint64_t)nchunks * 64 * 4);
 
-    auto issue = [&](int q, bf16_t* sc, float* smeta) {
+    auto issue = [&](int q, bf16_t* sc, float* sn2) {
       const bool pad = q >= nchunks;
+      // rows past K read zeros through the resource bound (K % 32 == 0)
 #pragma unroll
-      for (int jb = 0; jb < CBLK; ++jb) {
-        const int row = (wave * CBLK + jb) * RPB + lane / CPR;
-        const bool ok = !pad && q * RQ_CW + row < a.K;
+      for (int jb = 0; jb < CBLK; ++jb)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (rq_lds_ptr)(sc + (wave * CBLK + jb) * 512), 16,
-                                                 ok ? (uint32_t)(q * RQ_CW) * (uint32_t)(R * 2) + c_off[jb] : RQ_OOB,
+                                                 (!pad && c_off[jb] != RQ_OOB)
+                                                     ? (uint32_t)(q * RQ_CW) * (uint32_t)(R * 2) + c_off[jb]
+                                                     : RQ_OOB,
                                                  0, 0, 0);
-      }
-      // 768 B of constants: lanes 0..47 carry 16 B each, the rest read zeros
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (rq_lds_ptr)(smeta + wave * 256), 16,
-                                               (!pad && lane < 48) ? (uint32_t)q * 768u + (uint32_t)lane * 16u
+      // 256 B of norms: lanes 0..15 carry 16 B each, the rest read zeros
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (rq_lds_ptr)(sn2 + wave * 256), 16,
+                                               (!pad && lane < 16) ? (uint32_t)q * 256u + (uint32_t)lane * 16u
                                                                    : RQ_OOB,
                                                0, 0, 0);
     };
 
-    // ---- residual R_l in fp32 (B-fragment layout), its bf16 image and norm;
-    // the first two codebook chunks are already in flight meanwhile
-    issue(0, S0.c, &S0.meta[0][0]);
-    issue(1, S1.c, &S1.meta[0][0]);
+    // ---- the first two chunks are in flight while the residual is built
+    issue(0, S0.c, &S0.n2[0][0]);
+    issue(1, S1.c, &S1.n2[0][0]);
+
+    // largest ||C_j||^2 of the round (entries past K are zero)
+    float n2max = 0.f;
+    for (int j = tid; j < nchunks * 64; j += RQ_THREADS) n2max = fmaxf(n2max, n2g[j]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) n2max = fmaxf(n2max, __shfl_xor(n2max, o, WAVE));
+    if (lane == 0) red_s[wave] = n2max;
+
+    // bf16(-2 R_l) in B-fragment layout and ||R_l||^2 from the fp32 residual
     uint4 rb[NK16];
     float rn2 = 0.f;
 #pragma unroll
     for (int s = 0; s < NK16; ++s) {
-      float v[8];
-      const int c0 = 16 * s + 8 * half;
-      if (valid) {
-        const float4* zp = (const float4*)(a.Z0 + (int64_t)t * R + c0);
-        float4 z0 = zp[0], z1 = zp[1];
-        v[0] = z0.x; v[1] = z0.y; v[2] = z0.z; v[3] = z0.w;
-        v[4] = z1.x; v[5] = z1.y; v[6] = z1.z; v[7] = z1.w;
-        for (int i = 0; i < l; ++i) {
-          const float4* cw = (const float4*)(a.C + ((int64_t)i * a.K + codes_s[tl][i]) * R + c0);
-          const float4 p0 = cw[0], p1 = cw[1];
-          v[0] -= p0.x; v[1] -= p0.y; v[2] -= p0.z; v[3] -= p0.w;
-          v[4] -= p1.x; v[5] -= p1.y; v[6] -= p1.z; v[7] -= p1.w;
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = 0.f;
-      }
+      const float* v = res[s];
 #pragma unroll
       for (int e = 0; e < 8; ++e) rn2 += v[e] * v[e];
-      rb[s] = make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7]));
+      rb[s] = make_uint4(pack_bf2(-2.f * v[0], -2.f * v[1]), pack_bf2(-2.f * v[2], -2.f * v[3]),
+                         pack_bf2(-2.f * v[4], -2.f * v[5]), pack_bf2(-2.f * v[6], -2.f * v[7]));
     }
     rn2 += __shfl_xor(rn2, 32, WAVE);
-    const float kappa = rvq_margin_k1(R) * sqrtf(rn2) * 1.0001f;
+    __syncthreads();  // red_s
+    n2max = fmaxf(fmaxf(red_s[0], red_s[1]), fmaxf(red_s[2], red_s[3]));
+    const float delta =
+        rvq_margin_k1(R) * sqrtf(rn2) * sqrtf(n2max) * 1.0002f + rvq_margin_k2(R) * n2max + 1e-30f;
 
-    // One screening pass over all chunks; fn(j, score, margin) per codeword.
-    auto pass = [&](auto&& fn, bool first) {
+    // One screening pass over all chunks.  Per 32-codeword tile the fold
+    // callbacks see begin(), score(acc, tile, e) for e = 0..15, end(tile).
+    // Software pipeline per 64-codeword chunk (asm LDS reads, see
+    // lds_read_b128; sched_barrier keeps the interleave):
+    //   reads(tile 0) | fold(last tile of the previous chunk) | wait
+    //   tile 0 products, each followed by a share of the reads of tile 1
+    //   wait | tile 1 products, each followed by a share of the fold of tile 0
+    // Reads of an invalid second tile (K % 64 == 32) hit zero-filled rows and
+    // are discarded.
+    constexpr int NR = NK16 + 4;                 // 128-bit reads per tile
+    constexpr int RPS = (NR + NK16 - 1) / NK16;  // reads per product step
+    constexpr int FPS = 16 / NK16;               // scores folded per product step
+    auto pass = [&](auto&& fbegin, auto&& fscore, auto&& fend, bool first) {
       if (!first) {
-        issue(0, S0.c, &S0.meta[0][0]);
-        issue(1, S1.c, &S1.meta[0][0]);
+        issue(0, S0.c, &S0.n2[0][0]);
+        issue(1, S1.c, &S1.n2[0][0]);
       }
-      auto stage = [&](int q, const bf16_t* sc, const float* smeta, bf16_t* nc, float* nmeta) {
+      f32x16_t pend;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) pend[e] = 3.0e38f;
+      int pend_tile = -1;
+      auto fold_all = [&](const f32x16_t& acc, int tile) {
+        fbegin();
+        static_for<0, 16>([&](auto ec) { fscore(acc, tile, ec); });
+        fend(tile);
+      };
+      auto stage = [&](int q, const bf16_t* sc, const float* sn2, bf16_t* nc, float* nn2) {
         if (q + 1 < total)
           asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS) : "memory");
         else
           asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __builtin_amdgcn_s_barrier();
-        if (q + 2 < total) issue(q + 2, nc, nmeta);
+        if (q + 2 < total) issue(q + 2, nc, nn2);
         if (q >= nchunks) return;
-        const float* mw = smeta + wave * 256;
-#pragma unroll
-        for (int ct = 0; ct < RQ_CW / 32; ++ct) {
-          if (q * RQ_CW + ct * 32 >= a.K) continue;  // K % 32 == 0: whole tile valid or not
-          f32x16_t acc = f32x16_t{};
-#pragma unroll
-          for (int s = 0; s < NK16; ++s) {
-            const int row = ct * 32 + (lane & 31);
-            const int lch = (2 * s + half) ^ (row & 15 & (CPR - 1));
-            const uint4 af = *(const uint4*)(sc + row * R + lch * 8);
-            acc = mfma32x32x16(af, rb[s], acc);
-          }
+        const bool t1ok = q * RQ_CW + 32 < a.K;
+        // rows lane % 32 of a tile, 16 B chunk 2s + lane / 32; the lane's
+        // norms are rows 8 e4 + 4 (lane / 32) + 0..3
+        const uint32_t cbase = lds_addr(sc) + (lane & 31) * RB + half * 16;
+        const uint32_t nbase = lds_addr(sn2 + wave * 256) + half * 16;
+        u32x4 f0[NR], f1[NR];  // [0..3] norms, [4..] codeword fragments
+        auto read = [&](auto ctc, auto rc, u32x4(&f)[NR]) {
+          constexpr int CT = decltype(ctc)::value, RI = decltype(rc)::value;
+          if constexpr (RI < 4)
+            f[RI] = lds_read_b128<CT * 128 + 32 * RI>(nbase);
+          else if constexpr (RI < NR)
+            f[RI] = lds_read_b128<CT * 32 * RB + 32 * (RI - 4)>(cbase);
+        };
+        auto init = [&](const u32x4(&f)[NR]) {
+          f32x16_t acc;
 #pragma unroll
           for (int e4 = 0; e4 < 4; ++e4) {
-            const int jl0 = ct * 32 + 8 * e4 + 4 * half;  // rows jl0..jl0+3 of this lane
-            const float4 n2 = *(const float4*)(mw + jl0);
-            const float4 cr = *(const float4*)(mw + 64 + jl0);
-            const float4 nk = *(const float4*)(mw + 128 + jl0);
-            const float n2v[4] = {n2.x, n2.y, n2.z, n2.w}, crv[4] = {cr.x, cr.y, cr.z, cr.w},
-                        nkv[4] = {nk.x, nk.y, nk.z, nk.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float sc2 = fmaf(-2.f, acc[4 * e4 + e], n2v[e]);
-              const float dl = fmaf(kappa, crv[e], nkv[e]);
-              fn(q * RQ_CW + jl0 + e, sc2, dl);
-            }
+            acc[4 * e4] = __uint_as_float(f[e4].x);
+            acc[4 * e4 + 1] = __uint_as_float(f[e4].y);
+            acc[4 * e4 + 2] = __uint_as_float(f[e4].z);
+            acc[4 * e4 + 3] = __uint_as_float(f[e4].w);
           }
+          return acc;
+        };
+        static_for<0, NR>([&](auto rc) { read(std::integral_constant<int, 0>{}, rc, f0); });
+        fold_all(pend, pend_tile);
+        lds_wait0();
+        reg_pin(f0);
+        f32x16_t acc0 = init(f0);
+        static_for<0, NK16>([&](auto sc2) {
+          constexpr int S = decltype(sc2)::value;
+          acc0 = mfma32x32x16(as_uint4(f0[4 + S]), rb[S], acc0);
+          __builtin_amdgcn_sched_barrier(0);
+          static_for<S * RPS, (S + 1) * RPS>([&](auto rc) { read(std::integral_constant<int, 1>{}, rc, f1); });
+          __builtin_amdgcn_sched_barrier(0);
+        });
+        lds_wait0();
+        reg_pin(f1);
+        if (t1ok) {
+          f32x16_t acc1 = init(f1);
+          fbegin();
+          static_for<0, NK16>([&](auto sc2) {
+            constexpr int S = decltype(sc2)::value;
+            acc1 = mfma32x32x16(as_uint4(f1[4 + S]), rb[S], acc1);
+            __builtin_amdgcn_sched_barrier(0);
+            static_for<S * FPS, (S + 1) * FPS>([&](auto ec) { fscore(acc0, 2 * q, ec); });
+            __builtin_amdgcn_sched_barrier(0);
+          });
+          fend(2 * q);
+          pend = acc1;
+          pend_tile = 2 * q + 1;
+        } else {
+          fold_all(acc0, 2 * q);
+#pragma unroll
+          for (int e = 0; e < 16; ++e) pend[e] = 3.0e38f;
+          pend_tile = -1;
         }
       };
       for (int q = 0; q < total; q += 3) {
-        stage(q, S0.c, &S0.meta[0][0], S2.c, &S2.meta[0][0]);
-        stage(q + 1, S1.c, &S1.meta[0][0], S0.c, &S0.meta[0][0]);
-        stage(q + 2, S2.c, &S2.meta[0][0], S1.c, &S1.meta[0][0]);
+        stage(q, S0.c, &S0.n2[0][0], S2.c, &S2.n2[0][0]);
+        stage(q + 1, S1.c, &S1.n2[0][0], S0.c, &S0.n2[0][0]);
+        stage(q + 2, S2.c, &S2.n2[0][0], S1.c, &S1.n2[0][0]);
       }
+      fold_all(pend, pend_tile);
     };
 
-    // ---- pass 1
-    float ub_min = INFINITY, lb1 = INFINITY, lb2 = INFINITY;
-    int j1 = 0;
-    pass(
-        [&](int j, float sc, float dl) {
-          const float ub = sc + dl, lb = sc - dl;
-          ub_min = fminf(ub_min, ub);
-          lb2 = fminf(lb2, fmaxf(lb1, lb));
-          const bool better = lb < lb1;
-          j1 = better ? j : j1;
-          lb1 = fminf(lb1, lb);
-        },
-        true);
+    // ---- pass 1: smallest and second-smallest tagged score per lane
+    float m1 = INFINITY, m2 = INFINITY, m1_in = INFINITY;
+    int tile1 = 0;
+    pass([&]() { m1_in = m1; },
+         [&](const f32x16_t& acc, int, auto ec) {
+           constexpr int E = decltype(ec)::value;
+           const float key = rq_tag(acc[E], E);
+           m2 = __builtin_amdgcn_fmed3f(m1, m2, key);
+           m1 = __builtin_amdgcn_fmed3f(m1, key, -3.40282347e38f);  // min for finite keys
+         },
+         [&](int tile) { tile1 = m1 < m1_in ? tile : tile1; }, true);
+    int j1 = tile1 * 32 + rq_row((int)(__float_as_uint(m1) & 15u), half);
     {
-      const float o_ub = __shfl_xor(ub_min, 32, WAVE);
-      const float o_lb1 = __shfl_xor(lb1, 32, WAVE);
-      const float o_lb2 = __shfl_xor(lb2, 32, WAVE);
+      const float o_m1 = __shfl_xor(m1, 32, WAVE);
+      const float o_m2 = __shfl_xor(m2, 32, WAVE);
       const int o_j1 = __shfl_xor(j1, 32, WAVE);
-      ub_min = fminf(ub_min, o_ub);
-      const float nlb2 = fminf(fmaxf(lb1, o_lb1), fminf(lb2, o_lb2));
-      if (o_lb1 < lb1 || (o_lb1 == lb1 && o_j1 < j1)) j1 = o_j1;
-      lb1 = fminf(lb1, o_lb1);
-      lb2 = nlb2;
+      const float nm2 = fminf(fmaxf(m1, o_m1), fminf(m2, o_m2));
+      if (o_m1 < m1 || (o_m1 == m1 && o_j1 < j1)) j1 = o_j1;
+      m1 = fminf(m1, o_m1);
+      m2 = nm2;
     }
-    const bool amb = valid && !(lb2 > ub_min);
+    const float thr = m1 + 2.0002f * delta;
+    const bool amb = valid && !(m2 > thr);
     if (half == 0) {
       amb_s[tl] = amb ? 1 : 0;
       cand_cnt[tl] = 0;
@@ -227,15 +311,15 @@ __global__ __launch_bounds__(RQ_THREADS) void k_rvq(RvqArgs a) {
     int jstar = j1;
     if (any_amb) {
       // ---- pass 2: list every candidate of the ambiguous tokens
-      const float ustar = ub_min;
-      pass(
-          [&](int j, float sc, float dl) {
-            if (amb && sc - dl <= ustar) {
-              const int idx = atomicAdd(&cand_cnt[tl], 1);
-              if (idx < RQ_CAP) cand[tl][idx] = (uint16_t)j;
-            }
-          },
-          false);
+      pass([&]() {},
+           [&](const f32x16_t& acc, int tile, auto ec) {
+             constexpr int E = decltype(ec)::value;
+             if (amb && tile >= 0 && rq_tag(acc[E], E) <= thr) {
+               const int idx = atomicAdd(&cand_cnt[tl], 1);
+               if (idx < RQ_CAP) cand[tl][idx] = (uint16_t)(tile * 32 + rq_row(E, half));
+             }
+           },
+           [&](int) {}, false);
       // ---- exact fp32 rescoring, one wave per token of its own 32
       for (int u = 0; u < 32; ++u) {
         const int tu = wave * 32 + u;
@@ -293,6 +377,18 @@ __global__ __launch_bounds__(RQ_THREADS) void k_rvq(RvqArgs a) {
       }
       __syncthreads();
       if (amb) jstar = cand_cnt[tl];
+    }
+    if (jstar < 0 || jstar >= a.K) jstar = 0;  // only reachable with non-finite inputs
+    if (l + 1 < a.L) {
+      const float* cw = a.C + ((int64_t)l * a.K + jstar) * R + 8 * half;
+#pragma unroll
+      for (int s = 0; s < NK16; ++s) {
+        const float4 p0 = *(const float4*)(cw + 16 * s), p1 = *(const float4*)(cw + 16 * s + 4);
+        if (valid) {
+          res[s][0] -= p0.x; res[s][1] -= p0.y; res[s][2] -= p0.z; res[s][3] -= p0.w;
+          res[s][4] -= p1.x; res[s][5] -= p1.y; res[s][6] -= p1.z; res[s][7] -= p1.w;
+        }
+      }
     }
     if (half == 0 && valid) {
       codes_s[tl][l] = (uint16_t)jstar;

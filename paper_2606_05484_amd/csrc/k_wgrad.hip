@@ -44,12 +44,6 @@ __device__ __forceinline__ int wg_sw(int row, int cpr) { return (4 * (row & 3)) 
 // drain all of those first.  The caller completes them with tr_wait(),
 // whose in/out operands keep every use of the fragments after the wait;
 // stage completion itself is guaranteed by the pipeline's vmcnt + barrier.
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-
 __device__ __forceinline__ u32x4 tr_frag(const bf16_t* tile, int cpr, int k0, int col0, int lane) {
   const int g = lane >> 4, sidx = lane & 15, j = sidx >> 2, q = sidx & 3;
   const int col = col0 + 16 * (g & 1) + 4 * q;

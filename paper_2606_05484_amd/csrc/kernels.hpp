@@ -80,10 +80,10 @@ hipError_t launch_prep_u(const float* U, int d, int r, bf16_t* Ub, int64_t ldub,
 // or bf16 source.
 hipError_t launch_transpose_into(const void* src, int src_f32, int rows, int cols, int64_t lds,
                                  float scale, bf16_t* dst, int64_t ldd, int off, hipStream_t s);
-// Cb[l][j][c] = bf16(C[l][j][c]); meta: per 64-codeword chunk, the arrays
-// ||C_j||^2, ||C_j|| and rvq_margin_k2(r) ||C_j||^2 (zero past K).
+// Cb[l][j][c] = bf16(C[l][j][c]); meta[l][chunk][64]: ||C_j||^2 in fp32 per
+// 64-codeword chunk (zero past K).
 hipError_t launch_prep_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* meta, hipStream_t s);
-inline int64_t rvq_meta_floats(int L, int K) { return (int64_t)L * ((K + 63) / 64) * 192; }
+inline int64_t rvq_meta_floats(int L, int K) { return (int64_t)L * ((K + 63) / 64) * 64; }
 
 // ---------------------------------------------------------------- receiver-side operand
 // out[t][0:r]   = Zhat[t]: payload row (bf16) or sum_l C[l][codes[t,l]] (fp32 -> bf16)
@@ -108,7 +108,7 @@ struct RvqArgs {
   const float* Z0;     // [T,r] fp32 unquantised coordinates
   const bf16_t* Cb;    // [L,K,r] bf16 screening copy
   const float* C;      // [L,K,r] fp32 codebooks
-  const float* meta;   // [L][ceil(K/64)][3][64]: ||C||^2, ||C||, k2 ||C||^2 (rvq_meta_floats)
+  const float* meta;   // [L][ceil(K/64)][64]: ||C_j||^2 (rvq_meta_floats)
   int T, r, L, K;
   void* codes; int code_bytes;  // [T,L]
   int* stats;          // [4] optional counters (candidates, overflow), may be null
