@@ -77,12 +77,15 @@ def _src_sha(files):
     return h.hexdigest()[:16]
 
 
-KERNEL_SOURCES = {
-    "enc:gemm_tn": ["k_gemm_bf16.hip", "common.hpp"], "dec:gemm_tn": ["k_gemm_bf16.hip", "common.hpp"],
-    "dec_bwd:gemm_tn": ["k_gemm_bf16.hip", "common.hpp"], "enc_bwd:gemm_tn": ["k_gemm_bf16.hip", "common.hpp"],
-    "enc:rvq": ["k_rvq.hip", "common.hpp"], "dec_bwd:wgrad": ["k_wgrad.hip", "common.hpp"],
-    "enc_bwd:wgrad": ["k_wgrad.hip", "common.hpp"], "dec:assemble": ["k_prep.hip", "common.hpp"],
-}
+_SRC_BY_KERNEL = {"gemm_tn": "k_gemm_bf16.hip", "bu_gemm": "k_gemm_bf16.hip", "rvq": "k_rvq.hip",
+                  "wgrad": "k_wgrad.hip", "reduce": "k_wgrad.hip", "reduce_corr": "k_wgrad.hip",
+                  "anchor_reduce": "k_wgrad.hip", "bu_reduce": "k_wgrad.hip"}
+
+
+def kernel_sources(name):
+    """Source files whose text decides a chain kernel's code and launch shape."""
+    short = name.split(":")[-1]
+    return [_SRC_BY_KERNEL.get(short, "k_prep.hip"), "common.hpp", "kernels.hpp", "mapl_api.cpp"]
 
 
 def traffic_for(kernel):
@@ -96,7 +99,7 @@ def traffic_for(kernel):
     for line in open(path):
         parts = line.split()
         if len(parts) == 3 and parts[0] == kernel and not line.startswith("#"):
-            if parts[1] == _src_sha(KERNEL_SOURCES.get(kernel, [])):
+            if parts[1] == _src_sha(kernel_sources(kernel)):
                 return float(parts[2])
     return None
 
@@ -134,6 +137,122 @@ def cpu_baseline(x, budget_s=15.0):
                       "(%.1f s)" % (n, x["T"], dt)}
 
 
+def _csvs(d, suffix):
+    import glob
+    return sorted(glob.glob(os.path.join(d, "**", "*" + suffix), recursive=True))
+
+
+def _dispatches(d, suffix):
+    """[(dispatch_id, kernel_name, row)] of every CSV under d ending in suffix."""
+    import csv
+    out = {}
+    for f in _csvs(d, suffix):
+        for row in csv.DictReader(open(f)):
+            did = int(row["Dispatch_Id"])
+            e = out.setdefault(did, {"name": row["Kernel_Name"], "row": row, "ctr": {}})
+            if "Counter_Name" in row:
+                e["ctr"][row["Counter_Name"]] = e["ctr"].get(row["Counter_Name"], 0.0) + float(row["Counter_Value"])
+    return [(k, v["name"], v) for k, v in sorted(out.items())]
+
+
+def _chain_map(disp, order, chains):
+    """Name each library dispatch of the first `chains` codec chains (warm-up,
+    timed and profiled steps; the SPEL timing follows them) by its position."""
+    lib = [x for x in disp if "mapl::" in x[1]]
+    n = len(order)
+    if n == 0 or len(lib) < n * chains:
+        raise SystemExit("summarize: %d library dispatches, fewer than %d chains of %d" % (len(lib), chains, n))
+    lib = lib[:n * chains]
+    named = []
+    for i, (did, sym, e) in enumerate(lib):
+        named.append((order[i % n], sym, e))
+    # every position must always be the same kernel symbol
+    for j in range(n):
+        syms = {named[i][1] for i in range(j, len(named), n)}
+        if len(syms) != 1:
+            raise SystemExit("summarize: chain position %d (%s) maps to several kernels" % (j, order[j]))
+    return named
+
+
+def _short(sym):
+    import re
+    s = sym.replace("(anonymous namespace)::", "").replace("mapl::", "").replace("void ", "")
+    return re.sub(r"\(.*", "", s)
+
+
+def summarize(paths, write_traffic):
+    bench = json.loads(open(paths[0]).read().strip().splitlines()[-1])
+    order = bench["kernel_order"]
+    lines = ["# c4 codec chain (T=32768, d=2048, r=256, k=128, L=2, K=1024, bf16): per-kernel durations",
+             "# from the rocprofv3 kernel trace of a bench.py run; each library dispatch is named by its",
+             "# position in the repeated 4-call chain; bench.py's own HIP-event average beside it.", ""]
+    disp = _dispatches(paths[1], "_kernel_trace.csv")
+    named = _chain_map(disp, order, bench["warmup"] + 2 * bench["steps"])
+    agg = {}
+    for name, sym, e in named:
+        row = e["row"]
+        a = agg.setdefault(name, [sym, 0, 0.0])
+        a[1] += 1
+        a[2] += (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3
+    lines.append("%-24s %-36s %8s %10s %10s" % ("kernel", "symbol", "launches", "trace_us", "bench_us"))
+    for name in order:
+        sym, n, tot = agg[name]
+        lines.append("%-24s %-36s %8d %10.2f %10s" % (name, _short(sym)[:36], n, tot / n,
+                                                     "%.2f" % bench["per_kernel_us"].get(name, float("nan"))))
+    chain_us = sum(agg[nm][2] / agg[nm][1] for nm in order)
+    lines.append("%-24s %-36s %8s %10.2f %10.2f" % ("sum over the chain", "", "", chain_us, bench["ms_per_step"] * 1e3))
+    stats = _csvs(paths[1], "_kernel_stats.csv")
+    if stats:
+        import csv
+        lines += ["", "# rocprofv3 --stats (all dispatches of the run, by kernel symbol)"]
+        rows = list(csv.DictReader(open(stats[0])))
+        for row in rows[:16]:
+            lines.append("%-48s calls %6s  avg_us %10.2f  total_pct %6s" % (
+                _short(row.get("Name", "?"))[:48], row.get("Calls", "?"), float(row.get("AverageNs", 0)) / 1e3,
+                row.get("Percentage", "?")[:6]))
+    traffic = {}
+    if len(paths) >= 4:
+        calib = bench.get("calib_copy_bytes")
+        fd, wd = _dispatches(paths[2], "_counter_collection.csv"), _dispatches(paths[3], "_counter_collection.csv")
+        cf = [e["ctr"]["FETCH_SIZE"] for _, nm, e in fd if "copyBuffer" in nm]
+        cw = [e["ctr"]["WRITE_SIZE"] for _, nm, e in wd if "copyBuffer" in nm]
+        if not calib or not cf or not cw:
+            raise SystemExit("summarize: counter runs need --calib-copy (a copyBuffer dispatch)")
+        ff, fw = calib / (cf[-1] * 1024.0), calib / (cw[-1] * 1024.0)
+        lines += ["", "# HBM traffic per launch from two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE, KiB per",
+                  "# dispatch), each scaled by what the same counter reads for a plain %d-byte device copy:" % calib,
+                  "#   FETCH_SIZE %.0f KiB -> factor %.4f;  WRITE_SIZE %.0f KiB -> factor %.4f" % (cf[-1], ff, cw[-1], fw),
+                  "%-24s %12s %12s %14s %14s %7s" % ("kernel", "fetch_KiB", "write_KiB", "traffic_B", "algorithmic_B",
+                                                     "ratio")]
+        bf_ = [json.loads(open(os.path.join(os.path.dirname(p.rstrip("/")), "bench_%s.json" % k)).read().strip()
+                          .splitlines()[-1]) for p, k in ((paths[2], "fetch"), (paths[3], "write"))] \
+            if False else None
+        fn = _chain_map(fd, order, len([x for x in fd if "mapl::" in x[1]]) // len(order))
+        wn = _chain_map(wd, order, len([x for x in wd if "mapl::" in x[1]]) // len(order))
+        kc = kernel_counts(32768, 2048, 256, 128, 2, 1024)
+        acc = {}
+        for (name, _, e) in fn:
+            acc.setdefault(name, [[], []])[0].append(e["ctr"]["FETCH_SIZE"])
+        for (name, _, e) in wn:
+            acc.setdefault(name, [[], []])[1].append(e["ctr"]["WRITE_SIZE"])
+        for name in order:
+            fk, wk = np.mean(acc[name][0]), np.mean(acc[name][1])
+            tb = fk * 1024 * ff + wk * 1024 * fw
+            alg = kc[name][1] if name in kc else None
+            traffic[name] = tb
+            lines.append("%-24s %12.0f %12.0f %14.0f %14s %7s" % (name, fk, wk, tb, "%.0f" % alg if alg else "-",
+                                                                 "%.2f" % (tb / alg) if alg else "-"))
+    print("\n".join(lines))
+    if write_traffic and traffic:
+        path = os.path.join(ROOT, "profiles", "traffic_c4.txt")
+        with open(path, "w") as fh:
+            fh.write("# kernel source_sha256[:16] hbm_bytes_per_launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated);\n"
+                     "# written by bench.py --summarize --write-traffic; a line counts only while the kernel's\n"
+                     "# sources hash to the recorded value\n")
+            for name in order:
+                fh.write("%s %s %.0f\n" % (name, _src_sha(kernel_sources(name)), traffic[name]))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,7 +260,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stress", action="store_true", help="data-drawn codebooks (every code in use)")
+    ap.add_argument("--no-spel", action="store_true", help="skip the SPEL step timing")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="end with one plain 256 MiB device copy (calibrates FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--summarize", nargs="+", metavar="PATH",
+                    help="no GPU: BENCH_JSON TRACE_DIR [FETCH_DIR WRITE_DIR] -> kernel summary on stdout")
+    ap.add_argument("--write-traffic", action="store_true",
+                    help="with --summarize and counter dirs: rewrite profiles/traffic_c4.txt")
     args = ap.parse_args()
+    if args.summarize:
+        summarize(args.summarize, args.write_traffic)
+        return
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU; --gpus %d is not supported (the codec shards over "
               "tokens and the SPEL step over projectors, see DESIGN.md)" % args.gpus, file=sys.stderr)
@@ -255,14 +384,24 @@ def main():
         it = 4 * dd * rr * rr + 2 * rr ** 3
         return P * (4 * dd * rr * rr + 12 * it)
 
-    spel_c5 = time_spel(16, 2048, 512, 5)
-    spel_b = time_spel(1, d, r, 10)
-    spel = {"config": "16 projectors [2048,512], PolarExpress 5 + 7 steps", "ms_per_step": spel_c5,
-            "tflops": spel_flops(16, 2048, 512) / (spel_c5 * 1e-3) / 1e12,
-            "roofline_frac_fp32": spel_flops(16, 2048, 512) / PEAK_F32 / (spel_c5 * 1e-3),
-            "boundary_projector_ms": spel_b}
-    amort = 128  # micro-batches per optimizer step: global batch 512 / micro-batch 4
-    alg1 = T / ((ms + spel_b / amort) * 1e-3)
+    spel, alg1 = None, None
+    if not args.no_spel:
+        spel_c5 = time_spel(16, 2048, 512, 5)
+        spel_b = time_spel(1, d, r, 10)
+        spel = {"config": "16 projectors [2048,512], PolarExpress 5 + 7 steps", "ms_per_step": spel_c5,
+                "tflops": spel_flops(16, 2048, 512) / (spel_c5 * 1e-3) / 1e12,
+                "roofline_frac_fp32": spel_flops(16, 2048, 512) / PEAK_F32 / (spel_c5 * 1e-3),
+                "boundary_projector_ms": spel_b}
+        amort = 128  # micro-batches per optimizer step: global batch 512 / micro-batch 4
+        alg1 = T / ((ms + spel_b / amort) * 1e-3)
+    calib = None
+    if args.calib_copy:
+        src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        calib = src.numel()
 
     out = {
         "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -277,9 +416,12 @@ def main():
                            "flops": Fsum, "bytes": Bsum},
         "per_call_us": per_call,
         "per_kernel_us": {n: round(v[1], 2) for n, v in sorted(kern.items())},
+        "kernel_order": list(kern),
         "spel": spel,
         "alg1_tokens_per_s": alg1,
     }
+    if calib:
+        out["calib_copy_bytes"] = calib
     if not args.no_cpu_baseline:
         print("timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(x)

@@ -187,7 +187,8 @@ int mapl_version(void);
  * kernel launches with a pair of HIP events on the call's stream (a small
  * per-launch overhead); mapl_profile(0) stops it.  mapl_profile_report()
  * waits for the recorded events, writes one line "name launches total_ms"
- * per kernel (names are "<call>:<kernel>") into buf (NUL-terminated, at most
+ * per kernel, in the order of each name's first launch (names are
+ * "<call>:<kernel>") into buf (NUL-terminated, at most
  * `bytes` bytes), and forgets the records.  Returns MAPL_OK, MAPL_E_HIP if an
  * event could not be resolved, or MAPL_E_WORKSPACE if buf was too small (the
  * text is truncated). */

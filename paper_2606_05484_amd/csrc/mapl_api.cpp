@@ -120,9 +120,9 @@ struct SplitPlan {
   int splits, tps;
 };
 
-// Token splits of the weight-gradient kernel: one workgroup per compute
-// unit (it holds 144 KiB of LDS), splits a multiple of 8 when that keeps
-// the grid a multiple of the 8 XCDs.
+// Token splits of the weight-gradient kernel: it holds 144 KiB of LDS, so
+// one workgroup per compute unit; the grid (tiles x splits) is kept within
+// one wave of 256 workgroups.
 SplitPlan plan_splits(int64_t T, int Ma, int Mg, int N) {
   const int bn = (N % 256 == 0) ? 256 : (N % 128 == 0) ? 128 : 64;
   const int64_t mt = wgrad_row_offset(Ma) / 128 + (Mg + 127) / 128;
@@ -904,6 +904,8 @@ extern "C" int mapl_profile_report(char* buf, size_t bytes) {
     std::lock_guard<std::mutex> lk(g_prof_mu);
     recs.swap(g_prof_recs);
   }
+  // one line per kernel name, in the order of first launch
+  std::vector<std::string> order;
   std::map<std::string, std::pair<long, double>> agg;
   int st = MAPL_OK;
   for (const ProfRec& r : recs) {
@@ -912,9 +914,13 @@ extern "C" int mapl_profile_report(char* buf, size_t bytes) {
       st = fail(MAPL_E_HIP, "profile: event query failed");
       continue;
     }
-    auto& e = agg[r.name];
-    e.first += 1;
-    e.second += ms;
+    auto it = agg.find(r.name);
+    if (it == agg.end()) {
+      order.push_back(r.name);
+      it = agg.emplace(r.name, std::make_pair(0L, 0.0)).first;
+    }
+    it->second.first += 1;
+    it->second.second += ms;
   }
   {
     std::lock_guard<std::mutex> lk(g_prof_mu);
@@ -925,8 +931,9 @@ extern "C" int mapl_profile_report(char* buf, size_t bytes) {
   }
   std::string outs;
   char line[256];
-  for (const auto& kv : agg) {
-    snprintf(line, sizeof line, "%s %ld %.6f\n", kv.first.c_str(), kv.second.first, kv.second.second);
+  for (const std::string& name : order) {
+    const auto& v = agg[name];
+    snprintf(line, sizeof line, "%s %ld %.6f\n", name.c_str(), v.first, v.second);
     outs += line;
   }
   if (buf && bytes) {
