@@ -84,15 +84,23 @@ __global__ __launch_bounds__(WG_THREADS) void k_wgrad(WgradArgs g, int mtiles, i
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int G = gridDim.x;
-  const int lin = blockIdx.x;
-  // workgroups of one token split land on one XCD (dispatch is round-robin
-  // over the 8 XCDs), so they share the split's Q rows in that XCD's L2
-  const int idx = xcd_map ? (lin % 8) * (G / 8) + lin / 8 : lin;
+  // Workgroup ids are dispatched round-robin over the 8 XCDs (id % 8).  The
+  // k-th workgroup of XCD x takes work item x q' + k (q' = its share), so
+  // every XCD owns a contiguous run of (split, m-tile, n-tile) items and the
+  // workgroups of a token split share its Q rows in one L2.
+  const int NY = gridDim.y;
+  const int Gt = gridDim.x * NY;
+  const int lin = blockIdx.x + blockIdx.y * gridDim.x;
+  int item = lin;
+  if (xcd_map) {
+    const int xcd = lin % 8, k = lin / 8, q = Gt / 8, rem = Gt % 8;
+    item = xcd < rem ? xcd * (q + 1) + k : rem * (q + 1) + (xcd - rem) * q + k;
+  }
+  const int ny = item % NY, idx = item / NY;
   const int split = idx / mtiles, mt = idx % mtiles;
   const int Mao = (g.Ma + WG_BM - 1) / WG_BM * WG_BM;
   const int m0 = mt * WG_BM;
-  const int n0 = blockIdx.y * BN;
+  const int n0 = ny * BN;
   const int t_begin = split * g.tokens_per_split;
   const int t_end = min(g.T, t_begin + g.tokens_per_split);
   const int KS = t_end > t_begin ? (t_end - t_begin + WG_KT - 1) / WG_KT : 0;
@@ -380,7 +388,7 @@ hipError_t launch_wgrad(const WgradArgs& g, hipStream_t s) {
   if (mtiles <= 0 || g.N <= 0) return hipSuccess;
   if (g.Ma % 8 || g.Mg % 8 || g.ldp % 8 || g.ldq % 8) return hipErrorInvalidValue;
   const int G = mtiles * g.splits;
-  const int xcd = G % 8 == 0 ? 1 : 0;
+  const int xcd = 1;
   if (g.N % 256 == 0) {
     hipLaunchKernelGGL(k_wgrad<256>, dim3(G, g.N / 256), dim3(WG_THREADS), 0, s, g, mtiles, xcd);
   } else if (g.N % 128 == 0) {
