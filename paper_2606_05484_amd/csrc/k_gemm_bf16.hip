@@ -63,7 +63,10 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
   constexpr int LOADS = ABLK + WBLK;            // buffer_load...lds per wave per stage
   __shared__ __attribute__((aligned(1024))) TnSmem<BN> S0;
   __shared__ __attribute__((aligned(1024))) TnSmem<BN> S1;
-  __shared__ __attribute__((aligned(1024))) TnSmem<NS == 3 ? BN : 64> S2;
+  // third stage (NS == 3 only; a token array otherwise)
+  __shared__ __attribute__((aligned(1024))) bf16_t S2buf[NS == 3 ? (GM + BN) * GK : 8];
+  bf16_t* const S2a = S2buf;
+  bf16_t* const S2w = S2buf + GM * GK;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -205,9 +208,9 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
     for (int ks = 0; ks < KSP; ks += NS) {
       const int s = tile * KSP + ks;
       if constexpr (NS == 3) {
-        step(s, ks, S0.a, S0.w, S2.a, S2.w);
+        step(s, ks, S0.a, S0.w, S2a, S2w);
         step(s + 1, ks + 1, S1.a, S1.w, S0.a, S0.w);
-        step(s + 2, ks + 2, S2.a, S2.w, S1.a, S1.w);
+        step(s + 2, ks + 2, S2a, S2w, S1.a, S1.w);
       } else {
         step(s, ks, S0.a, S0.w, S1.a, S1.w);
         step(s + 1, ks + 1, S1.a, S1.w, S0.a, S0.w);
@@ -248,7 +251,8 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
       constexpr int FJ = FN >= 2 ? 2 : 1;  // fragments per half
       constexpr int COLS = FJ * 32, CPR = COLS / 8;  // staged columns, 16 B chunks per row
       static_assert(4 * 64 * COLS <= GM * GK + BN * GK, "staging fits the stage buffer");
-      const uint32_t stg = lds_addr(S2.a) + wave * (64 * COLS * 2);
+      // the buffer consumed by the tile's last step: S2 (NS = 3) or S1 (NS = 2)
+      const uint32_t stg = lds_addr(NS == 3 ? S2a : S1.a) + wave * (64 * COLS * 2);
 #pragma unroll
       for (int h = 0; h < HALVES; ++h) {
 #pragma unroll
@@ -318,8 +322,11 @@ hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
 
 template <int BN>
 hipError_t launch_ns(const TnArgs& g, hipStream_t s) {
-  // three stages throughout; short K pads its step count to a multiple of
-  // three (padding steps only rotate the pipeline)
+  // Three stages, unless a short K would pad its step count (a multiple of
+  // the stage count) by a large fraction: then two.
+  const int kz = g.kz > 0 ? g.kz : g.Ka;
+  const int KS = (kz + GK - 1) / GK + (g.Kg + GK - 1) / GK;
+  if (KS % 3 != 0 && KS < 24 && KS % 2 == 0) return launch_bn<BN, 2>(g, s);
   return launch_bn<BN, 3>(g, s);
 }
 
