@@ -16,10 +16,11 @@ namespace {
 
 // 32x32 tiles through LDS so both the read of U and the write of U^T are
 // coalesced.
-__global__ void k_prep_u(const float* __restrict__ U, int d, int r, bf16_t* __restrict__ Ub,
-                         int64_t ldub, bf16_t* __restrict__ Ut, int64_t ldut) {
+__device__ __forceinline__ void prep_u_tile(int bx, int by, const float* __restrict__ U, int d, int r,
+                                            bf16_t* __restrict__ Ub, int64_t ldub, bf16_t* __restrict__ Ut,
+                                            int64_t ldut) {
   __shared__ bf16_t tile[32][33];
-  const int j0 = blockIdx.x * 32, c0 = blockIdx.y * 32;
+  const int j0 = bx * 32, c0 = by * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 256 threads: 32 x 8
   for (int y = ty; y < 32; y += 8) {
     const int j = j0 + y, c = c0 + tx;
@@ -37,11 +38,11 @@ __global__ void k_prep_u(const float* __restrict__ U, int d, int r, bf16_t* __re
   }
 }
 
-__global__ void k_transpose_into(const void* __restrict__ src, int src_f32, int rows, int cols,
-                                 int64_t lds, float scale, bf16_t* __restrict__ dst, int64_t ldd,
-                                 int off) {
+__device__ __forceinline__ void transpose_tile(int bx, int by, const void* __restrict__ src, int src_f32,
+                                               int rows, int cols, int64_t lds, float scale,
+                                               bf16_t* __restrict__ dst, int64_t ldd, int off) {
   __shared__ float tile[32][33];
-  const int i0 = blockIdx.y * 32, j0 = blockIdx.x * 32;
+  const int i0 = by * 32, j0 = bx * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
   for (int y = ty; y < 32; y += 8) {
     const int i = i0 + y, j = j0 + tx;
@@ -59,10 +60,10 @@ __global__ void k_transpose_into(const void* __restrict__ src, int src_f32, int 
 
 // One wave per (stage, codeword slot of a 64-codeword chunk): bf16 copy and
 // the fp32 squared norm, laid out per chunk as 64 consecutive floats.
-__global__ void k_prep_codebook(const float* __restrict__ C, int L, int K, int r, bf16_t* __restrict__ Cb,
-                                float* __restrict__ meta) {
+__device__ __forceinline__ void prep_codebook_block(int bx, const float* __restrict__ C, int L, int K, int r,
+                                                    bf16_t* __restrict__ Cb, float* __restrict__ meta) {
   const int nch = (K + 63) / 64;
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int w = bx * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (w >= L * nch * 64) return;
   const int l = w / (nch * 64), slot = w % (nch * 64);
   const int j = slot;  // codeword index within stage l
@@ -81,9 +82,9 @@ __global__ void k_prep_codebook(const float* __restrict__ C, int L, int K, int r
 
 // One thread per (token, 8 columns): 16 B stores, independent gathers.
 // Requires r % 8 == 0 and, for the anchor columns, k % 8 == 0.
-__global__ void k_assemble(AssembleArgs a) {
+__device__ __forceinline__ void assemble_block(int bx, const AssembleArgs& a) {
   const int per_row = a.ldo / 8;
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t e = (int64_t)bx * blockDim.x + threadIdx.x;
   if (e >= (int64_t)a.T * per_row) return;
   const int t = (int)(e / per_row), c0 = (int)(e % per_row) * 8;
   bf16_t* out = a.out + (int64_t)t * a.ldo + c0;
@@ -131,13 +132,110 @@ __global__ void k_assemble(AssembleArgs a) {
 }
 
 // One thread per 8 columns of a gathered row (16 B copies).
-__global__ void k_gather_rows_bf16(const bf16_t* __restrict__ A, int k, const int32_t* __restrict__ ids, int V,
-                                   int T, bf16_t* __restrict__ out) {
+__device__ __forceinline__ void gather_rows_block(int bx, const bf16_t* __restrict__ A, int k,
+                                                  const int32_t* __restrict__ ids, int V, int T,
+                                                  bf16_t* __restrict__ out) {
   const int cpr = k / 8;
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t e = (int64_t)bx * blockDim.x + threadIdx.x;
   if (e >= (int64_t)T * cpr) return;
   const int t = (int)(e / cpr), c = (int)(e % cpr) * 8;
   *(uint4*)(out + (int64_t)t * k + c) = *(const uint4*)(A + (int64_t)clamp_id(ids[t], V) * k + c);
+}
+
+__global__ void k_prep_u(const float* __restrict__ U, int d, int r, bf16_t* __restrict__ Ub, int64_t ldub,
+                         bf16_t* __restrict__ Ut, int64_t ldut) {
+  prep_u_tile(blockIdx.x, blockIdx.y, U, d, r, Ub, ldub, Ut, ldut);
+}
+__global__ void k_transpose_into(const void* __restrict__ src, int src_f32, int rows, int cols, int64_t lds,
+                                 float scale, bf16_t* __restrict__ dst, int64_t ldd, int off) {
+  transpose_tile(blockIdx.x, blockIdx.y, src, src_f32, rows, cols, lds, scale, dst, ldd, off);
+}
+__global__ void k_prep_codebook(const float* __restrict__ C, int L, int K, int r, bf16_t* __restrict__ Cb,
+                                float* __restrict__ meta) {
+  prep_codebook_block(blockIdx.x, C, L, K, r, Cb, meta);
+}
+__global__ void k_assemble(AssembleArgs a) { assemble_block(blockIdx.x, a); }
+__global__ void k_gather_rows_bf16(const bf16_t* __restrict__ A, int k, const int32_t* __restrict__ ids, int V,
+                                   int T, bf16_t* __restrict__ out) {
+  gather_rows_block(blockIdx.x, A, k, ids, V, T, out);
+}
+
+// dst[c * ldd + off + i] = bf16(scale * sum_j P[i][j] bf16(Q(j, c))) for a
+// 32 x 32 output tile (i0 = 32 by, c0 = 32 bx): P bf16 [M, Kd] row-major,
+// Q(j, c) = Q[j * ldq + c] (qt = 0) or Q[c * ldq + j] (qt = 1), fp32, rounded
+// to bf16 where it enters the matrix units; fp32 accumulation.  The four
+// waves take every fourth 16-wide k-step and add their partial tiles
+// through LDS in a fixed order.  Kd % 16 == 0, N % 32 == 0; rows >= M are
+// not written.
+__device__ __forceinline__ void small_gemm_tile(int bx, int by, const PrepJob& j) {
+  __shared__ float part[3][32 * 32];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5;
+  const int i0 = by * 32, c0 = bx * 32;
+  const int prow = min(i0 + (lane & 31), j.M - 1);
+  const bf16_t* P = (const bf16_t*)j.P + (int64_t)prow * j.ldp;
+  const int c = c0 + (lane & 31);
+  f32x16_t acc = f32x16_t{};
+  // batches of up to four k-steps: all loads of a batch are issued before
+  // its products, so their latencies overlap
+  constexpr int NB = 4;
+  for (int kb = 16 * wave; kb < j.Kd; kb += 64 * NB) {
+    uint4 a[NB], b[NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const int k0 = min(kb + 64 * u, j.Kd - 16);  // past the end: a repeat, not used
+      a[u] = *(const uint4*)(P + k0 + 8 * half);
+      float qv[8];
+      if (j.qt) {
+        const float4* q4 = (const float4*)(j.Q + (int64_t)c * j.ldq + k0 + 8 * half);
+        const float4 x0 = q4[0], x1 = q4[1];
+        qv[0] = x0.x; qv[1] = x0.y; qv[2] = x0.z; qv[3] = x0.w; qv[4] = x1.x; qv[5] = x1.y; qv[6] = x1.z; qv[7] = x1.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qv[e] = j.Q[(int64_t)(k0 + 8 * half + e) * j.ldq + c];
+      }
+      b[u] = make_uint4(pack_bf2(qv[0], qv[1]), pack_bf2(qv[2], qv[3]), pack_bf2(qv[4], qv[5]),
+                        pack_bf2(qv[6], qv[7]));
+    }
+#pragma unroll
+    for (int u = 0; u < NB; ++u)
+      if (kb + 64 * u < j.Kd) acc = mfma32x32x16(a[u], b[u], acc);
+  }
+  // acc e: row 8(e/4) + 4 half + e%4 of the tile, column lane % 32
+  if (wave > 0) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) part[wave - 1][acc_row(e, lane) * 32 + (lane & 31)] = acc[e];
+  }
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int row = acc_row(e, lane), col = lane & 31;
+      const float v = ((acc[e] + part[0][row * 32 + col]) + part[1][row * 32 + col]) + part[2][row * 32 + col];
+      if (i0 + row < j.M) j.dst[(int64_t)(c0 + col) * j.ldd + j.off + i0 + row] = (bf16_t)f2bf(j.scale * v);
+    }
+  }
+}
+
+// Several independent preparation jobs in one launch: block b runs job q
+// where q is the first job whose cumulative block count exceeds b.
+__global__ __launch_bounds__(256) void k_prep_batch(PrepBatch batch) {
+  int b = blockIdx.x, q = 0;
+  while (q + 1 < batch.n && b >= batch.job[q].blocks) {
+    b -= batch.job[q].blocks;
+    ++q;
+  }
+  const PrepJob& j = batch.job[q];
+  switch (j.kind) {
+    case PJ_PREP_U: prep_u_tile(b % j.gx, b / j.gx, j.U, j.d, j.r, j.Ub, j.ldub, j.Ut, j.ldut); break;
+    case PJ_TRANSPOSE:
+      transpose_tile(b % j.gx, b / j.gx, j.src, j.src_f32, j.rows, j.cols, j.lds, j.scale, j.dst, j.ldd, j.off);
+      break;
+    case PJ_CODEBOOK: prep_codebook_block(b, j.C, j.L, j.K, j.r, j.Cb, j.meta); break;
+    case PJ_ASSEMBLE: assemble_block(b, j.asm_args); break;
+    case PJ_GATHER: gather_rows_block(b, j.A, j.k, j.ids, j.V, j.T, j.out); break;
+    case PJ_SMALL_GEMM: small_gemm_tile(b % j.gx, b / j.gx, j); break;
+    default: break;
+  }
 }
 
 __global__ void k_check_ids(const int32_t* __restrict__ ids, int T, int64_t V, int* flag) {
@@ -191,6 +289,83 @@ hipError_t launch_gather_rows_bf16(const bf16_t* A, int k, const int32_t* ids, i
   const int64_t n = (int64_t)T * (k / 8);
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_gather_rows_bf16, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, A, k, ids, V, T, out);
+  return hipGetLastError();
+}
+
+PrepJob prep_job_u(const float* U, int d, int r, bf16_t* Ub, int64_t ldub, bf16_t* Ut, int64_t ldut) {
+  PrepJob j{};
+  j.kind = PJ_PREP_U;
+  j.U = U; j.d = d; j.r = r; j.Ub = Ub; j.ldub = ldub; j.Ut = Ut; j.ldut = ldut;
+  // only the d x r values: padding columns of the operands are never read
+  j.gx = (d + 31) / 32;
+  j.blocks = j.gx * ((r + 31) / 32);
+  return j;
+}
+
+PrepJob prep_job_transpose(const void* src, int src_f32, int rows, int cols, int64_t lds, float scale, bf16_t* dst,
+                           int64_t ldd, int off) {
+  PrepJob j{};
+  j.kind = PJ_TRANSPOSE;
+  j.src = src; j.src_f32 = src_f32; j.rows = rows; j.cols = cols; j.lds = lds; j.scale = scale;
+  j.dst = dst; j.ldd = ldd; j.off = off;
+  j.gx = (cols + 31) / 32;
+  j.blocks = rows > 0 && cols > 0 ? j.gx * ((rows + 31) / 32) : 0;
+  return j;
+}
+
+PrepJob prep_job_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* meta) {
+  PrepJob j{};
+  j.kind = PJ_CODEBOOK;
+  j.C = C; j.L = L; j.K = K; j.r = r; j.Cb = Cb; j.meta = meta;
+  j.blocks = (int)(((int64_t)L * ((K + 63) / 64) * 64 + 3) / 4);
+  return j;
+}
+
+PrepJob prep_job_assemble(const AssembleArgs& a) {
+  PrepJob j{};
+  j.kind = PJ_ASSEMBLE;
+  j.asm_args = a;
+  j.blocks = a.T > 0 ? (int)(((int64_t)a.T * (a.ldo / 8) + 255) / 256) : 0;
+  return j;
+}
+
+PrepJob prep_job_gather(const bf16_t* A, int k, const int32_t* ids, int V, int T, bf16_t* out) {
+  PrepJob j{};
+  j.kind = PJ_GATHER;
+  j.A = A; j.k = k; j.ids = ids; j.V = V; j.T = T; j.out = out;
+  j.blocks = T > 0 ? (int)(((int64_t)T * (k / 8) + 255) / 256) : 0;
+  return j;
+}
+
+PrepJob prep_job_small_gemm(const bf16_t* P, int64_t ldp, const float* Q, int64_t ldq, int qt, int M, int N,
+                            int Kd, float scale, bf16_t* dst, int64_t ldd, int off) {
+  PrepJob j{};
+  j.kind = PJ_SMALL_GEMM;
+  j.P = P; j.ldp = ldp; j.Q = Q; j.ldq = ldq; j.qt = qt; j.M = M; j.N = N; j.Kd = Kd; j.scale = scale;
+  j.dst = dst; j.ldd = ldd; j.off = off;
+  j.gx = N / 32;
+  j.blocks = M > 0 ? ((M + 31) / 32) * (N / 32) : 0;
+  return j;
+}
+
+hipError_t launch_prep_batch(const PrepJob* jobs, int n, hipStream_t s) {
+  PrepBatch b{};
+  int total = 0;
+  for (int i = 0; i < n; ++i) {
+    if (jobs[i].blocks <= 0) continue;
+    if (b.n == PREP_MAX_JOBS) return hipErrorInvalidValue;
+    if (jobs[i].kind == PJ_SMALL_GEMM &&
+        (jobs[i].Kd % 16 || jobs[i].N % 32 || jobs[i].ldp % 8 || (jobs[i].qt && jobs[i].ldq % 4)))
+      return hipErrorInvalidValue;
+    if (jobs[i].kind == PJ_ASSEMBLE && (jobs[i].asm_args.r % 8 || jobs[i].asm_args.ldo % 8 ||
+                                        (jobs[i].asm_args.A != nullptr && jobs[i].asm_args.k % 8)))
+      return hipErrorInvalidValue;
+    if (jobs[i].kind == PJ_GATHER && jobs[i].k % 8) return hipErrorInvalidValue;
+    b.job[b.n++] = jobs[i];
+    total += jobs[i].blocks;
+  }
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_prep_batch, dim3((unsigned)total), dim3(256), 0, s, b);
   return hipGetLastError();
 }
 

@@ -102,6 +102,41 @@ struct AssembleArgs {
 };
 hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s);
 
+// ---------------------------------------------------------------- batched preparation
+// Independent preparation jobs of one call issued as a single launch
+// (launch_prep_batch); each job behaves like the corresponding launcher.
+enum { PJ_PREP_U = 1, PJ_TRANSPOSE, PJ_CODEBOOK, PJ_ASSEMBLE, PJ_GATHER, PJ_SMALL_GEMM };
+struct PrepJob {
+  int kind, blocks, gx;
+  // PJ_PREP_U
+  const float* U; int d, r; bf16_t* Ub; int64_t ldub; bf16_t* Ut; int64_t ldut;
+  // PJ_TRANSPOSE, PJ_SMALL_GEMM (dst, ldd, off, scale)
+  const void* src; int src_f32, rows, cols; int64_t lds; float scale; bf16_t* dst; int64_t ldd; int off;
+  // PJ_CODEBOOK
+  const float* C; int L, K; bf16_t* Cb; float* meta;
+  // PJ_ASSEMBLE
+  AssembleArgs asm_args;
+  // PJ_GATHER
+  const bf16_t* A; int k; const int32_t* ids; int V, T; bf16_t* out;
+  // PJ_SMALL_GEMM: dst[c*ldd + off + i] = bf16(scale * sum_j P[i][j] bf16(Q(j, c))),
+  // Q(j, c) = Q[j*ldq + c] (qt = 0) or Q[c*ldq + j] (qt = 1)
+  const void* P; int64_t ldp; const float* Q; int64_t ldq; int qt, M, N, Kd;
+};
+constexpr int PREP_MAX_JOBS = 4;
+struct PrepBatch {
+  PrepJob job[PREP_MAX_JOBS];
+  int n;
+};
+PrepJob prep_job_u(const float* U, int d, int r, bf16_t* Ub, int64_t ldub, bf16_t* Ut, int64_t ldut);
+PrepJob prep_job_transpose(const void* src, int src_f32, int rows, int cols, int64_t lds, float scale, bf16_t* dst,
+                           int64_t ldd, int off);
+PrepJob prep_job_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* meta);
+PrepJob prep_job_assemble(const AssembleArgs& a);
+PrepJob prep_job_gather(const bf16_t* A, int k, const int32_t* ids, int V, int T, bf16_t* out);
+PrepJob prep_job_small_gemm(const bf16_t* P, int64_t ldp, const float* Q, int64_t ldq, int qt, int M, int N,
+                            int Kd, float scale, bf16_t* dst, int64_t ldd, int off);
+hipError_t launch_prep_batch(const PrepJob* jobs, int n, hipStream_t s);
+
 // ---------------------------------------------------------------- RVQ (bf16 screen + fp32 rescore)
 // r in {32, 64, 128, 256}.
 struct RvqArgs {

@@ -148,8 +148,6 @@ struct Layout {
   SplitPlan sp{1, 64};
 };
 
-// K slice of the split-K anchor-factor product B_s U~ (columns of d per slice).
-inline int64_t bu_kz(int64_t d) { return d % 128 == 0 ? 128 : 64; }
 
 Layout layout(const mapl_codec_desc& D, int call) {
   Layout Lo;
@@ -165,7 +163,6 @@ Layout layout(const mapl_codec_desc& D, int call) {
       case MAPL_CALL_ENCODE:
         Lo.kw = d + Lo.kp;
         Lo.w = c.take((size_t)r * Lo.kw * 2);
-        if (k > 0 && amb) Lo.bu = c.take((size_t)(d / bu_kz(d)) * k * r * 4);
         if (D.L > 0) {
           Lo.z0 = c.take((size_t)T * r * 4);
           Lo.cb = c.take((size_t)D.L * D.K * r * 2);
@@ -177,7 +174,6 @@ Layout layout(const mapl_codec_desc& D, int call) {
         Lo.kw = r + Lo.kp;
         Lo.w2 = c.take((size_t)d * Lo.kw * 2);
         if (D.L > 0) Lo.ahat = c.take((size_t)T * r * 2);
-        if (k > 0 && !amb) Lo.bu = c.take((size_t)k * d * 4);
         break;
       case MAPL_CALL_DECODE_BWD:
         Lo.w = c.take((size_t)r * d * 2);
@@ -373,25 +369,23 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
   const int cbytes = (int)code_bytes(D);
 
   if (D.x_dtype == MAPL_BF16) {
+    // one launch: Wt = [U~^T | -(B_s U~)^T] (or the coordinate anchor's
+    // -B_s^T), and the bf16 codebook copy with its norms
     bf16_t* Wt = at<bf16_t>(ws, Lo.w);
-    LAUNCH("enc:prep_u", launch_prep_u(U, (int)d, (int)r, nullptr, 0, Wt, Lo.kw, s));
+    bf16_t* Cb = D.L > 0 ? at<bf16_t>(ws, Lo.cb) : nullptr;
+    float* meta = D.L > 0 ? at<float>(ws, Lo.cn2) : nullptr;
+    PrepJob jobs[3];
+    int nj = 0;
+    jobs[nj++] = prep_job_u(U, (int)d, (int)r, nullptr, 0, Wt, Lo.kw);
     if (k > 0) {
-      if (amb) {
-        // Wt[c][d+i] = -bf16( (B_s U~)[i][c] ): split-K over d, fixed-order reduce
-        const int kz = (int)bu_kz(d), S = (int)(d / kz);
-        float* part = at<float>(ws, Lo.bu);
-        TnArgs b{};
-        b.A = (const bf16_t*)B_s; b.lda = d; b.Ka = (int)d; b.kz = kz; b.out_z = k * r;
-        b.W = Wt; b.ldw = Lo.kw;
-        b.M = (int)k; b.N = (int)r;
-        b.out = part; b.ldo = r; b.out_f32 = 1;
-        LAUNCH("enc:bu_gemm", launch_gemm_tn(b, s));
-        LAUNCH("enc:bu_reduce", launch_reduce_splits_t_bf16(part, S, (int)k, (int)r, k * r, -1.f, Wt, Lo.kw,
-                                                             (int)d, s));
-      } else {
-        LAUNCH("enc:transpose_into", launch_transpose_into(B_s, 0, (int)k, (int)r, r, -1.f, Wt, Lo.kw, (int)d, s));
-      }
+      if (amb)  // Wt[c][d+i] = -bf16( (B_s U~)[i][c] )
+        jobs[nj++] = prep_job_small_gemm((const bf16_t*)B_s, d, U, r, 0, (int)k, (int)r, (int)d, -1.f, Wt, Lo.kw,
+                                         (int)d);
+      else
+        jobs[nj++] = prep_job_transpose(B_s, 0, (int)k, (int)r, r, -1.f, Wt, Lo.kw, (int)d);
     }
+    if (D.L > 0) jobs[nj++] = prep_job_codebook(C, D.L, D.K, (int)r, Cb, meta);
+    LAUNCH("enc:prep", launch_prep_batch(jobs, nj, s));
     TnArgs g{};
     g.A = (const bf16_t*)X; g.lda = d; g.Ka = (int)d;
     g.T = (const bf16_t*)A_s; g.ldt = k; g.ids = ids; g.Kg = (int)k; g.V = (int)D.V;
@@ -405,9 +399,6 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
     float* Z0 = at<float>(ws, Lo.z0);
     g.out = Z0; g.ldo = r; g.out_f32 = 1;
     LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
-    bf16_t* Cb = at<bf16_t>(ws, Lo.cb);
-    float* meta = at<float>(ws, Lo.cn2);
-    LAUNCH("enc:prep_codebook", launch_prep_codebook(C, D.L, D.K, (int)r, Cb, meta, s));
     RvqArgs a{};
     a.Z0 = Z0; a.Cb = Cb; a.C = C; a.meta = meta;
     a.T = (int)T; a.r = (int)r; a.L = D.L; a.K = D.K;
@@ -479,23 +470,18 @@ extern "C" int mapl_decode(const mapl_codec_desc* desc, const void* payload, con
   const int cbytes = (int)code_bytes(D);
 
   if (D.x_dtype == MAPL_BF16) {
+    // one launch: W2 = [U~ | B_r^T] (or the coordinate anchor's (B_r U~^T)^T)
+    // and, for codes, Zhat = sum_l C_l[code_l]
     bf16_t* W2 = at<bf16_t>(ws, Lo.w2);
-    LAUNCH("dec:prep_u", launch_prep_u(U, (int)d, (int)r, W2, Lo.kw, nullptr, 0, s));
+    PrepJob jobs[3];
+    int nj = 0;
+    jobs[nj++] = prep_job_u(U, (int)d, (int)r, W2, Lo.kw, nullptr, 0);
     if (k > 0) {
-      if (amb) {
-        LAUNCH("dec:transpose_into", launch_transpose_into(B_r, 0, (int)k, (int)d, d, 1.f, W2, Lo.kw, (int)r, s));
-      } else {
-        // W2[j][r+i] = bf16( (B_r U~^T)[i][j] )
-        float* part = at<float>(ws, Lo.bu);
-        TnArgs b{};
-        b.A = (const bf16_t*)B_r; b.lda = r; b.Ka = (int)r;
-        b.W = W2; b.ldw = Lo.kw;
-        b.M = (int)k; b.N = (int)d;
-        b.out = part; b.ldo = d; b.out_f32 = 1;
-        LAUNCH("dec:bu_gemm", launch_gemm_tn(b, s));
-        LAUNCH("dec:bu_reduce", launch_reduce_splits_t_bf16(part, 1, (int)k, (int)d, k * d, 1.f, W2, Lo.kw,
-                                                             (int)r, s));
-      }
+      if (amb)
+        jobs[nj++] = prep_job_transpose(B_r, 0, (int)k, (int)d, d, 1.f, W2, Lo.kw, (int)r);
+      else  // W2[j][r+i] = bf16( sum_c B_r[i][c] U~[j][c] )
+        jobs[nj++] = prep_job_small_gemm((const bf16_t*)B_r, r, U, r, 1, (int)k, (int)d, (int)r, 1.f, W2, Lo.kw,
+                                         (int)r);
     }
     const bf16_t* Aop = (const bf16_t*)payload;
     if (D.L > 0) {
@@ -503,9 +489,10 @@ extern "C" int mapl_decode(const mapl_codec_desc* desc, const void* payload, con
       AssembleArgs a{};
       a.codes = payload; a.code_bytes = cbytes; a.C = C; a.L = D.L; a.K = D.K;
       a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah;
-      LAUNCH("dec:assemble", launch_assemble(a, s));
+      jobs[nj++] = prep_job_assemble(a);
       Aop = Ah;
     }
+    LAUNCH("dec:prep", launch_prep_batch(jobs, nj, s));
     TnArgs g{};
     g.A = Aop; g.lda = r; g.Ka = (int)r;
     g.T = (const bf16_t*)A_r; g.ldt = k; g.ids = ids; g.Kg = (int)k; g.V = (int)D.V;
@@ -592,14 +579,12 @@ extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, c
   }
 
   if (D.x_dtype == MAPL_BF16) {
+    // one launch: Ut = U~^T and the second operand of dU (Zhat, plus the
+    // coordinate anchor)
     bf16_t* Ut = at<bf16_t>(ws, Lo.w);
-    LAUNCH("dec_bwd:prep_u", launch_prep_u(U, (int)d, (int)r, nullptr, 0, Ut, d, s));
-    TnArgs g{};
-    g.A = (const bf16_t*)dXhat; g.lda = d; g.Ka = (int)d;
-    g.W = Ut; g.ldw = d;
-    g.M = (int)T; g.N = (int)r;
-    g.out = dZ; g.ldo = r; g.out_f32 = 0;
-    LAUNCH("dec_bwd:gemm_tn", launch_gemm_tn(g, s));
+    PrepJob jobs[2];
+    int nj = 0;
+    jobs[nj++] = prep_job_u(U, (int)d, (int)r, nullptr, 0, Ut, d);
     const bf16_t* Q = (const bf16_t*)payload;
     if (D.L > 0 || need_anchor) {
       bf16_t* Ah = at<bf16_t>(ws, Lo.ahat);
@@ -608,9 +593,16 @@ extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, c
       a.codes = payload; a.code_bytes = cbytes; a.C = C; a.L = D.L; a.K = D.K;
       if (need_anchor) { a.A = (const bf16_t*)A_r; a.k = (int)k; a.Bc = (const bf16_t*)B_r; a.ids = ids; a.V = (int)D.V; }
       a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah;
-      LAUNCH("dec_bwd:assemble", launch_assemble(a, s));
+      jobs[nj++] = prep_job_assemble(a);
       Q = Ah;
     }
+    LAUNCH("dec_bwd:prep", launch_prep_batch(jobs, nj, s));
+    TnArgs g{};
+    g.A = (const bf16_t*)dXhat; g.lda = d; g.Ka = (int)d;
+    g.W = Ut; g.ldw = d;
+    g.M = (int)T; g.N = (int)r;
+    g.out = dZ; g.ldo = r; g.out_f32 = 0;
+    LAUNCH("dec_bwd:gemm_tn", launch_gemm_tn(g, s));
     WgradArgs w{};
     w.Pa = (const bf16_t*)dXhat; w.ldp = d; w.Ma = (int)d;
     w.Q = Q; w.ldq = r;
@@ -695,8 +687,14 @@ extern "C" int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, cons
   }
 
   if (D.x_dtype == MAPL_BF16) {
+    // one launch: Ub = U~ and the gathered sender anchors a_s
     bf16_t* Ub = at<bf16_t>(ws, Lo.w2);
-    LAUNCH("enc_bwd:prep_u", launch_prep_u(U, (int)d, (int)r, Ub, r, nullptr, 0, s));
+    bf16_t* ga = need_anchor ? at<bf16_t>(ws, Lo.ga) : nullptr;
+    PrepJob jobs[2];
+    int nj = 0;
+    jobs[nj++] = prep_job_u(U, (int)d, (int)r, Ub, r, nullptr, 0);
+    if (need_anchor) jobs[nj++] = prep_job_gather((const bf16_t*)A_s, (int)k, ids, (int)D.V, (int)T, ga);
+    LAUNCH("enc_bwd:prep", launch_prep_batch(jobs, nj, s));
     TnArgs g{};
     g.A = (const bf16_t*)dZ; g.lda = r; g.Ka = (int)r;
     g.W = Ub; g.ldw = r;
@@ -706,8 +704,6 @@ extern "C" int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, cons
     WgradArgs w{};
     w.Pa = (const bf16_t*)X; w.ldp = d; w.Ma = (int)d;
     if (need_anchor) {
-      bf16_t* ga = at<bf16_t>(ws, Lo.ga);
-      LAUNCH("enc_bwd:gather", launch_gather_rows_bf16((const bf16_t*)A_s, (int)k, ids, (int)D.V, (int)T, ga, s));
       w.Tg = ga; w.Mg = (int)k;
     }
     w.Q = (const bf16_t*)dZ; w.ldq = r;
