@@ -53,7 +53,7 @@ struct TnSmem {
 };
 
 // NS pipeline stages (2 or 3), one __shared__ array each.
-template <int BN, int NS>
+template <int BN, int NS, bool FULLK>
 __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_wg) {
 #if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature (launch stub)
   static_assert(NS == 2 || NS == 3, "stages");
@@ -68,7 +68,8 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
   bf16_t* const S2a = S2buf;
   bf16_t* const S2w = S2buf + GM * GK;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar LDS addresses
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = blockIdx.x * GM;
   const int nt0 = blockIdx.y * ntiles_per_wg;
@@ -80,6 +81,11 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
   const int KS = ka_steps + kg_steps;
   const int KSP = (KS + NS - 1) / NS * NS;      // padded: stage buffers repeat every tile
   const int total = ntiles * KSP;
+  // Workgroups start their K walk at different k-steps (the same for the
+  // eight consecutive ids spread over the XCDs): at any moment the token
+  // rows in flight then sit at different column offsets, which spreads the
+  // strided row reads over more HBM channels and banks.
+  const int rot = KS > 0 ? (int)(blockIdx.x >> 3) % KS : 0;
 
   // Buffer resources: A rows of this workgroup, the anchor table, W.
   const int mrows = min(GM, g.M - m0);
@@ -90,7 +96,9 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
   // Per-lane DMA geometry: lane i of block b fills row 8b + i/8, physical
   // chunk i%8, so it loads logical chunk (i%8) ^ ((row >> 1) & 7), which
   // depends only on the parity of b.  All offsets are 32-bit byte offsets
-  // from the resource bases (validated on the host).
+  // from the resource bases (validated on the host).  The per-lane part
+  // (row, chunk) is fixed for the whole kernel; a stage adds its column
+  // offset, uniform across the wave.
   const int lrow = lane >> 3;
   const uint32_t lchp[2] = {(uint32_t)((lane & 7) ^ (lane >> 4)), (uint32_t)((lane & 7) ^ (4 + (lane >> 4)))};
   uint32_t a_off[ABLK], t_off[ABLK], w_off[WBLK];
@@ -108,41 +116,93 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
     w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lchp[j & 1];
   }
 
-  // Every stage issues exactly LOADS loads per wave (padding steps read
-  // zeros), so the wait count below is exact.  Straight-line code: validity
-  // is a select on the offset, never a branch around a load.
-  auto issue = [&](int step, bf16_t* sa, bf16_t* sw) {
-    const int nt = nt0 + step / KSP, ks = step % KSP;
-    const bool pad = ks >= KS;
-    const bool gathered = ks >= ka_steps;
-    const int kc = gathered ? (ks - ka_steps) * GK : ks * GK;
-    // this lane's first column in the stage, per block parity
-    const int col0 = kc + 8 * (int)lchp[0], col1 = kc + 8 * (int)lchp[1];
-    if (!gathered || pad) {
-      const bool ok0 = !pad && col0 < kz, ok1 = !pad && col1 < kz;
-      const uint32_t add = (uint32_t)(kbase + kc) * 2u;
-#pragma unroll
-      for (int j = 0; j < ABLK; ++j)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(sa + (wave * ABLK + j) * 512), 16,
-                                                 ((j & 1) ? ok1 : ok0) ? a_off[j] + add : OOB, 0, 0, 0);
-    } else {
-      const bool ok0 = col0 < g.Kg, ok1 = col1 < g.Kg;
-      const uint32_t add = (uint32_t)kc * 2u;
-#pragma unroll
-      for (int j = 0; j < ABLK; ++j)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, (lds_ptr)(sa + (wave * ABLK + j) * 512), 16,
-                                                 (((j & 1) ? ok1 : ok0) && t_off[j] != OOB) ? t_off[j] + add : OOB,
-                                                 0, 0, 0);
+  // A real step issues exactly LOADS loads per wave; a padding step issues
+  // none (the wait before a step accounts for that).  A step's loads are
+  // planned once (steps in order), then issued a few at a time between the
+  // products of the step before (see compute): a burst of them would hold up
+  // the wave's instruction stream while the memory pipeline drains it.
+  // FULLK: every K dimension is a multiple of GK, so each real step covers
+  // whole stages: a load takes the lane's fixed offset as its VGPR operand
+  // and the stage's column offset as its scalar operand (rows past the last
+  // token still fall outside the A resource and read zeros), and planning
+  // costs no vector arithmetic.  Otherwise per-lane checks select each
+  // offset or OOB.
+  struct Plan {
+    bf16_t *sa, *sw;
+    int sA, sW;
+    bool live, gathered;
+    uint32_t vA[FULLK ? 1 : ABLK], vW[FULLK ? 1 : WBLK];  // per-lane offsets (not FULLK)
+  };
+  int pl_ks = 0, pl_nt = nt0;  // next step to plan
+  auto plan_next = [&](bf16_t* sa, bf16_t* sw) {
+    Plan p;
+    p.sa = sa;
+    p.sw = sw;
+    // uniform by construction; readfirstlane lets the compiler see it, so
+    // the choices and offsets below stay in scalar registers
+    const int ks0 = __builtin_amdgcn_readfirstlane(pl_ks), nt = __builtin_amdgcn_readfirstlane(pl_nt);
+    if (++pl_ks == KSP) {
+      pl_ks = 0;
+      ++pl_nt;
     }
-    const int wcol0 = gathered ? g.Ka + kc : kbase + kc;
-    const int wlim = pad ? 0 : gathered ? g.Ka + g.Kg : kbase + kz;
-    const int wc0 = wcol0 + 8 * (int)lchp[0], wc1 = wcol0 + 8 * (int)lchp[1];
-    const bool wok0 = wc0 < wlim && wc0 < g.ldw, wok1 = wc1 < wlim && wc1 < g.ldw;
+    p.live = ks0 < KS;
+    int ks = ks0 + rot;
+    if (ks >= KS) ks -= KS;
+    p.gathered = p.live && ks >= ka_steps;
+    const int kc = p.gathered ? (ks - ka_steps) * GK : ks * GK;
+    const uint32_t aadd = (uint32_t)(p.gathered ? kc : kbase + kc) * 2u;
+    const int wcol0 = p.gathered ? g.Ka + kc : kbase + kc;
     const uint32_t wadd = (uint32_t)nt * BN * (uint32_t)g.ldw * 2u + (uint32_t)wcol0 * 2u;
+    if constexpr (FULLK) {
+      p.sA = (int)aadd;
+      p.sW = (int)wadd;
+    } else {
+      const int alim = p.gathered ? g.Kg : kz;
+      const int wlim = p.gathered ? g.Ka + g.Kg : kbase + kz;
+      // this lane's first column in the stage, per block parity
+      const int col0 = kc + 8 * (int)lchp[0], col1 = kc + 8 * (int)lchp[1];
+      const int wc0 = wcol0 + 8 * (int)lchp[0], wc1 = wcol0 + 8 * (int)lchp[1];
+      const bool ok0 = col0 < alim, ok1 = col1 < alim;
+      const bool wok0 = wc0 < wlim && wc0 < g.ldw, wok1 = wc1 < wlim && wc1 < g.ldw;
 #pragma unroll
-    for (int j = 0; j < WBLK; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(sw + (wave * WBLK + j) * 512), 16,
-                                               ((j & 1) ? wok1 : wok0) ? w_off[j] + wadd : OOB, 0, 0, 0);
+      for (int j = 0; j < ABLK; ++j) {
+        const uint32_t o = p.gathered ? t_off[j] : a_off[j];
+        p.vA[j] = ((j & 1) ? ok1 : ok0) && o != OOB ? o + aadd : OOB;
+      }
+#pragma unroll
+      for (int j = 0; j < WBLK; ++j) p.vW[j] = ((j & 1) ? wok1 : wok0) ? w_off[j] + wadd : OOB;
+      p.sA = 0;
+      p.sW = 0;
+    }
+    return p;
+  };
+  // loads [B0, B1) of a step: A (or anchor) block li < ABLK, else W block li - ABLK
+  auto issue_range = [&](const Plan& p, auto b0c, auto b1c) {
+    constexpr int B0 = decltype(b0c)::value, B1 = decltype(b1c)::value;
+    if (!p.live) return;
+    auto go = [&](auto gc) {
+      constexpr bool GATH = decltype(gc)::value;
+      static_for<B0, B1>([&](auto lic) {
+        constexpr int LI = decltype(lic)::value;
+        if constexpr (LI < ABLK) {
+          const lds_ptr dst = (lds_ptr)(p.sa + (wave * ABLK + LI) * 512);
+          const uint32_t v = FULLK ? (GATH ? t_off[LI] : a_off[LI]) : p.vA[FULLK ? 0 : LI];
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(GATH ? rt : ra, dst, 16, v, p.sA, 0, 0);
+        } else {
+          constexpr int J = LI - ABLK;
+          const lds_ptr dst = (lds_ptr)(p.sw + (wave * WBLK + J) * 512);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, dst, 16, FULLK ? w_off[J] : p.vW[FULLK ? 0 : J], p.sW, 0, 0);
+        }
+      });
+    };
+    if (p.gathered)
+      go(std::true_type{});
+    else
+      go(std::false_type{});
+  };
+  auto issue_next = [&](bf16_t* sa, bf16_t* sw) {
+    const Plan p = plan_next(sa, sw);
+    issue_range(p, std::integral_constant<int, 0>{}, std::integral_constant<int, LOADS>{});
   };
 
   f32x16_t acc[FM][FN];
@@ -162,7 +222,10 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #pragma unroll
   for (int kk = 0; kk < GK / 16; ++kk)
     koff[kk] = (uint32_t)((lane & 31) * (GK * 2) + 16 * ((2 * kk + half) ^ (((lane & 31) >> 1) & 7)));
-  auto compute = [&](const bf16_t* sa, const bf16_t* sw) {
+  // Products of one stage; the next step's loads (if any) are issued in
+  // KSTEP groups after the products of each 16-wide k-step.
+  constexpr int KSTEP = GK / 16, PER = (LOADS + KSTEP - 1) / KSTEP;
+  auto compute = [&](const bf16_t* sa, const bf16_t* sw, const Plan& nx, bool has_next) {
     const uint32_t ba = lds_addr(sa) + wm * 64 * (GK * 2), bw = lds_addr(sw) + wn * (BN / 2) * (GK * 2);
     u32x4 fr[2][FM + FN];
     auto load = [&](int kk, u32x4 (&f)[FM + FN]) {
@@ -177,32 +240,43 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
     };
     load(0, fr[0]);
     lds_wait(fr[0]);
-#pragma unroll
-    for (int kk = 0; kk < GK / 16; ++kk) {
-      const int cb = kk & 1;
-      if (kk + 1 < GK / 16) load(kk + 1, fr[cb ^ 1]);
+    static_for<0, KSTEP>([&](auto kkc) {
+      constexpr int KK = decltype(kkc)::value, CB = KK & 1;
+      if constexpr (KK + 1 < KSTEP) load(KK + 1, fr[CB ^ 1]);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(as_uint4(fr[cb][FM + j]), as_uint4(fr[cb][i]), acc[i][j]);
-      if (kk + 1 < GK / 16) lds_wait(fr[cb ^ 1]);
-    }
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(as_uint4(fr[CB][FM + j]), as_uint4(fr[CB][i]), acc[i][j]);
+      constexpr int B0 = KK * PER < LOADS ? KK * PER : LOADS;
+      constexpr int B1 = (KK + 1) * PER < LOADS ? (KK + 1) * PER : LOADS;
+      if (has_next) issue_range(nx, std::integral_constant<int, B0>{}, std::integral_constant<int, B1>{});
+      if constexpr (KK + 1 < KSTEP) lds_wait(fr[CB ^ 1]);
+    });
   };
 
   // One pipeline step: stage s (in buffer `cur`) is consumed; stage s + NS - 1
   // is issued into `nxt` (the buffer consumed at step s - 1).
   auto step = [&](int s, int ks, const bf16_t* ca, const bf16_t* cw, bf16_t* na, bf16_t* nw) {
-    if (s + 1 < total)
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS * (NS - 2)) : "memory");
+    // stage s must be complete; only stage s + 1 (if it loads anything) may
+    // still be in flight (NS = 3)
+    const bool next_loads = s + 1 < total && !(ks + 1 < KSP && ks + 1 >= KS);
+    if (NS == 3 && next_loads)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS) : "memory");
     else
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
-    if (s + NS - 1 < total) issue(s + NS - 1, na, nw);
-    if (ks < KS) compute(ca, cw);
+    const bool has_next = s + NS - 1 < total;
+    if (ks < KS) {
+      Plan p{};
+      if (has_next) p = plan_next(na, nw);
+      compute(ca, cw, p, has_next);
+    } else if (has_next) {
+      issue_next(na, nw);
+    }
   };
 
-  issue(0, S0.a, S0.w);
-  if (NS == 3 && total > 1) issue(1, S1.a, S1.w);
+  issue_next(S0.a, S0.w);
+  if (NS == 3 && total > 1) issue_next(S1.a, S1.w);
   char* obase = (char*)g.out + (g.kz > 0 ? (int64_t)blockIdx.z * g.out_z * 4 : 0);
   for (int tile = 0; tile < ntiles; ++tile) {
     for (int ks = 0; ks < KSP; ks += NS) {
@@ -309,6 +383,8 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 
 template <int BN, int NS>
 hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
+  const int kz = g.kz > 0 ? g.kz : g.Ka;
+  const bool fullk = kz % GK == 0 && g.Kg % GK == 0 && g.Ka + g.Kg <= g.ldw;
   const int mt = (g.M + GM - 1) / GM;
   const int nt = g.N / BN;
   const int zs = g.kz > 0 ? g.Ka / g.kz : 1;
@@ -316,7 +392,10 @@ hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
   int per = 1;
   while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) * zs >= 256) per *= 2;
   dim3 grid(mt, (nt + per - 1) / per, zs);
-  hipLaunchKernelGGL((k_gemm_tn<BN, NS>), grid, dim3(GTHREADS), 0, s, g, per);
+  if (fullk)
+    hipLaunchKernelGGL((k_gemm_tn<BN, NS, true>), grid, dim3(GTHREADS), 0, s, g, per);
+  else
+    hipLaunchKernelGGL((k_gemm_tn<BN, NS, false>), grid, dim3(GTHREADS), 0, s, g, per);
   return hipGetLastError();
 }
 
