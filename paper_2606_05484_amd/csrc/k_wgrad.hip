@@ -82,7 +82,8 @@ __global__ __launch_bounds__(WG_THREADS) void k_wgrad(WgradArgs g, int mtiles, i
   __shared__ __attribute__((aligned(1024))) WgSmem<BN> S1;
   __shared__ __attribute__((aligned(1024))) WgSmem<BN> S2;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar LDS addresses
   const int wm = wave >> 1, wn = wave & 1;
   // Workgroup ids are dispatched round-robin over the 8 XCDs (id % 8).  The
   // k-th workgroup of XCD x takes work item x q' + k (q' = its share), so
@@ -139,25 +140,70 @@ __global__ __launch_bounds__(WG_THREADS) void k_wgrad(WgradArgs g, int mtiles, i
     q_off[jb] = (uint32_t)(n0 + 8 * c) * 2u;
   }
 
+  // lane part of each load's offset (row within the step, column chunk);
+  // a step adds its first token's row offset, uniform across the wave
+  uint32_t p_lane[PBLK], q_lane[QBLK];
+#pragma unroll
+  for (int jb = 0; jb < PBLK; ++jb)
+    p_lane[jb] = p_off[jb] != WG_OOB ? (uint32_t)p_row[jb] * (uint32_t)pld * 2u + p_off[jb] : WG_OOB;
+#pragma unroll
+  for (int jb = 0; jb < QBLK; ++jb) q_lane[jb] = (uint32_t)q_row[jb] * (uint32_t)g.ldq * 2u + q_off[jb];
+
+  // A real step issues exactly LOADS loads per wave, a padding step none
+  // (the wait before a step accounts for that).  The next step's loads are
+  // issued a few at a time between the products (see compute): a burst of
+  // them would hold up the wave's instruction stream.  A step whose 64
+  // tokens all exist takes the lane's fixed offset as the VGPR operand and
+  // the step's row offset as the scalar one (no vector arithmetic); the last
+  // step of a ragged split checks each lane's token.
+  struct Plan {
+    bf16_t *sp, *sq;
+    int t0;
+    bool live, full;
+  };
+  auto plan = [&](int step, bf16_t* sp, bf16_t* sq) {
+    Plan p;
+    p.sp = sp;
+    p.sq = sq;
+    p.t0 = __builtin_amdgcn_readfirstlane(step * WG_KT);  // relative to t_begin
+    p.live = p.t0 < KS * WG_KT;
+    p.full = p.t0 + WG_KT <= nt_rows;
+    return p;
+  };
+  auto issue_range = [&](const Plan& p, auto b0c, auto b1c) {
+    constexpr int B0 = decltype(b0c)::value, B1 = decltype(b1c)::value;
+    if (!p.live) return;
+    const int sP = (int)((uint32_t)p.t0 * (uint32_t)pld * 2u), sQ = (int)((uint32_t)p.t0 * (uint32_t)g.ldq * 2u);
+    if (p.full) {
+      static_for<B0, B1>([&](auto lic) {
+        constexpr int LI = decltype(lic)::value;
+        if constexpr (LI < PBLK)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rp, (wg_lds_ptr)(p.sp + (wave * PBLK + LI) * 512), 16, p_lane[LI],
+                                                   sP, 0, 0);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (wg_lds_ptr)(p.sq + (wave * QBLK + LI - PBLK) * 512), 16,
+                                                   q_lane[LI - PBLK], sQ, 0, 0);
+      });
+    } else {
+      static_for<B0, B1>([&](auto lic) {
+        constexpr int LI = decltype(lic)::value;
+        if constexpr (LI < PBLK) {
+          const int t = p.t0 + p_row[LI];
+          const bool ok = t < nt_rows && p_off[LI] != WG_OOB;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rp, (wg_lds_ptr)(p.sp + (wave * PBLK + LI) * 512), 16,
+                                                   ok ? (uint32_t)t * (uint32_t)pld * 2u + p_off[LI] : WG_OOB, 0, 0, 0);
+        } else {
+          constexpr int J = LI - PBLK;
+          const int t = p.t0 + q_row[J];
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (wg_lds_ptr)(p.sq + (wave * QBLK + J) * 512), 16,
+                                                   t < nt_rows ? (uint32_t)t * (uint32_t)g.ldq * 2u + q_off[J] : WG_OOB,
+                                                   0, 0, 0);
+        }
+      });
+    }
+  };
   auto issue = [&](int step, bf16_t* sp, bf16_t* sq) {
-    const int t0 = step * WG_KT;  // relative to t_begin
-    const bool pad = step >= KS;
-#pragma unroll
-    for (int jb = 0; jb < PBLK; ++jb) {
-      const int t = t0 + p_row[jb];
-      const bool ok = !pad && t < nt_rows && p_off[jb] != WG_OOB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rp, (wg_lds_ptr)(sp + (wave * PBLK + jb) * 512), 16,
-                                               ok ? (uint32_t)t * (uint32_t)pld * 2u + p_off[jb] : WG_OOB, 0, 0,
-                                               0);
-    }
-#pragma unroll
-    for (int jb = 0; jb < QBLK; ++jb) {
-      const int t = t0 + q_row[jb];
-      const bool ok = !pad && t < nt_rows;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (wg_lds_ptr)(sq + (wave * QBLK + jb) * 512), 16,
-                                               ok ? (uint32_t)t * (uint32_t)g.ldq * 2u + q_off[jb] : WG_OOB, 0,
-                                               0, 0);
-    }
+    issue_range(plan(step, sp, sq), std::integral_constant<int, 0>{}, std::integral_constant<int, LOADS>{});
   };
 
   f32x16_t acc[FM][FN];
@@ -184,31 +230,38 @@ __global__ __launch_bounds__(WG_THREADS) void k_wgrad(WgradArgs g, int mtiles, i
     else
       asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0])::"memory");
   };
-  auto compute = [&](const bf16_t* sp, const bf16_t* sq) {
+  constexpr int KSTEP = WG_KT / 16, PER = (LOADS + KSTEP - 1) / KSTEP;
+  auto compute = [&](const bf16_t* sp, const bf16_t* sq, const Plan& nx) {
     load_frags(sp, sq, 0, fa[0], fb[0]);
     wait_frags(fa[0], fb[0]);
-#pragma unroll
-    for (int kk = 0; kk < WG_KT / 16; ++kk) {
-      const int cb = kk & 1, nb = cb ^ 1;
-      if (kk + 1 < WG_KT / 16) load_frags(sp, sq, kk + 1, fa[nb], fb[nb]);
+    static_for<0, KSTEP>([&](auto kkc) {
+      constexpr int KK = decltype(kkc)::value, CB = KK & 1, NB = CB ^ 1;
+      if constexpr (KK + 1 < KSTEP) load_frags(sp, sq, KK + 1, fa[NB], fb[NB]);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = mfma32x32x16(__builtin_bit_cast(uint4, fa[cb][i]), __builtin_bit_cast(uint4, fb[cb][j]),
+          acc[i][j] = mfma32x32x16(__builtin_bit_cast(uint4, fa[CB][i]), __builtin_bit_cast(uint4, fb[CB][j]),
                                    acc[i][j]);
-      if (kk + 1 < WG_KT / 16) wait_frags(fa[nb], fb[nb]);
-    }
+      constexpr int B0 = KK * PER < LOADS ? KK * PER : LOADS;
+      constexpr int B1 = (KK + 1) * PER < LOADS ? (KK + 1) * PER : LOADS;
+      issue_range(nx, std::integral_constant<int, B0>{}, std::integral_constant<int, B1>{});
+      if constexpr (KK + 1 < KSTEP) wait_frags(fa[NB], fb[NB]);
+    });
   };
 
   auto step = [&](int s, const bf16_t* cp, const bf16_t* cq, bf16_t* np, bf16_t* nq) {
-    if (s + 1 < total)
+    // step s must be complete; only step s + 1 (if it loads) may be in flight
+    if (s + 1 < KS)
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS) : "memory");
     else
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
-    if (s + 2 < total) issue(s + 2, np, nq);
-    if (s < KS) compute(cp, cq);
+    const Plan nx = plan(s + 2, np, nq);  // not live past KS
+    if (s < KS)
+      compute(cp, cq, nx);
+    else
+      issue_range(nx, std::integral_constant<int, 0>{}, std::integral_constant<int, LOADS>{});
   };
 
   if (total > 0) {
