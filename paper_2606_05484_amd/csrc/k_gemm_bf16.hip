@@ -52,6 +52,142 @@ struct TnSmem {
   bf16_t w[BN * GK];
 };
 
+// Fragment geometry shared by the kernels: per 16-wide k-step kk the lane
+// reads row lane % 32 (+ multiples of 16, which keep the swizzle), logical
+// chunk 2 kk + lane / 32 of a 128 B-row stage.
+__device__ __forceinline__ uint32_t tn_koff(int kk, int lane) {
+  return (uint32_t)((lane & 31) * (GK * 2) + 16 * ((2 * kk + (lane >> 5)) ^ (((lane & 31) >> 1) & 7)));
+}
+
+// The products of one GK-deep stage for a wave's 64 x BN/2 sub-tile: A
+// fragments at LDS byte address ba (token rows), W fragments at bw.
+// acc[i][j] is the transposed 32 x 32 block: rows = output columns (W
+// fragment j), columns = tokens (A fragment i).  Fragment reads are inline
+// asm (see lds_read_b128), double-buffered in registers: the reads of
+// k-step kk + 1 are in flight while the matrix units work on kk.  After the
+// products of k-step kk, after(kk) runs (the caller issues a share of the
+// next stage's loads there).
+template <int BN, typename After>
+__device__ __forceinline__ void tn_products(f32x16_t (&acc)[2][BN / 64], uint32_t ba, uint32_t bw,
+                                            const uint32_t (&koff)[GK / 16], After&& after) {
+  constexpr int FM = 2, FN = BN / 64, KSTEP = GK / 16;
+  u32x4 fr[2][FM + FN];
+  auto load = [&](int kk, u32x4 (&f)[FM + FN]) {
+    static_for<0, FM>([&](auto ic) {
+      constexpr int I = decltype(ic)::value;
+      f[I] = lds_read_b128<I * 32 * GK * 2>(ba + koff[kk]);
+    });
+    static_for<0, FN>([&](auto jc) {
+      constexpr int J = decltype(jc)::value;
+      f[FM + J] = lds_read_b128<J * 32 * GK * 2>(bw + koff[kk]);
+    });
+  };
+  load(0, fr[0]);
+  lds_wait(fr[0]);
+  static_for<0, KSTEP>([&](auto kkc) {
+    constexpr int KK = decltype(kkc)::value, CB = KK & 1;
+    if constexpr (KK + 1 < KSTEP) load(KK + 1, fr[CB ^ 1]);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(as_uint4(fr[CB][FM + j]), as_uint4(fr[CB][i]), acc[i][j]);
+    after(kkc);
+    if constexpr (KK + 1 < KSTEP) lds_wait(fr[CB ^ 1]);
+  });
+}
+
+// Epilogue of one 128 x BN output tile (columns nt BN ..): lane l holds
+// token (l % 32) of fragment i and, for q = 0..3, output columns
+// 8q + 4(l / 32) + 0..3 of fragment j.  fp32 results leave as 16 B stores
+// (optionally accumulating).  bf16: after the cross-half swap lane (t, h)
+// holds the 16 B segment of token t covering columns 8(2q + h) .. +7 of
+// fragment j (q = 0, 1); segments are staged through STG_BYTES of LDS at
+// byte address stg (free for the duration: the caller syncs the workgroup
+// before), 128 B rows with chunks swizzled by ((row >> 1) & 7), then
+// stored as full rows.  The accumulators are cleared.
+template <int BN, int STG_BYTES>
+__device__ __forceinline__ void tn_epilogue(f32x16_t (&acc)[2][BN / 64], const TnArgs& g, char* obase, int m0, int nt,
+                                            uint32_t stg_base, int wave, int lane) {
+  constexpr int FM = 2, FN = BN / 64;
+  const int wm = wave >> 1, wn = wave & 1, half = lane >> 5;
+  if (g.out_f32) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int t = m0 + wm * 64 + i * 32 + (lane & 31);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        if (t < g.M) {
+          float* o = (float*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + j * 32 + 4 * half;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+            if (g.out_accum) {
+              const float4 p = *(const float4*)(o + 8 * q);
+              v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+            }
+            *(float4*)(o + 8 * q) = v;
+          }
+        }
+        acc[i][j] = f32x16_t{};
+      }
+    }
+    return;
+  }
+  constexpr int HALVES = FN >= 2 ? FN / 2 : 1;
+  constexpr int FJ = FN >= 2 ? 2 : 1;            // fragments per half
+  constexpr int COLS = FJ * 32, CPR = COLS / 8;  // staged columns, 16 B chunks per row
+  static_assert(4 * 64 * COLS * 2 <= STG_BYTES, "staging fits the free buffer");
+  const uint32_t stg = stg_base + wave * (64 * COLS * 2);
+#pragma unroll
+  for (int h = 0; h < HALVES; ++h) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int jj = 0; jj < FJ; ++jj) {
+        const f32x16_t& c = acc[i][h * FJ + jj];
+        uint32_t p[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) p[e] = pack_bf2(c[2 * e], c[2 * e + 1]);
+        // p[2g], p[2g+1]: columns 8g + 4h + 0..3; swap groups (0,1) and (2,3)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int w = 0; w < 2; ++w) {
+            const auto sw2 = __builtin_amdgcn_permlane32_swap(p[4 * q + w], p[4 * q + 2 + w], false, false);
+            p[4 * q + w] = sw2[0];
+            p[4 * q + 2 + w] = sw2[1];
+          }
+        const int row = i * 32 + (lane & 31);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int ch = jj * 4 + 2 * q + half;
+          lds_write_b128(stg + row * COLS * 2 + 16 * (ch ^ ((row >> 1) & (CPR - 1))),
+                         u32x4{p[4 * q], p[4 * q + 1], p[4 * q + 2], p[4 * q + 3]});
+        }
+      }
+    u32x4 v[CPR];
+#pragma unroll
+    for (int q = 0; q < CPR; ++q) {
+      const int c = lane + 64 * q;
+      const int row = c / CPR, ch = c % CPR;
+      v[q] = lds_read_b128(stg + row * COLS * 2 + 16 * (ch ^ ((row >> 1) & (CPR - 1))));
+    }
+    lds_wait(v);
+#pragma unroll
+    for (int q = 0; q < CPR; ++q) {
+      const int c = lane + 64 * q;
+      const int row = c / CPR, ch = c % CPR;
+      const int t = m0 + wm * 64 + row;
+      if (t < g.M)
+        *(uint4*)((bf16_t*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + h * COLS + ch * 8) = as_uint4(v[q]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
+}
+
 // NS pipeline stages (2 or 3), one __shared__ array each.
 template <int BN, int NS, bool FULLK>
 __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_wg) {
@@ -211,46 +347,19 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
 
-  // acc[i][j] is the transposed 32 x 32 block: rows = output columns
-  // (W fragment j), columns = tokens (A fragment i).  Fragment reads are
-  // inline asm (see lds_read_b128), double-buffered in registers: the reads
-  // of k-step kk + 1 are in flight while the matrix units work on kk.  The
-  // lane's row is lane % 32 (+ multiples of 16, which keep the swizzle), its
-  // logical chunk 2 kk + lane / 32.
-  const int half = lane >> 5;
   uint32_t koff[GK / 16];
 #pragma unroll
-  for (int kk = 0; kk < GK / 16; ++kk)
-    koff[kk] = (uint32_t)((lane & 31) * (GK * 2) + 16 * ((2 * kk + half) ^ (((lane & 31) >> 1) & 7)));
+  for (int kk = 0; kk < GK / 16; ++kk) koff[kk] = tn_koff(kk, lane);
   // Products of one stage; the next step's loads (if any) are issued in
   // KSTEP groups after the products of each 16-wide k-step.
   constexpr int KSTEP = GK / 16, PER = (LOADS + KSTEP - 1) / KSTEP;
   auto compute = [&](const bf16_t* sa, const bf16_t* sw, const Plan& nx, bool has_next) {
     const uint32_t ba = lds_addr(sa) + wm * 64 * (GK * 2), bw = lds_addr(sw) + wn * (BN / 2) * (GK * 2);
-    u32x4 fr[2][FM + FN];
-    auto load = [&](int kk, u32x4 (&f)[FM + FN]) {
-      static_for<0, FM>([&](auto ic) {
-        constexpr int I = decltype(ic)::value;
-        f[I] = lds_read_b128<I * 32 * GK * 2>(ba + koff[kk]);
-      });
-      static_for<0, FN>([&](auto jc) {
-        constexpr int J = decltype(jc)::value;
-        f[FM + J] = lds_read_b128<J * 32 * GK * 2>(bw + koff[kk]);
-      });
-    };
-    load(0, fr[0]);
-    lds_wait(fr[0]);
-    static_for<0, KSTEP>([&](auto kkc) {
-      constexpr int KK = decltype(kkc)::value, CB = KK & 1;
-      if constexpr (KK + 1 < KSTEP) load(KK + 1, fr[CB ^ 1]);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32x32x16(as_uint4(fr[CB][FM + j]), as_uint4(fr[CB][i]), acc[i][j]);
+    tn_products<BN>(acc, ba, bw, koff, [&](auto kkc) {
+      constexpr int KK = decltype(kkc)::value;
       constexpr int B0 = KK * PER < LOADS ? KK * PER : LOADS;
       constexpr int B1 = (KK + 1) * PER < LOADS ? (KK + 1) * PER : LOADS;
       if (has_next) issue_range(nx, std::integral_constant<int, B0>{}, std::integral_constant<int, B1>{});
-      if constexpr (KK + 1 < KSTEP) lds_wait(fr[CB ^ 1]);
     });
   };
 
@@ -290,92 +399,161 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
         step(s + 1, ks + 1, S1.a, S1.w, S0.a, S0.w);
       }
     }
-    // epilogue: lane l holds token (l % 32) of fragment i and, for g = 0..3,
-    // output columns 8g + 4(l / 32) + 0..3 of fragment j
-    const int nt = nt0 + tile;
-    if (g.out_f32) {
+    // epilogue, staging bf16 results through the buffer consumed by the
+    // tile's last step (no DMA targets it before the next tile's first step)
+    if (!g.out_f32) __builtin_amdgcn_s_barrier();  // every wave is done reading that buffer
+    tn_epilogue<BN, (GM + BN) * GK * 2>(acc, g, obase, m0, nt0 + tile, lds_addr(NS == 3 ? S2a : S1.a), wave, lane);
+  }
+#endif
+}
+
+// A-resident variant for a short K walked over many output tiles (decode,
+// encode_bwd: K = r (+ k), N = d): the workgroup's 128 token rows of
+// [A | anchors] (KS <= AKS stages of 128 x 64) are loaded into LDS once and
+// stay there while the W stages of its N tiles stream through an NSW-deep
+// ring, so A is read from memory once instead of once per tile.  Requires
+// every K dimension to be a multiple of GK, no split-K and bf16 or fp32
+// output as the streaming kernel; the bf16 epilogue stages through the W
+// buffer the tile's last step consumed.
+template <int BN, int NSW, int AKS>
+__global__ __launch_bounds__(GTHREADS) void k_gemm_tn_ares(TnArgs g, int ntiles_per_wg) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  static_assert(NSW >= 2 && NSW <= 4, "W stages");
+  static_assert(AKS * GM * GK * 2 + NSW * BN * GK * 2 <= 160 * 1024, "LDS");
+  constexpr int FN = BN / 64;
+  constexpr int ABLK = GM / 8 / 4;  // A: 1 KiB blocks (8 rows) per wave per stage
+  constexpr int WBLK = BN / 8 / 4;  // W: 1 KiB blocks per wave per stage
+  __shared__ __attribute__((aligned(1024))) bf16_t SA[AKS * GM * GK];
+  __shared__ __attribute__((aligned(1024))) bf16_t SW[NSW][BN * GK];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.x * GM;
+  const int nt0 = blockIdx.y * ntiles_per_wg;
+  const int ntiles = min(ntiles_per_wg, g.N / BN - nt0);
+  const int ka_steps = g.Ka / GK, KS = ka_steps + g.Kg / GK;
+  const int total = ntiles * KS;
+
+  const int mrows = min(GM, g.M - m0);
+  const __amdgpu_buffer_rsrc_t ra = rsrc(g.A + (int64_t)m0 * g.lda, (uint64_t)(mrows > 0 ? mrows : 0) * g.lda * 2);
+  const __amdgpu_buffer_rsrc_t rt = rsrc(g.T, g.T ? (uint64_t)g.V * g.ldt * 2 : 0);
+  const __amdgpu_buffer_rsrc_t rw = rsrc(g.W, (uint64_t)g.N * g.ldw * 2);
+
+  // lane offsets, as in the streaming kernel (block parity swizzle)
+  const int lrow = lane >> 3;
+  const uint32_t lchp[2] = {(uint32_t)((lane & 7) ^ (lane >> 4)), (uint32_t)((lane & 7) ^ (4 + (lane >> 4)))};
+  uint32_t w_off[WBLK];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int t = m0 + wm * 64 + i * 32 + (lane & 31);
+  for (int j = 0; j < WBLK; ++j) {
+    const int row = 8 * (wave * WBLK + j) + lrow;
+    w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lchp[j & 1];
+  }
+
+  // the resident A tile: stage ks at SA + ks * GM * GK, columns ks GK .. of
+  // [A | anchors]; the loads go first, so waiting for W stage 0 covers them
+  for (int ks = 0; ks < KS; ++ks) {
+    const bool gath = ks >= ka_steps;
+    const int soff = (gath ? (ks - ka_steps) * GK : ks * GK) * 2;
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          if (t < g.M) {
-            float* o = (float*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + j * 32 + 4 * half;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              float4 v = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-              if (g.out_accum) {
-                const float4 p = *(const float4*)(o + 8 * q);
-                v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
-              }
-              *(float4*)(o + 8 * q) = v;
-            }
-          }
-          acc[i][j] = f32x16_t{};
-        }
+    for (int j = 0; j < ABLK; ++j) {
+      const int row = 8 * (wave * ABLK + j) + lrow;
+      const uint32_t lc = lchp[j & 1];
+      const lds_ptr dst = (lds_ptr)(SA + ks * GM * GK + (wave * ABLK + j) * 512);
+      if (gath) {
+        const uint32_t to = m0 + row < g.M ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + 16u * lc
+                                           : OOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, dst, 16, to, soff, 0, 0);
+      } else {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, dst, 16, (uint32_t)row * (uint32_t)g.lda * 2u + 16u * lc, soff,
+                                                 0, 0);
       }
-    } else {
-      // bf16: after the cross-half swap lane (t, h) holds the 16 B segment
-      // of token t covering columns 8(2q + h) .. +7 of fragment j (q = 0, 1).
-      // Segments are staged through the stage buffer consumed last (no DMA
-      // targets it before the next tile's first step), 128 B rows with
-      // chunks swizzled by ((row >> 1) & 7), then stored as full rows.
-      __builtin_amdgcn_s_barrier();  // every wave is done reading that buffer
-      constexpr int HALVES = FN >= 2 ? FN / 2 : 1;
-      constexpr int FJ = FN >= 2 ? 2 : 1;  // fragments per half
-      constexpr int COLS = FJ * 32, CPR = COLS / 8;  // staged columns, 16 B chunks per row
-      static_assert(4 * 64 * COLS <= GM * GK + BN * GK, "staging fits the stage buffer");
-      // the buffer consumed by the tile's last step: S2 (NS = 3) or S1 (NS = 2)
-      const uint32_t stg = lds_addr(NS == 3 ? S2a : S1.a) + wave * (64 * COLS * 2);
-#pragma unroll
-      for (int h = 0; h < HALVES; ++h) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int jj = 0; jj < FJ; ++jj) {
-            const f32x16_t& c = acc[i][h * FJ + jj];
-            uint32_t p[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) p[e] = pack_bf2(c[2 * e], c[2 * e + 1]);
-            // p[2g], p[2g+1]: columns 8g + 4h + 0..3; swap groups (0,1) and (2,3)
-#pragma unroll
-            for (int q = 0; q < 2; ++q)
-#pragma unroll
-              for (int w = 0; w < 2; ++w) {
-                const auto sw2 = __builtin_amdgcn_permlane32_swap(p[4 * q + w], p[4 * q + 2 + w], false, false);
-                p[4 * q + w] = sw2[0];
-                p[4 * q + 2 + w] = sw2[1];
-              }
-            const int row = i * 32 + (lane & 31);
-#pragma unroll
-            for (int q = 0; q < 2; ++q) {
-              const int ch = jj * 4 + 2 * q + half;
-              lds_write_b128(stg + row * COLS * 2 + 16 * (ch ^ ((row >> 1) & (CPR - 1))),
-                             u32x4{p[4 * q], p[4 * q + 1], p[4 * q + 2], p[4 * q + 3]});
-            }
-          }
-        u32x4 v[CPR];
-#pragma unroll
-        for (int q = 0; q < CPR; ++q) {
-          const int c = lane + 64 * q;
-          const int row = c / CPR, ch = c % CPR;
-          v[q] = lds_read_b128(stg + row * COLS * 2 + 16 * (ch ^ ((row >> 1) & (CPR - 1))));
-        }
-        lds_wait(v);
-#pragma unroll
-        for (int q = 0; q < CPR; ++q) {
-          const int c = lane + 64 * q;
-          const int row = c / CPR, ch = c % CPR;
-          const int t = m0 + wm * 64 + row;
-          if (t < g.M)
-            *(uint4*)((bf16_t*)obase + (int64_t)t * g.ldo + nt * BN + wn * (BN / 2) + h * COLS + ch * 8) = as_uint4(v[q]);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
     }
+  }
+
+  // W step s: tile nt0 + s / KS, k-step s % KS (planned in order)
+  int pl_ks = 0, pl_nt = nt0, pl_s = 0;
+  struct WPlan {
+    bf16_t* sw;
+    int soff;
+    bool live;
+  };
+  auto plan_next = [&](bf16_t* sw) {
+    WPlan p;
+    p.sw = sw;
+    const int ks = __builtin_amdgcn_readfirstlane(pl_ks), nt = __builtin_amdgcn_readfirstlane(pl_nt);
+    p.live = __builtin_amdgcn_readfirstlane(pl_s) < total;
+    ++pl_s;
+    if (++pl_ks == KS) {
+      pl_ks = 0;
+      ++pl_nt;
+    }
+    const int wcol0 = ks < ka_steps ? ks * GK : g.Ka + (ks - ka_steps) * GK;
+    p.soff = (int)((uint32_t)nt * BN * (uint32_t)g.ldw * 2u + (uint32_t)wcol0 * 2u);
+    return p;
+  };
+  auto issue_range = [&](const WPlan& p, auto b0c, auto b1c) {
+    if (!p.live) return;
+    static_for<decltype(b0c)::value, decltype(b1c)::value>([&](auto jc) {
+      constexpr int J = decltype(jc)::value;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(p.sw + (wave * WBLK + J) * 512), 16, w_off[J], p.soff, 0,
+                                               0);
+    });
+  };
+
+  f32x16_t acc[2][FN];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
+  uint32_t koff[GK / 16];
+#pragma unroll
+  for (int kk = 0; kk < GK / 16; ++kk) koff[kk] = tn_koff(kk, lane);
+  constexpr int KSTEP = GK / 16, PER = (WBLK + KSTEP - 1) / KSTEP;
+  char* obase = (char*)g.out;
+  const uint32_t sa0 = lds_addr(SA) + wm * 64 * (GK * 2);
+
+  // W buffer u at LDS byte address swb + u * WSTG (u uniform, run time)
+  constexpr uint32_t WSTG = BN * GK * 2;
+  const uint32_t swb = lds_addr(&SW[0][0]);
+  auto wbuf = [&](int u) { return (bf16_t*)&SW[0][0] + u * (BN * GK); };
+  // prologue: W stages 0 .. NSW - 2 in flight
+  static_for<0, NSW - 1>([&](auto uc) {
+    constexpr int U = decltype(uc)::value;
+    issue_range(plan_next(wbuf(U)), std::integral_constant<int, 0>{}, std::integral_constant<int, WBLK>{});
+  });
+  // step s consumes W buffer u = s % NSW and issues W step s + NSW - 1 into
+  // buffer (s - 1) % NSW, consumed at step s - 1
+  int s = 0, u = 0;
+  for (int tile = 0; tile < ntiles; ++tile) {
+    for (int ks = 0; ks < KS; ++ks, ++s) {
+      // W step s complete; W steps s + 1 .. s + NSW - 2 (those that exist) may be in flight
+      const int ahead = min(NSW - 2, total - 1 - s);
+      if constexpr (NSW >= 4) {
+        if (ahead >= 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * WBLK) : "memory");
+        else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WBLK) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      } else if constexpr (NSW == 3) {
+        if (ahead >= 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WBLK) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      } else {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      }
+      __builtin_amdgcn_s_barrier();
+      const int un = u == 0 ? NSW - 1 : u - 1;
+      const WPlan nx = plan_next(wbuf(un));
+      tn_products<BN>(acc, sa0 + ks * (GM * GK * 2), swb + u * WSTG + wn * (BN / 2) * (GK * 2), koff, [&](auto kkc) {
+        constexpr int KK = decltype(kkc)::value;
+        constexpr int B0 = KK * PER < WBLK ? KK * PER : WBLK;
+        constexpr int B1 = (KK + 1) * PER < WBLK ? (KK + 1) * PER : WBLK;
+        issue_range(nx, std::integral_constant<int, B0>{}, std::integral_constant<int, B1>{});
+      });
+      if (ks + 1 < KS) u = u + 1 == NSW ? 0 : u + 1;
+    }
+    // stage through the W buffer the tile's last step consumed
+    if (!g.out_f32) __builtin_amdgcn_s_barrier();  // every wave is done reading it
+    tn_epilogue<BN, BN * GK * 2>(acc, g, obase, m0, nt0 + tile, swb + u * WSTG, wave, lane);
+    u = u + 1 == NSW ? 0 : u + 1;
   }
 #endif
 }
@@ -392,6 +570,17 @@ hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
   int per = 1;
   while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) * zs >= 256) per *= 2;
   dim3 grid(mt, (nt + per - 1) / per, zs);
+  // a short K walked over several tiles: keep A resident (up to 4 stages,
+  // leaving LDS for a three-deep W ring; with a two-deep ring the W loads
+  // of a step have only the step before to land, which costs more than
+  // re-reading A)
+  const int KS = (g.Ka + g.Kg) / GK;
+  if constexpr (BN == 256) {
+    if (fullk && g.kz == 0 && per >= 2 && KS <= 4) {
+      hipLaunchKernelGGL((k_gemm_tn_ares<BN, 3, 4>), grid, dim3(GTHREADS), 0, s, g, per);
+      return hipGetLastError();
+    }
+  }
   if (fullk)
     hipLaunchKernelGGL((k_gemm_tn<BN, NS, true>), grid, dim3(GTHREADS), 0, s, g, per);
   else

@@ -235,3 +235,30 @@ def test_c4_full_size_sampled():
     e = rel_fro(res["dU"], dUd + dUe)
     print("c4 dU rel err", e)
     assert e <= BF16_TOL
+
+
+@pytest.mark.slow
+def test_large_ragged_tail_sampled():
+    """A token count that is not a multiple of the 128-token tile at the
+    benchmark's widths (d=2048, r=256, k=128; no RVQ): the products that walk
+    many output tiles per workgroup (decode, encode_bwd) run in the same
+    launch configuration as at full size, with a partial last tile.  Every
+    row of the last tile and 256 others are checked against the oracle."""
+    x = _x("c4", T=32768 - 37, L=0, K=0)
+    res = _chain(x)
+    X, A, B = f64(x, "X"), f64(x, "A"), f64(x, "B")
+    T = x["T"]
+    last = np.arange(T - T % 128, T)
+    rows = np.concatenate([last, np.random.default_rng(5).choice(T - T % 128, 256, replace=False)])
+    Z_ref = ocodec.project(X[rows], x["ids"][rows], x["U"], A, B, "ambient", "bf16")
+    Zg = host_f64(res["payload"])
+    assert rel_fro(Zg[rows], Z_ref) <= BF16_TOL
+    Xh_ref = ocodec.decode(Zg[rows], x["ids"][rows], x["U"], A, B, None, "ambient", "bf16")
+    e = rel_fro(res["Xh"][rows], Xh_ref)
+    print("Xhat rel err", e)
+    assert np.isfinite(res["Xh"]).all() and e <= BF16_TOL
+    P = ocodec._projector(x["U"], "bf16")
+    assert rel_fro(res["dZ"][rows], f64(x, "dXhat")[rows] @ P) <= BF16_TOL
+    e = rel_fro(res["dX"][rows], f64(x, "dZ")[rows] @ P.T)
+    print("dX rel err", e)
+    assert np.isfinite(res["dX"]).all() and e <= BF16_TOL
