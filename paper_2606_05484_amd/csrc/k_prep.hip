@@ -177,28 +177,33 @@ __device__ __forceinline__ void small_gemm_tile(int bx, int by, const PrepJob& j
   f32x16_t acc = f32x16_t{};
   // batches of up to four k-steps: all loads of a batch are issued before
   // its products, so their latencies overlap
+  // (every load of a batch is issued before the first conversion: a
+  // conversion right after its own loads would wait for them one k-step at
+  // a time)
   constexpr int NB = 4;
   for (int kb = 16 * wave; kb < j.Kd; kb += 64 * NB) {
-    uint4 a[NB], b[NB];
+    uint4 a[NB];
+    float qv[NB][8];
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
       const int k0 = min(kb + 64 * u, j.Kd - 16);  // past the end: a repeat, not used
       a[u] = *(const uint4*)(P + k0 + 8 * half);
-      float qv[8];
       if (j.qt) {
         const float4* q4 = (const float4*)(j.Q + (int64_t)c * j.ldq + k0 + 8 * half);
         const float4 x0 = q4[0], x1 = q4[1];
-        qv[0] = x0.x; qv[1] = x0.y; qv[2] = x0.z; qv[3] = x0.w; qv[4] = x1.x; qv[5] = x1.y; qv[6] = x1.z; qv[7] = x1.w;
+        qv[u][0] = x0.x; qv[u][1] = x0.y; qv[u][2] = x0.z; qv[u][3] = x0.w;
+        qv[u][4] = x1.x; qv[u][5] = x1.y; qv[u][6] = x1.z; qv[u][7] = x1.w;
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) qv[e] = j.Q[(int64_t)(k0 + 8 * half + e) * j.ldq + c];
+        for (int e = 0; e < 8; ++e) qv[u][e] = j.Q[(int64_t)(k0 + 8 * half + e) * j.ldq + c];
       }
-      b[u] = make_uint4(pack_bf2(qv[0], qv[1]), pack_bf2(qv[2], qv[3]), pack_bf2(qv[4], qv[5]),
-                        pack_bf2(qv[6], qv[7]));
     }
 #pragma unroll
-    for (int u = 0; u < NB; ++u)
-      if (kb + 64 * u < j.Kd) acc = mfma32x32x16(a[u], b[u], acc);
+    for (int u = 0; u < NB; ++u) {
+      const uint4 b = make_uint4(pack_bf2(qv[u][0], qv[u][1]), pack_bf2(qv[u][2], qv[u][3]),
+                                 pack_bf2(qv[u][4], qv[u][5]), pack_bf2(qv[u][6], qv[u][7]));
+      if (kb + 64 * u < j.Kd) acc = mfma32x32x16(a[u], b, acc);
+    }
   }
   // acc e: row 8(e/4) + 4 half + e%4 of the tile, column lane % 32
   if (wave > 0) {
