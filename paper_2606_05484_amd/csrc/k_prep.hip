@@ -97,16 +97,36 @@ __device__ __forceinline__ void assemble_block(int bx, const AssembleArgs& a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) { v[2 * q] = bf2f(w[q] & 0xFFFFu); v[2 * q + 1] = bf2f(w[q] >> 16); }
     } else {
+      // all codes, then all codeword rows, then the sum in stage order: the
+      // loads of every stage are in flight together (L <= 8)
+      constexpr int LMAX = 8;
+      int code[LMAX];
+#pragma unroll
+      for (int l = 0; l < LMAX; ++l) {
+        if (l < a.L) {
+          const int c = a.code_bytes == 1 ? ((const uint8_t*)a.codes)[(int64_t)t * a.L + l]
+                                          : ((const uint16_t*)a.codes)[(int64_t)t * a.L + l];
+          code[l] = c < a.K ? c : a.K - 1;
+        }
+      }
+      float4 cw[LMAX][2];
+#pragma unroll
+      for (int l = 0; l < LMAX; ++l) {
+        if (l < a.L) {
+          const float4* p = (const float4*)(a.C + ((int64_t)l * a.K + code[l]) * a.r + c0);
+          cw[l][0] = p[0];
+          cw[l][1] = p[1];
+        }
+      }
 #pragma unroll
       for (int q = 0; q < 8; ++q) v[q] = 0.f;
-      for (int l = 0; l < a.L; ++l) {
-        int code = a.code_bytes == 1 ? ((const uint8_t*)a.codes)[(int64_t)t * a.L + l]
-                                     : ((const uint16_t*)a.codes)[(int64_t)t * a.L + l];
-        code = code < a.K ? code : a.K - 1;
-        const float4* cw = (const float4*)(a.C + ((int64_t)l * a.K + code) * a.r + c0);
-        const float4 p = cw[0], q4 = cw[1];
-        v[0] += p.x; v[1] += p.y; v[2] += p.z; v[3] += p.w;
-        v[4] += q4.x; v[5] += q4.y; v[6] += q4.z; v[7] += q4.w;
+#pragma unroll
+      for (int l = 0; l < LMAX; ++l) {
+        if (l < a.L) {
+          const float4 p = cw[l][0], q4 = cw[l][1];
+          v[0] += p.x; v[1] += p.y; v[2] += p.z; v[3] += p.w;
+          v[4] += q4.x; v[5] += q4.y; v[6] += q4.z; v[7] += q4.w;
+        }
       }
     }
     if (a.Bc != nullptr) {
