@@ -58,8 +58,12 @@ __device__ __forceinline__ void transpose_tile(int bx, int by, const void* __res
   }
 }
 
-// One wave per (stage, codeword slot of a 64-codeword chunk): bf16 copy and
-// the fp32 squared norm, laid out per chunk as 64 consecutive floats.
+// One wave per (stage, codeword slot of a 64-codeword chunk): the bf16 copy
+// with the squared norm appended as three bf16 pieces (rows of r + 16), and
+// the fp32 squared norm, laid out per chunk as 64 consecutive floats.  The
+// pieces: hi = bf16(s), mid = bf16(s - hi), lo = bf16(s - hi - mid); each
+// difference is exact in fp32 and an fp32 value has 24 significant bits, so
+// hi + mid + lo = s exactly, in any order of addition.
 __device__ __forceinline__ void prep_codebook_block(int bx, const float* __restrict__ C, int L, int K, int r,
                                                     bf16_t* __restrict__ Cb, float* __restrict__ meta) {
   const int nch = (K + 63) / 64;
@@ -67,16 +71,24 @@ __device__ __forceinline__ void prep_codebook_block(int bx, const float* __restr
   if (w >= L * nch * 64) return;
   const int l = w / (nch * 64), slot = w % (nch * 64);
   const int j = slot;  // codeword index within stage l
+  const int cols = rvq_cb_cols(r);
   float s = 0.f;
   if (j < K) {
     const float* row = C + ((int64_t)l * K + j) * r;
     for (int c = lane; c < r; c += 64) {
       const float v = row[c];
       s += v * v;
-      Cb[((int64_t)l * K + j) * r + c] = (bf16_t)f2bf(v);
+      Cb[((int64_t)l * K + j) * cols + c] = (bf16_t)f2bf(v);
     }
   }
   s = wave_sum(s);
+  if (j < K && lane < 16) {
+    const uint32_t hi = f2bf(s);
+    const float r1 = s - bf2f(hi);
+    const uint32_t mid = f2bf(r1);
+    const uint32_t lo = f2bf(r1 - bf2f(mid));
+    Cb[((int64_t)l * K + j) * cols + r + lane] = (bf16_t)(lane == 0 ? hi : lane == 1 ? mid : lane == 2 ? lo : 0u);
+  }
   if (lane == 0) meta[((int64_t)l * nch + j / 64) * 64 + (j % 64)] = s;
 }
 

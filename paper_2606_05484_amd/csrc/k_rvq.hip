@@ -4,8 +4,11 @@
 //
 // Decision procedure (exact with respect to the fp32 residual):
 //   screen  s~_j = ||C_j||^2 - 2 R~ . C~_j on the bf16 matrix units with
-//           R~ = bf16(R), C~ = bf16(C): the accumulator starts at ||C_j||^2
-//           (fp32) and the second operand is bf16(-2R) = -2 R~ exactly.  The
+//           R~ = bf16(R), C~ = bf16(C): the first k-step of every tile
+//           multiplies three extra codeword columns (||C_j||^2 split into
+//           three bf16 pieces that sum to it exactly) by ones, so the
+//           accumulator holds ||C_j||^2 (fp32, exact) before the products
+//           with the second operand bf16(-2R) = -2 R~ (exact) follow.  The
 //           true s_j = ||C_j||^2 - 2 R.C_j differs from s~_j by at most
 //           Delta = k1 ||R|| max_j||C_j|| + k2 max_j||C_j||^2 (bf16 rounding
 //           of both operands, fp32 accumulation and norms, the index tag
@@ -21,15 +24,16 @@
 //   pass 2  (only when a token of the workgroup is ambiguous) re-screens
 //           and lists every candidate; the candidates are rescored exactly
 //           in fp32 as sum_c (R_c - C_jc)^2.
-// The residual is rebuilt in fp32 for every round from Z0 and the codes
-// already chosen, so screening and rescoring see the same R.
+// The fp32 residual stays in registers across rounds, updated as
+// R_{l+1} = R_l - C_l[code_l]: the operation sequence the rescoring uses to
+// rebuild it from Z0 and the codes, so both see the same R.
 //
 // Layout: a workgroup of 4 waves owns 128 tokens, 32 per wave.  A wave keeps
 // its tokens' bf16(-2R) as the B operand of v_mfma_f32_32x32x16_bf16 in
-// registers (tokens along N); 64-codeword chunks of C~ stream through three
-// LDS stages filled by buffer_load ... lds (direct-to-LDS, one __shared__
-// array per stage) as the A operand (codewords along M), together with the
-// chunk's ||C_j||^2 (a wave-private copy, the accumulator's initial value).
+// registers (tokens along N); 64-codeword chunks of C~ (with the norm
+// columns) stream through three LDS stages filled by buffer_load ... lds
+// (direct-to-LDS, one __shared__ array per stage) as the A operand
+// (codewords along M).
 // Each lane thus sees the scores of ONE token for 16 codewords per tile;
 // the fold of one tile into (m1, m2) overlaps the matrix products of the
 // next.  The two lane halves that share a token merge at the end of a pass.
@@ -49,11 +53,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rq_rsrc(const void* base, uint
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, n, 0x00020000);
 }
 
-// Codeword rows are stored 2R + 16 bytes apart, so the 16 rows that read one
-// 16 B column chunk of a fragment start 4 banks apart: conflict-free reads
-// whose addresses differ per k-step by an immediate offset only.
+// Codeword rows (R + 16 bf16: the coordinates, then the norm columns) are
+// stored 2(R + 16) + 16 bytes apart, an odd number of 16 B chunks, so the 16
+// rows that read one 16 B column chunk of a fragment hit 16 distinct bank
+// groups: conflict-free reads whose addresses differ per k-step by an
+// immediate offset only.
 template <int R>
-constexpr int rq_row_bytes() { return 2 * R + 16; }
+constexpr int rq_row_bytes() { return 2 * (R + 16) + 16; }
 template <int R>
 constexpr int rq_blocks() {  // 1 KiB DMA blocks per wave covering the 64 padded rows
   return (RQ_CW * rq_row_bytes<R>() + 4 * 1024 - 1) / (4 * 1024);
@@ -61,9 +67,7 @@ constexpr int rq_blocks() {  // 1 KiB DMA blocks per wave covering the 64 padded
 
 template <int R>
 struct RqStage {
-  bf16_t c[4 * rq_blocks<R>() * 512];  // 64 codeword rows of 2R + 16 bytes (+ tail)
-  float n2[4][256];      // per wave: ||C_j||^2 of the chunk's 64 codewords (wave-private
-                         // copy; the DMA writes 16 B for each of the 64 lanes)
+  bf16_t c[4 * rq_blocks<R>() * 512];  // 64 padded codeword rows (+ tail)
 };
 
 __device__ __forceinline__ int load_code(const void* codes, int cb, int64_t idx) {
@@ -80,9 +84,9 @@ __device__ __forceinline__ float rq_tag(float s, int e) {
 template <int R>
 __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_rvq(RvqArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature (launch stub)
-  constexpr int NK16 = R / 16;
-  constexpr int CPR = R / 8;                       // 16 B chunks per codeword row
-  constexpr int LOADS = rq_blocks<R>() + 1;        // DMA blocks per wave per stage + the norms
+  constexpr int NK16 = R / 16;                     // k-steps of the coordinates
+  constexpr int CPR = (R + 16) / 8;                // 16 B chunks per codeword row
+  constexpr int LOADS = rq_blocks<R>();            // DMA blocks per wave per stage
   __shared__ __attribute__((aligned(1024))) RqStage<R> S0;
   __shared__ __attribute__((aligned(1024))) RqStage<R> S1;
   __shared__ __attribute__((aligned(1024))) RqStage<R> S2;
@@ -110,7 +114,7 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
   for (int jb = 0; jb < CBLK; ++jb) {
     const int byte = (wave * CBLK + jb) * 1024 + lane * 16;
     const int row = byte / RB, ch = (byte % RB) / 16;
-    c_off[jb] = (row < RQ_CW && ch < CPR) ? (uint32_t)row * (uint32_t)(R * 2) + (uint32_t)ch * 16u : RQ_OOB;
+    c_off[jb] = (row < RQ_CW && ch < CPR) ? (uint32_t)row * (uint32_t)((R + 16) * 2) + (uint32_t)ch * 16u : RQ_OOB;
   }
 
   // fp32 residual of the lane's token, columns 16 s + 8 (lane / 32) + 0..7:
@@ -130,30 +134,25 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
   }
 
   for (int l = 0; l < a.L; ++l) {
-    const __amdgpu_buffer_rsrc_t rc = rq_rsrc(a.Cb + (int64_t)l * a.K * R, (uint64_t)a.K * R * 2);
+    const __amdgpu_buffer_rsrc_t rc =
+        rq_rsrc(a.Cb + (int64_t)l * a.K * (R + 16), (uint64_t)a.K * (R + 16) * 2);
     const float* n2g = a.meta + (int64_t)l * nchunks * 64;
-    const __amdgpu_buffer_rsrc_t rm = rq_rsrc(n2g, (uint64_t)nchunks * 64 * 4);
 
-    auto issue = [&](int q, bf16_t* sc, float* sn2) {
+    auto issue = [&](int q, bf16_t* sc) {
       const bool pad = q >= nchunks;
       // rows past K read zeros through the resource bound (K % 32 == 0)
 #pragma unroll
       for (int jb = 0; jb < CBLK; ++jb)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (rq_lds_ptr)(sc + (wave * CBLK + jb) * 512), 16,
                                                  (!pad && c_off[jb] != RQ_OOB)
-                                                     ? (uint32_t)(q * RQ_CW) * (uint32_t)(R * 2) + c_off[jb]
+                                                     ? (uint32_t)(q * RQ_CW) * (uint32_t)((R + 16) * 2) + c_off[jb]
                                                      : RQ_OOB,
                                                  0, 0, 0);
-      // 256 B of norms: lanes 0..15 carry 16 B each, the rest read zeros
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (rq_lds_ptr)(sn2 + wave * 256), 16,
-                                               (!pad && lane < 16) ? (uint32_t)q * 256u + (uint32_t)lane * 16u
-                                                                   : RQ_OOB,
-                                               0, 0, 0);
     };
 
     // ---- the first two chunks are in flight while the residual is built
-    issue(0, S0.c, &S0.n2[0][0]);
-    issue(1, S1.c, &S1.n2[0][0]);
+    issue(0, S0.c);
+    issue(1, S1.c);
 
     // largest ||C_j||^2 of the round (entries past K are zero)
     float n2max = 0.f;
@@ -188,13 +187,16 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
     //   wait | tile 1 products, each followed by a share of the fold of tile 0
     // Reads of an invalid second tile (K % 64 == 32) hit zero-filled rows and
     // are discarded.
-    constexpr int NR = NK16 + 4;                 // 128-bit reads per tile
-    constexpr int RPS = (NR + NK16 - 1) / NK16;  // reads per product step
-    constexpr int FPS = 16 / NK16;               // scores folded per product step
+    // Products per tile: the norm step, then the NK16 coordinate k-steps;
+    // one fragment read per product.
+    constexpr int P = NK16 + 1;
+    constexpr int FPS = (16 + P - 1) / P;  // scores folded per product step
+    // second operand of the norm step: ones in k = 0..2 of the block
+    const uint4 rbn = half == 0 ? make_uint4(0x3F803F80u, 0x00003F80u, 0u, 0u) : make_uint4(0u, 0u, 0u, 0u);
     auto pass = [&](auto&& fbegin, auto&& fscore, auto&& fend, bool first) {
       if (!first) {
-        issue(0, S0.c, &S0.n2[0][0]);
-        issue(1, S1.c, &S1.n2[0][0]);
+        issue(0, S0.c);
+        issue(1, S1.c);
       }
       f32x16_t pend;
 #pragma unroll
@@ -205,60 +207,56 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
         static_for<0, 16>([&](auto ec) { fscore(acc, tile, ec); });
         fend(tile);
       };
-      auto stage = [&](int q, const bf16_t* sc, const float* sn2, bf16_t* nc, float* nn2) {
+      auto stage = [&](int q, const bf16_t* sc, bf16_t* nc) {
         if (q + 1 < total)
           asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS) : "memory");
         else
           asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __builtin_amdgcn_s_barrier();
-        if (q + 2 < total) issue(q + 2, nc, nn2);
+        if (q + 2 < total) issue(q + 2, nc);
         if (q >= nchunks) return;
         const bool t1ok = q * RQ_CW + 32 < a.K;
-        // rows lane % 32 of a tile, 16 B chunk 2s + lane / 32; the lane's
-        // norms are rows 8 e4 + 4 (lane / 32) + 0..3
+        // rows lane % 32 of a tile, 16 B chunk 2s + lane / 32 (s = NK16: the
+        // norm columns)
         const uint32_t cbase = lds_addr(sc) + (lane & 31) * RB + half * 16;
-        const uint32_t nbase = lds_addr(sn2 + wave * 256) + half * 16;
-        u32x4 f0[NR], f1[NR];  // [0..3] norms, [4..] codeword fragments
-        auto read = [&](auto ctc, auto rc, u32x4(&f)[NR]) {
+        u32x4 f0[P], f1[P];  // [0] norm step, [1 + s] coordinate k-step s
+        auto read = [&](auto ctc, auto rc, u32x4(&f)[P]) {
           constexpr int CT = decltype(ctc)::value, RI = decltype(rc)::value;
-          if constexpr (RI < 4)
-            f[RI] = lds_read_b128<CT * 128 + 32 * RI>(nbase);
-          else if constexpr (RI < NR)
-            f[RI] = lds_read_b128<CT * 32 * RB + 32 * (RI - 4)>(cbase);
+          if constexpr (RI == 0)
+            f[0] = lds_read_b128<CT * 32 * RB + 32 * NK16>(cbase);
+          else if constexpr (RI < P)
+            f[RI] = lds_read_b128<CT * 32 * RB + 32 * (RI - 1)>(cbase);
         };
-        auto init = [&](const u32x4(&f)[NR]) {
-          f32x16_t acc;
-#pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4) {
-            acc[4 * e4] = __uint_as_float(f[e4].x);
-            acc[4 * e4 + 1] = __uint_as_float(f[e4].y);
-            acc[4 * e4 + 2] = __uint_as_float(f[e4].z);
-            acc[4 * e4 + 3] = __uint_as_float(f[e4].w);
-          }
-          return acc;
+        auto opnd = [&](auto sc2) -> const uint4& {
+          constexpr int S = decltype(sc2)::value;
+          if constexpr (S == 0)
+            return rbn;
+          else
+            return rb[S - 1];
         };
-        static_for<0, NR>([&](auto rc) { read(std::integral_constant<int, 0>{}, rc, f0); });
+        static_for<0, P>([&](auto rc) { read(std::integral_constant<int, 0>{}, rc, f0); });
         fold_all(pend, pend_tile);
         lds_wait0();
         reg_pin(f0);
-        f32x16_t acc0 = init(f0);
-        static_for<0, NK16>([&](auto sc2) {
+        f32x16_t acc0 = f32x16_t{};
+        static_for<0, P>([&](auto sc2) {
           constexpr int S = decltype(sc2)::value;
-          acc0 = mfma32x32x16(as_uint4(f0[4 + S]), rb[S], acc0);
+          acc0 = mfma32x32x16(as_uint4(f0[S]), opnd(sc2), acc0);
           __builtin_amdgcn_sched_barrier(0);
-          static_for<S * RPS, (S + 1) * RPS>([&](auto rc) { read(std::integral_constant<int, 1>{}, rc, f1); });
+          read(std::integral_constant<int, 1>{}, sc2, f1);
           __builtin_amdgcn_sched_barrier(0);
         });
         lds_wait0();
         reg_pin(f1);
         if (t1ok) {
-          f32x16_t acc1 = init(f1);
+          f32x16_t acc1 = f32x16_t{};
           fbegin();
-          static_for<0, NK16>([&](auto sc2) {
+          static_for<0, P>([&](auto sc2) {
             constexpr int S = decltype(sc2)::value;
-            acc1 = mfma32x32x16(as_uint4(f1[4 + S]), rb[S], acc1);
+            acc1 = mfma32x32x16(as_uint4(f1[S]), opnd(sc2), acc1);
             __builtin_amdgcn_sched_barrier(0);
-            static_for<S * FPS, (S + 1) * FPS>([&](auto ec) { fscore(acc0, 2 * q, ec); });
+            constexpr int E0 = S * FPS < 16 ? S * FPS : 16, E1 = (S + 1) * FPS < 16 ? (S + 1) * FPS : 16;
+            static_for<E0, E1>([&](auto ec) { fscore(acc0, 2 * q, ec); });
             __builtin_amdgcn_sched_barrier(0);
           });
           fend(2 * q);
@@ -272,9 +270,9 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
         }
       };
       for (int q = 0; q < total; q += 3) {
-        stage(q, S0.c, &S0.n2[0][0], S2.c, &S2.n2[0][0]);
-        stage(q + 1, S1.c, &S1.n2[0][0], S0.c, &S0.n2[0][0]);
-        stage(q + 2, S2.c, &S2.n2[0][0], S1.c, &S1.n2[0][0]);
+        stage(q, S0.c, S2.c);
+        stage(q + 1, S1.c, S0.c);
+        stage(q + 2, S2.c, S1.c);
       }
       fold_all(pend, pend_tile);
     };

@@ -80,10 +80,14 @@ hipError_t launch_prep_u(const float* U, int d, int r, bf16_t* Ub, int64_t ldub,
 // or bf16 source.
 hipError_t launch_transpose_into(const void* src, int src_f32, int rows, int cols, int64_t lds,
                                  float scale, bf16_t* dst, int64_t ldd, int off, hipStream_t s);
-// Cb[l][j][c] = bf16(C[l][j][c]); meta[l][chunk][64]: ||C_j||^2 in fp32 per
+// Screening copy of the codebooks, rows of rvq_cb_cols(r) = r + 16 bf16:
+// Cb[l][j][0:r] = bf16(C[l][j]), Cb[l][j][r:r+3] = hi, mid, lo with
+// hi + mid + lo = ||C_j||^2 exactly (fp32 split into three bf16 pieces),
+// Cb[l][j][r+3:r+16] = 0.  meta[l][chunk][64]: ||C_j||^2 in fp32 per
 // 64-codeword chunk (zero past K).
 hipError_t launch_prep_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* meta, hipStream_t s);
 inline int64_t rvq_meta_floats(int L, int K) { return (int64_t)L * ((K + 63) / 64) * 64; }
+__host__ __device__ constexpr int rvq_cb_cols(int r) { return r + 16; }
 
 // ---------------------------------------------------------------- receiver-side operand
 // out[t][0:r]   = Zhat[t]: payload row (bf16) or sum_l C[l][codes[t,l]] (fp32 -> bf16)
@@ -141,7 +145,7 @@ hipError_t launch_prep_batch(const PrepJob* jobs, int n, hipStream_t s);
 // r in {32, 64, 128, 256}.
 struct RvqArgs {
   const float* Z0;     // [T,r] fp32 unquantised coordinates
-  const bf16_t* Cb;    // [L,K,r] bf16 screening copy
+  const bf16_t* Cb;    // [L,K,r+16] bf16 screening copy with the split norms (rvq_cb_cols)
   const float* C;      // [L,K,r] fp32 codebooks
   const float* meta;   // [L][ceil(K/64)][64]: ||C_j||^2 (rvq_meta_floats)
   int T, r, L, K;

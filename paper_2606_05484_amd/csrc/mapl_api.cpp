@@ -165,7 +165,7 @@ Layout layout(const mapl_codec_desc& D, int call) {
         Lo.w = c.take((size_t)r * Lo.kw * 2);
         if (D.L > 0) {
           Lo.z0 = c.take((size_t)T * r * 4);
-          Lo.cb = c.take((size_t)D.L * D.K * r * 2);
+          Lo.cb = c.take((size_t)D.L * D.K * rvq_cb_cols((int)r) * 2);
           Lo.cn2 = c.take((size_t)rvq_meta_floats(D.L, D.K) * 4);
           Lo.stats = c.take(16);
         }
