@@ -105,10 +105,167 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32(GemmF32Args g) {
       }
 }
 
+
+// Pipelined variant for the aligned case (every operand has a unit-stride
+// dimension, the other stride and that dimension's extent multiples of 4,
+// 16-byte (fp32) or 8-byte (bf16) aligned bases): 128 x 128 tiles, K staged
+// 32 at a time with 16-byte global loads into registers one stage ahead and
+// two LDS buffers, so the matrix units work on one stage while the next is
+// in flight (one barrier per stage).  A is either m-contiguous (AK = false:
+// A(m,k) at A + m + k*sAk) or k-contiguous (AK = true: A + m*sAm + k); B is
+// n-contiguous.  LDS holds both operands k-major (s[k][m]), rows padded to
+// 132 floats.
+constexpr int GV_BM = 128, GV_BN = 128, GV_BK = 32, GV_LD = GV_BM + 4;
+
+template <typename T>
+__device__ __forceinline__ float4 ld4(const T* p);
+template <>
+__device__ __forceinline__ float4 ld4<float>(const float* p) { return *(const float4*)p; }
+template <>
+__device__ __forceinline__ float4 ld4<bf16_t>(const bf16_t* p) {
+  const uint2 v = *(const uint2*)p;
+  return make_float4(bf2f(v.x & 0xFFFFu), bf2f(v.x >> 16), bf2f(v.y & 0xFFFFu), bf2f(v.y >> 16));
+}
+
+template <typename TA, typename TB, typename TO, bool AK>
+__global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
+  __shared__ __attribute__((aligned(16))) float As[2][GV_BK][GV_LD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][GV_BK][GV_LD];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, 64 x 64 each
+  const int b = blockIdx.z;
+  const int m0 = blockIdx.x * GV_BM, n0 = blockIdx.y * GV_BN;
+  const TA* A = (const TA*)g.A + b * g.sAb;
+  const TB* B = (const TB*)g.B + b * g.sBb;
+
+  // per thread and stage: four 4-element groups of A and of B
+  float4 ra[4], rb[4];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int idx = tid + GF_THREADS * v;
+      {  // B: k = idx / 32, n = 4 (idx % 32) .. +3
+        const int k = k0 + (idx >> 5), n = n0 + 4 * (idx & 31);
+        rb[v] = (k < g.K && n < g.N) ? ld4<TB>(B + (int64_t)k * g.sBk + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      if constexpr (AK) {  // A: m = idx / 8, k = 4 (idx % 8) .. +3
+        const int m = m0 + (idx >> 3), k = k0 + 4 * (idx & 7);
+        ra[v] = (m < g.M && k < g.K) ? ld4<TA>(A + (int64_t)m * g.sAm + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {  // A: k = idx / 32, m = 4 (idx % 32) .. +3
+        const int k = k0 + (idx >> 5), m = m0 + 4 * (idx & 31);
+        ra[v] = (k < g.K && m < g.M) ? ld4<TA>(A + (int64_t)k * g.sAk + m) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int idx = tid + GF_THREADS * v;
+      *(float4*)&Bs[buf][idx >> 5][4 * (idx & 31)] = rb[v];
+      if constexpr (AK) {
+        const int m = idx >> 3, k = 4 * (idx & 7);
+        As[buf][k][m] = ra[v].x;
+        As[buf][k + 1][m] = ra[v].y;
+        As[buf][k + 2][m] = ra[v].z;
+        As[buf][k + 3][m] = ra[v].w;
+      } else {
+        *(float4*)&As[buf][idx >> 5][4 * (idx & 31)] = ra[v];
+      }
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+
+  const int nk = (g.K + GV_BK - 1) / GV_BK;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int it = 0; it < nk; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < nk) load((it + 1) * GV_BK);
+#pragma unroll
+    for (int kk = 0; kk < GV_BK; kk += 2) {
+      float a[2], bb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = As[buf][kk + (lane >> 5)][wm * 64 + i * 32 + (lane & 31)];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) bb[j] = Bs[buf][kk + (lane >> 5)][wn * 64 + j * 32 + (lane & 31)];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32x32x2f32(a[i], bb[j], acc[i][j]);
+    }
+    // the other buffer was last read in the previous stage, before the barrier
+    if (it + 1 < nk) store(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
+  const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
+  const float* Cin = g.Cin ? g.Cin + b * g.sCinb : nullptr;
+  TO* C = (TO*)g.C + b * g.sCb;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        int m = m0 + wm * 64 + i * 32 + acc_row(e, lane);
+        int n = n0 + wn * 64 + j * 32 + (lane & 31);
+        if (m < g.M && n < g.N) {
+          float v = alpha * acc[i][j][e];
+          if (Cin && beta != 0.f) v += beta * Cin[m * g.sCinm + n * g.sCinn];
+          if constexpr (sizeof(TO) == 4)
+            C[m * g.sCm + n * g.sCn] = v;
+          else
+            C[m * g.sCm + n * g.sCn] = (TO)f2bf(v);
+        }
+      }
+}
+
+// The aligned case of the pipelined kernel: returns 0 (A m-contiguous), 1
+// (A k-contiguous) or -1 (use the general kernel).
+int gemm_f32_vec_mode(const GemmF32Args& g, int ta, int tb) {
+  const int ea = ta ? 2 : 4, eb = tb ? 2 : 4;
+  auto al = [](const void* p, int e) { return ((uintptr_t)p % (uintptr_t)(4 * e)) == 0; };
+  auto m4 = [](int64_t v) { return v % 4 == 0; };
+  if (!al(g.A, ea) || !al(g.B, eb)) return -1;
+  if (!(g.sBn == 1 && m4(g.sBk) && m4(g.N) && m4(g.sBb))) return -1;
+  if (g.sAm == 1 && m4(g.sAk) && m4(g.M) && m4(g.sAb)) return 0;
+  if (g.sAk == 1 && m4(g.sAm) && m4(g.K) && m4(g.sAb)) return 1;
+  return -1;
+}
+
 }  // namespace
 
 hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return hipSuccess;
+  const int vm = gemm_f32_vec_mode(g, ta, tb);
+  if (vm >= 0) {
+    dim3 grid((g.M + GV_BM - 1) / GV_BM, (g.N + GV_BN - 1) / GV_BN, g.batch);
+#define MAPL_GV(TA_, TB_, TO_)                                                                        \
+  do {                                                                                                \
+    if (vm)                                                                                           \
+      hipLaunchKernelGGL((k_gemm_f32v<TA_, TB_, TO_, true>), grid, dim3(GF_THREADS), 0, s, g);        \
+    else                                                                                              \
+      hipLaunchKernelGGL((k_gemm_f32v<TA_, TB_, TO_, false>), grid, dim3(GF_THREADS), 0, s, g);       \
+  } while (0)
+    if (ta == 0 && tb == 0 && to == 0) MAPL_GV(float, float, float);
+    else if (ta == 1 && tb == 0 && to == 0) MAPL_GV(bf16_t, float, float);
+    else if (ta == 0 && tb == 1 && to == 0) MAPL_GV(float, bf16_t, float);
+    else if (ta == 1 && tb == 1 && to == 0) MAPL_GV(bf16_t, bf16_t, float);
+    else if (ta == 1 && tb == 1 && to == 1) MAPL_GV(bf16_t, bf16_t, bf16_t);
+    else if (ta == 0 && tb == 0 && to == 1) MAPL_GV(float, float, bf16_t);
+    else if (ta == 1 && tb == 0 && to == 1) MAPL_GV(bf16_t, float, bf16_t);
+    else if (ta == 0 && tb == 1 && to == 1) MAPL_GV(float, bf16_t, bf16_t);
+    else return hipErrorInvalidValue;
+#undef MAPL_GV
+    return hipGetLastError();
+  }
   dim3 grid((g.M + GF_BM - 1) / GF_BM, (g.N + GF_BN - 1) / GF_BN, g.batch);
   dim3 block(GF_THREADS);
 #define MAPL_GF(TA_, TB_, TO_) hipLaunchKernelGGL((k_gemm_f32<TA_, TB_, TO_>), grid, block, 0, s, g)
