@@ -290,14 +290,24 @@ __global__ __launch_bounds__(WG_THREADS) void k_wgrad(WgradArgs g, int mtiles, i
 #endif
 }
 
+// dst (+)= sum_s part[s], the splits added in order; the loads of up to
+// eight splits are in flight together.
 __global__ void k_reduce_splits(const float* __restrict__ part, int splits, int64_t n4,
                                 int64_t stride, float* __restrict__ dst, int accumulate) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n4) return;
   float4 v = accumulate ? ((const float4*)dst)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < splits; ++s) {
-    float4 p = ((const float4*)(part + s * stride))[i];
-    v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+  constexpr int B = 8;
+  for (int s0 = 0; s0 < splits; s0 += B) {
+    float4 p[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u)
+      if (s0 + u < splits) p[u] = ((const float4*)(part + (s0 + u) * stride))[i];
+#pragma unroll
+    for (int u = 0; u < B; ++u)
+      if (s0 + u < splits) {
+        v.x += p[u].x; v.y += p[u].y; v.z += p[u].z; v.w += p[u].w;
+      }
   }
   ((float4*)dst)[i] = v;
 }
@@ -341,23 +351,22 @@ __global__ __launch_bounds__(256) void k_reduce_dU(const float* __restrict__ par
     for (int e = 0; e < 8; ++e) v[e] = 0.f;
   }
   if (own) {
-    int s = 0;
-    for (; s + 4 <= splits; s += 4) {
-      float4 q[8];
+    // the splits added in order, the loads of up to eight in flight together
+    constexpr int B = 8;
+    for (int s = 0; s < splits; s += B) {
+      float4 q[2 * B];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        q[2 * u] = *(const float4*)(part + (s + u) * stride + o);
-        q[2 * u + 1] = *(const float4*)(part + (s + u) * stride + o + 4);
-      }
+      for (int u = 0; u < B; ++u)
+        if (s + u < splits) {
+          q[2 * u] = *(const float4*)(part + (s + u) * stride + o);
+          q[2 * u + 1] = *(const float4*)(part + (s + u) * stride + o + 4);
+        }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        v[0] += q[2 * u].x; v[1] += q[2 * u].y; v[2] += q[2 * u].z; v[3] += q[2 * u].w;
-        v[4] += q[2 * u + 1].x; v[5] += q[2 * u + 1].y; v[6] += q[2 * u + 1].z; v[7] += q[2 * u + 1].w;
-      }
-    }
-    for (; s < splits; ++s) {
-      const float4 p0 = *(const float4*)(part + s * stride + o), p1 = *(const float4*)(part + s * stride + o + 4);
-      v[0] += p0.x; v[1] += p0.y; v[2] += p0.z; v[3] += p0.w; v[4] += p1.x; v[5] += p1.y; v[6] += p1.z; v[7] += p1.w;
+      for (int u = 0; u < B; ++u)
+        if (s + u < splits) {
+          v[0] += q[2 * u].x; v[1] += q[2 * u].y; v[2] += q[2 * u].z; v[3] += q[2 * u].w;
+          v[4] += q[2 * u + 1].x; v[5] += q[2 * u + 1].y; v[6] += q[2 * u + 1].z; v[7] += q[2 * u + 1].w;
+        }
     }
   }
   if (Wa != nullptr && k > 0) {

@@ -116,6 +116,16 @@ def test_ragged_small_both_anchor_spaces(space, L, K):
     _check_chain(x, _chain(x, C=C), C=C)
 
 
+@pytest.mark.parametrize("space", ["ambient", "coord"])
+def test_fp32_ragged_odd_tokens(space):
+    """fp32 operands with an odd token count: the fp32 products that
+    contract over tokens (dU) take the general element-load GEMM (K not a
+    multiple of 4), the others the pipelined 16-byte-load GEMM with a
+    ragged last tile."""
+    x = _x(None, seed=11, anchor_space=space, **dict(SMALL, T=509, dtype="f32", L=2, K=64))
+    _check_chain(x, _chain(x))
+
+
 def test_fp32_coord_anchor():
     x = _x("c1", anchor_space="coord")
     _check_chain(x, _chain(x))
