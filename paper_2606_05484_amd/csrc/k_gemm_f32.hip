@@ -97,6 +97,7 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32(GemmF32Args g) {
         if (m < g.M && n < g.N) {
           float v = alpha * acc[i][j][e];
           if (Cin && beta != 0.f) v += beta * Cin[m * g.sCinm + n * g.sCinn];
+          if (m == n) v += g.diag;
           if constexpr (sizeof(TO) == 4)
             C[m * g.sCm + n * g.sCn] = v;
           else
@@ -113,63 +114,121 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32(GemmF32Args g) {
 // two LDS buffers, so the matrix units work on one stage while the next is
 // in flight (one barrier per stage).  A is either m-contiguous (AK = false:
 // A(m,k) at A + m + k*sAk) or k-contiguous (AK = true: A + m*sAm + k); B is
-// n-contiguous.  LDS holds both operands k-major (s[k][m]), rows padded to
-// 132 floats.
-constexpr int GV_BM = 128, GV_BN = 128, GV_BK = 32, GV_LD = GV_BM + 4;
+// n-contiguous.  LDS holds both operands as k-pairs: s[k/2][m'][k%2], so the
+// 64 lanes of one operand read (rows m0 .. m0+31, k and k+1) touch one
+// 64-float span, every bank once; m' permutes the rows inside each group of
+// 32 so that the 8-byte stores of 32 lanes also land in distinct banks:
+// m' = m ^ ((m / 32) % 4) for tiles loaded row by row (B, m-contiguous A),
+// m' = m ^ 4 ((k / 2) % 8) for the k-contiguous A.
+constexpr int GV_BM = 128, GV_BN = 128, GV_BK = 32;
+
+// Operand loads are raw buffer loads (out-of-range offsets read zero) into
+// registers that are converted to fp32 only when the stage is written to LDS,
+// so nothing waits for the loads before the products of the current stage.
+constexpr uint32_t GV_OOB = 0x80000000u;  // any offset >= num_records reads zero
 
 template <typename T>
-__device__ __forceinline__ float4 ld4(const T* p);
+struct Raw4;  // four consecutive elements as loaded
 template <>
-__device__ __forceinline__ float4 ld4<float>(const float* p) { return *(const float4*)p; }
+struct Raw4<float> {
+  typedef __attribute__((ext_vector_type(4))) uint32_t type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  }
+  static __device__ __forceinline__ float4 cvt(type v) {
+    return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+  }
+};
 template <>
-__device__ __forceinline__ float4 ld4<bf16_t>(const bf16_t* p) {
-  const uint2 v = *(const uint2*)p;
-  return make_float4(bf2f(v.x & 0xFFFFu), bf2f(v.x >> 16), bf2f(v.y & 0xFFFFu), bf2f(v.y >> 16));
+struct Raw4<bf16_t> {
+  typedef __attribute__((ext_vector_type(2))) uint32_t type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  }
+  static __device__ __forceinline__ float4 cvt(type v) {
+    return make_float4(bf2f(v[0] & 0xFFFFu), bf2f(v[0] >> 16), bf2f(v[1] & 0xFFFFu), bf2f(v[1] >> 16));
+  }
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t gv_rsrc(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)(bytes > 0 ? bytes : 0), 0x00020000);
 }
 
 template <typename TA, typename TB, typename TO, bool AK>
 __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
-  __shared__ __attribute__((aligned(16))) float As[2][GV_BK][GV_LD];
-  __shared__ __attribute__((aligned(16))) float Bs[2][GV_BK][GV_LD];
+  __shared__ __attribute__((aligned(16))) float As[2][GV_BK / 2][GV_BM][2];
+  __shared__ __attribute__((aligned(16))) float Bs[2][GV_BK / 2][GV_BN][2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, 64 x 64 each
   const int b = blockIdx.z;
   const int m0 = blockIdx.x * GV_BM, n0 = blockIdx.y * GV_BN;
-  const TA* A = (const TA*)g.A + b * g.sAb;
-  const TB* B = (const TB*)g.B + b * g.sBb;
+  // the host guarantees that each operand's extent fits 31-bit byte offsets
+  const __amdgpu_buffer_rsrc_t rA =
+      gv_rsrc((const TA*)g.A + b * g.sAb,
+              (AK ? (int64_t)(g.M - 1) * g.sAm + g.K : (int64_t)(g.K - 1) * g.sAk + g.M) * (int64_t)sizeof(TA));
+  const __amdgpu_buffer_rsrc_t rB =
+      gv_rsrc((const TB*)g.B + b * g.sBb, ((int64_t)(g.K - 1) * g.sBk + g.N) * (int64_t)sizeof(TB));
 
-  // per thread and stage: four 4-element groups of A and of B
-  float4 ra[4], rb[4];
+  // per thread and stage: B (and an m-contiguous A) as two k-pairs of four
+  // consecutive columns ([pair][row of the pair]); a k-contiguous A as four
+  // runs of four k
+  typename Raw4<TA>::type ra[4];
+  typename Raw4<TB>::type rb[4];
   auto load = [&](int k0) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int idx = tid + GF_THREADS * v;
-      {  // B: k = idx / 32, n = 4 (idx % 32) .. +3
-        const int k = k0 + (idx >> 5), n = n0 + 4 * (idx & 31);
-        rb[v] = (k < g.K && n < g.N) ? ld4<TB>(B + (int64_t)k * g.sBk + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int v = 0; v < 2; ++v) {
+      const int idx = tid + GF_THREADS * v;  // k-pair idx / 32, columns 4 (idx % 32) .. +3
+      const int k = k0 + 2 * (idx >> 5), n = n0 + 4 * (idx & 31);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const bool ok = k + h < g.K && n < g.N;
+        rb[2 * v + h] = Raw4<TB>::load(rB, ok ? (uint32_t)(((int64_t)(k + h) * g.sBk + n) * sizeof(TB)) : GV_OOB);
       }
-      if constexpr (AK) {  // A: m = idx / 8, k = 4 (idx % 8) .. +3
+      if constexpr (!AK) {
+        const int m = m0 + 4 * (idx & 31);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const bool ok = k + h < g.K && m < g.M;
+          ra[2 * v + h] = Raw4<TA>::load(rA, ok ? (uint32_t)(((int64_t)(k + h) * g.sAk + m) * sizeof(TA)) : GV_OOB);
+        }
+      }
+    }
+    if constexpr (AK) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int idx = tid + GF_THREADS * v;  // m = idx / 8, k = 4 (idx % 8) .. +3
         const int m = m0 + (idx >> 3), k = k0 + 4 * (idx & 7);
-        ra[v] = (m < g.M && k < g.K) ? ld4<TA>(A + (int64_t)m * g.sAm + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-      } else {  // A: k = idx / 32, m = 4 (idx % 32) .. +3
-        const int k = k0 + (idx >> 5), m = m0 + 4 * (idx & 31);
-        ra[v] = (k < g.K && m < g.M) ? ld4<TA>(A + (int64_t)k * g.sAk + m) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const bool ok = m < g.M && k < g.K;
+        ra[v] = Raw4<TA>::load(rA, ok ? (uint32_t)(((int64_t)m * g.sAm + k) * sizeof(TA)) : GV_OOB);
       }
     }
   };
   auto store = [&](int buf) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
+    for (int v = 0; v < 2; ++v) {
       const int idx = tid + GF_THREADS * v;
-      *(float4*)&Bs[buf][idx >> 5][4 * (idx & 31)] = rb[v];
-      if constexpr (AK) {
-        const int m = idx >> 3, k = 4 * (idx & 7);
-        As[buf][k][m] = ra[v].x;
-        As[buf][k + 1][m] = ra[v].y;
-        As[buf][k + 2][m] = ra[v].z;
-        As[buf][k + 3][m] = ra[v].w;
-      } else {
-        *(float4*)&As[buf][idx >> 5][4 * (idx & 31)] = ra[v];
+      const int kp = idx >> 5, c4 = 4 * (idx & 31), sw = (idx & 31) >> 3;
+      const float4 r0 = Raw4<TB>::cvt(rb[2 * v]), r1 = Raw4<TB>::cvt(rb[2 * v + 1]);
+      *(float2*)&Bs[buf][kp][c4 + (0 ^ sw)][0] = make_float2(r0.x, r1.x);
+      *(float2*)&Bs[buf][kp][c4 + (1 ^ sw)][0] = make_float2(r0.y, r1.y);
+      *(float2*)&Bs[buf][kp][c4 + (2 ^ sw)][0] = make_float2(r0.z, r1.z);
+      *(float2*)&Bs[buf][kp][c4 + (3 ^ sw)][0] = make_float2(r0.w, r1.w);
+      if constexpr (!AK) {
+        const float4 a0 = Raw4<TA>::cvt(ra[2 * v]), a1 = Raw4<TA>::cvt(ra[2 * v + 1]);
+        *(float2*)&As[buf][kp][c4 + (0 ^ sw)][0] = make_float2(a0.x, a1.x);
+        *(float2*)&As[buf][kp][c4 + (1 ^ sw)][0] = make_float2(a0.y, a1.y);
+        *(float2*)&As[buf][kp][c4 + (2 ^ sw)][0] = make_float2(a0.z, a1.z);
+        *(float2*)&As[buf][kp][c4 + (3 ^ sw)][0] = make_float2(a0.w, a1.w);
+      }
+    }
+    if constexpr (AK) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int idx = tid + GF_THREADS * v;
+        const int m = (idx >> 3) ^ ((idx & 7) << 2), kp = 2 * (idx & 7);
+        const float4 a = Raw4<TA>::cvt(ra[v]);
+        *(float2*)&As[buf][kp][m][0] = make_float2(a.x, a.y);
+        *(float2*)&As[buf][kp + 1][m][0] = make_float2(a.z, a.w);
       }
     }
   };
@@ -188,12 +247,15 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
     const int buf = it & 1;
     if (it + 1 < nk) load((it + 1) * GV_BK);
 #pragma unroll
-    for (int kk = 0; kk < GV_BK; kk += 2) {
+    for (int kp = 0; kp < GV_BK / 2; ++kp) {
       float a[2], bb[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = As[buf][kk + (lane >> 5)][wm * 64 + i * 32 + (lane & 31)];
+      for (int i = 0; i < 2; ++i) {
+        const int sw = AK ? (kp >> 1) << 2 : (2 * wm + i) & 3;
+        a[i] = As[buf][kp][wm * 64 + i * 32 + ((lane & 31) ^ sw)][lane >> 5];
+      }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) bb[j] = Bs[buf][kk + (lane >> 5)][wn * 64 + j * 32 + (lane & 31)];
+      for (int j = 0; j < 2; ++j) bb[j] = Bs[buf][kp][wn * 64 + j * 32 + ((lane & 31) ^ ((2 * wn + j) & 3))][lane >> 5];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -219,6 +281,7 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
         if (m < g.M && n < g.N) {
           float v = alpha * acc[i][j][e];
           if (Cin && beta != 0.f) v += beta * Cin[m * g.sCinm + n * g.sCinn];
+          if (m == n) v += g.diag;
           if constexpr (sizeof(TO) == 4)
             C[m * g.sCm + n * g.sCn] = v;
           else
@@ -233,10 +296,13 @@ int gemm_f32_vec_mode(const GemmF32Args& g, int ta, int tb) {
   const int ea = ta ? 2 : 4, eb = tb ? 2 : 4;
   auto al = [](const void* p, int e) { return ((uintptr_t)p % (uintptr_t)(4 * e)) == 0; };
   auto m4 = [](int64_t v) { return v % 4 == 0; };
-  if (!al(g.A, ea) || !al(g.B, eb)) return -1;
+  if (g.K <= 0 || !al(g.A, ea) || !al(g.B, eb)) return -1;
   if (!(g.sBn == 1 && m4(g.sBk) && m4(g.N) && m4(g.sBb))) return -1;
-  if (g.sAm == 1 && m4(g.sAk) && m4(g.M) && m4(g.sAb)) return 0;
-  if (g.sAk == 1 && m4(g.sAm) && m4(g.K) && m4(g.sAb)) return 1;
+  // buffer offsets are 31-bit byte offsets
+  const int64_t lim = 0x7fffffffll - 16;
+  if (((int64_t)(g.K - 1) * g.sBk + g.N) * eb > lim) return -1;
+  if (g.sAm == 1 && m4(g.sAk) && m4(g.M) && m4(g.sAb) && ((int64_t)(g.K - 1) * g.sAk + g.M) * ea <= lim) return 0;
+  if (g.sAk == 1 && m4(g.sAm) && m4(g.K) && m4(g.sAb) && ((int64_t)(g.M - 1) * g.sAm + g.K) * ea <= lim) return 1;
   return -1;
 }
 

@@ -129,24 +129,39 @@ __global__ void k_axpy(const float* __restrict__ U, const float* __restrict__ D,
   if (i < n) Y[i] = U[i] - lr * D[i];
 }
 
-// One block per projector: nu2 = max_i sum_j |S_ij|.
-__global__ void k_inf_norm_scales(const float* __restrict__ S, int r, float* inv_nu, float* inv_nu2,
-                                  float* inv_nu4) {
-  __shared__ float red[4];
-  const int p = blockIdx.x;
+// One block of 16 waves per projector: nu2 = max_i sum_j |S_ij|.  A wave
+// reads whole rows (lane + 64 q), four rows at a time, so the loads are
+// coalesced and several rows are in flight; r <= 1024.
+__global__ __launch_bounds__(1024) void k_inf_norm_scales(const float* __restrict__ S, int r, float* inv_nu,
+                                                          float* inv_nu2, float* inv_nu4) {
+  __shared__ float red[16];
+  const int p = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float* Sp = S + (int64_t)p * r * r;
+  constexpr int RB = 4, QMAX = 16;  // rows per batch; 64-column groups (r <= 1024)
+  const int nq = (r + 63) / 64;
   float m = 0.f;
-  for (int i = threadIdx.x; i < r; i += blockDim.x) {
-    float s = 0.f;
-    for (int j = 0; j < r; ++j) s += fabsf(Sp[(int64_t)i * r + j]);
-    m = fmaxf(m, s);
-  }
+  for (int i0 = wave * RB; i0 < r; i0 += 16 * RB) {
+    float part[RB];
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, WAVE));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    for (int u = 0; u < RB; ++u) {
+      part[u] = 0.f;
+      const int i = i0 + u;
+      if (i < r) {
+#pragma unroll
+        for (int q = 0; q < QMAX; ++q) {
+          const int c = lane + 64 * q;
+          if (q < nq && c < r) part[u] += fabsf(Sp[(int64_t)i * r + c]);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < RB; ++u) m = fmaxf(m, wave_sum(part[u]));
+  }
+  if (lane == 0) red[wave] = m;
   __syncthreads();
   if (threadIdx.x == 0) {
-    const float nu2 = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    float nu2 = red[0];
+    for (int w = 1; w < 16; ++w) nu2 = fmaxf(nu2, red[w]);
     const float in2 = 1.f / nu2;
     inv_nu2[p] = in2;
     inv_nu4[p] = in2 * in2;
@@ -213,7 +228,8 @@ hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64
 
 hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* inv_nu, float* inv_nu2, float* inv_nu4,
                                   hipStream_t s) {
-  hipLaunchKernelGGL(k_inf_norm_scales, dim3(P), dim3(256), 0, s, S, r, inv_nu, inv_nu2, inv_nu4);
+  if (r > 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_inf_norm_scales, dim3(P), dim3(1024), 0, s, S, r, inv_nu, inv_nu2, inv_nu4);
   return hipGetLastError();
 }
 

@@ -37,6 +37,7 @@ struct GemmF32Args {
   int M, N, K, batch;
   float alpha, beta;
   const float* alpha_ptr; const float* beta_ptr;
+  float diag;  // added to every element with m == n after the scaling
 };
 hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStream_t s);
 

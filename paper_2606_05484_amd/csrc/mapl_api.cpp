@@ -803,26 +803,24 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.alpha_ptr = aptr;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  auto poly = [&](double b, double cc, const float* aptr, const float* bptr) {  // Qm = c S S + b S
+  auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr) {  // Qm = a I + b S + c S S
     GemmF32Args g = gemm((int)r, (int)r, (int)r);
     g.batch = (int)P;
     g.A = S; g.sAm = r; g.sAk = 1; g.sAb = rr;
     g.B = S; g.sBk = r; g.sBn = 1; g.sBb = rr;
     g.Cin = S; g.sCinm = r; g.sCinn = 1; g.sCinb = rr;
     g.C = Qm; g.sCm = r; g.sCn = 1; g.sCb = rr;
-    g.alpha = (float)cc; g.beta = (float)b;
+    g.alpha = (float)cc; g.beta = (float)b; g.diag = (float)a;
     g.alpha_ptr = aptr; g.beta_ptr = bptr;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  auto apply = [&](const float* X, float* Xo, double a, const float* sptr) {  // Xo = s (a X + X Qm)
+  auto apply = [&](const float* X, float* Xo, const float* sptr) {  // Xo = s X Qm
     GemmF32Args g = gemm((int)d, (int)r, (int)r);
     g.batch = (int)P;
     g.A = X; g.sAm = r; g.sAk = 1; g.sAb = n;
     g.B = Qm; g.sBk = r; g.sBn = 1; g.sBb = rr;
-    g.Cin = X; g.sCinm = r; g.sCinn = 1; g.sCinb = n;
     g.C = Xo; g.sCm = r; g.sCn = 1; g.sCb = n;
-    g.alpha = 1.f; g.beta = (float)a;
-    g.alpha_ptr = sptr; g.beta_ptr = sptr;
+    g.alpha_ptr = sptr;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
 
@@ -860,9 +858,9 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     const double a = kLmoCoef[i][0], b = kLmoCoef[i][1], cc = kLmoCoef[i][2];
     const bool first = i == 0;
     LAUNCH("stiefel:gram", gram(Xin, first ? scale2 : nullptr));
-    LAUNCH("stiefel:poly", poly(b, cc, nullptr, nullptr));
+    LAUNCH("stiefel:poly", poly(a, b, cc, nullptr, nullptr));
     float* Xo = bufs[cur];
-    LAUNCH("stiefel:apply", apply(Xin, Xo, a, first ? scale : nullptr));
+    LAUNCH("stiefel:apply", apply(Xin, Xo, first ? scale : nullptr));
     Xin = Xo;
     cur ^= 1;
   }
@@ -878,9 +876,9 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     const double a = kRetractCoef[i][0], b = kRetractCoef[i][1], cc = kRetractCoef[i][2];
     const bool first = i == 0;
     if (!first) LAUNCH("stiefel:gram", gram(Xin, nullptr));
-    LAUNCH("stiefel:poly", poly(b, cc, first ? inv_nu4 : nullptr, first ? inv_nu2 : nullptr));
+    LAUNCH("stiefel:poly", poly(a, b, cc, first ? inv_nu4 : nullptr, first ? inv_nu2 : nullptr));
     float* Xo = (i == retract_steps - 1) ? U : bufs[cur];
-    LAUNCH("stiefel:apply", apply(Xin, Xo, a, first ? inv_nu : nullptr));
+    LAUNCH("stiefel:apply", apply(Xin, Xo, first ? inv_nu : nullptr));
     Xin = Xo;
     cur ^= 1;
   }
