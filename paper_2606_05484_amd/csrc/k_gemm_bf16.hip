@@ -407,23 +407,51 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #endif
 }
 
-// A-resident variant for a short K walked over many output tiles (decode,
-// encode_bwd: K = r (+ k), N = d): the workgroup's 128 token rows of
-// [A | anchors] (KS <= AKS stages of 128 x 64) are loaded into LDS once and
-// stay there while the W stages of its N tiles stream through an NSW-deep
-// ring, so A is read from memory once instead of once per tile.  Requires
-// every K dimension to be a multiple of GK, no split-K and bf16 or fp32
-// output as the streaming kernel; the bf16 epilogue stages through the W
-// buffer the tile's last step consumed.
-template <int BN, int NSW, int AKS>
-__global__ __launch_bounds__(GTHREADS) void k_gemm_tn_ares(TnArgs g, int ntiles_per_wg) {
+// The products of one GK-deep stage with the token operand in registers:
+// afr[i][q] is the fragment of token block i for the 16-wide k-step q of
+// the whole K (stage KSI covers q = 4 KSI .. 4 KSI + 3); W fragments are
+// read from LDS at bw as in tn_products.
+template <int BN, int KSI, int KST, typename After>
+__device__ __forceinline__ void tn_products_areg(f32x16_t (&acc)[2][BN / 64], const u32x4 (&afr)[2][KST], uint32_t bw,
+                                                 const uint32_t (&koff)[GK / 16], After&& after) {
+  constexpr int FN = BN / 64, KSTEP = GK / 16;
+  u32x4 fr[2][FN];
+  auto load = [&](int kk, u32x4 (&f)[FN]) {
+    static_for<0, FN>([&](auto jc) {
+      constexpr int J = decltype(jc)::value;
+      f[J] = lds_read_b128<J * 32 * GK * 2>(bw + koff[kk]);
+    });
+  };
+  load(0, fr[0]);
+  lds_wait(fr[0]);
+  static_for<0, KSTEP>([&](auto kkc) {
+    constexpr int KK = decltype(kkc)::value, CB = KK & 1;
+    if constexpr (KK + 1 < KSTEP) load(KK + 1, fr[CB ^ 1]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = mfma32x32x16(as_uint4(fr[CB][j]), as_uint4(afr[i][KSI * KSTEP + KK]), acc[i][j]);
+    after(kkc);
+    if constexpr (KK + 1 < KSTEP) lds_wait(fr[CB ^ 1]);
+  });
+}
+
+// Register-resident variant for a short K (KS <= 6 stages) walked over many
+// output tiles (decode: K = r + k, encode_bwd: K = r; N = d): each wave
+// loads the token fragments of its 64 rows for the whole K once, straight
+// from memory into registers in the matrix unit's operand layout (16 B per
+// lane and fragment: token row l % 32, k 8 (l / 32) .. +7 of a 16-wide
+// k-step; anchor rows gathered by id), so the token operand is read from
+// memory once and costs neither LDS space nor LDS bandwidth.  Only the W
+// stages stream through a three-deep LDS ring.  Requires every K dimension
+// to be a multiple of GK and no split-K; the bf16 epilogue stages through
+// the W buffer the tile's last step consumed.
+template <int BN, int KS>
+__global__ __launch_bounds__(GTHREADS) void k_gemm_tn_areg(TnArgs g, int ntiles_per_wg) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  static_assert(NSW >= 2 && NSW <= 4, "W stages");
-  static_assert(AKS * GM * GK * 2 + NSW * BN * GK * 2 <= 160 * 1024, "LDS");
-  constexpr int FN = BN / 64;
-  constexpr int ABLK = GM / 8 / 4;  // A: 1 KiB blocks (8 rows) per wave per stage
+  constexpr int NSW = 3, FN = BN / 64, KSTEP = GK / 16, KST = KS * KSTEP;
   constexpr int WBLK = BN / 8 / 4;  // W: 1 KiB blocks per wave per stage
-  __shared__ __attribute__((aligned(1024))) bf16_t SA[AKS * GM * GK];
   __shared__ __attribute__((aligned(1024))) bf16_t SW[NSW][BN * GK];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -432,7 +460,6 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_ares(TnArgs g, int ntiles_
   const int m0 = blockIdx.x * GM;
   const int nt0 = blockIdx.y * ntiles_per_wg;
   const int ntiles = min(ntiles_per_wg, g.N / BN - nt0);
-  const int ka_steps = g.Ka / GK, KS = ka_steps + g.Kg / GK;
   const int total = ntiles * KS;
 
   const int mrows = min(GM, g.M - m0);
@@ -440,7 +467,26 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_ares(TnArgs g, int ntiles_
   const __amdgpu_buffer_rsrc_t rt = rsrc(g.T, g.T ? (uint64_t)g.V * g.ldt * 2 : 0);
   const __amdgpu_buffer_rsrc_t rw = rsrc(g.W, (uint64_t)g.N * g.ldw * 2);
 
-  // lane offsets, as in the streaming kernel (block parity swizzle)
+  // token fragments; rows past the last token read zeros (OOB offsets)
+  u32x4 afr[2][KST];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int row = wm * 64 + i * 32 + (lane & 31);
+    const bool in = m0 + row < g.M;
+    const uint32_t ch = 16u * (uint32_t)(lane >> 5);
+    const uint32_t aoff = in ? (uint32_t)row * (uint32_t)g.lda * 2u + ch : OOB;
+    const uint32_t toff =
+        in && g.Kg > 0 ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + ch : OOB;
+#pragma unroll
+    for (int q = 0; q < KST; ++q) {
+      const int kc = q * 16;  // first column of the k-step in [A | anchors]
+      if (kc < g.Ka)
+        afr[i][q] = __builtin_amdgcn_raw_buffer_load_b128(ra, aoff, kc * 2, 0);
+      else
+        afr[i][q] = __builtin_amdgcn_raw_buffer_load_b128(rt, toff, (kc - g.Ka) * 2, 0);
+    }
+  }
+
   const int lrow = lane >> 3;
   const uint32_t lchp[2] = {(uint32_t)((lane & 7) ^ (lane >> 4)), (uint32_t)((lane & 7) ^ (4 + (lane >> 4)))};
   uint32_t w_off[WBLK];
@@ -448,27 +494,6 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_ares(TnArgs g, int ntiles_
   for (int j = 0; j < WBLK; ++j) {
     const int row = 8 * (wave * WBLK + j) + lrow;
     w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lchp[j & 1];
-  }
-
-  // the resident A tile: stage ks at SA + ks * GM * GK, columns ks GK .. of
-  // [A | anchors]; the loads go first, so waiting for W stage 0 covers them
-  for (int ks = 0; ks < KS; ++ks) {
-    const bool gath = ks >= ka_steps;
-    const int soff = (gath ? (ks - ka_steps) * GK : ks * GK) * 2;
-#pragma unroll
-    for (int j = 0; j < ABLK; ++j) {
-      const int row = 8 * (wave * ABLK + j) + lrow;
-      const uint32_t lc = lchp[j & 1];
-      const lds_ptr dst = (lds_ptr)(SA + ks * GM * GK + (wave * ABLK + j) * 512);
-      if (gath) {
-        const uint32_t to = m0 + row < g.M ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + 16u * lc
-                                           : OOB;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, dst, 16, to, soff, 0, 0);
-      } else {
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, dst, 16, (uint32_t)row * (uint32_t)g.lda * 2u + 16u * lc, soff,
-                                                 0, 0);
-      }
-    }
   }
 
   // W step s: tile nt0 + s / KS, k-step s % KS (planned in order)
@@ -488,7 +513,7 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_ares(TnArgs g, int ntiles_
       pl_ks = 0;
       ++pl_nt;
     }
-    const int wcol0 = ks < ka_steps ? ks * GK : g.Ka + (ks - ka_steps) * GK;
+    const int wcol0 = ks * GK;  // [A | anchors] columns map to W columns one to one
     p.soff = (int)((uint32_t)nt * BN * (uint32_t)g.ldw * 2u + (uint32_t)wcol0 * 2u);
     return p;
   };
@@ -506,50 +531,49 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_ares(TnArgs g, int ntiles_
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
-  uint32_t koff[GK / 16];
+  uint32_t koff[KSTEP];
 #pragma unroll
-  for (int kk = 0; kk < GK / 16; ++kk) koff[kk] = tn_koff(kk, lane);
-  constexpr int KSTEP = GK / 16, PER = (WBLK + KSTEP - 1) / KSTEP;
+  for (int kk = 0; kk < KSTEP; ++kk) koff[kk] = tn_koff(kk, lane);
+  constexpr int PER = (WBLK + KSTEP - 1) / KSTEP;
   char* obase = (char*)g.out;
-  const uint32_t sa0 = lds_addr(SA) + wm * 64 * (GK * 2);
-
-  // W buffer u at LDS byte address swb + u * WSTG (u uniform, run time)
   constexpr uint32_t WSTG = BN * GK * 2;
   const uint32_t swb = lds_addr(&SW[0][0]);
   auto wbuf = [&](int u) { return (bf16_t*)&SW[0][0] + u * (BN * GK); };
-  // prologue: W stages 0 .. NSW - 2 in flight
-  static_for<0, NSW - 1>([&](auto uc) {
-    constexpr int U = decltype(uc)::value;
-    issue_range(plan_next(wbuf(U)), std::integral_constant<int, 0>{}, std::integral_constant<int, WBLK>{});
-  });
-  // step s consumes W buffer u = s % NSW and issues W step s + NSW - 1 into
-  // buffer (s - 1) % NSW, consumed at step s - 1
+
+  // prologue: W steps 0 and 1 in flight
+  issue_range(plan_next(wbuf(0)), std::integral_constant<int, 0>{}, std::integral_constant<int, WBLK>{});
+  issue_range(plan_next(wbuf(1)), std::integral_constant<int, 0>{}, std::integral_constant<int, WBLK>{});
+  // The token fragments were loaded before both W steps: wait for them here
+  // (the compiler sees the register uses below and counts the DMA issued
+  // since), so no wait for them remains inside the tile loop.
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < KST; ++q) asm volatile("" : "+v"(afr[i][q]));
+
+  // step s consumes W buffer u = s % 3 and issues W step s + 2 into buffer
+  // (s - 1) % 3, consumed at step s - 1
   int s = 0, u = 0;
   for (int tile = 0; tile < ntiles; ++tile) {
-    for (int ks = 0; ks < KS; ++ks, ++s) {
-      // W step s complete; W steps s + 1 .. s + NSW - 2 (those that exist) may be in flight
-      const int ahead = min(NSW - 2, total - 1 - s);
-      if constexpr (NSW >= 4) {
-        if (ahead >= 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * WBLK) : "memory");
-        else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WBLK) : "memory");
-        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      } else if constexpr (NSW == 3) {
-        if (ahead >= 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WBLK) : "memory");
-        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      } else {
+    static_for<0, KS>([&](auto ksc) {
+      constexpr int KSI = decltype(ksc)::value;
+      // W step s complete; W step s + 1 (if any) may be in flight
+      if (s + 1 < total)
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WBLK) : "memory");
+      else
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      }
       __builtin_amdgcn_s_barrier();
       const int un = u == 0 ? NSW - 1 : u - 1;
       const WPlan nx = plan_next(wbuf(un));
-      tn_products<BN>(acc, sa0 + ks * (GM * GK * 2), swb + u * WSTG + wn * (BN / 2) * (GK * 2), koff, [&](auto kkc) {
+      tn_products_areg<BN, KSI>(acc, afr, swb + u * WSTG + wn * (BN / 2) * (GK * 2), koff, [&](auto kkc) {
         constexpr int KK = decltype(kkc)::value;
         constexpr int B0 = KK * PER < WBLK ? KK * PER : WBLK;
         constexpr int B1 = (KK + 1) * PER < WBLK ? (KK + 1) * PER : WBLK;
         issue_range(nx, std::integral_constant<int, B0>{}, std::integral_constant<int, B1>{});
       });
-      if (ks + 1 < KS) u = u + 1 == NSW ? 0 : u + 1;
-    }
+      ++s;
+      if (KSI + 1 < KS) u = u + 1 == NSW ? 0 : u + 1;
+    });
     // stage through the W buffer the tile's last step consumed
     if (!g.out_f32) __builtin_amdgcn_s_barrier();  // every wave is done reading it
     tn_epilogue<BN, BN * GK * 2>(acc, g, obase, m0, nt0 + tile, swb + u * WSTG, wave, lane);
@@ -570,14 +594,19 @@ hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
   int per = 1;
   while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) * zs >= 256) per *= 2;
   dim3 grid(mt, (nt + per - 1) / per, zs);
-  // a short K walked over several tiles: keep A resident (up to 4 stages,
-  // leaving LDS for a three-deep W ring; with a two-deep ring the W loads
-  // of a step have only the step before to land, which costs more than
-  // re-reading A)
+  // a short K (2 to 6 stages) walked over several tiles: token operand in
+  // registers, read once (the register budget of one wave per SIMD holds up
+  // to 6 stages of it next to the accumulators)
   const int KS = (g.Ka + g.Kg) / GK;
   if constexpr (BN == 256) {
-    if (fullk && g.kz == 0 && per >= 2 && KS <= 4) {
-      hipLaunchKernelGGL((k_gemm_tn_ares<BN, 3, 4>), grid, dim3(GTHREADS), 0, s, g, per);
+    if (fullk && g.kz == 0 && per >= 2 && KS >= 2 && KS <= 6) {
+      switch (KS) {
+        case 2: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 2>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        case 3: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 3>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        case 4: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 4>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        case 5: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 5>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        default: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 6>), grid, dim3(GTHREADS), 0, s, g, per); break;
+      }
       return hipGetLastError();
     }
   }

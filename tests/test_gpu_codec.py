@@ -247,6 +247,16 @@ def test_c4_full_size_sampled():
     assert e <= BF16_TOL
 
 
+@pytest.mark.parametrize("r", [64, 128, 256])
+def test_short_k_many_tiles(r):
+    """Decode and encode_bwd at d=2048 with enough tokens (8192 + a ragged
+    77) that each workgroup walks several output tiles: the K depths
+    r + k = 128, 192, 320 (decode) and r = 128, 256 (encode_bwd) of the
+    register-resident token operand, besides the benchmark's 384 and 256."""
+    x = _x("c4", T=8192 + 77, r=r, k=64, L=0, K=0)
+    _check_chain(x, _chain(x))
+
+
 @pytest.mark.slow
 def test_large_ragged_tail_sampled():
     """A token count that is not a multiple of the 128-token tile at the
