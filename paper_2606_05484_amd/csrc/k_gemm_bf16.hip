@@ -407,56 +407,26 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #endif
 }
 
-// The products of one GK-deep stage with the token operand in registers:
-// afr[i][q] is the fragment of token block i for the 16-wide k-step q of
-// the whole K (stage KSI covers q = 4 KSI .. 4 KSI + 3); W fragments are
-// read from LDS at bw as in tn_products.
-template <int BN, int KSI, int KST, typename After>
-__device__ __forceinline__ void tn_products_areg(f32x16_t (&acc)[2][BN / 64], const u32x4 (&afr)[2][KST], uint32_t bw,
-                                                 const uint32_t (&koff)[GK / 16], After&& after) {
-  constexpr int FN = BN / 64, KSTEP = GK / 16;
-  u32x4 fr[2][FN];
-  auto load = [&](int kk, u32x4 (&f)[FN]) {
-    static_for<0, FN>([&](auto jc) {
-      constexpr int J = decltype(jc)::value;
-      f[J] = lds_read_b128<J * 32 * GK * 2>(bw + koff[kk]);
-    });
-  };
-  load(0, fr[0]);
-  lds_wait(fr[0]);
-  static_for<0, KSTEP>([&](auto kkc) {
-    constexpr int KK = decltype(kkc)::value, CB = KK & 1;
-    if constexpr (KK + 1 < KSTEP) load(KK + 1, fr[CB ^ 1]);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        acc[i][j] = mfma32x32x16(as_uint4(fr[CB][j]), as_uint4(afr[i][KSI * KSTEP + KK]), acc[i][j]);
-    after(kkc);
-    if constexpr (KK + 1 < KSTEP) lds_wait(fr[CB ^ 1]);
-  });
-}
-
-// Register-resident variant for a short K (KS <= 6 stages) walked over many
-// output tiles (decode: K = r + k, encode_bwd: K = r; N = d): each wave
-// loads the token fragments of its 64 rows for the whole K once, straight
-// from memory into registers in the matrix unit's operand layout (16 B per
-// lane and fragment: token row l % 32, k 8 (l / 32) .. +7 of a 16-wide
-// k-step; anchor rows gathered by id), so the token operand is read from
-// memory once and costs neither LDS space nor LDS bandwidth.  Only the W
-// stages stream through a three-deep LDS ring.  Requires every K dimension
-// to be a multiple of GK and no split-K; the bf16 epilogue stages through
-// the W buffer the tile's last step consumed.
-template <int BN, int KS>
-__global__ __launch_bounds__(GTHREADS) void k_gemm_tn_areg(TnArgs g, int ntiles_per_wg) {
+// Short-K, write-heavy products with bf16 output (decode: K = r + k,
+// encode_bwd: K = r; N = d), walked over many output tiles per 128-token
+// block: 128 x 128 tiles, each of the 4 waves owning 32 token rows and all
+// 128 columns.  A wave loads the token fragments of its rows for the whole
+// K (up to 6 stages) once, straight from memory into registers in the
+// matrix unit's operand layout (16 B per lane and fragment: token row
+// l % 32, k 8 (l / 32) .. +7 of a 16-wide k-step; anchor rows gathered by
+// id), so the token operand uses no LDS; W streams through a three-deep
+// ring of 16 KiB stages.  48 KiB of LDS and at most 216 registers per lane
+// let two workgroups share a CU, so one's output stores overlap the
+// other's products.  Epilogue: as tn_epilogue, for 32-row waves.
+template <int KS>
+__global__ __launch_bounds__(GTHREADS, 2) void k_gemm_tn_short(TnArgs g, int ntiles_per_wg) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int NSW = 3, FN = BN / 64, KSTEP = GK / 16, KST = KS * KSTEP;
+  constexpr int BN = 128, NSW = 3, FN = BN / 32, KSTEP = GK / 16, KST = KS * KSTEP;
   constexpr int WBLK = BN / 8 / 4;  // W: 1 KiB blocks per wave per stage
   __shared__ __attribute__((aligned(1024))) bf16_t SW[NSW][BN * GK];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
   const int m0 = blockIdx.x * GM;
   const int nt0 = blockIdx.y * ntiles_per_wg;
   const int ntiles = min(ntiles_per_wg, g.N / BN - nt0);
@@ -467,11 +437,10 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_areg(TnArgs g, int ntiles_
   const __amdgpu_buffer_rsrc_t rt = rsrc(g.T, g.T ? (uint64_t)g.V * g.ldt * 2 : 0);
   const __amdgpu_buffer_rsrc_t rw = rsrc(g.W, (uint64_t)g.N * g.ldw * 2);
 
-  // token fragments; rows past the last token read zeros (OOB offsets)
-  u32x4 afr[2][KST];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int row = wm * 64 + i * 32 + (lane & 31);
+  // token fragments of rows 32 wave .. +31; rows past the last token read zeros
+  u32x4 afr[KST];
+  {
+    const int row = wave * 32 + (lane & 31);
     const bool in = m0 + row < g.M;
     const uint32_t ch = 16u * (uint32_t)(lane >> 5);
     const uint32_t aoff = in ? (uint32_t)row * (uint32_t)g.lda * 2u + ch : OOB;
@@ -479,11 +448,11 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_areg(TnArgs g, int ntiles_
         in && g.Kg > 0 ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + ch : OOB;
 #pragma unroll
     for (int q = 0; q < KST; ++q) {
-      const int kc = q * 16;  // first column of the k-step in [A | anchors]
+      const int kc = q * 16;
       if (kc < g.Ka)
-        afr[i][q] = __builtin_amdgcn_raw_buffer_load_b128(ra, aoff, kc * 2, 0);
+        afr[q] = __builtin_amdgcn_raw_buffer_load_b128(ra, aoff, kc * 2, 0);
       else
-        afr[i][q] = __builtin_amdgcn_raw_buffer_load_b128(rt, toff, (kc - g.Ka) * 2, 0);
+        afr[q] = __builtin_amdgcn_raw_buffer_load_b128(rt, toff, (kc - g.Ka) * 2, 0);
     }
   }
 
@@ -495,8 +464,6 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_areg(TnArgs g, int ntiles_
     const int row = 8 * (wave * WBLK + j) + lrow;
     w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lchp[j & 1];
   }
-
-  // W step s: tile nt0 + s / KS, k-step s % KS (planned in order)
   int pl_ks = 0, pl_nt = nt0, pl_s = 0;
   struct WPlan {
     bf16_t* sw;
@@ -513,8 +480,7 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_areg(TnArgs g, int ntiles_
       pl_ks = 0;
       ++pl_nt;
     }
-    const int wcol0 = ks * GK;  // [A | anchors] columns map to W columns one to one
-    p.soff = (int)((uint32_t)nt * BN * (uint32_t)g.ldw * 2u + (uint32_t)wcol0 * 2u);
+    p.soff = (int)((uint32_t)nt * BN * (uint32_t)g.ldw * 2u + (uint32_t)(ks * GK) * 2u);
     return p;
   };
   auto issue_range = [&](const WPlan& p, auto b0c, auto b1c) {
@@ -526,38 +492,27 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_areg(TnArgs g, int ntiles_
     });
   };
 
-  f32x16_t acc[2][FN];
+  f32x16_t acc[FN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
+  for (int j = 0; j < FN; ++j) acc[j] = f32x16_t{};
   uint32_t koff[KSTEP];
 #pragma unroll
   for (int kk = 0; kk < KSTEP; ++kk) koff[kk] = tn_koff(kk, lane);
   constexpr int PER = (WBLK + KSTEP - 1) / KSTEP;
-  char* obase = (char*)g.out;
   constexpr uint32_t WSTG = BN * GK * 2;
   const uint32_t swb = lds_addr(&SW[0][0]);
   auto wbuf = [&](int u) { return (bf16_t*)&SW[0][0] + u * (BN * GK); };
 
-  // prologue: W steps 0 and 1 in flight
   issue_range(plan_next(wbuf(0)), std::integral_constant<int, 0>{}, std::integral_constant<int, WBLK>{});
   issue_range(plan_next(wbuf(1)), std::integral_constant<int, 0>{}, std::integral_constant<int, WBLK>{});
-  // The token fragments were loaded before both W steps: wait for them here
-  // (the compiler sees the register uses below and counts the DMA issued
-  // since), so no wait for them remains inside the tile loop.
+  // wait for the token fragments here, not inside the tile loop
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int q = 0; q < KST; ++q) asm volatile("" : "+v"(afr[i][q]));
+  for (int q = 0; q < KST; ++q) asm volatile("" : "+v"(afr[q]));
 
-  // step s consumes W buffer u = s % 3 and issues W step s + 2 into buffer
-  // (s - 1) % 3, consumed at step s - 1
   int s = 0, u = 0;
   for (int tile = 0; tile < ntiles; ++tile) {
     static_for<0, KS>([&](auto ksc) {
       constexpr int KSI = decltype(ksc)::value;
-      // W step s complete; W step s + 1 (if any) may be in flight
       if (s + 1 < total)
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WBLK) : "memory");
       else
@@ -565,18 +520,84 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn_areg(TnArgs g, int ntiles_
       __builtin_amdgcn_s_barrier();
       const int un = u == 0 ? NSW - 1 : u - 1;
       const WPlan nx = plan_next(wbuf(un));
-      tn_products_areg<BN, KSI>(acc, afr, swb + u * WSTG + wn * (BN / 2) * (GK * 2), koff, [&](auto kkc) {
-        constexpr int KK = decltype(kkc)::value;
+      const uint32_t bw = swb + u * WSTG;
+      u32x4 fr[2][FN];
+      auto load = [&](int kk, u32x4 (&f)[FN]) {
+        static_for<0, FN>([&](auto jc) {
+          constexpr int J = decltype(jc)::value;
+          f[J] = lds_read_b128<J * 32 * GK * 2>(bw + koff[kk]);
+        });
+      };
+      load(0, fr[0]);
+      lds_wait(fr[0]);
+      static_for<0, KSTEP>([&](auto kkc) {
+        constexpr int KK = decltype(kkc)::value, CB = KK & 1;
+        if constexpr (KK + 1 < KSTEP) load(KK + 1, fr[CB ^ 1]);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[j] = mfma32x32x16(as_uint4(fr[CB][j]), as_uint4(afr[KSI * KSTEP + KK]), acc[j]);
         constexpr int B0 = KK * PER < WBLK ? KK * PER : WBLK;
         constexpr int B1 = (KK + 1) * PER < WBLK ? (KK + 1) * PER : WBLK;
         issue_range(nx, std::integral_constant<int, B0>{}, std::integral_constant<int, B1>{});
+        if constexpr (KK + 1 < KSTEP) lds_wait(fr[CB ^ 1]);
       });
       ++s;
       if (KSI + 1 < KS) u = u + 1 == NSW ? 0 : u + 1;
     });
-    // stage through the W buffer the tile's last step consumed
-    if (!g.out_f32) __builtin_amdgcn_s_barrier();  // every wave is done reading it
-    tn_epilogue<BN, BN * GK * 2>(acc, g, obase, m0, nt0 + tile, swb + u * WSTG, wave, lane);
+
+    // epilogue through the W buffer the tile's last step consumed: per half
+    // of the columns, each wave stages its 32 x 64 block (4 KiB) and stores
+    // full 128 B row segments
+    __builtin_amdgcn_s_barrier();  // every wave is done reading it
+    {
+      constexpr int COLS = 64, CPR = COLS / 8;
+      const int half = lane >> 5;
+      const uint32_t stg = swb + u * WSTG + wave * (32 * COLS * 2);
+      const int nt = nt0 + tile;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const f32x16_t& c = acc[h * 2 + jj];
+          uint32_t p[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) p[e] = pack_bf2(c[2 * e], c[2 * e + 1]);
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int w = 0; w < 2; ++w) {
+              const auto sw2 = __builtin_amdgcn_permlane32_swap(p[4 * q + w], p[4 * q + 2 + w], false, false);
+              p[4 * q + w] = sw2[0];
+              p[4 * q + 2 + w] = sw2[1];
+            }
+          const int row = lane & 31;
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const int chn = jj * 4 + 2 * q + half;
+            lds_write_b128(stg + row * COLS * 2 + 16 * (chn ^ ((row >> 1) & (CPR - 1))),
+                           u32x4{p[4 * q], p[4 * q + 1], p[4 * q + 2], p[4 * q + 3]});
+          }
+        }
+        u32x4 v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = lane + 64 * q;
+          const int row = c / CPR, chn = c % CPR;
+          v[q] = lds_read_b128(stg + row * COLS * 2 + 16 * (chn ^ ((row >> 1) & (CPR - 1))));
+        }
+        lds_wait(v);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = lane + 64 * q;
+          const int row = c / CPR, chn = c % CPR;
+          const int t = m0 + wave * 32 + row;
+          if (t < g.M)
+            *(uint4*)((bf16_t*)g.out + (int64_t)t * g.ldo + nt * BN + h * COLS + chn * 8) = as_uint4(v[q]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[j] = f32x16_t{};
+    }
     u = u + 1 == NSW ? 0 : u + 1;
   }
 #endif
@@ -594,18 +615,23 @@ hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
   int per = 1;
   while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) * zs >= 256) per *= 2;
   dim3 grid(mt, (nt + per - 1) / per, zs);
-  // a short K (2 to 6 stages) walked over several tiles: token operand in
-  // registers, read once (the register budget of one wave per SIMD holds up
-  // to 6 stages of it next to the accumulators)
+  // a short K (2 to 6 stages) walked over many tiles with bf16 output
+  // (decode, encode_bwd): token operand in registers, read once, 128-wide
+  // tiles, two workgroups per CU; each workgroup walks per2 tiles and the
+  // grid fills two workgroups per CU
   const int KS = (g.Ka + g.Kg) / GK;
   if constexpr (BN == 256) {
-    if (fullk && g.kz == 0 && per >= 2 && KS >= 2 && KS <= 6) {
+    const int nt2 = g.N / 128;
+    int per2 = 1;
+    while (per2 < nt2 && (int64_t)mt * ((nt2 + per2 * 2 - 1) / (per2 * 2)) >= 512) per2 *= 2;
+    if (!g.out_f32 && fullk && g.kz == 0 && per2 >= 2 && KS >= 2 && KS <= 6) {
+      dim3 grid2(mt, (nt2 + per2 - 1) / per2, 1);
       switch (KS) {
-        case 2: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 2>), grid, dim3(GTHREADS), 0, s, g, per); break;
-        case 3: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 3>), grid, dim3(GTHREADS), 0, s, g, per); break;
-        case 4: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 4>), grid, dim3(GTHREADS), 0, s, g, per); break;
-        case 5: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 5>), grid, dim3(GTHREADS), 0, s, g, per); break;
-        default: hipLaunchKernelGGL((k_gemm_tn_areg<BN, 6>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        case 2: hipLaunchKernelGGL((k_gemm_tn_short<2>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
+        case 3: hipLaunchKernelGGL((k_gemm_tn_short<3>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
+        case 4: hipLaunchKernelGGL((k_gemm_tn_short<4>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
+        case 5: hipLaunchKernelGGL((k_gemm_tn_short<5>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
+        default: hipLaunchKernelGGL((k_gemm_tn_short<6>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
       }
       return hipGetLastError();
     }
