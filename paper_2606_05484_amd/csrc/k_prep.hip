@@ -163,6 +163,63 @@ __device__ __forceinline__ void assemble_block(int bx, const AssembleArgs& a) {
   }
 }
 
+// The common decode case of assemble_block: Zhat = sum of L <= 2 codewords,
+// no anchor columns (ldo == r).  One thread per 8 columns of four tokens
+// (4 g .. 4 g + 3): all codes, then all codeword rows of the four tokens are
+// loaded before any sum, so a thread has up to sixteen independent loads in
+// flight and a quarter of the threads cover the rows.  Same sums in the same
+// order as assemble_block.
+__device__ __forceinline__ void assemble_sum_block(int bx, const AssembleArgs& a) {
+  constexpr int TPT = 4, LM = 2;
+  const int per_row = a.r / 8;
+  const int64_t e = (int64_t)bx * blockDim.x + threadIdx.x;
+  if (e >= ((int64_t)a.T + TPT - 1) / TPT * per_row) return;
+  const int g = (int)(e / per_row), c0 = (int)(e % per_row) * 8;
+  int code[TPT][LM];
+#pragma unroll
+  for (int u = 0; u < TPT; ++u) {
+    const int t = min(g * TPT + u, a.T - 1);
+#pragma unroll
+    for (int l = 0; l < LM; ++l) {
+      if (l < a.L) {
+        const int c = a.code_bytes == 1 ? ((const uint8_t*)a.codes)[(int64_t)t * a.L + l]
+                                        : ((const uint16_t*)a.codes)[(int64_t)t * a.L + l];
+        code[u][l] = c < a.K ? c : a.K - 1;
+      }
+    }
+  }
+  float4 cw[TPT][LM][2];
+#pragma unroll
+  for (int u = 0; u < TPT; ++u)
+#pragma unroll
+    for (int l = 0; l < LM; ++l) {
+      if (l < a.L) {
+        const float4* p = (const float4*)(a.C + ((int64_t)l * a.K + code[u][l]) * a.r + c0);
+        cw[u][l][0] = p[0];
+        cw[u][l][1] = p[1];
+      }
+    }
+#pragma unroll
+  for (int u = 0; u < TPT; ++u) {
+    const int t = g * TPT + u;
+    if (t < a.T) {
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = 0.f;
+#pragma unroll
+      for (int l = 0; l < LM; ++l) {
+        if (l < a.L) {
+          const float4 p = cw[u][l][0], q4 = cw[u][l][1];
+          v[0] += p.x; v[1] += p.y; v[2] += p.z; v[3] += p.w;
+          v[4] += q4.x; v[5] += q4.y; v[6] += q4.z; v[7] += q4.w;
+        }
+      }
+      *(uint4*)(a.out + (int64_t)t * a.ldo + c0) =
+          make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7]));
+    }
+  }
+}
+
 // One thread per 8 columns of a gathered row (16 B copies).
 __device__ __forceinline__ void gather_rows_block(int bx, const bf16_t* __restrict__ A, int k,
                                                   const int32_t* __restrict__ ids, int V, int T,
@@ -269,6 +326,7 @@ __global__ __launch_bounds__(256) void k_prep_batch(PrepBatch batch) {
       break;
     case PJ_CODEBOOK: prep_codebook_block(b, j.C, j.L, j.K, j.r, j.Cb, j.meta); break;
     case PJ_ASSEMBLE: assemble_block(b, j.asm_args); break;
+    case PJ_ASSEMBLE_SUM: assemble_sum_block(b, j.asm_args); break;
     case PJ_GATHER: gather_rows_block(b, j.A, j.k, j.ids, j.V, j.T, j.out); break;
     case PJ_SMALL_GEMM: small_gemm_tile(b % j.gx, b / j.gx, j); break;
     default: break;
@@ -360,9 +418,14 @@ PrepJob prep_job_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float
 
 PrepJob prep_job_assemble(const AssembleArgs& a) {
   PrepJob j{};
-  j.kind = PJ_ASSEMBLE;
   j.asm_args = a;
-  j.blocks = a.T > 0 ? (int)(((int64_t)a.T * (a.ldo / 8) + 255) / 256) : 0;
+  if (a.L >= 1 && a.L <= 2 && a.A == nullptr && a.Bc == nullptr && a.ldo == a.r) {
+    j.kind = PJ_ASSEMBLE_SUM;
+    j.blocks = a.T > 0 ? (int)(((int64_t)(a.T + 3) / 4 * (a.r / 8) + 255) / 256) : 0;
+  } else {
+    j.kind = PJ_ASSEMBLE;
+    j.blocks = a.T > 0 ? (int)(((int64_t)a.T * (a.ldo / 8) + 255) / 256) : 0;
+  }
   return j;
 }
 
@@ -394,7 +457,8 @@ hipError_t launch_prep_batch(const PrepJob* jobs, int n, hipStream_t s) {
     if (jobs[i].kind == PJ_SMALL_GEMM &&
         (jobs[i].Kd % 16 || jobs[i].N % 32 || jobs[i].ldp % 8 || (jobs[i].qt && jobs[i].ldq % 4)))
       return hipErrorInvalidValue;
-    if (jobs[i].kind == PJ_ASSEMBLE && (jobs[i].asm_args.r % 8 || jobs[i].asm_args.ldo % 8 ||
+    if ((jobs[i].kind == PJ_ASSEMBLE || jobs[i].kind == PJ_ASSEMBLE_SUM) &&
+        (jobs[i].asm_args.r % 8 || jobs[i].asm_args.ldo % 8 ||
                                         (jobs[i].asm_args.A != nullptr && jobs[i].asm_args.k % 8)))
       return hipErrorInvalidValue;
     if (jobs[i].kind == PJ_GATHER && jobs[i].k % 8) return hipErrorInvalidValue;

@@ -110,7 +110,7 @@ hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- batched preparation
 // Independent preparation jobs of one call issued as a single launch
 // (launch_prep_batch); each job behaves like the corresponding launcher.
-enum { PJ_PREP_U = 1, PJ_TRANSPOSE, PJ_CODEBOOK, PJ_ASSEMBLE, PJ_GATHER, PJ_SMALL_GEMM };
+enum { PJ_PREP_U = 1, PJ_TRANSPOSE, PJ_CODEBOOK, PJ_ASSEMBLE, PJ_GATHER, PJ_SMALL_GEMM, PJ_ASSEMBLE_SUM };
 struct PrepJob {
   int kind, blocks, gx;
   // PJ_PREP_U
@@ -119,7 +119,7 @@ struct PrepJob {
   const void* src; int src_f32, rows, cols; int64_t lds; float scale; bf16_t* dst; int64_t ldd; int off;
   // PJ_CODEBOOK
   const float* C; int L, K; bf16_t* Cb; float* meta;
-  // PJ_ASSEMBLE
+  // PJ_ASSEMBLE, PJ_ASSEMBLE_SUM (codeword sums only: L <= 2, no anchor columns)
   AssembleArgs asm_args;
   // PJ_GATHER
   const bf16_t* A; int k; const int32_t* ids; int V, T; bf16_t* out;
