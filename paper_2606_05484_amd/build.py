@@ -26,9 +26,15 @@ FLAGS = ["--offload-arch=%s" % ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wn
          "-I", os.path.join(ROOT, "include")]
 
 
+# Per-file flags: the RVQ kernel keeps its accumulators in ordinary VGPRs
+# (its score fold reads every accumulator element; the AGPR form would add
+# a copy per element).
+EXTRA = {"k_rvq.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+
+
 def _compile(src):
     obj = os.path.join(BUILD, src + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC] + FLAGS + EXTRA.get(src, []) + ["-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     p = subprocess.run(cmd, capture_output=True, text=True)

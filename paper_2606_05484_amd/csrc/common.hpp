@@ -129,6 +129,17 @@ __device__ __forceinline__ void lds_wait(u32x4 (&v)[N]) {
 // reg_pin() on the registers loaded before it.
 __device__ __forceinline__ void lds_wait0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// Wait until at most N LDS operations of this wave are outstanding; v is
+// defined only after the wait.  Valid only while no scalar memory load is in
+// flight (those count too and complete out of order); LDS operations
+// complete in order, so with the N reads issued after v's among the
+// outstanding ones, v has landed.
+template <int N>
+__device__ __forceinline__ void lds_wait_n(u32x4& v) {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt is 4 bits");
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(v) : "n"(N) : "memory");
+}
+
 // Pins registers after an earlier lds_wait0() / lds_wait() (no instruction
 // emitted): both are volatile asm, so their order is kept, and every later
 // use of the registers depends on the pin.

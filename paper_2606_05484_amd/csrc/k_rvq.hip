@@ -219,13 +219,18 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
         // rows lane % 32 of a tile, 16 B chunk 2s + lane / 32 (s = NK16: the
         // norm columns)
         const uint32_t cbase = lds_addr(sc) + (lane & 31) * RB + half * 16;
-        u32x4 f0[P], f1[P];  // [0] norm step, [1 + s] coordinate k-step s
-        auto read = [&](auto ctc, auto rc, u32x4(&f)[P]) {
-          constexpr int CT = decltype(ctc)::value, RI = decltype(rc)::value;
+        // The chunk's 2P products read one fragment each, in order, through
+        // a window of W registers: fragment p + W is read right after
+        // product p, and product p waits until at most the reads issued
+        // after fragment p are outstanding (LDS reads complete in order).
+        constexpr int W = 4, NP2 = 2 * P;
+        u32x4 fw[W];
+        auto read = [&](auto pc) {
+          constexpr int PI = decltype(pc)::value, CT = PI / P, RI = PI % P;
           if constexpr (RI == 0)
-            f[0] = lds_read_b128<CT * 32 * RB + 32 * NK16>(cbase);
-          else if constexpr (RI < P)
-            f[RI] = lds_read_b128<CT * 32 * RB + 32 * (RI - 1)>(cbase);
+            fw[PI % W] = lds_read_b128<CT * 32 * RB + 32 * NK16>(cbase);
+          else
+            fw[PI % W] = lds_read_b128<CT * 32 * RB + 32 * (RI - 1)>(cbase);
         };
         auto opnd = [&](auto sc2) -> const uint4& {
           constexpr int S = decltype(sc2)::value;
@@ -234,36 +239,34 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
           else
             return rb[S - 1];
         };
-        static_for<0, P>([&](auto rc) { read(std::integral_constant<int, 0>{}, rc, f0); });
+        static_for<0, W>([&](auto pc) { read(pc); });
         fold_all(pend, pend_tile);
-        lds_wait0();
-        reg_pin(f0);
-        f32x16_t acc0 = f32x16_t{};
-        static_for<0, P>([&](auto sc2) {
-          constexpr int S = decltype(sc2)::value;
-          acc0 = mfma32x32x16(as_uint4(f0[S]), opnd(sc2), acc0);
+        // an invalid second tile (K % 64 == 32) reads zero rows; its
+        // products are computed and discarded
+        f32x16_t acc0 = f32x16_t{}, acc1 = f32x16_t{};
+        static_for<0, NP2>([&](auto pc) {
+          constexpr int PI = decltype(pc)::value, CT = PI / P, S = PI % P;
+          constexpr int AHEAD = (NP2 - 1 - PI) < (W - 1) ? (NP2 - 1 - PI) : (W - 1);
+          lds_wait_n<AHEAD>(fw[PI % W]);
+          if constexpr (CT == 0)
+            acc0 = mfma32x32x16(as_uint4(fw[PI % W]), opnd(std::integral_constant<int, S>{}), acc0);
+          else
+            acc1 = mfma32x32x16(as_uint4(fw[PI % W]), opnd(std::integral_constant<int, S>{}), acc1);
           __builtin_amdgcn_sched_barrier(0);
-          read(std::integral_constant<int, 1>{}, sc2, f1);
-          __builtin_amdgcn_sched_barrier(0);
-        });
-        lds_wait0();
-        reg_pin(f1);
-        if (t1ok) {
-          f32x16_t acc1 = f32x16_t{};
-          fbegin();
-          static_for<0, P>([&](auto sc2) {
-            constexpr int S = decltype(sc2)::value;
-            acc1 = mfma32x32x16(as_uint4(f1[S]), opnd(sc2), acc1);
-            __builtin_amdgcn_sched_barrier(0);
+          if constexpr (PI + W < NP2) read(std::integral_constant<int, PI + W>{});
+          if constexpr (CT == 1) {
+            // the first tile's scores, folded a share per product of the second
+            if constexpr (S == 0) fbegin();
             constexpr int E0 = S * FPS < 16 ? S * FPS : 16, E1 = (S + 1) * FPS < 16 ? (S + 1) * FPS : 16;
             static_for<E0, E1>([&](auto ec) { fscore(acc0, 2 * q, ec); });
-            __builtin_amdgcn_sched_barrier(0);
-          });
-          fend(2 * q);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        });
+        fend(2 * q);
+        if (t1ok) {
           pend = acc1;
           pend_tile = 2 * q + 1;
         } else {
-          fold_all(acc0, 2 * q);
 #pragma unroll
           for (int e = 0; e < 16; ++e) pend[e] = 3.0e38f;
           pend_tile = -1;
