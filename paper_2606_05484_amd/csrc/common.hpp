@@ -35,8 +35,17 @@ __device__ __forceinline__ f32x16_t mfma32x32x16(const uint4& a, const uint4& b,
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, c, 0, 0, 0);
 }
 
+// 16x16x32 bf16 MFMA, fp32 accumulate.
+// Lane l holds A[m = l%16][k = 8(l/16) .. +7] and B[k = 8(l/16) .. +7][n = l%16];
+// accumulator j of lane l is D[m = 4(l/16) + j][n = l%16].
+__device__ __forceinline__ f32x4_t mfma16x16x32(const uint4& a, const uint4& b, f32x4_t c) {
+  bf16x8_t av = __builtin_bit_cast(bf16x8_t, a);
+  bf16x8_t bv = __builtin_bit_cast(bf16x8_t, b);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, c, 0, 0, 0);
+}
+
 // 32x32x2 fp32 MFMA: lane l holds A[m = l%32][k = l/32], B[k = l/32][n = l%32];
-// accumulator layout as above.
+// accumulator layout as for mfma32x32x16.
 __device__ __forceinline__ f32x16_t mfma32x32x2f32(float a, float b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
@@ -47,7 +56,8 @@ __device__ __forceinline__ int clamp_id(int id, int V) { return (unsigned)id < (
 __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
 
 // Screening margin of the RVQ kernel for residual width R: with the
-// accumulator started at ||C_j||^2 and bf16 operands,
+// accumulator holding ||C_j||^2 exactly after the first k-step (three bf16
+// pieces that sum to it exactly, times ones) and bf16 operands,
 //   |s~_j - s_j| <= k1 ||R|| ||C_j|| + k2 ||C_j||^2, where
 //   k1 = 2 (2 * 2^-8 + 2^-16)  (bf16 rounding of both operands, doubled)
 //      + 8 R 2^-24             (fp32 accumulation of 2R~.C~, any order,

@@ -250,61 +250,59 @@ __global__ void k_gather_rows_bf16(const bf16_t* __restrict__ A, int k, const in
 }
 
 // dst[c * ldd + off + i] = bf16(scale * sum_j P[i][j] bf16(Q(j, c))) for a
-// 32 x 32 output tile (i0 = 32 by, c0 = 32 bx): P bf16 [M, Kd] row-major,
+// 16 x 16 output tile (i0 = 16 by, c0 = 16 bx): P bf16 [M, Kd] row-major,
 // Q(j, c) = Q[j * ldq + c] (qt = 0) or Q[c * ldq + j] (qt = 1), fp32, rounded
-// to bf16 where it enters the matrix units; fp32 accumulation.  The four
-// waves take every fourth 16-wide k-step and add their partial tiles
-// through LDS in a fixed order.  Kd % 16 == 0, N % 32 == 0; rows >= M are
-// not written.
+// to bf16 where it enters the matrix units; fp32 accumulation
+// (v_mfma_f32_16x16x32_bf16).  The four waves take every fourth 32-wide
+// k-step and add their partial tiles through LDS in a fixed order; small
+// tiles give many workgroups, so each wave's chain of dependent loads over
+// K stays short.  Kd % 32 == 0, N % 16 == 0; rows >= M are not written.
 __device__ __forceinline__ void small_gemm_tile(int bx, int by, const PrepJob& j) {
-  __shared__ float part[3][32 * 32];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5;
-  const int i0 = by * 32, c0 = bx * 32;
-  const int prow = min(i0 + (lane & 31), j.M - 1);
+  __shared__ float part[3][16 * 16];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, quad = lane >> 4;
+  const int i0 = by * 16, c0 = bx * 16;
+  const int prow = min(i0 + (lane & 15), j.M - 1);
   const bf16_t* P = (const bf16_t*)j.P + (int64_t)prow * j.ldp;
-  const int c = c0 + (lane & 31);
-  f32x16_t acc = f32x16_t{};
-  // batches of up to four k-steps: all loads of a batch are issued before
-  // its products, so their latencies overlap
-  // (every load of a batch is issued before the first conversion: a
-  // conversion right after its own loads would wait for them one k-step at
-  // a time)
+  const int c = c0 + (lane & 15);
+  f32x4_t acc = f32x4_t{};
+  // batches of up to four k-steps: every load of a batch is issued before
+  // the first conversion, so their latencies overlap
   constexpr int NB = 4;
-  for (int kb = 16 * wave; kb < j.Kd; kb += 64 * NB) {
+  for (int kb = 32 * wave; kb < j.Kd; kb += 128 * NB) {
     uint4 a[NB];
     float qv[NB][8];
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
-      const int k0 = min(kb + 64 * u, j.Kd - 16);  // past the end: a repeat, not used
-      a[u] = *(const uint4*)(P + k0 + 8 * half);
+      const int k0 = min(kb + 128 * u, j.Kd - 32);  // past the end: a repeat, not used
+      a[u] = *(const uint4*)(P + k0 + 8 * quad);
       if (j.qt) {
-        const float4* q4 = (const float4*)(j.Q + (int64_t)c * j.ldq + k0 + 8 * half);
+        const float4* q4 = (const float4*)(j.Q + (int64_t)c * j.ldq + k0 + 8 * quad);
         const float4 x0 = q4[0], x1 = q4[1];
         qv[u][0] = x0.x; qv[u][1] = x0.y; qv[u][2] = x0.z; qv[u][3] = x0.w;
         qv[u][4] = x1.x; qv[u][5] = x1.y; qv[u][6] = x1.z; qv[u][7] = x1.w;
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) qv[u][e] = j.Q[(int64_t)(k0 + 8 * half + e) * j.ldq + c];
+        for (int e = 0; e < 8; ++e) qv[u][e] = j.Q[(int64_t)(k0 + 8 * quad + e) * j.ldq + c];
       }
     }
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
       const uint4 b = make_uint4(pack_bf2(qv[u][0], qv[u][1]), pack_bf2(qv[u][2], qv[u][3]),
                                  pack_bf2(qv[u][4], qv[u][5]), pack_bf2(qv[u][6], qv[u][7]));
-      if (kb + 64 * u < j.Kd) acc = mfma32x32x16(a[u], b, acc);
+      if (kb + 128 * u < j.Kd) acc = mfma16x16x32(a[u], b, acc);
     }
   }
-  // acc e: row 8(e/4) + 4 half + e%4 of the tile, column lane % 32
+  // acc e: row 4 quad + e of the tile, column lane % 16
   if (wave > 0) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) part[wave - 1][acc_row(e, lane) * 32 + (lane & 31)] = acc[e];
+    for (int e = 0; e < 4; ++e) part[wave - 1][(4 * quad + e) * 16 + (lane & 15)] = acc[e];
   }
   __syncthreads();
   if (wave == 0) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int row = acc_row(e, lane), col = lane & 31;
-      const float v = ((acc[e] + part[0][row * 32 + col]) + part[1][row * 32 + col]) + part[2][row * 32 + col];
+    for (int e = 0; e < 4; ++e) {
+      const int row = 4 * quad + e, col = lane & 15;
+      const float v = ((acc[e] + part[0][row * 16 + col]) + part[1][row * 16 + col]) + part[2][row * 16 + col];
       if (i0 + row < j.M) j.dst[(int64_t)(c0 + col) * j.ldd + j.off + i0 + row] = (bf16_t)f2bf(j.scale * v);
     }
   }
@@ -443,8 +441,8 @@ PrepJob prep_job_small_gemm(const bf16_t* P, int64_t ldp, const float* Q, int64_
   j.kind = PJ_SMALL_GEMM;
   j.P = P; j.ldp = ldp; j.Q = Q; j.ldq = ldq; j.qt = qt; j.M = M; j.N = N; j.Kd = Kd; j.scale = scale;
   j.dst = dst; j.ldd = ldd; j.off = off;
-  j.gx = N / 32;
-  j.blocks = M > 0 ? ((M + 31) / 32) * (N / 32) : 0;
+  j.gx = N / 16;
+  j.blocks = M > 0 ? ((M + 15) / 16) * (N / 16) : 0;
   return j;
 }
 
@@ -455,7 +453,7 @@ hipError_t launch_prep_batch(const PrepJob* jobs, int n, hipStream_t s) {
     if (jobs[i].blocks <= 0) continue;
     if (b.n == PREP_MAX_JOBS) return hipErrorInvalidValue;
     if (jobs[i].kind == PJ_SMALL_GEMM &&
-        (jobs[i].Kd % 16 || jobs[i].N % 32 || jobs[i].ldp % 8 || (jobs[i].qt && jobs[i].ldq % 4)))
+        (jobs[i].Kd % 32 || jobs[i].N % 16 || jobs[i].ldp % 8 || (jobs[i].qt && jobs[i].ldq % 4)))
       return hipErrorInvalidValue;
     if ((jobs[i].kind == PJ_ASSEMBLE || jobs[i].kind == PJ_ASSEMBLE_SUM) &&
         (jobs[i].asm_args.r % 8 || jobs[i].asm_args.ldo % 8 ||

@@ -1,13 +1,13 @@
 // Projector gradient: dU-type products that contract over tokens,
 //   part[s](m,n) = sum_{t in split s} P[t,m] Q[t,n],
 // with P = dXhat (receiver, Eq. 2 backward) or [X | a_s] (sender, Eq. 1
-// backward; the anchor columns a_s = A_s[ids] are gathered in flight).  Both
-// operands are token-major in HBM, i.e. K-strided for the matrix units, so
-// each thread loads an 8 token x 8 column block with 16 B row loads,
-// transposes it in registers and writes 8 K-contiguous 16 B rows to LDS
-// under an XOR swizzle of the 16 B chunks (conflict-free writes and
-// fragment reads).  Splits over tokens fill the chip; a second kernel sums
-// the splits in a fixed order, so results are bitwise reproducible.
+// backward; the anchor columns come from the gathered copy of A_s[ids]).
+// Both operands are token-major in HBM, i.e. K-strided for the matrix units:
+// 64-token stages of both are copied as they are (16 B chunks, XOR-swizzled
+// per row) into LDS by direct-to-LDS loads, and the matrix units' fragments
+// are read transposed with ds_read_b64_tr_b16 (see tr_frag).  Splits over
+// tokens fill the chip; a second kernel sums the splits in a fixed order, so
+// results are bitwise reproducible.
 #include "common.hpp"
 #include "kernels.hpp"
 
