@@ -186,6 +186,40 @@ def _short(sym):
     return re.sub(r"\(.*", "", s)
 
 
+def _counter_table(d, order, agg):
+    """Mean of every counter of one rocprofv3 --pmc run per chain kernel; with
+    MfmaFlopsBF16 / MfmaFlopsF32 also the matrix rate they imply over the
+    kernel's trace duration, against the dense MFMA peak of its type."""
+    disp = _dispatches(d, "_counter_collection.csv")
+    named = _chain_map(disp, order, len([x for x in disp if "mapl::" in x[1]]) // len(order))
+    acc = {}
+    for name, _, e in named:
+        for c, v in e["ctr"].items():
+            acc.setdefault(name, {}).setdefault(c, []).append(v)
+    ctrs = sorted({c for v in acc.values() for c in v})
+    rate = [c for c in ("MfmaFlopsBF16", "MfmaFlopsF32") if c in ctrs]
+    out = ["", "# rocprofv3 --pmc %s (mean per launch; percentages as rocprofv3 derives them)" % " ".join(ctrs)]
+    if rate:
+        out.append("# TFLOP/s = counted matrix flops over the kernel's trace duration; frac against the dense "
+                   "peak of that type (bf16 2516.6, fp32 157.3)")
+    hdr = "%-24s" % "kernel" + "".join(" %16s" % c for c in ctrs) + ("  %9s %6s" % ("TFLOP/s", "frac") if rate else "")
+    out.append(hdr)
+    for name in order:
+        v = acc.get(name, {})
+        row = "%-24s" % name + "".join(" %16.4g" % np.mean(v[c]) if c in v else " %16s" % "-" for c in ctrs)
+        if rate:
+            us = agg[name][2] / agg[name][1]
+            fl = {c: np.mean(v[c]) for c in rate if c in v}
+            best = max(fl, key=fl.get) if fl else None
+            if best and fl[best] > 0:
+                tf = fl[best] / us / 1e6
+                row += "  %9.1f %6.3f" % (tf, tf * 1e12 / (PEAK_BF16 if best == "MfmaFlopsBF16" else PEAK_F32))
+            else:
+                row += "  %9s %6s" % ("-", "-")
+        out.append(row)
+    return out
+
+
 def summarize(paths, write_traffic):
     bench = json.loads(open(paths[0]).read().strip().splitlines()[-1])
     order = bench["kernel_order"]
@@ -228,11 +262,9 @@ def summarize(paths, write_traffic):
         lines += ["", "# HBM traffic per launch from two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE, KiB per",
                   "# dispatch), each scaled by what the same counter reads for a plain %d-byte device copy:" % calib,
                   "#   FETCH_SIZE %.0f KiB -> factor %.4f;  WRITE_SIZE %.0f KiB -> factor %.4f" % (cf[-1], ff, cw[-1], fw),
-                  "%-24s %12s %12s %14s %14s %7s" % ("kernel", "fetch_KiB", "write_KiB", "traffic_B", "algorithmic_B",
-                                                     "ratio")]
-        bf_ = [json.loads(open(os.path.join(os.path.dirname(p.rstrip("/")), "bench_%s.json" % k)).read().strip()
-                          .splitlines()[-1]) for p, k in ((paths[2], "fetch"), (paths[3], "write"))] \
-            if False else None
+                  "# GB/s = traffic over the kernel's trace duration above; frac = GB/s over 8000 GB/s",
+                  "%-24s %12s %12s %14s %14s %7s %8s %6s" % ("kernel", "fetch_KiB", "write_KiB", "traffic_B",
+                                                           "algorithmic_B", "ratio", "GB/s", "frac")]
         fn = _chain_map(fd, order, len([x for x in fd if "mapl::" in x[1]]) // len(order))
         wn = _chain_map(wd, order, len([x for x in wd if "mapl::" in x[1]]) // len(order))
         kc = kernel_counts(32768, 2048, 256, 128, 2, 1024)
@@ -246,8 +278,12 @@ def summarize(paths, write_traffic):
             tb = fk * 1024 * ff + wk * 1024 * fw
             alg = kc[name][1] if name in kc else None
             traffic[name] = tb
-            lines.append("%-24s %12.0f %12.0f %14.0f %14s %7s" % (name, fk, wk, tb, "%.0f" % alg if alg else "-",
-                                                                 "%.2f" % (tb / alg) if alg else "-"))
+            gbs = tb / (agg[name][2] / agg[name][1]) / 1e3
+            lines.append("%-24s %12.0f %12.0f %14.0f %14s %7s %8.0f %6.3f" % (
+                name, fk, wk, tb, "%.0f" % alg if alg else "-", "%.2f" % (tb / alg) if alg else "-", gbs,
+                gbs * 1e9 / PEAK_HBM))
+    for d in paths[4:]:
+        lines += _counter_table(d, order, agg)
     print("\n".join(lines))
     if write_traffic and traffic:
         path = os.path.join(ROOT, "profiles", "traffic_c4.txt")
@@ -270,7 +306,8 @@ def main():
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with one plain 256 MiB device copy (calibrates FETCH_SIZE / WRITE_SIZE counters)")
     ap.add_argument("--summarize", nargs="+", metavar="PATH",
-                    help="no GPU: BENCH_JSON TRACE_DIR [FETCH_DIR WRITE_DIR] -> kernel summary on stdout")
+                    help="no GPU: BENCH_JSON TRACE_DIR [FETCH_DIR WRITE_DIR [PMC_DIR ...]] -> kernel summary on "
+                         "stdout (each PMC_DIR: one more rocprofv3 --pmc run, every counter tabulated)")
     ap.add_argument("--write-traffic", action="store_true",
                     help="with --summarize and counter dirs: rewrite profiles/traffic_c4.txt")
     args = ap.parse_args()
