@@ -58,6 +58,7 @@ def kernel_counts(T, d, r, k, L, K):
     Bytes count each kernel's compulsory HBM inputs and outputs at the
     element sizes the kernel uses (bf16 activations, fp32 Z0 / partials)."""
     return {
+        "enc:gemm_rvq": (2 * T * r * (d + k) + 2 * T * L * r * K, T * (2 * d + 4 + 2 * k) + T * L * 2),
         "enc:gemm_tn": (2 * T * r * (d + k), T * (2 * d + 4 + 2 * k) + T * r * 4),
         "enc:rvq": (2 * T * L * r * K, T * r * 4 + T * L * 2),
         "dec:gemm_tn": (2 * T * d * (r + k), T * (2 * r + 4 + 2 * k) + T * d * 2),
@@ -78,6 +79,7 @@ def _src_sha(files):
 
 
 _SRC_BY_KERNEL = {"gemm_tn": "k_gemm_bf16.hip", "bu_gemm": "k_gemm_bf16.hip", "rvq": "k_rvq.hip",
+                  "gemm_rvq": "k_rvq.hip",
                   "wgrad": "k_wgrad.hip", "reduce": "k_wgrad.hip", "reduce_corr": "k_wgrad.hip",
                   "anchor_reduce": "k_wgrad.hip", "bu_reduce": "k_wgrad.hip"}
 
@@ -85,7 +87,7 @@ _SRC_BY_KERNEL = {"gemm_tn": "k_gemm_bf16.hip", "bu_gemm": "k_gemm_bf16.hip", "r
 def kernel_sources(name):
     """Source files whose text decides a chain kernel's code and launch shape."""
     short = name.split(":")[-1]
-    return [_SRC_BY_KERNEL.get(short, "k_prep.hip"), "common.hpp", "kernels.hpp", "mapl_api.cpp"]
+    return [_SRC_BY_KERNEL.get(short, "k_prep.hip"), "tn_gemm.hpp", "common.hpp", "kernels.hpp", "mapl_api.cpp"]
 
 
 def traffic_for(kernel):

@@ -25,8 +25,8 @@
 //           and lists every candidate; the candidates are rescored exactly
 //           in fp32 as sum_c (R_c - C_jc)^2.
 // The fp32 residual stays in registers across rounds, updated as
-// R_{l+1} = R_l - C_l[code_l]: the operation sequence the rescoring uses to
-// rebuild it from Z0 and the codes, so both see the same R.
+// R_{l+1} = R_l - C_l[code_l]; the rescoring reads it from there (through a
+// per-wave LDS row), so screening and rescoring see the same R.
 //
 // Layout: a workgroup of 4 waves owns 128 tokens, 32 per wave.  A wave keeps
 // its tokens' bf16(-2R) as the B operand of v_mfma_f32_32x32x16_bf16 in
@@ -37,8 +37,7 @@
 // Each lane thus sees the scores of ONE token for 16 codewords per tile;
 // the fold of one tile into (m1, m2) overlaps the matrix products of the
 // next.  The two lane halves that share a token merge at the end of a pass.
-#include "common.hpp"
-#include "kernels.hpp"
+#include "tn_gemm.hpp"
 
 namespace mapl {
 
@@ -81,20 +80,33 @@ __device__ __forceinline__ float rq_tag(float s, int e) {
   return __uint_as_float((__float_as_uint(s) & ~15u) | (uint32_t)e);
 }
 
+// Per-workgroup LDS of the rounds besides the three codebook stages.
+struct RqSmall {
+  uint16_t codes_s[RQ_TOK][RQ_LMAX];  // decisions of the earlier rounds
+  int cand_cnt[RQ_TOK];
+  uint16_t cand[RQ_TOK][RQ_CAP];
+  int amb_s[RQ_TOK];
+  float red_s[4];
+};
+
+// The L rounds for the workgroup's 128 tokens (blockIdx.x), given each
+// lane's fp32 residual R_0 = Z0 (columns 16 s + 8 (lane / 32) + 0..7 of
+// token 32 wave + lane % 32; zeros past T).  s0, s1, s2: three stage
+// buffers of at least sizeof(RqStage<R>) bytes, each its own __shared__
+// object; rvs: 4 R floats of LDS (one token's residual per wave while it is
+// rescored).  No load may be in flight on entry and the workgroup must have
+// passed a barrier after its last use of the buffers.
 template <int R>
-__global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_rvq(RvqArgs a) {
-#if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature (launch stub)
+__device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t* s1, bf16_t* s2, RqSmall& sm,
+                                           float* rvs, float (&res)[R / 16][8]) {
   constexpr int NK16 = R / 16;                     // k-steps of the coordinates
   constexpr int CPR = (R + 16) / 8;                // 16 B chunks per codeword row
   constexpr int LOADS = rq_blocks<R>();            // DMA blocks per wave per stage
-  __shared__ __attribute__((aligned(1024))) RqStage<R> S0;
-  __shared__ __attribute__((aligned(1024))) RqStage<R> S1;
-  __shared__ __attribute__((aligned(1024))) RqStage<R> S2;
-  __shared__ uint16_t codes_s[RQ_TOK][RQ_LMAX];
-  __shared__ int cand_cnt[RQ_TOK];
-  __shared__ uint16_t cand[RQ_TOK][RQ_CAP];
-  __shared__ int amb_s[RQ_TOK];
-  __shared__ float red_s[4];
+  auto& codes_s = sm.codes_s;
+  auto& cand_cnt = sm.cand_cnt;
+  auto& cand = sm.cand;
+  auto& amb_s = sm.amb_s;
+  auto& red_s = sm.red_s;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
   const int tl = wave * 32 + (lane & 31);  // token within the workgroup
@@ -117,22 +129,7 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
     c_off[jb] = (row < RQ_CW && ch < CPR) ? (uint32_t)row * (uint32_t)((R + 16) * 2) + (uint32_t)ch * 16u : RQ_OOB;
   }
 
-  // fp32 residual of the lane's token, columns 16 s + 8 (lane / 32) + 0..7:
-  // R_0 = Z0, R_{l+1} = R_l - C_l[code_l] (the same operation sequence as
-  // rebuilding it from Z0 and the codes)
-  float res[NK16][8];
-#pragma unroll
-  for (int s = 0; s < NK16; ++s) {
-    float4 z0 = make_float4(0.f, 0.f, 0.f, 0.f), z1 = z0;
-    if (valid) {
-      const float4* zp = (const float4*)(a.Z0 + (int64_t)t * R + 16 * s + 8 * half);
-      z0 = zp[0];
-      z1 = zp[1];
-    }
-    res[s][0] = z0.x; res[s][1] = z0.y; res[s][2] = z0.z; res[s][3] = z0.w;
-    res[s][4] = z1.x; res[s][5] = z1.y; res[s][6] = z1.z; res[s][7] = z1.w;
-  }
-
+  // res: fp32 residual of the lane's token, R_{l+1} = R_l - C_l[code_l]
   for (int l = 0; l < a.L; ++l) {
     const __amdgpu_buffer_rsrc_t rc =
         rq_rsrc(a.Cb + (int64_t)l * a.K * (R + 16), (uint64_t)a.K * (R + 16) * 2);
@@ -151,8 +148,8 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
     };
 
     // ---- the first two chunks are in flight while the residual is built
-    issue(0, S0.c);
-    issue(1, S1.c);
+    issue(0, s0);
+    issue(1, s1);
 
     // largest ||C_j||^2 of the round (entries past K are zero)
     float n2max = 0.f;
@@ -195,8 +192,8 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
     const uint4 rbn = half == 0 ? make_uint4(0x3F803F80u, 0x00003F80u, 0u, 0u) : make_uint4(0u, 0u, 0u, 0u);
     auto pass = [&](auto&& fbegin, auto&& fscore, auto&& fend, bool first) {
       if (!first) {
-        issue(0, S0.c);
-        issue(1, S1.c);
+        issue(0, s0);
+        issue(1, s1);
       }
       f32x16_t pend;
 #pragma unroll
@@ -273,9 +270,9 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
         }
       };
       for (int q = 0; q < total; q += 3) {
-        stage(q, S0.c, S2.c);
-        stage(q + 1, S1.c, S0.c);
-        stage(q + 2, S2.c, S1.c);
+        stage(q, s0, s2);
+        stage(q + 1, s1, s0);
+        stage(q + 2, s2, s1);
       }
       fold_all(pend, pend_tile);
     };
@@ -325,18 +322,24 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
       for (int u = 0; u < 32; ++u) {
         const int tu = wave * 32 + u;
         if (!amb_s[tu]) continue;  // wave-uniform
-        const int tg = blockIdx.x * RQ_TOK + tu;
+        // the token's residual R_l, from the registers of its two lanes
         constexpr int PER = (R + 63) / 64;
+        float* rw = rvs + wave * R;
+        if ((lane & 31) == u) {
+#pragma unroll
+          for (int s = 0; s < NK16; ++s) {
+            *(float4*)(rw + 16 * s + 8 * half) = make_float4(res[s][0], res[s][1], res[s][2], res[s][3]);
+            *(float4*)(rw + 16 * s + 8 * half + 4) = make_float4(res[s][4], res[s][5], res[s][6], res[s][7]);
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         float rv[PER];
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
           const int c = lane + 64 * p;
-          float v = 0.f;
-          if (c < R) {
-            v = a.Z0[(int64_t)tg * R + c];
-            for (int i = 0; i < l; ++i) v -= a.C[((int64_t)i * a.K + codes_s[tu][i]) * R + c];
-          }
-          rv[p] = v;
+          rv[p] = c < R ? rw[c] : 0.f;
         }
         const float* Cl = a.C + (int64_t)l * a.K * R;
         auto dist = [&](int j) {
@@ -400,10 +403,136 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
     }
     __syncthreads();
   }
+}
+
+template <int R>
+__global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_rvq(RvqArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)  // the host pass needs only the signature (launch stub)
+  __shared__ __attribute__((aligned(1024))) RqStage<R> S0;
+  __shared__ __attribute__((aligned(1024))) RqStage<R> S1;
+  __shared__ __attribute__((aligned(1024))) RqStage<R> S2;
+  __shared__ RqSmall sm;
+  __shared__ __attribute__((aligned(16))) float rvs[4 * R];
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int t = blockIdx.x * RQ_TOK + (threadIdx.x >> 6) * 32 + (lane & 31);
+  float res[R / 16][8];
+#pragma unroll
+  for (int s = 0; s < R / 16; ++s) {
+    float4 z0 = make_float4(0.f, 0.f, 0.f, 0.f), z1 = z0;
+    if (t < a.T) {
+      const float4* zp = (const float4*)(a.Z0 + (int64_t)t * R + 16 * s + 8 * half);
+      z0 = zp[0];
+      z1 = zp[1];
+    }
+    res[s][0] = z0.x; res[s][1] = z0.y; res[s][2] = z0.z; res[s][3] = z0.w;
+    res[s][4] = z1.x; res[s][5] = z1.y; res[s][6] = z1.z; res[s][7] = z1.w;
+  }
+  rvq_rounds<R>(a, S0.c, S1.c, S2.c, sm, rvs, res);
+#endif
+}
+
+// Encoder in one launch for r = 256: the projection Z0 = [X | a] W of the
+// workgroup's 128 tokens (the GEMM's K loop, one 128 x 256 tile), handed
+// to the RVQ rounds through LDS instead of HBM, so the unquantised
+// coordinates never leave the CU.  The GEMM's three stage buffers hold the
+// fp32 tile (row t of 1 KiB: stage t / 48, 16 B chunks XOR-swizzled by
+// t % 8 so 8 consecutive rows hit distinct bank groups) and then serve as
+// the RVQ's codebook stages.
+constexpr int FU_R = 256;
+static_assert(sizeof(RqStage<FU_R>) <= sizeof(TnSmem<FU_R>), "RVQ stages fit the GEMM stages");
+static_assert(GM == RQ_TOK, "one token block");
+
+template <bool FULLK>
+__global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_enc_rvq(TnArgs g,
+                                                                                                    RvqArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int R = FU_R, NK16 = R / 16;
+  __shared__ __attribute__((aligned(1024))) TnSmem<R> S0;
+  __shared__ __attribute__((aligned(1024))) TnSmem<R> S1;
+  __shared__ __attribute__((aligned(1024))) bf16_t S2buf[(GM + R) * GK];
+  __shared__ RqSmall sm;
+  __shared__ __attribute__((aligned(16))) float rvs[4 * R];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
+  constexpr int ROWS = (int)(sizeof(TnSmem<R>) / 1024);  // 1 KiB fp32 rows per stage buffer
+  static_assert(3 * ROWS >= GM, "the tile fits the stage buffers");
+  auto hrow = [&](int t) -> uint32_t {
+    return t < ROWS ? lds_addr(&S0) + (uint32_t)t * 1024u
+                    : t < 2 * ROWS ? lds_addr(&S1) + (uint32_t)(t - ROWS) * 1024u
+                                   : lds_addr(S2buf) + (uint32_t)(t - 2 * ROWS) * 1024u;
+  };
+  tn_mainloop<R, 3, FULLK>(g, 1, S0.a, S0.w, S1.a, S1.w, S2buf, S2buf + GM * GK,
+                           [&](f32x16_t (&acc)[2][R / 64], int) {
+                             __syncthreads();  // every wave is done reading the stages
+                             const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+                             for (int i = 0; i < 2; ++i) {
+                               const int row = wm * 64 + i * 32 + (lane & 31);
+                               const uint32_t base = hrow(row);
+                               const int sw = row & 7;
+#pragma unroll
+                               for (int j = 0; j < R / 64; ++j) {
+#pragma unroll
+                                 for (int q = 0; q < 4; ++q) {
+                                   // columns 128 wn + 32 j + 8 q + 4 half + 0..3
+                                   const int ch = wn * 32 + 8 * j + 2 * q + half;
+                                   lds_write_b128(base + 16u * (uint32_t)(ch ^ sw),
+                                                  u32x4{__float_as_uint(acc[i][j][4 * q]),
+                                                        __float_as_uint(acc[i][j][4 * q + 1]),
+                                                        __float_as_uint(acc[i][j][4 * q + 2]),
+                                                        __float_as_uint(acc[i][j][4 * q + 3])});
+                                 }
+                                 acc[i][j] = f32x16_t{};
+                               }
+                             }
+                           });
+  lds_wait0();
+  __syncthreads();  // the tile is in LDS
+  float res[NK16][8];
+  {
+    const int row = wave * 32 + (lane & 31), sw = row & 7;
+    const uint32_t base = hrow(row);
+#pragma unroll
+    for (int s0 = 0; s0 < NK16; s0 += 4) {
+      u32x4 v[8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        // columns 16 (s0 + u) + 8 half + 0..7: chunks 4 (s0 + u) + 2 half (+1)
+        const int ch = 4 * (s0 + u) + 2 * half;
+        v[2 * u] = lds_read_b128(base + 16u * (uint32_t)(ch ^ sw));
+        v[2 * u + 1] = lds_read_b128(base + 16u * (uint32_t)((ch + 1) ^ sw));
+      }
+      lds_wait(v);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          res[s0 + u][e] = __uint_as_float(v[2 * u][e]);
+          res[s0 + u][4 + e] = __uint_as_float(v[2 * u + 1][e]);
+        }
+    }
+  }
+  __syncthreads();  // the stages are free for the codebook
+  rvq_rounds<R>(a, S0.a, S1.a, S2buf, sm, rvs, res);
 #endif
 }
 
 }  // namespace
+
+bool enc_rvq_fusable(int r, int L) { return r == FU_R && L >= 1 && L <= RQ_LMAX; }
+
+hipError_t launch_enc_rvq(const TnArgs& g, const RvqArgs& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  if (!enc_rvq_fusable(a.r, a.L) || g.N != FU_R || g.M != a.T || g.kz != 0) return hipErrorInvalidValue;
+  if (g.Ka % 32 || g.Kg % 16 || g.Ka + g.Kg > g.ldw || g.lda % 8 || g.ldt % 8 || g.ldw % 8)
+    return hipErrorInvalidValue;
+  const bool fullk = g.Ka % GK == 0 && g.Kg % GK == 0;
+  dim3 grid((a.T + RQ_TOK - 1) / RQ_TOK);
+  if (fullk)
+    hipLaunchKernelGGL(k_enc_rvq<true>, grid, dim3(RQ_THREADS), 0, s, g, a);
+  else
+    hipLaunchKernelGGL(k_enc_rvq<false>, grid, dim3(RQ_THREADS), 0, s, g, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_rvq(const RvqArgs& a, hipStream_t s) {
   if (a.T <= 0 || a.L <= 0) return hipSuccess;

@@ -154,6 +154,11 @@ struct RvqArgs {
   int* stats;          // [4] optional counters (candidates, overflow), may be null
 };
 hipError_t launch_rvq(const RvqArgs& a, hipStream_t s);
+// The encoder in one launch: Z0 = [X | a] W as launch_gemm_tn computes it
+// (g.N == r, fp32, never stored; g.out unused), then the RVQ rounds of
+// launch_rvq on it (a.Z0 unused).  Only where enc_rvq_fusable(r, L).
+bool enc_rvq_fusable(int r, int L);
+hipError_t launch_enc_rvq(const TnArgs& g, const RvqArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- fp32 codec path helpers
 // out[t][i] = A[ids[t]][i] (fp32) for i < k.

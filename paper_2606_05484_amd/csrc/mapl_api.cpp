@@ -397,13 +397,18 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
       return MAPL_OK;
     }
     float* Z0 = at<float>(ws, Lo.z0);
-    g.out = Z0; g.ldo = r; g.out_f32 = 1;
-    LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
     RvqArgs a{};
     a.Z0 = Z0; a.Cb = Cb; a.C = C; a.meta = meta;
     a.T = (int)T; a.r = (int)r; a.L = D.L; a.K = D.K;
     a.codes = payload; a.code_bytes = cbytes;
     a.stats = nullptr;
+    if (enc_rvq_fusable((int)r, D.L)) {
+      // projection and RVQ in one launch: Z0 stays on chip
+      LAUNCH("enc:gemm_rvq", launch_enc_rvq(g, a, s));
+      return MAPL_OK;
+    }
+    g.out = Z0; g.ldo = r; g.out_f32 = 1;
+    LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
     LAUNCH("enc:rvq", launch_rvq(a, s));
     return MAPL_OK;
   }

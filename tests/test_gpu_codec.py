@@ -216,6 +216,40 @@ def test_planted_codewords_and_duplicate_tie():
         assert codes[t_, 1] == 0
 
 
+@pytest.mark.parametrize("k,L,K", [(64, 2, 96), (48, 1, 64), (0, 3, 128)])
+def test_fused_encoder_r256(k, L, K):
+    """At r = 256 the projection and the RVQ run as one launch (Z0 stays on
+    chip): a ragged token count, anchors whose width is and is not a
+    multiple of the 64-wide K stage, no anchor, one to three rounds, a
+    codebook whose last 64-codeword chunk is half empty, stress codebooks."""
+    x = _x(None, seed=40 + k + L, **dict(SMALL, T=1000 + 37, d=512, r=256, k=k, L=L, K=K))
+    C = stress_codebooks(x, 211 + L)
+    _check_chain(x, _chain(x, C=C), C=C)
+
+
+def test_fused_encoder_planted_and_tied_r256():
+    """The fused encoder's exact fp32 rescoring of ambiguous tokens: codewords
+    planted at oracle coordinates are picked (later rounds then pick the zero
+    codeword); a duplicated codeword (an exact tie) resolves to the lower
+    index."""
+    x = _x(None, seed=15, **dict(SMALL, T=700, d=512, r=256, L=2, K=128))
+    Z0 = ocodec.project(f64(x, "X"), x["ids"], x["U"], f64(x, "A"), f64(x, "B"), "ambient", "bf16")
+    C = np.zeros((2, 128, x["r"]), dtype=np.float32)
+    rng = np.random.default_rng(1)
+    C[:, 1:] = (5 + rng.standard_normal((2, 127, x["r"]))).astype(np.float32)
+    plant = {3: 9, 130: 70, 699: 127}
+    for t_, j in plant.items():
+        C[0, j] = Z0[t_].astype(np.float32)
+    C[0, 120] = C[0, 70]  # duplicate of 70
+    C[0, 110] = C[0, 9]  # duplicate of 9
+    D = descr(x)
+    g = Dev(x, C)
+    codes = codes_np(run_encode(x, D, g), D)
+    for t_, j in plant.items():
+        assert codes[t_, 0] == j, (t_, codes[t_])
+        assert codes[t_, 1] == 0
+
+
 @pytest.mark.slow
 def test_c4_full_size_sampled():
     """The benchmark workload (T=32768, d=2048, r=256, k=128, L=2, K=1024)
