@@ -164,7 +164,8 @@ Layout layout(const mapl_codec_desc& D, int call) {
         Lo.kw = d + Lo.kp;
         Lo.w = c.take((size_t)r * Lo.kw * 2);
         if (D.L > 0) {
-          Lo.z0 = c.take((size_t)T * r * 4);
+          // fp32 Z0 between the projection and the RVQ, unless one launch does both
+          if (!enc_rvq_fusable((int)r, D.L)) Lo.z0 = c.take((size_t)T * r * 4);
           Lo.cb = c.take((size_t)D.L * D.K * rvq_cb_cols((int)r) * 2);
           Lo.cn2 = c.take((size_t)rvq_meta_floats(D.L, D.K) * 4);
           Lo.stats = c.take(16);
@@ -396,9 +397,8 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
       LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
       return MAPL_OK;
     }
-    float* Z0 = at<float>(ws, Lo.z0);
     RvqArgs a{};
-    a.Z0 = Z0; a.Cb = Cb; a.C = C; a.meta = meta;
+    a.Z0 = nullptr; a.Cb = Cb; a.C = C; a.meta = meta;
     a.T = (int)T; a.r = (int)r; a.L = D.L; a.K = D.K;
     a.codes = payload; a.code_bytes = cbytes;
     a.stats = nullptr;
@@ -407,8 +407,10 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
       LAUNCH("enc:gemm_rvq", launch_enc_rvq(g, a, s));
       return MAPL_OK;
     }
+    float* Z0 = at<float>(ws, Lo.z0);
     g.out = Z0; g.ldo = r; g.out_f32 = 1;
     LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
+    a.Z0 = Z0;
     LAUNCH("enc:rvq", launch_rvq(a, s));
     return MAPL_OK;
   }
