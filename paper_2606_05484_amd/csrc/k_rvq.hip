@@ -82,7 +82,6 @@ __device__ __forceinline__ float rq_tag(float s, int e) {
 
 // Per-workgroup LDS of the rounds besides the three codebook stages.
 struct RqSmall {
-  uint16_t codes_s[RQ_TOK][RQ_LMAX];  // decisions of the earlier rounds
   int cand_cnt[RQ_TOK];
   uint16_t cand[RQ_TOK][RQ_CAP];
   int amb_s[RQ_TOK];
@@ -102,7 +101,6 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
   constexpr int NK16 = R / 16;                     // k-steps of the coordinates
   constexpr int CPR = (R + 16) / 8;                // 16 B chunks per codeword row
   constexpr int LOADS = rq_blocks<R>();            // DMA blocks per wave per stage
-  auto& codes_s = sm.codes_s;
   auto& cand_cnt = sm.cand_cnt;
   auto& cand = sm.cand;
   auto& amb_s = sm.amb_s;
@@ -129,31 +127,39 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
     c_off[jb] = (row < RQ_CW && ch < CPR) ? (uint32_t)row * (uint32_t)((R + 16) * 2) + (uint32_t)ch * 16u : RQ_OOB;
   }
 
-  // res: fp32 residual of the lane's token, R_{l+1} = R_l - C_l[code_l]
-  for (int l = 0; l < a.L; ++l) {
+  // chunk q of round l's codebook into stage buffer sc
+  auto issue_l = [&](int l, int q, bf16_t* sc) {
     const __amdgpu_buffer_rsrc_t rc =
         rq_rsrc(a.Cb + (int64_t)l * a.K * (R + 16), (uint64_t)a.K * (R + 16) * 2);
-    const float* n2g = a.meta + (int64_t)l * nchunks * 64;
-
-    auto issue = [&](int q, bf16_t* sc) {
-      const bool pad = q >= nchunks;
-      // rows past K read zeros through the resource bound (K % 32 == 0)
+    const bool pad = q >= nchunks;
+    // rows past K read zeros through the resource bound (K % 32 == 0)
 #pragma unroll
-      for (int jb = 0; jb < CBLK; ++jb)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (rq_lds_ptr)(sc + (wave * CBLK + jb) * 512), 16,
-                                                 (!pad && c_off[jb] != RQ_OOB)
-                                                     ? (uint32_t)(q * RQ_CW) * (uint32_t)((R + 16) * 2) + c_off[jb]
-                                                     : RQ_OOB,
-                                                 0, 0, 0);
-    };
+    for (int jb = 0; jb < CBLK; ++jb)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (rq_lds_ptr)(sc + (wave * CBLK + jb) * 512), 16,
+                                               (!pad && c_off[jb] != RQ_OOB)
+                                                   ? (uint32_t)(q * RQ_CW) * (uint32_t)((R + 16) * 2) + c_off[jb]
+                                                   : RQ_OOB,
+                                               0, 0, 0);
+  };
+  // this thread's share of the largest ||C_j||^2 of round l (zero past K)
+  auto n2share = [&](int l) {
+    const float* n2g = a.meta + (int64_t)l * nchunks * 64;
+    float m = 0.f;
+    for (int j = tid; j < nchunks * 64; j += RQ_THREADS) m = fmaxf(m, n2g[j]);
+    return m;
+  };
 
-    // ---- the first two chunks are in flight while the residual is built
-    issue(0, s0);
-    issue(1, s1);
+  // A round's first two chunks and its norm maxima are requested before the
+  // previous round's residual update, so their latencies overlap.
+  issue_l(0, 0, s0);
+  issue_l(0, 1, s1);
+  float n2next = n2share(0);
 
-    // largest ||C_j||^2 of the round (entries past K are zero)
-    float n2max = 0.f;
-    for (int j = tid; j < nchunks * 64; j += RQ_THREADS) n2max = fmaxf(n2max, n2g[j]);
+  // res: fp32 residual of the lane's token, R_{l+1} = R_l - C_l[code_l]
+  for (int l = 0; l < a.L; ++l) {
+    auto issue = [&](int q, bf16_t* sc) { issue_l(l, q, sc); };
+
+    float n2max = n2next;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) n2max = fmaxf(n2max, __shfl_xor(n2max, o, WAVE));
     if (lane == 0) red_s[wave] = n2max;
@@ -384,6 +390,11 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
     }
     if (jstar < 0 || jstar >= a.K) jstar = 0;  // only reachable with non-finite inputs
     if (l + 1 < a.L) {
+      // every wave is past this round's last stage barrier (and the
+      // rescoring's), so stages 0 and 1 are free
+      issue_l(l + 1, 0, s0);
+      issue_l(l + 1, 1, s1);
+      n2next = n2share(l + 1);
       const float* cw = a.C + ((int64_t)l * a.K + jstar) * R + 8 * half;
 #pragma unroll
       for (int s = 0; s < NK16; ++s) {
@@ -395,13 +406,14 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       }
     }
     if (half == 0 && valid) {
-      codes_s[tl][l] = (uint16_t)jstar;
       if (a.code_bytes == 1)
         ((uint8_t*)a.codes)[(int64_t)t * a.L + l] = (uint8_t)jstar;
       else
         ((uint16_t*)a.codes)[(int64_t)t * a.L + l] = (uint16_t)jstar;
     }
-    __syncthreads();
+    // no barrier: the next round's shared state (red_s, and amb_s, cand_cnt,
+    // cand and rvs, which only the token's own wave touches) is written
+    // after barriers that every wave reaches only once done with this round
   }
 }
 
