@@ -216,14 +216,16 @@ def test_planted_codewords_and_duplicate_tie():
         assert codes[t_, 1] == 0
 
 
-@pytest.mark.parametrize("k,L,K", [(64, 2, 96), (48, 1, 64), (0, 3, 128)])
-def test_fused_encoder_r256(k, L, K):
+@pytest.mark.parametrize("T,k,L,K", [(1037, 64, 2, 96), (1037, 48, 1, 64), (1037, 0, 3, 128), (1, 16, 2, 32),
+                                     (129, 64, 1, 32)])
+def test_fused_encoder_r256(T, k, L, K):
     """At r = 256 the projection and the RVQ run as one launch (Z0 stays on
-    chip): a ragged token count, anchors whose width is and is not a
-    multiple of the 64-wide K stage, no anchor, one to three rounds, a
-    codebook whose last 64-codeword chunk is half empty, stress codebooks."""
-    x = _x(None, seed=40 + k + L, **dict(SMALL, T=1000 + 37, d=512, r=256, k=k, L=L, K=K))
-    C = stress_codebooks(x, 211 + L)
+    chip): ragged token counts (one token; one block and one token), anchors
+    whose width is and is not a multiple of the 64-wide K stage, no anchor,
+    one to three rounds, codebooks whose last 64-codeword chunk is half empty
+    (K = 32: the only chunk), stress codebooks."""
+    x = _x(None, seed=40 + k + L, **dict(SMALL, T=T, d=512, r=256, k=k, L=L, K=K))
+    C = stress_codebooks(x, 211 + L) if T >= K else None
     _check_chain(x, _chain(x, C=C), C=C)
 
 
