@@ -185,9 +185,11 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
     // callbacks see begin(), score(acc, tile, e) for e = 0..15, end(tile).
     // Software pipeline per 64-codeword chunk (asm LDS reads, see
     // lds_read_b128; sched_barrier keeps the interleave):
-    //   reads(tile 0) | fold(last tile of the previous chunk) | wait
-    //   tile 0 products, each followed by a share of the reads of tile 1
-    //   wait | tile 1 products, each followed by a share of the fold of tile 0
+    //   first fragment reads
+    //   tile 0 products, each followed by a later fragment read and a share
+    //     of the fold of the previous chunk's tile 1
+    //   tile 1 products, each followed by a later fragment read and a share
+    //     of the fold of tile 0
     // Reads of an invalid second tile (K % 64 == 32) hit zero-filled rows and
     // are discarded.
     // Products per tile: the norm step, then the NK16 coordinate k-steps;
@@ -243,7 +245,6 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
             return rb[S - 1];
         };
         static_for<0, W>([&](auto pc) { read(pc); });
-        fold_all(pend, pend_tile);
         // an invalid second tile (K % 64 == 32) reads zero rows; its
         // products are computed and discarded
         f32x16_t acc0 = f32x16_t{}, acc1 = f32x16_t{};
@@ -257,10 +258,16 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
             acc1 = mfma32x32x16(as_uint4(fw[PI % W]), opnd(std::integral_constant<int, S>{}), acc1);
           __builtin_amdgcn_sched_barrier(0);
           if constexpr (PI + W < NP2) read(std::integral_constant<int, PI + W>{});
-          if constexpr (CT == 1) {
+          constexpr int E0 = S * FPS < 16 ? S * FPS : 16, E1 = (S + 1) * FPS < 16 ? (S + 1) * FPS : 16;
+          if constexpr (CT == 0) {
+            // the previous chunk's second tile, folded a share per product
+            // of this chunk's first
+            if constexpr (S == 0) fbegin();
+            static_for<E0, E1>([&](auto ec) { fscore(pend, pend_tile, ec); });
+            if constexpr (S == P - 1) fend(pend_tile);
+          } else {
             // the first tile's scores, folded a share per product of the second
             if constexpr (S == 0) fbegin();
-            constexpr int E0 = S * FPS < 16 ? S * FPS : 16, E1 = (S + 1) * FPS < 16 ? (S + 1) * FPS : 16;
             static_for<E0, E1>([&](auto ec) { fscore(acc0, 2 * q, ec); });
           }
           __builtin_amdgcn_sched_barrier(0);
