@@ -89,7 +89,9 @@ enum mapl_call {
 /* One boundary, one micro-batch.
  *   T  tokens (B*T of the paper flattened), 0 <= T < 2^31
  *   d  model width, multiple of 64, 64 <= d <= 16384
- *   r  projector rank, multiple of 32, 32 <= r <= min(d, 1024)
+ *   r  projector rank, multiple of 32, 32 <= r <= min(d, 1024); the bf16
+ *      path needs r % 64 == 0, and r in {64, 128, 256} when L > 0
+ *      (MAPL_E_UNSUPPORTED otherwise)
  *   V  vocabulary size (rows of A), >= 1 when k > 0
  *   k  anchor rank, multiple of 16, 0 <= k <= min(d, 512); 0 = no anchor
  *   anchor_space  enum mapl_anchor_space

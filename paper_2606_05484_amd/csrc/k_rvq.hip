@@ -558,7 +558,6 @@ hipError_t launch_rvq(const RvqArgs& a, hipStream_t s) {
   if (a.L > RQ_LMAX) return hipErrorInvalidValue;
   dim3 grid((a.T + RQ_TOK - 1) / RQ_TOK);
   switch (a.r) {
-    case 32: hipLaunchKernelGGL(k_rvq<32>, grid, dim3(RQ_THREADS), 0, s, a); break;
     case 64: hipLaunchKernelGGL(k_rvq<64>, grid, dim3(RQ_THREADS), 0, s, a); break;
     case 128: hipLaunchKernelGGL(k_rvq<128>, grid, dim3(RQ_THREADS), 0, s, a); break;
     case 256: hipLaunchKernelGGL(k_rvq<256>, grid, dim3(RQ_THREADS), 0, s, a); break;

@@ -236,6 +236,9 @@ int check_desc(const mapl_codec_desc* D) {
     return fail(MAPL_E_SHAPE, "V=%lld: need V >= 1 and an anchor table under 2 GiB", (long long)D->V);
   if (D->anchor_space != MAPL_ANCHOR_AMBIENT && D->anchor_space != MAPL_ANCHOR_COORD)
     return fail(MAPL_E_SHAPE, "anchor_space=%d unknown", D->anchor_space);
+  if (D->x_dtype == MAPL_BF16 && D->r % 64)
+    return fail(MAPL_E_UNSUPPORTED, "the bf16 path needs r %% 64 == 0 (got r=%lld; r = 32 runs in fp32)",
+                (long long)D->r);
   if (D->L < 0 || D->L > 8) return fail(MAPL_E_SHAPE, "L=%d: need 0 <= L <= 8", D->L);
   if (D->L > 0) {
     if (D->K < 32 || D->K > 65536 || D->K % 32) return fail(MAPL_E_SHAPE, "K=%d: need 32 <= K <= 65536, K %% 32 == 0", D->K);
@@ -244,8 +247,8 @@ int check_desc(const mapl_codec_desc* D) {
     } else if (D->code_dtype != MAPL_U16) {
       return fail(MAPL_E_DTYPE, "code_dtype must be MAPL_U8 or MAPL_U16 (got %d)", D->code_dtype);
     }
-    if (D->x_dtype == MAPL_BF16 && D->r != 32 && D->r != 64 && D->r != 128 && D->r != 256)
-      return fail(MAPL_E_UNSUPPORTED, "RVQ on the bf16 path supports r in {32, 64, 128, 256} (got %lld)", (long long)D->r);
+    if (D->x_dtype == MAPL_BF16 && D->r != 64 && D->r != 128 && D->r != 256)
+      return fail(MAPL_E_UNSUPPORTED, "RVQ on the bf16 path supports r in {64, 128, 256} (got %lld)", (long long)D->r);
   }
   return MAPL_OK;
 }

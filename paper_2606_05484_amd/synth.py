@@ -95,7 +95,9 @@ def codec_inputs(name=None, seed=None, anchor_space="ambient", chunk=4096, **ove
     """Draw one codec workload.  Returns a dict of NumPy arrays plus sizes.
 
     Arrays with dtype "bf16" are uint16 bit patterns; "f32" arrays are float32.
-    Keyword overrides replace preset fields (T, d, r, V, k, L, K, dtype, ...).
+    Keyword overrides replace preset fields (T, d, r, V, k, L, K, dtype, ...);
+    rotate=False keeps the power-law spectrum on the coordinate axes instead
+    of behind a random orthogonal Q (no d x d QR: for the widest d).
     """
     cfg = dict(PRESETS[name]) if name else {}
     cfg.update(over)
@@ -105,17 +107,18 @@ def codec_inputs(name=None, seed=None, anchor_space="ambient", chunk=4096, **ove
     L, K = int(cfg["L"]), int(cfg["K"])
     dt = cfg["dtype"]
     rng = np.random.default_rng(seed)
-    Q = _sign_fixed_qr(rng, d, d)
+    rotate = bool(cfg.get("rotate", True))
+    Q = _sign_fixed_qr(rng, d, d) if rotate else None
     out_ch = rng.choice(d, size=int(cfg["n_out"]), replace=False)
     s = np.arange(1, d + 1, dtype=np.float64) ** (-float(cfg["alpha"]))
-    QsT = (Q * s[None, :]).T  # (Z * s) Q^T = Z (Q diag(s))^T
+    QsT = (Q * s[None, :]).T if rotate else None  # (Z * s) Q^T = Z (Q diag(s))^T
     X = np.empty((T, d), dtype=np.uint16 if dt == BF16 else np.float32)
     sq = 0.0
     for t0 in range(0, T, chunk):
         n = min(chunk, T - t0)
         Zc = rng.standard_normal((n, d))
         Nc = rng.standard_normal((n, d))
-        Xc = Zc @ QsT + 0.1 * Nc
+        Xc = (Zc @ QsT if rotate else Zc * s[None, :]) + 0.1 * Nc
         Xc[:, out_ch] *= 20.0
         Xc32 = Xc.astype(np.float32)
         X[t0:t0 + n] = _store(Xc32, dt)

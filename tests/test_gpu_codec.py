@@ -252,6 +252,21 @@ def test_fused_encoder_planted_and_tied_r256():
         assert codes[t_, 1] == 0
 
 
+@pytest.mark.parametrize("over", [
+    dict(T=300, d=512, r=256, k=16, L=8, K=64),        # the most rounds (fused encoder)
+    dict(T=513, d=256, r=64, k=0, L=1, K=65536),       # the largest codebook, u16 codes
+    dict(T=257, d=1024, r=64, k=512, L=2, K=96),       # the widest anchor
+    dict(T=130, d=16384, r=64, k=16, L=1, K=32, rotate=False),  # the widest activations, smallest codebook
+], ids=["L8", "K65536", "k512", "d16384"])
+def test_extreme_shapes(over):
+    """The limits the library accepts (L <= 8, K <= 65536, k <= 512,
+    d <= 16384), each with ragged token counts: the whole chain against the
+    oracle (stress codebooks where there are enough tokens to draw them)."""
+    x = _x(None, seed=50, **dict(SMALL, **over))
+    C = stress_codebooks(x, 223) if x["L"] and x["T"] >= x["K"] else None
+    _check_chain(x, _chain(x, C=C), C=C)
+
+
 @pytest.mark.slow
 def test_c4_full_size_sampled():
     """The benchmark workload (T=32768, d=2048, r=256, k=128, L=2, K=1024)

@@ -65,6 +65,16 @@ def test_rvq_above_r256_on_bf16_unsupported():
     assert _enc(D) == -8
 
 
+@pytest.mark.parametrize("L", [0, 2])
+def test_bf16_rank_not_multiple_of_64_unsupported(L):
+    """The bf16 GEMM and weight-gradient tiles need r % 64 == 0; r = 32 and
+    r = 96 are refused up front (the fp32 path takes r = 32)."""
+    for r in (32, 96):
+        D = mapl.desc(T=64, d=256, r=r, V=100, k=16, L=L, K=64)
+        assert _enc(D) == -8
+        assert "r % 64" in mapl.last_error()
+
+
 def test_null_and_alignment_and_alias_and_workspace():
     D = mapl.desc(T=64, d=256, r=64, V=100, k=16, L=0)
     assert _enc(D, X=None) == -1
