@@ -257,7 +257,10 @@ def test_fused_encoder_planted_and_tied_r256():
     dict(T=513, d=256, r=64, k=0, L=1, K=65536),       # the largest codebook, u16 codes
     dict(T=257, d=1024, r=64, k=512, L=2, K=96),       # the widest anchor
     dict(T=130, d=16384, r=64, k=16, L=1, K=32, rotate=False),  # the widest activations, smallest codebook
-], ids=["L8", "K65536", "k512", "d16384"])
+    dict(T=300, d=512, r=192, k=16, L=0, K=0),         # a rank between the 128- and 256-wide tiles
+    dict(T=200, d=1024, r=1024, k=64, L=0, K=0),       # the largest rank
+    dict(T=1, d=64, r=64, k=16, L=1, K=32),            # the smallest of everything
+], ids=["L8", "K65536", "k512", "d16384", "r192", "r1024", "min"])
 def test_extreme_shapes(over):
     """The limits the library accepts (L <= 8, K <= 65536, k <= 512,
     d <= 16384), each with ragged token counts: the whole chain against the
