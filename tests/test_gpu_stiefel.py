@@ -94,3 +94,18 @@ def test_symmetric_gradient_moves_little():
     Un, _ = _gpu_step(U, G, np.zeros_like(U), 1e-2, 0.95)
     assert _orth_err(Un) <= 1e-5
     print("symmetric-gradient move", np.abs(Un - U).max())
+
+
+@pytest.mark.parametrize("P,d,r", [(1, 256, 256), (3, 96, 32), (1, 1024, 1024)], ids=["square", "odd", "r1024"])
+def test_step_at_shape_limits(P, d, r):
+    """Square projectors (r = d: the Stiefel manifold is the orthogonal
+    group), widths that are multiples of 32 but not of 64 or 128 with several
+    projectors, and the largest rank, against the iteration-matched oracle."""
+    st = synth.stiefel_inputs(None, seed=60 + r, P=P, d=d, r=r, gscale=1.0, lr=1e-2, beta=0.95, steps=1)
+    U, G, M = st["U"], st["G"], st["M"]
+    Un, Mn = _gpu_step(U, G, M, st["lr"], st["beta"])
+    Ur, Mr = spel.stiefel_step_batched(U, G, M, st["lr"], st["beta"], mode="pe")
+    e_u, e_m = rel_fro(Un, Ur), rel_fro(Mn, Mr)
+    print(P, d, r, "U rel err", e_u, "M rel err", e_m, "orth", _orth_err(Un))
+    assert e_u <= 1e-5 and e_m <= 1e-5
+    assert _orth_err(Un) <= 1e-5
