@@ -126,6 +126,18 @@ def test_fp32_ragged_odd_tokens(space):
     _check_chain(x, _chain(x))
 
 
+@pytest.mark.parametrize("over", [
+    dict(T=257, d=256, r=32, k=16, L=8, K=64),      # the most rounds, the smallest rank
+    dict(T=130, d=128, r=96, k=0, L=1, K=2048),     # a rank the bf16 path refuses, a large codebook
+], ids=["L8r32", "r96K2048"])
+def test_fp32_limits(over):
+    """The fp32 path at shapes the bf16 kernels do not take (r = 32, 96) and
+    at the most rounds: the whole chain against the oracle at the fp32
+    tolerance."""
+    x = _x(None, seed=12, **dict(SMALL, dtype="f32", **over))
+    _check_chain(x, _chain(x))
+
+
 def test_fp32_coord_anchor():
     x = _x("c1", anchor_space="coord")
     _check_chain(x, _chain(x))
