@@ -479,7 +479,7 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
                     : t < 2 * ROWS ? lds_addr(&S1) + (uint32_t)(t - ROWS) * 1024u
                                    : lds_addr(S2buf) + (uint32_t)(t - 2 * ROWS) * 1024u;
   };
-  tn_mainloop<R, 3, FULLK>(g, 1, S0.a, S0.w, S1.a, S1.w, S2buf, S2buf + GM * GK,
+  tn_mainloop<R, 3, FULLK, false>(g, 1, S0.a, S0.w, S1.a, S1.w, S2buf, S2buf + GM * GK,
                            [&](f32x16_t (&acc)[2][R / 64], int) {
                              __syncthreads();  // every wave is done reading the stages
                              const int wm = wave >> 1, wn = wave & 1;

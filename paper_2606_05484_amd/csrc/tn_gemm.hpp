@@ -169,7 +169,7 @@ __device__ __forceinline__ void tn_epilogue(f32x16_t (&acc)[2][BN / 64], const T
 // accumulators (layout as for tn_epilogue) and must leave them cleared; no
 // load is in flight then, and every wave has finished its fragment reads of
 // the stages once the workgroup passes a barrier.
-template <int BN, int NS, bool FULLK, typename Epi>
+template <int BN, int NS, bool FULLK, bool ROT = true, typename Epi>
 __device__ __forceinline__ void tn_mainloop(const TnArgs& g, int ntiles_per_wg, bf16_t* s0a, bf16_t* s0w,
                                             bf16_t* s1a, bf16_t* s1w, bf16_t* s2a, bf16_t* s2w, Epi&& epi) {
   static_assert(NS == 2 || NS == 3, "stages");
@@ -195,7 +195,9 @@ __device__ __forceinline__ void tn_mainloop(const TnArgs& g, int ntiles_per_wg, 
   // eight consecutive ids spread over the XCDs): at any moment the token
   // rows in flight then sit at different column offsets, which spreads the
   // strided row reads over more HBM channels and banks.
-  const int rot = KS > 0 ? (int)(blockIdx.x >> 3) % KS : 0;
+  // (ROT = false: every workgroup starts at step 0; measured faster for the
+  // fused encoder, whose RVQ phase follows, and slower for the other uses)
+  const int rot = ROT && KS > 0 ? (int)(blockIdx.x >> 3) % KS : 0;
 
   // Buffer resources: A rows of this workgroup, the anchor table, W.
   const int mrows = min(GM, g.M - m0);
