@@ -161,6 +161,8 @@ int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, const void* X,
  *   g_R = G - U sym(U^T G)                     (Eq. 4, sym(S) = (S+S^T)/2)
  *   M   = beta M + (1 - beta) g_R              (Eq. 5, in place)
  *   D   = PolarExpress_{lmo_steps}(M / (||M||_F + 1e-7))          (Eq. 6)
+ *         and D = 0 when ||M||_F <= 2^-20 ||G||_F (a momentum below the
+ *         fp32 resolution of the gradient has no direction)
  *   Y   = U - lr D
  *   U   = PolarExpress_{retract_steps}(Y / nu), nu^2 = max row sum of
  *         |Y^T Y| (an upper bound of sigma_max(Y)^2)                (Eq. 7)
@@ -187,13 +189,19 @@ int mapl_version(void);
 
 /* Tracing.  mapl_profile(1) makes every later call bracket each of its
  * kernel launches with a pair of HIP events on the call's stream (a small
- * per-launch overhead); mapl_profile(0) stops it.  mapl_profile_report()
+ * per-launch overhead); mapl_profile(0) stops it.  mapl_profile(2) also
+ * counts the decisions of the bf16 RVQ encoder (every such mapl_encode call
+ * then synchronises its stream to read them).  mapl_profile_report()
  * waits for the recorded events, writes one line "name launches total_ms"
  * per kernel, in the order of each name's first launch (names are
- * "<call>:<kernel>") into buf (NUL-terminated, at most
- * `bytes` bytes), and forgets the records.  Returns MAPL_OK, MAPL_E_HIP if an
- * event could not be resolved, or MAPL_E_WORKSPACE if buf was too small (the
- * text is truncated). */
+ * "<call>:<kernel>"), followed, after RVQ counting, by lines "name count 0"
+ * for rvq:tokens_rescored, rvq:candidates (summed over rescored tokens),
+ * rvq:list_overflows, rvq:second_pass_blocks and rvq:blocks ((workgroup,
+ * round) pairs with a second screening pass, and in total), into buf
+ * (NUL-terminated, at most `bytes` bytes), and forgets the records.  Not for
+ * use under stream capture.  Returns MAPL_OK, MAPL_E_HIP if an event could
+ * not be resolved, or MAPL_E_WORKSPACE if buf was too small (the text is
+ * truncated). */
 int mapl_profile(int enable);
 int mapl_profile_report(char* buf, size_t bytes);
 

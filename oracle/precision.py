@@ -1,6 +1,6 @@
 """Rounding helpers for the oracle (test infrastructure, see oracle/__init__).
 
-The paper trains in bf16 (Sec. 4.1 and App. B).  Where a floating-point value
+The paper trains in bf16 (Sec. 4.1 and App. E).  Where a floating-point value
 decides an integer (the RVQ argmin of Sec. 3.5) both sides must take that
 decision from operands of the same precision, so the oracle rounds the
 projector U (and the anchor factor B.U) to bf16 exactly where the bf16 codec

@@ -23,15 +23,24 @@ which PolarExpress approximates.  Two modes:
                 S = X^T X, with the greedy minimax schedule of
                 oracle.polar_schedule, carried out in float64:
                   LMO:        X0 = M / (||M||_F + 1e-7), schedule
-                              designed for [1e-3, 1]; the 1e-7 keeps a
-                              rounding-noise M (the float image of M = 0)
-                              from being blown up to unit scale;
+                              designed for [1e-3, 1]; D = 0 when
+                              ||M||_F <= 2^-20 ||G||_F (zero rule below);
                   retraction: X0 = Y / nu, nu = sqrt(max_i sum_j |(Y^T Y)_ij|)
                               (an upper bound of sigma_max(Y)), schedule
                               designed for [0.5, 1].
                 polar(cY) = polar(Y) for c > 0, so both normalisations leave
                 the limit unchanged; they fix where the finite schedule is
                 accurate.
+
+Zero rule of the LMO (a reading of Eq. 6, where the paper is silent on a
+vanishing momentum).  The linear minimisation over the spectral-norm ball
+has no unique answer at M = 0; D = 0 is taken there.  Gradients reach the
+step as fp32 values, so a tangent part below the fp32 resolution of G is
+indistinguishable from zero: G = U S with S symmetric, stored in fp32,
+keeps a tangent residue of about 3e-8 ||G||_F, and the scale-invariant polar
+factor would blow that residue up to a full unit-singular-value step.  The
+iteration-matched mode therefore maps M to D = 0 whenever
+||M||_F <= 2^-20 ||G||_F (about 16 fp32 units of G's norm).
 """
 import numpy as np
 
@@ -40,6 +49,7 @@ from . import polar_schedule
 LMO_LOWER = 1e-3
 RETRACT_LOWER = 0.5
 LMO_EPS = 1e-7
+LMO_ZERO_REL = 2.0 ** -20
 
 
 def sym(S):
@@ -75,10 +85,13 @@ def pe_iterate(X, coefs):
     return X
 
 
-def lmo_pe(M, steps):
-    """Eq. 6 with PolarExpress: D = PE_steps(M / (||M||_F + 1e-7))."""
+def lmo_pe(M, steps, zero_below=0.0):
+    """Eq. 6 with PolarExpress: D = PE_steps(M / (||M||_F + 1e-7)), and
+    D = 0 when ||M||_F <= zero_below (the zero rule above)."""
     coefs, _ = polar_schedule.greedy_schedule(LMO_LOWER, steps)
     M = np.asarray(M, dtype=np.float64)
+    if np.linalg.norm(M) <= zero_below:
+        return np.zeros_like(M)
     X0 = M / (np.linalg.norm(M) + LMO_EPS)
     return pe_iterate(X0, coefs)
 
@@ -103,7 +116,7 @@ def stiefel_step(U, G, M, lr, beta, mode="exact", lmo_steps=5, retract_steps=7):
         D = polar_exact(Mn, zero_tol=zt)
         Un = polar_exact(U - lr * D)
     elif mode == "pe":
-        D = lmo_pe(Mn, lmo_steps)
+        D = lmo_pe(Mn, lmo_steps, zero_below=LMO_ZERO_REL * np.linalg.norm(G))
         Un = retract_pe(U - lr * D, retract_steps)
     else:
         raise ValueError(mode)

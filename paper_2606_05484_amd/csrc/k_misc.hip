@@ -92,32 +92,53 @@ __global__ void k_symmetrize(float* S, int r) {
 }
 
 // grid (nblk, P): block-stride loop, one partial sum of M^2 per block.
-__global__ void k_momentum(float* __restrict__ M, const float* __restrict__ gR, int64_t n, float beta,
-                           float* __restrict__ partial) {
-  __shared__ float red[4];
+// M <- beta M + (1 - beta) gR; per-block partial sums of M^2 (partial[p][b])
+// and of G^2 (partial[P + p][b]: the gradient's norm for the zero rule).
+__global__ void k_momentum(float* __restrict__ M, const float* __restrict__ gR, const float* __restrict__ G,
+                           int64_t n, float beta, float* __restrict__ partial) {
+  __shared__ float red[2][4];
   const int p = blockIdx.y;
   float* Mp = M + (int64_t)p * n;
   const float* gp = gR + (int64_t)p * n;
-  float s = 0.f;
+  const float* Gp = G + (int64_t)p * n;
+  float s = 0.f, sg = 0.f;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     const float v = beta * Mp[i] + (1.f - beta) * gp[i];
     Mp[i] = v;
     s = fmaf(v, v, s);
+    const float gv = Gp[i];
+    sg = fmaf(gv, gv, sg);
   }
   s = wave_sum(s);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  sg = wave_sum(sg);
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = s;
+    red[1][threadIdx.x >> 6] = sg;
+  }
   __syncthreads();
-  if (threadIdx.x == 0) partial[(int64_t)p * gridDim.x + blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+  if (threadIdx.x == 0) {
+    const int64_t nb = gridDim.x, P = gridDim.y;
+    partial[(int64_t)p * nb + blockIdx.x] = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    partial[(P + p) * nb + blockIdx.x] = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+  }
 }
 
-__global__ void k_fro_scale(const float* __restrict__ partial, int nblk, float eps, float* scale,
-                            float* scale2) {
+// LMO normalisation of Eq. 6: scale = 1 / (||M||_F + eps), scale2 = scale^2;
+// both 0 (so the LMO returns D = 0) when ||M||_F <= zero_rel ||G||_F: a
+// momentum below the fp32 resolution of the gradient carries no direction.
+__global__ void k_fro_scale(const float* __restrict__ partial, int nblk, int P, float eps, float zero_rel,
+                            float* scale, float* scale2) {
   const int p = blockIdx.x, lane = threadIdx.x;
-  float s = 0.f;
-  for (int i = lane; i < nblk; i += 64) s += partial[(int64_t)p * nblk + i];
+  float s = 0.f, sg = 0.f;
+  for (int i = lane; i < nblk; i += 64) {
+    s += partial[(int64_t)p * nblk + i];
+    sg += partial[(int64_t)(P + p) * nblk + i];
+  }
   s = wave_sum(s);
+  sg = wave_sum(sg);
   if (lane == 0) {
-    const float sc = 1.f / (sqrtf(s) + eps);
+    const float nm = sqrtf(s);
+    const float sc = nm <= zero_rel * sqrtf(sg) ? 0.f : 1.f / (nm + eps);
     scale[p] = sc;
     scale2[p] = sc * sc;
   }
@@ -208,15 +229,15 @@ hipError_t launch_symmetrize(float* S, int P, int r, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_momentum(float* M, const float* gR, int64_t n, int P, float beta, float* partial, int nblk,
-                           hipStream_t s) {
-  hipLaunchKernelGGL(k_momentum, dim3(nblk, P), dim3(256), 0, s, M, gR, n, beta, partial);
+hipError_t launch_momentum(float* M, const float* gR, const float* G, int64_t n, int P, float beta, float* partial,
+                           int nblk, hipStream_t s) {
+  hipLaunchKernelGGL(k_momentum, dim3(nblk, P), dim3(256), 0, s, M, gR, G, n, beta, partial);
   return hipGetLastError();
 }
 
-hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float* scale, float* scale2,
-                            hipStream_t s) {
-  hipLaunchKernelGGL(k_fro_scale, dim3(P), dim3(64), 0, s, partial, nblk, eps, scale, scale2);
+hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float zero_rel, float* scale,
+                            float* scale2, hipStream_t s) {
+  hipLaunchKernelGGL(k_fro_scale, dim3(P), dim3(64), 0, s, partial, nblk, P, eps, zero_rel, scale, scale2);
   return hipGetLastError();
 }
 

@@ -318,6 +318,10 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       cand_cnt[tl] = 0;
     }
     const int any_amb = __syncthreads_or(amb ? 1 : 0);
+    if (a.stats && tid == 0) {
+      atomicAdd(&a.stats[4], 1);
+      if (any_amb) atomicAdd(&a.stats[3], 1);
+    }
 
     int jstar = j1;
     if (any_amb) {

@@ -151,7 +151,9 @@ struct RvqArgs {
   const float* meta;   // [L][ceil(K/64)][64]: ||C_j||^2 (rvq_meta_floats)
   int T, r, L, K;
   void* codes; int code_bytes;  // [T,L]
-  int* stats;          // [4] optional counters (candidates, overflow), may be null
+  int* stats;          // [8] optional counters, may be null: tokens rescored, their candidates,
+                       // candidate-list overflows, (workgroup, round) pairs with a second
+                       // screening pass, (workgroup, round) pairs in total
 };
 hipError_t launch_rvq(const RvqArgs& a, hipStream_t s);
 // The encoder in one launch: Z0 = [X | a] W as launch_gemm_tn computes it
@@ -176,11 +178,12 @@ hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t 
 // S <- (S + S^T)/2 for each of P [r,r] matrices, in place.
 hipError_t launch_symmetrize(float* S, int P, int r, hipStream_t s);
 // M <- beta M + (1-beta) gR (n elements per projector, P projectors);
-// partial sums of M^2 -> partial[P][nblk].
-hipError_t launch_momentum(float* M, const float* gR, int64_t n, int P, float beta, float* partial,
+// partial sums of M^2 -> partial[p][nblk], of G^2 -> partial[P + p][nblk].
+hipError_t launch_momentum(float* M, const float* gR, const float* G, int64_t n, int P, float beta, float* partial,
                            int nblk, hipStream_t s);
-// scale[p] = 1/(sqrt(sum partial[p]) + eps), scale2[p] = scale^2.
-hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float* scale,
+// scale[p] = 1/(||M_p|| + eps), scale2[p] = scale^2; both 0 when
+// ||M_p|| <= zero_rel ||G_p|| (norms from launch_momentum's partials).
+hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float zero_rel, float* scale,
                             float* scale2, hipStream_t s);
 // Y = U - lr D.
 hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64_t n, hipStream_t s);

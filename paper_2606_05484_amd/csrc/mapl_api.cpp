@@ -71,6 +71,10 @@ struct ProfRec {
 };
 std::mutex g_prof_mu;
 bool g_prof = false;
+bool g_prof_rvq = false;      // mapl_profile(2): also collect the RVQ decision counters
+long long g_rvq_stats[5] = {0, 0, 0, 0, 0};
+const char* const kRvqStatNames[5] = {"rvq:tokens_rescored", "rvq:candidates", "rvq:list_overflows",
+                                      "rvq:second_pass_blocks", "rvq:blocks"};
 std::vector<ProfRec> g_prof_recs;
 std::vector<hipEvent_t> g_prof_pool;
 
@@ -168,7 +172,7 @@ Layout layout(const mapl_codec_desc& D, int call) {
           if (!enc_rvq_fusable((int)r, D.L)) Lo.z0 = c.take((size_t)T * r * 4);
           Lo.cb = c.take((size_t)D.L * D.K * rvq_cb_cols((int)r) * 2);
           Lo.cn2 = c.take((size_t)rvq_meta_floats(D.L, D.K) * 4);
-          Lo.stats = c.take(16);
+          Lo.stats = c.take(32);
         }
         break;
       case MAPL_CALL_DECODE:
@@ -333,7 +337,7 @@ extern "C" size_t mapl_workspace_bytes(const mapl_codec_desc* desc, int call, in
     c.take((size_t)P * r * r * 4);   // Q
     c.take((size_t)P * d * r * 4);   // X0
     c.take((size_t)P * d * r * 4);   // X1
-    c.take((size_t)P * 1024 * 4);    // partial sums
+    c.take((size_t)P * 2048 * 4);    // partial sums of M^2 and G^2
     c.take((size_t)P * 8 * 4);       // scalars
     return c.off;
   }
@@ -405,16 +409,28 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
     a.T = (int)T; a.r = (int)r; a.L = D.L; a.K = D.K;
     a.codes = payload; a.code_bytes = cbytes;
     a.stats = nullptr;
+    if (g_prof_rvq) {
+      a.stats = at<int>(ws, Lo.stats);
+      MAPL_HIP(launch_zero_bytes(a.stats, 32, s));
+    }
     if (enc_rvq_fusable((int)r, D.L)) {
       // projection and RVQ in one launch: Z0 stays on chip
       LAUNCH("enc:gemm_rvq", launch_enc_rvq(g, a, s));
-      return MAPL_OK;
+    } else {
+      float* Z0 = at<float>(ws, Lo.z0);
+      g.out = Z0; g.ldo = r; g.out_f32 = 1;
+      LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
+      a.Z0 = Z0;
+      LAUNCH("enc:rvq", launch_rvq(a, s));
     }
-    float* Z0 = at<float>(ws, Lo.z0);
-    g.out = Z0; g.ldo = r; g.out_f32 = 1;
-    LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
-    a.Z0 = Z0;
-    LAUNCH("enc:rvq", launch_rvq(a, s));
+    if (a.stats) {
+      // diagnostics mode only: read the counters back (synchronises the stream)
+      int h[8];
+      MAPL_HIP(hipMemcpyAsync(h, a.stats, sizeof h, hipMemcpyDeviceToHost, s));
+      MAPL_HIP(hipStreamSynchronize(s));
+      std::lock_guard<std::mutex> lk(g_prof_mu);
+      for (int i = 0; i < 5; ++i) g_rvq_stats[i] += h[i];
+    }
     return MAPL_OK;
   }
 
@@ -799,7 +815,7 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   float* Qm = at<float>(ws, c.take((size_t)P * r * r * 4));
   float* X0 = at<float>(ws, c.take((size_t)P * d * r * 4));
   float* X1 = at<float>(ws, c.take((size_t)P * d * r * 4));
-  float* partial = at<float>(ws, c.take((size_t)P * 1024 * 4));
+  float* partial = at<float>(ws, c.take((size_t)P * 2048 * 4));
   float* sc = at<float>(ws, c.take((size_t)P * 8 * 4));
   float* scale = sc, *scale2 = sc + P, *inv_nu = sc + 2 * P, *inv_nu2 = sc + 3 * P, *inv_nu4 = sc + 4 * P;
   const int64_t n = d * r, rr = r * r;
@@ -854,11 +870,12 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.alpha = -1.f;
     LAUNCH("stiefel:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
   }
-  // Eq. 5 and the LMO normalisation 1 / (||M||_F + 1e-7)
+  // Eq. 5 and the LMO normalisation 1 / (||M||_F + 1e-7); the LMO is 0 for
+  // a momentum at or below 2^-20 ||G||_F (under fp32 resolution of G)
   int nblk = (int)((n + 255) / 256);
   if (nblk > 1024) nblk = 1024;
-  LAUNCH("stiefel:momentum", launch_momentum(M, X0, n, (int)P, beta, partial, nblk, s));
-  LAUNCH("stiefel:fro_scale", launch_fro_scale(partial, nblk, (int)P, 1e-7f, scale, scale2, s));
+  LAUNCH("stiefel:momentum", launch_momentum(M, X0, G, n, (int)P, beta, partial, nblk, s));
+  LAUNCH("stiefel:fro_scale", launch_fro_scale(partial, nblk, (int)P, 1e-7f, 1.0f / 1048576.0f, scale, scale2, s));
 
   // Eq. 6: D = PE(M / (||M|| + eps))
   const float* Xin = M;
@@ -899,14 +916,20 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
 extern "C" int mapl_profile(int enable) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   g_prof = enable != 0;
+  g_prof_rvq = enable >= 2;
   return MAPL_OK;
 }
 
 extern "C" int mapl_profile_report(char* buf, size_t bytes) {
   std::vector<ProfRec> recs;
+  long long rvq[5];
   {
     std::lock_guard<std::mutex> lk(g_prof_mu);
     recs.swap(g_prof_recs);
+    for (int i = 0; i < 5; ++i) {
+      rvq[i] = g_rvq_stats[i];
+      g_rvq_stats[i] = 0;
+    }
   }
   // one line per kernel name, in the order of first launch
   std::vector<std::string> order;
@@ -940,6 +963,11 @@ extern "C" int mapl_profile_report(char* buf, size_t bytes) {
     snprintf(line, sizeof line, "%s %ld %.6f\n", name.c_str(), v.first, v.second);
     outs += line;
   }
+  if (rvq[4] > 0)
+    for (int i = 0; i < 5; ++i) {
+      snprintf(line, sizeof line, "%s %lld 0\n", kRvqStatNames[i], rvq[i]);
+      outs += line;
+    }
   if (buf && bytes) {
     const size_t n = outs.size() < bytes - 1 ? outs.size() : bytes - 1;
     memcpy(buf, outs.data(), n);

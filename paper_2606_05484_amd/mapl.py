@@ -158,8 +158,9 @@ def stiefel_step(P, d, r, U, G, M, lr, beta, lmo_steps, retract_steps, ws, ws_by
 
 
 def profile(enable):
-    """Turn per-kernel event tracing on or off (see mapl_profile_report)."""
-    _check(lib().mapl_profile(1 if enable else 0))
+    """Per-kernel event tracing: 0 off, 1 (True) on, 2 also RVQ decision
+    counters (see mapl_profile_report)."""
+    _check(lib().mapl_profile(int(enable)))
 
 
 def profile_report():

@@ -4,7 +4,7 @@ This module only draws random inputs; it holds none of the codec's or the
 Stiefel step's arithmetic, and it is the one piece shared by the tests, the
 benchmark and the oracle checks.  It depends on NumPy alone.
 
-Workloads (boundary activations of the paper's LLaMA stages, App. B: d = 1024
+Workloads (boundary activations of the paper's LLaMA stages, App. E: d = 1024
 for 150M, d = 2048 for 1B, vocabulary 32000, micro-batches of 4 x 2048 tokens):
 
   c1        T=512,   d=256,  r=32,  V=1024,  k=16,  L=2, K=64,   fp32
@@ -22,7 +22,11 @@ Recipe (PCG64 ``numpy.random.default_rng(seed)``, draws in this order):
      channels of X multiplied by 20.  Stored as fp32 (c1) or bf16 (RNE of
      the fp32 value).
   4. U = QR(N(0,1)[d,r]), sign-fixed, stored fp32
-  5. A = 0.02 N(0,1)[V,k];  B = 0.02 N(0,1)[k,d] (ambient) or [k,r] (coord)
+  5. A = 0.02 N(0,1)[V,k];  B = 0.02 N(0,1)[k,d] (ambient) or [k,r] (coord).
+     anchor="orthonormal" instead draws A = a_scale N(0,1)[V,k] and B with
+     orthonormal rows, B = Q^T for Q = QR(N(0,1)[cols,k]) sign-fixed (the
+     frozen "random orthonormal" companion of Eq. 3 and the hyperparameter
+     table): an anchor term as large as the activations themselves
   6. ids: finite Zipf(1.1), P(id = i) proportional to (i+1)^-1.1 on [0, V)
   7. codebooks C [L,K,r] fp32, C_l[0] = 0, other rows sigma_l N(0,1); sigma_l
      is 0.02 for c1 and the root-mean-square of the stored X for c3/c4 (the
@@ -91,7 +95,8 @@ def as_f64(arr, dtype):
     return np.asarray(arr, dtype=np.float64)
 
 
-def codec_inputs(name=None, seed=None, anchor_space="ambient", chunk=4096, **over):
+def codec_inputs(name=None, seed=None, anchor_space="ambient", chunk=4096, anchor="gauss", a_scale=1.0,
+                 **over):
     """Draw one codec workload.  Returns a dict of NumPy arrays plus sizes.
 
     Arrays with dtype "bf16" are uint16 bit patterns; "f32" arrays are float32.
@@ -124,9 +129,15 @@ def codec_inputs(name=None, seed=None, anchor_space="ambient", chunk=4096, **ove
         X[t0:t0 + n] = _store(Xc32, dt)
         sq += float(np.square(as_f64(X[t0:t0 + n], dt)).sum())
     U = _sign_fixed_qr(rng, d, r).astype(np.float32)
-    A32 = (0.02 * rng.standard_normal((V, k))).astype(np.float32)
     bdim = d if anchor_space == "ambient" else r
-    B32 = (0.02 * rng.standard_normal((k, bdim))).astype(np.float32)
+    if anchor == "gauss":
+        A32 = (0.02 * rng.standard_normal((V, k))).astype(np.float32)
+        B32 = (0.02 * rng.standard_normal((k, bdim))).astype(np.float32)
+    elif anchor == "orthonormal":
+        A32 = (a_scale * rng.standard_normal((V, k))).astype(np.float32)
+        B32 = (_sign_fixed_qr(rng, bdim, k).T if k else np.zeros((0, bdim))).astype(np.float32)
+    else:
+        raise ValueError(anchor)
     ids = zipf_ids(rng, V, T)
     C = np.zeros((L, max(K, 0), r), dtype=np.float32)
     sigma = cfg.get("cb_sigma")
@@ -141,7 +152,7 @@ def codec_inputs(name=None, seed=None, anchor_space="ambient", chunk=4096, **ove
     return dict(name=name, seed=seed, T=T, d=d, r=r, V=V, k=k, L=L, K=K, dtype=dt,
                 anchor_space=anchor_space, X=X, U=U, A=_store(A32, dt), B=_store(B32, dt),
                 ids=ids, C=C, dXhat=dXhat, dZ=dZ, G=G, cb_sigma=float(sigma),
-                code_dtype=("u8" if K <= 256 else "u16"), lr=float(cfg.get("lr", 1e-2)))
+                code_dtype=("u8" if K <= 256 else "u16"), lr=float(cfg.get("lr", 1e-2)), anchor=anchor)
 
 
 def stiefel_inputs(name=None, seed=None, **over):

@@ -132,3 +132,145 @@ def stress_codebooks(x, seed):
         codes, _, _ = ocodec.rvq_encode(R, C[l:l + 1].astype(np.float64))
         R = R - C[l].astype(np.float64)[codes[:, 0]]
     return C
+
+
+def chain(x, C=None, L=None, K=None, rx=None):
+    """encode -> decode -> decode_bwd -> encode_bwd on the GPU; returns host
+    results.  The sender's anchor tables (A, B of x) serve encode and
+    encode_bwd; the receiver's (those of rx, default x) serve decode and
+    decode_bwd, as in Eq. 2 where the next stage adds its own anchor."""
+    t = torch()
+    D = descr(x, L, K)
+    g = Dev(x, C)
+    rx = x if rx is None else rx
+    Ar, Br = dev(rx["A"], x["dtype"]), dev(rx["B"], x["dtype"])
+    payload = run_encode(x, D, g)
+    Xh = t.full((x["T"], x["d"]), float("nan"), dtype=g.tdt, device="cuda")
+    ws = mapl.workspace(max(mapl.workspace_bytes(D, c) for c in range(4)))
+    mapl.decode(D, payload, g.ids, g.U, Ar, Br, g.C, Xh, ws)
+    dZ = t.full((x["T"], x["r"]), float("nan"), dtype=g.tdt, device="cuda")
+    dU = t.full((x["d"], x["r"]), float("nan"), dtype=t.float32, device="cuda")
+    mapl.decode_bwd(D, g.dXhat, payload, g.ids, g.U, Ar, Br, g.C, dZ, dU, 0, ws)
+    dU_dec = dU.clone()
+    dX = t.full((x["T"], x["d"]), float("nan"), dtype=g.tdt, device="cuda")
+    mapl.encode_bwd(D, g.dZ, g.X, g.ids, g.U, g.A, g.B, dX, dU, 1, ws)
+    t.cuda.synchronize()
+    return dict(D=D, payload=payload, Xh=host_f64(Xh), dZ=host_f64(dZ), dU_dec=host_f64(dU_dec),
+                dU=host_f64(dU), dX=host_f64(dX))
+
+
+def chain_refs(x, payload, C=None, rx=None, ids=None):
+    """Oracle results of the four calls for the given payload (the one the
+    GPU produced: decode is judged on what it was handed).  ids overrides
+    the token ids of every anchor gather (used to show that a wrong-row
+    gather would be caught)."""
+    Cn = x["C"] if C is None else C
+    Cref = Cn if (Cn is not None and Cn.size and payload.dtype.kind in "iu") else None
+    rx = x if rx is None else rx
+    op, sp = operand(x), x["anchor_space"]
+    X, As, Bs = f64(x, "X"), f64(x, "A"), f64(x, "B")
+    Ar, Br = f64(rx, "A"), f64(rx, "B")
+    ids = x["ids"] if ids is None else ids
+    out = dict(Z0=ocodec.project(X, ids, x["U"], As, Bs, sp, op))
+    out["Xh"] = ocodec.decode(payload, ids, x["U"], Ar, Br, Cref, sp, op)
+    out["dZ"], out["dU_dec"] = ocodec.decode_bwd(f64(x, "dXhat"), payload, ids, x["U"], Ar, Br, Cref, sp, op)
+    out["dX"], out["dU_enc"] = ocodec.encode_bwd(f64(x, "dZ"), X, ids, x["U"], As, Bs, sp, op)
+    out["dU"] = out["dU_dec"] + out["dU_enc"]
+    return out
+
+
+def anchor_discrimination(x, payload, C=None, rx=None, seed=0):
+    """How far the oracle's outputs move when every anchor row is gathered
+    for the wrong token (ids permuted), and when the sender's table is used
+    on the receiving side: {quantity: relative Frobenius change}.  A parity
+    test of the anchor path can only fail for such a bug when the change is
+    well above its tolerance."""
+    rng = np.random.default_rng(seed)
+    ids = x["ids"]
+    perm = ids[rng.permutation(len(ids))]
+    true = chain_refs(x, payload, C, rx)
+    wrong = chain_refs(x, payload, C, rx, ids=perm)
+    # coord: dU_enc = X^T dZ has no anchor term; dU_dec does
+    keys = ["Xh", "dU"] + (["Z0"] if x["L"] == 0 else [])
+    keys.append("dU_dec" if x["anchor_space"] == "coord" else "dU_enc")
+    out = {"perm_" + k: rel_fro(wrong[k], true[k]) for k in keys}
+    if rx is not None:
+        swap = chain_refs(x, payload, C, rx=x)
+        out["swap_Xh"] = rel_fro(swap["Xh"], true["Xh"])
+    return out
+
+
+def check_chain(x, res, C=None, rx=None):
+    """Every output of chain() against the oracle, fed the same inputs the
+    GPU call saw: codes bit-exact except near-tie tokens, the rest within
+    the relative Frobenius tolerance of the path."""
+    Cn = x["C"] if C is None else C
+    D = res["D"]
+    if D.L == 0:
+        Zg = host_f64(res["payload"])
+        assert np.isfinite(Zg).all()
+        pay = Zg  # decode is checked on the payload the GPU produced
+    else:
+        cg = codes_np(res["payload"], D)
+        pay = cg
+    ref = chain_refs(x, pay, Cn, rx)
+    if D.L == 0:
+        e = rel_fro(Zg, ref["Z0"])
+        print("Z rel err", e)
+        assert e <= tol(x)
+    else:
+        codes_ref, gap, _ = ocodec.rvq_encode(ref["Z0"], Cn)
+        bad, ex = compare_codes(cg, codes_ref, gap)
+        print("codes: mismatched non-exempt", bad, "exempt", ex, "of", x["T"])
+        assert bad == 0
+    e = rel_fro(res["Xh"], ref["Xh"])
+    print("Xhat rel err", e)
+    assert np.isfinite(res["Xh"]).all() and e <= tol(x)
+    e1, e2 = rel_fro(res["dZ"], ref["dZ"]), rel_fro(res["dU_dec"], ref["dU_dec"])
+    print("dZ rel err", e1, "dU_dec rel err", e2)
+    assert e1 <= tol(x) and e2 <= tol(x)
+    e3, e4 = rel_fro(res["dX"], ref["dX"]), rel_fro(res["dU"], ref["dU"])
+    print("dX rel err", e3, "dU (enc+dec) rel err", e4)
+    assert e3 <= tol(x) and e4 <= tol(x)
+    return ref
+
+
+# Anchor-dominant workloads: B with orthonormal rows (the frozen random
+# orthonormal companion of Eq. 3), A ~ N(0,1), so the anchor term is as large
+# as the activations; the receiver's tables (seed + 1) differ from the
+# sender's.  Each is (generator keywords, codebook kind).
+ANCHOR_CASES = {
+    "small_amb": (dict(seed=70, T=1000, d=256, r=64, V=500, k=16, L=0, K=0), None),
+    "small_coord": (dict(seed=71, T=1000, d=256, r=64, V=500, k=16, L=0, K=0, anchor_space="coord"), None),
+    "small_amb_rvq": (dict(seed=72, T=1000, d=256, r=128, V=500, k=32, L=2, K=96), "stress"),
+    "small_coord_rvq": (dict(seed=73, T=777, d=256, r=64, V=300, k=16, L=2, K=64, anchor_space="coord"),
+                        "stress"),
+    "fused_r256_amb": (dict(seed=74, T=1037, d=512, r=256, V=700, k=64, L=2, K=128), "stress"),
+    "fused_r256_coord": (dict(seed=75, T=1037, d=512, r=256, V=700, k=48, L=2, K=128, anchor_space="coord"),
+                         "stress"),
+    "c4width_amb": (dict(seed=76, T=4096 + 37, d=2048, r=256, V=32000, k=128, L=0, K=0), None),
+    "c4width_coord": (dict(seed=77, T=4096 + 37, d=2048, r=256, V=32000, k=128, L=0, K=0,
+                           anchor_space="coord"), None),
+}
+_ANCHOR_BASE = dict(dtype="bf16", alpha=0.8, n_out=4, cb_sigma=None, gscale=1.0)
+
+
+def anchor_case(name):
+    """(sender workload, receiver workload, codebooks or None) of a case."""
+    kw, cb = ANCHOR_CASES[name]
+    kw = dict(kw)
+    seed = kw.pop("seed")
+    x = synth.codec_inputs(None, seed=seed, anchor="orthonormal", **dict(_ANCHOR_BASE, **kw))
+    rx = synth.codec_inputs(None, seed=seed + 1000, anchor="orthonormal", **dict(_ANCHOR_BASE, **kw))
+    C = stress_codebooks(x, seed + 2000) if cb == "stress" else None
+    return x, rx, C
+
+
+def oracle_payload(x, C=None):
+    """The payload the oracle itself would send: bf16-rounded Z0, or codes."""
+    Cn = x["C"] if C is None else C
+    Z0 = ocodec.project(f64(x, "X"), x["ids"], x["U"], f64(x, "A"), f64(x, "B"), x["anchor_space"], operand(x))
+    if x["L"] == 0:
+        from oracle.precision import round_bf16
+        return round_bf16(Z0)
+    return ocodec.rvq_encode(Z0, Cn)[0]

@@ -9,8 +9,9 @@ import pytest
 
 from oracle import codec as ocodec
 from paper_2606_05484_amd import mapl, synth
-from _helpers import (BF16_TOL, F32_TOL, Dev, codes_np, compare_codes, descr, f64, host_f64, operand,
-                      oracle_encode, rel_fro, run_encode, stress_codebooks, tol, torch)
+from _helpers import (BF16_TOL, F32_TOL, Dev, chain as _chain, check_chain as _check_chain, codes_np,
+                      compare_codes, descr, f64, host_f64, operand, oracle_encode, rel_fro, run_encode,
+                      stress_codebooks, tol, torch)
 
 pytestmark = pytest.mark.gpu
 
@@ -21,64 +22,6 @@ SMALL = dict(T=1000, d=256, r=64, V=500, k=16, L=0, K=0, dtype="bf16", alpha=0.8
 def _x(name=None, seed=None, **over):
     print("workload", name, seed, over, flush=True)
     return synth.codec_inputs(name, seed=seed, **over)
-
-
-def _chain(x, C=None, L=None, K=None):
-    """encode -> decode -> decode_bwd -> encode_bwd on the GPU; returns host results."""
-    t = torch()
-    D = descr(x, L, K)
-    g = Dev(x, C)
-    payload = run_encode(x, D, g)
-    Xh = t.full((x["T"], x["d"]), float("nan"), dtype=g.tdt, device="cuda")
-    ws = mapl.workspace(max(mapl.workspace_bytes(D, c) for c in range(4)))
-    mapl.decode(D, payload, g.ids, g.U, g.A, g.B, g.C, Xh, ws)
-    dZ = t.full((x["T"], x["r"]), float("nan"), dtype=g.tdt, device="cuda")
-    dU = t.full((x["d"], x["r"]), float("nan"), dtype=t.float32, device="cuda")
-    mapl.decode_bwd(D, g.dXhat, payload, g.ids, g.U, g.A, g.B, g.C, dZ, dU, 0, ws)
-    dU_dec = dU.clone()
-    dX = t.full((x["T"], x["d"]), float("nan"), dtype=g.tdt, device="cuda")
-    mapl.encode_bwd(D, g.dZ, g.X, g.ids, g.U, g.A, g.B, dX, dU, 1, ws)
-    t.cuda.synchronize()
-    return dict(D=D, payload=payload, Xh=host_f64(Xh), dZ=host_f64(dZ), dU_dec=host_f64(dU_dec),
-                dU=host_f64(dU), dX=host_f64(dX))
-
-
-def _check_chain(x, res, C=None):
-    """Oracle for each call, fed the same inputs the GPU call saw."""
-    Cn = x["C"] if C is None else C
-    op, sp = operand(x), x["anchor_space"]
-    X, A, B = f64(x, "X"), f64(x, "A"), f64(x, "B")
-    D = res["D"]
-    if D.L == 0:
-        Z0 = ocodec.project(X, x["ids"], x["U"], A, B, sp, op)
-        Zg = host_f64(res["payload"])
-        assert np.isfinite(Zg).all()
-        e = rel_fro(Zg, Z0)
-        print("Z rel err", e)
-        assert e <= tol(x)
-        pay_ref = Zg  # decode is checked on the payload the GPU produced
-        Cref = None
-    else:
-        codes_ref, gap, _ = ocodec.rvq_encode(ocodec.project(X, x["ids"], x["U"], A, B, sp, op), Cn)
-        cg = codes_np(res["payload"], D)
-        bad, ex = compare_codes(cg, codes_ref, gap)
-        print("codes: mismatched non-exempt", bad, "exempt", ex, "of", x["T"])
-        assert bad == 0
-        pay_ref = cg
-        Cref = Cn
-    Xh_ref = ocodec.decode(pay_ref, x["ids"], x["U"], A, B, Cref, sp, op)
-    e = rel_fro(res["Xh"], Xh_ref)
-    print("Xhat rel err", e)
-    assert np.isfinite(res["Xh"]).all() and e <= tol(x)
-    dXh = f64(x, "dXhat")
-    dZ_ref, dUd_ref = ocodec.decode_bwd(dXh, pay_ref, x["ids"], x["U"], A, B, Cref, sp, op)
-    e1, e2 = rel_fro(res["dZ"], dZ_ref), rel_fro(res["dU_dec"], dUd_ref)
-    print("dZ rel err", e1, "dU_dec rel err", e2)
-    assert e1 <= tol(x) and e2 <= tol(x)
-    dX_ref, dUe_ref = ocodec.encode_bwd(f64(x, "dZ"), X, x["ids"], x["U"], A, B, sp, op)
-    e3, e4 = rel_fro(res["dX"], dX_ref), rel_fro(res["dU"], dUd_ref + dUe_ref)
-    print("dX rel err", e3, "dU (enc+dec) rel err", e4)
-    assert e3 <= tol(x) and e4 <= tol(x)
 
 
 @pytest.mark.parametrize("r", [64, 128, 256, 512])
@@ -146,24 +89,6 @@ def test_fp32_coord_anchor():
 def test_no_anchor_k0():
     x = _x(None, seed=8, **dict(SMALL, k=0, T=333))
     _check_chain(x, _chain(x))
-
-
-def test_distinct_sender_receiver_anchors():
-    """Eq. 2 adds the *receiving* stage's anchor: decode with A_r, B_r that
-    differ from the sender's."""
-    t = torch()
-    x = _x(None, seed=9, **SMALL)
-    x2 = _x(None, seed=10, **SMALL)
-    D = descr(x)
-    g = Dev(x)
-    Ar, Br = Dev(x2).A, Dev(x2).B
-    Z = run_encode(x, D, g)
-    Xh = t.empty((x["T"], x["d"]), dtype=g.tdt, device="cuda")
-    ws = mapl.workspace(mapl.workspace_bytes(D, mapl.CALL_DECODE))
-    mapl.decode(D, Z, g.ids, g.U, Ar, Br, None, Xh, ws)
-    t.cuda.synchronize()
-    ref = ocodec.decode(host_f64(Z), x["ids"], x["U"], f64(x2, "A"), f64(x2, "B"), None, "ambient", "bf16")
-    assert rel_fro(host_f64(Xh), ref) <= BF16_TOL
 
 
 def test_empty_batch():
@@ -311,6 +236,74 @@ def test_c4_full_size_sampled():
     e = rel_fro(res["dU"], dUd + dUe)
     print("c4 dU rel err", e)
     assert e <= BF16_TOL
+
+
+@pytest.mark.slow
+def test_c4_full_size_stress_codebooks():
+    """The benchmark workload with codebooks drawn from the oracle's own
+    residuals (codeword 0 = 0, the others residual rows plus 5 % noise):
+    every code is in use, so the fused encoder decides near-ambiguous tokens
+    by exact fp32 rescoring in every workgroup, with the 16-chunk codebook
+    ring and u16 codes.  Codes on every token against the oracle (exempt
+    tokens counted), Xhat / dZ / dX on 512 sampled tokens, dU (with a
+    non-zero Zhat, so both halves) in full."""
+    x = _x("c4")
+    C = stress_codebooks(x, 104)
+    res = _chain(x, C=C)
+    D = res["D"]
+    X, A, B = f64(x, "X"), f64(x, "A"), f64(x, "B")
+    Z0 = ocodec.project(X, x["ids"], x["U"], A, B, "ambient", "bf16")
+    codes_ref, gap, _ = ocodec.rvq_encode(Z0, C)
+    cg = codes_np(res["payload"], D)
+    bad, ex = compare_codes(cg, codes_ref, gap)
+    used = [len(np.unique(cg[:, l])) for l in range(D.L)]
+    print("c4 stress codes: mismatched", bad, "exempt", ex, "of", x["T"], "distinct codes per round", used)
+    assert bad == 0
+    assert min(used) > 0.8 * x["K"]
+    rows = np.random.default_rng(6).choice(x["T"], 512, replace=False)
+    Xh_ref = ocodec.decode(cg[rows], x["ids"][rows], x["U"], A, B, C, "ambient", "bf16")
+    e = rel_fro(res["Xh"][rows], Xh_ref)
+    print("Xhat rel err", e)
+    assert e <= BF16_TOL
+    P = ocodec._projector(x["U"], "bf16")
+    assert rel_fro(res["dZ"][rows], f64(x, "dXhat")[rows] @ P) <= BF16_TOL
+    assert rel_fro(res["dX"][rows], f64(x, "dZ")[rows] @ P.T) <= BF16_TOL
+    _, dUd = ocodec.decode_bwd(f64(x, "dXhat"), cg, x["ids"], x["U"], A, B, C, "ambient", "bf16")
+    _, dUe = ocodec.encode_bwd(f64(x, "dZ"), X, x["ids"], x["U"], A, B, "ambient", "bf16")
+    e1, e2 = rel_fro(res["dU_dec"], dUd), rel_fro(res["dU"], dUd + dUe)
+    print("c4 stress dU_dec rel err", e1, "dU rel err", e2, "|dU_dec|/|dU_enc|",
+          np.linalg.norm(dUd) / np.linalg.norm(dUe))
+    assert e1 <= BF16_TOL and e2 <= BF16_TOL
+
+
+@pytest.mark.parametrize("d,r", [(512, 128), (512, 256)])
+def test_rvq_candidate_overflow_full_rescan(d, r):
+    """More codewords within the screening margin of one token than its
+    candidate list holds (16): that token is decided by a full fp32 rescan
+    of the codebook.  20 codewords are planted around token 5's Z0 at
+    squared distances (1e-3 + 5e-4 j) ||Z0||^2, j = 0..19 (all within the
+    margin, yet 5e-4 ||Z0||^2 apart: no near-tie); the nearest sits at the
+    highest of their indices, so a truncated list would miss it."""
+    x = _x(None, seed=16, **dict(SMALL, T=300, d=d, r=r, k=16, L=2, K=64))
+    Z0 = ocodec.project(f64(x, "X"), x["ids"], x["U"], f64(x, "A"), f64(x, "B"), "ambient", "bf16")
+    rng = np.random.default_rng(2)
+    C = np.zeros((2, 64, r), dtype=np.float32)
+    C[:, 1:] = (5 + rng.standard_normal((2, 63, r))).astype(np.float32)
+    z = Z0[5]
+    n2 = float(z @ z)
+    for j in range(20):
+        u = rng.standard_normal(r)
+        u /= np.linalg.norm(u)
+        C[0, 59 - j] = (z + np.sqrt((1e-3 + 5e-4 * j) * n2) * u).astype(np.float32)
+    codes_ref, gap, _ = ocodec.rvq_encode(Z0, C)
+    assert codes_ref[5, 0] == 59 and gap[5, 0] > 2e-4
+    D = descr(x)
+    g = Dev(x, C)
+    cg = codes_np(run_encode(x, D, g), D)
+    bad, ex = compare_codes(cg, codes_ref, gap)
+    print("overflow: token 5 codes", cg[5], "mismatched", bad, "exempt", ex)
+    assert cg[5, 0] == 59
+    assert bad == 0
 
 
 @pytest.mark.parametrize("r", [64, 128, 256])

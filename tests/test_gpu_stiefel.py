@@ -2,8 +2,11 @@
 
 Tolerances: U_new and M_new within 1e-5 relative Frobenius error of the
 iteration-matched oracle (same PolarExpress schedule and normalisations,
-float64); max |U^T U - I| <= 1e-5 after every step.  The gap to the exact
-(SVD) polar factor is printed, not gated."""
+float64); the step itself, dU = U_new - U, within 2e-4 (the fp32 error of
+U_new, about 2e-6 of ||U||_F at most, divided by lr ||D||_F / ||U||_F = lr:
+this pins the LMO direction of Eq. 6 to 2e-4); max |U^T U - I| <= 1e-5
+after every step.  The gap to the exact (SVD) polar factor is printed, not
+gated."""
 import numpy as np
 import pytest
 
@@ -12,6 +15,8 @@ from paper_2606_05484_amd import mapl, synth
 from _helpers import dev, rel_fro, torch
 
 pytestmark = pytest.mark.gpu
+
+DU_TOL = 2e-4  # relative Frobenius error of dU = U_new - U (see above)
 
 
 def _gpu_step(U, G, M, lr, beta, lmo=5, ret=7):
@@ -39,7 +44,7 @@ def test_c1_single_step():
     du = rel_fro(Un - U, Ur - U)
     print("c1: U rel err", e_u, "M rel err", e_m, "dU rel err", du, "orth", _orth_err(Un),
           "gap to exact polar", rel_fro(Ur, Ue))
-    assert e_u <= 1e-5 and e_m <= 1e-5
+    assert e_u <= 1e-5 and e_m <= 1e-5 and du <= DU_TOL
     assert _orth_err(Un) <= 1e-5
 
 
@@ -52,29 +57,25 @@ def test_c5_step_sampled_projectors():
     for p in (0, 7, 15):
         ur, mr, _, _ = spel.stiefel_step(U[p], G[p], M[p], st["lr"], st["beta"], mode="pe")
         e_u, e_m = rel_fro(Un[p], ur), rel_fro(Mn[p], mr)
-        print("c5 proj", p, "U rel err", e_u, "M rel err", e_m, "dU rel err", rel_fro(Un[p] - U[p], ur - U[p]))
-        assert e_u <= 1e-5 and e_m <= 1e-5
+        du = rel_fro(Un[p] - U[p], ur - U[p])
+        print("c5 proj", p, "U rel err", e_u, "M rel err", e_m, "dU rel err", du)
+        assert e_u <= 1e-5 and e_m <= 1e-5 and du <= DU_TOL
 
 
 def test_c5_trajectory_stays_orthonormal():
     """100 consecutive steps with fresh gradients: orthonormality after
-    every step; the drift of the final iterate against the oracle's own
-    100-step trajectory (projector 0) is printed."""
+    every step (the per-step parity is gated by the tests above)."""
     t = torch()
     st = synth.stiefel_inputs("c5")
     P, d, r = st["P"], st["d"], st["r"]
     Ug, Mg = dev(st["U"], "f32"), dev(st["M"], "f32")
     ws = mapl.workspace(mapl.workspace_bytes(None, mapl.CALL_STIEFEL, P, d, r))
-    U0 = st["U"][0].astype(np.float64)
-    M0 = np.zeros((d, r))
     worst = 0.0
     for step in range(st["steps"]):
         G = synth.next_gradient(st) if step else st["G"]
         mapl.stiefel_step(P, d, r, Ug, dev(G, "f32"), Mg, st["lr"], st["beta"], 5, 7, ws)
         Uh = Ug[0].double()
         worst = max(worst, float((Uh.T @ Uh - t.eye(r, dtype=t.float64, device="cuda")).abs().max()))
-        if step < 3:
-            U0, M0, _, _ = spel.stiefel_step(U0, G[0], M0, st["lr"], st["beta"], mode="pe")
     t.cuda.synchronize()
     print("max orthonormality error over 100 steps", worst)
     assert worst <= 1e-5
@@ -83,17 +84,23 @@ def test_c5_trajectory_stays_orthonormal():
 
 
 def test_symmetric_gradient_moves_little():
-    """G = U S (S symmetric) is normal to the manifold: the tangent part is
-    rounding noise, so U may move only by about lr times that noise."""
+    """G = U S (S symmetric, stored in fp32) is normal to the manifold: its
+    tangent part is a few 1e-8 of ||G||, below fp32 resolution, so the LMO
+    returns D = 0 (||M|| <= 2^-20 ||G||) and U moves only by the
+    retraction's rounding: |U_new - U| <= 1e-5, as the oracle."""
     rng = np.random.default_rng(3)
     P, d, r = 2, 256, 64
     U = np.stack([np.linalg.qr(rng.standard_normal((d, r)))[0] for _ in range(P)]).astype(np.float32)
     S = rng.standard_normal((P, r, r))
     S = S + S.transpose(0, 2, 1)
     G = np.einsum("pdr,prs->pds", U.astype(np.float64), S).astype(np.float32)
-    Un, _ = _gpu_step(U, G, np.zeros_like(U), 1e-2, 0.95)
+    Un, Mn = _gpu_step(U, G, np.zeros_like(U), 1e-2, 0.95)
+    Ur, Mr = spel.stiefel_step_batched(U, G, np.zeros_like(U), 1e-2, 0.95, mode="pe")
+    move, move_ref = np.abs(Un - U).max(), np.abs(Ur - U).max()
+    print("symmetric-gradient move", move, "oracle", move_ref, "U rel err", rel_fro(Un, Ur))
+    assert move <= 1e-5 and move_ref <= 1e-5
+    assert rel_fro(Un, Ur) <= 1e-5
     assert _orth_err(Un) <= 1e-5
-    print("symmetric-gradient move", np.abs(Un - U).max())
 
 
 @pytest.mark.parametrize("P,d,r", [(1, 256, 256), (3, 96, 32), (1, 1024, 1024)], ids=["square", "odd", "r1024"])
@@ -105,7 +112,7 @@ def test_step_at_shape_limits(P, d, r):
     U, G, M = st["U"], st["G"], st["M"]
     Un, Mn = _gpu_step(U, G, M, st["lr"], st["beta"])
     Ur, Mr = spel.stiefel_step_batched(U, G, M, st["lr"], st["beta"], mode="pe")
-    e_u, e_m = rel_fro(Un, Ur), rel_fro(Mn, Mr)
-    print(P, d, r, "U rel err", e_u, "M rel err", e_m, "orth", _orth_err(Un))
-    assert e_u <= 1e-5 and e_m <= 1e-5
+    e_u, e_m, du = rel_fro(Un, Ur), rel_fro(Mn, Mr), rel_fro(Un - U, Ur - U)
+    print(P, d, r, "U rel err", e_u, "M rel err", e_m, "dU rel err", du, "orth", _orth_err(Un))
+    assert e_u <= 1e-5 and e_m <= 1e-5 and du <= DU_TOL
     assert _orth_err(Un) <= 1e-5

@@ -33,6 +33,40 @@ def test_roundtrip_identity_full_rank(with_anchor):
     assert np.abs(Xh - X).max() < 1e-12
 
 
+@pytest.mark.parametrize("with_rvq", [False, True])
+def test_roundtrip_identity_full_rank_coord(with_rvq):
+    """Coordinate-space anchor (Eq. 1-2 with the anchor removed after the
+    projection and added back before the lift): with r = d and the same
+    anchor on both sides, decode(encode(X)) = X.  With RVQ the codebook
+    holds every token's Z0 exactly (plus a zero codeword), so the codes
+    reproduce Z0 and the round trip is still the identity.  Dropping the
+    anchor add-back, or adding it after the lift, breaks the identity by the
+    size of the anchor term (checked to be large)."""
+    rng = np.random.default_rng(15)
+    T, d, V, k = 29, 20, 40, 6
+    X = rng.standard_normal((T, d))
+    U = _orth(rng, d, d)
+    ids = rng.integers(0, V, T)
+    A = rng.standard_normal((V, k))
+    B = rng.standard_normal((k, d))   # coord: B is [k, r] and r = d
+    Z0 = codec.encode(X, ids, U, A, B, anchor_space="coord")
+    if with_rvq:
+        C = np.zeros((2, T + 1, d))
+        C[0, 1:] = Z0
+        C[1, 1:] = 3.0 + rng.standard_normal((T, d))
+        codes, _, rs = codec.rvq_encode(Z0, C)
+        assert np.array_equal(codes[:, 0], np.arange(1, T + 1)) and np.all(codes[:, 1] == 0)
+        Xh = codec.decode(codes, ids, U, A, B, C, anchor_space="coord")
+    else:
+        Xh = codec.decode(Z0, ids, U, A, B, anchor_space="coord")
+    assert np.abs(Xh - X).max() < 1e-12
+    anchor_term = (A[ids] @ B) @ U.T
+    assert np.abs(anchor_term).max() > 0.5
+    # the ambient reading adds a B (not a B U^T): a different map here
+    Xh_amb = codec.decode(Z0, ids, U, A, B, anchor_space="ambient")
+    assert np.abs(Xh_amb - X).max() > 0.1
+
+
 def test_roundtrip_identity_no_anchor_k0():
     rng = np.random.default_rng(12)
     X = rng.standard_normal((9, 16))
@@ -158,6 +192,34 @@ def test_rvq_planted_codewords_and_tie_break():
         assert rs[t, 1] == 0.0
         assert np.all(codes[t, 1:] == 0)
     assert gap[3, 0] == 0.0  # an exact tie is reported as a zero gap
+
+
+def test_rvq_top2_gap_hand_computed():
+    """The near-tie measure of the comparison rule, on numbers worked out by
+    hand: gap = (second-smallest - smallest squared distance) / ||R||^2,
+    where ||R||^2 is the round's residual norm (the distance to the zero
+    codeword).  Codewords on a line: (0,0), (1,0), (2,0), (5,0).
+
+      token a, R0 = (3,0): distances 9, 4, 1, 4  -> code 2, gap (4-1)/9 = 1/3
+               R1 = (1,0): distances 1, 0, 1, 16 -> code 1, gap (1-0)/1 = 1
+      token b, R0 = (0,2): distances 4, 5, 8, 29 -> code 0, gap (5-4)/4 = 1/4
+               R1 = (0,2): same                  -> code 0, gap 1/4
+      token c, R0 = (1.5,0): distances 2.25, 0.25, 0.25, 12.25 -> tie of 1
+               and 2, lowest index 1, gap 0; R1 = (0.5,0): distances 0.25,
+               0.25, 2.25, 20.25 -> code 0, gap 0
+
+    A denominator of the smallest distance instead of ||R||^2 would give 3
+    for token a's first round; a gap measured from the zero codeword would
+    give (9-1)/9."""
+    C = np.zeros((2, 4, 2))
+    C[:, :, 0] = [0.0, 1.0, 2.0, 5.0]
+    Z0 = np.array([[3.0, 0.0], [0.0, 2.0], [1.5, 0.0]])
+    codes, gap, rs = codec.rvq_encode(Z0, C, direct=True)
+    assert codes.tolist() == [[2, 1], [0, 0], [1, 0]]
+    assert np.allclose(gap, [[1 / 3, 1.0], [0.25, 0.25], [0.0, 0.0]], rtol=0, atol=1e-15)
+    assert np.allclose(rs, [[9.0, 1.0, 0.0], [4.0, 4.0, 4.0], [2.25, 0.25, 0.25]], rtol=0, atol=1e-15)
+    codes_e, gap_e, _ = codec.rvq_encode(Z0, C)
+    assert np.array_equal(codes_e, codes) and np.allclose(gap_e, gap, rtol=0, atol=1e-14)
 
 
 # ---------------------------------------------------------------- P6 adjoints and finite differences

@@ -102,6 +102,36 @@ def test_symmetric_gradient_leaves_U_unchanged():
     assert np.abs(Un2 - U).max() < 1e-8
 
 
+def test_fp32_symmetric_gradient_zero_rule():
+    """G = U S (S symmetric) stored in fp32, as the GPU receives it: the
+    stored G keeps a tangent residue of a few 1e-8 of ||G||_F, far below
+    fp32 resolution.  The iteration-matched step maps such a momentum to
+    D = 0 (||M||_F <= 2^-20 ||G||_F), so U moves only by the retraction's
+    rounding; without the rule the residue would be blown up to a full
+    lr-sized step.  A small but resolvable tangent gradient (1e-4 of ||G||)
+    still takes the full step."""
+    rng = np.random.default_rng(37)
+    d, r, lr = 256, 64, 1e-2
+    U = _orth(rng, d, r).astype(np.float32).astype(np.float64)
+    S = rng.standard_normal((r, r))
+    G = (U @ (S + S.T)).astype(np.float32).astype(np.float64)
+    gR = spel.tangent_project(U, G)
+    res = np.linalg.norm(gR) / np.linalg.norm(G)
+    assert 1e-9 < res < 1e-6, res
+    Un, Mn, D, _ = spel.stiefel_step(U, G, np.zeros((d, r)), lr, 0.95, mode="pe")
+    assert np.abs(D).max() == 0.0
+    assert np.abs(Un - U).max() < 1e-6
+    # without the rule (the bare normalisation) the step is lr-sized
+    D_raw = spel.lmo_pe(Mn, 5)
+    assert np.linalg.norm(D_raw) > 0.5 * np.sqrt(r)
+    # a resolvable tangent part is not suppressed
+    K = rng.standard_normal((r, r))
+    Gt = G + 1e-4 * np.linalg.norm(G) / np.linalg.norm(K) * U @ (K - K.T) / np.sqrt(2)
+    Un2, _, D2, _ = spel.stiefel_step(U, Gt, np.zeros((d, r)), lr, 0.95, mode="pe")
+    assert np.linalg.norm(D2) > 0.5 * np.sqrt(r)
+    assert np.abs(Un2 - U).max() > 1e-3
+
+
 # ---------------------------------------------------------------- P9 beta independence
 @pytest.mark.parametrize("mode", ["exact", "pe"])
 def test_first_step_independent_of_beta(mode):
