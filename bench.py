@@ -1,21 +1,25 @@
 """Benchmark of the MAPL boundary codec on one MI355X.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5]
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--graph] [--no-extra]
 
 One step is the codec chain of one pipeline boundary over one micro-batch
 with inputs resident in HBM: encode (Eq. 1 + RVQ) -> decode (Eq. 2) ->
 decode_bwd (dZhat, dU) -> encode_bwd (dX, dU accumulated), the r-dim
 gradient of decode_bwd feeding encode_bwd as it would cross the pipeline.
-Workload: the 1B-shaped boundary T = 16 x 2048 = 32768 tokens, d = 2048,
-r = 256, anchor rank k = 128 over V = 32000, L = 2 RVQ stages of K = 1024
-codewords, bf16 activations, synthetic seeded inputs.
+Headline workload: the 1B-shaped boundary T = 16 x 2048 = 32768 tokens,
+d = 2048, r = 256, anchor rank k = 128 over V = 32000, L = 2 RVQ stages of
+K = 1024 codewords, bf16 activations, synthetic seeded inputs.
 
-Prints one JSON line: tokens/s of the chain, the chain's fraction of its
-MFMA/HBM roofline, a live per-kernel roofline for the dominant kernel
-(HIP events on the launch stream), the SPEL step timed at its own
-configuration (16 projectors [2048,512]) and once for this boundary's
-projector, and the float64 oracle timed on a bounded token sample on the
-host cores (rank 0, N = 1 only).
+Prints one JSON line: tokens/s of the chain (warm-up steps, then the mean
+over a block of `steps` steps between two events; the median of `steps`
+event-separated steps beside it), eager and replayed as one HIP graph; the
+chain's fraction of its MFMA/HBM roofline; a live per-kernel roofline for
+the dominant kernel (HIP events around each launch on its stream); the same
+chain with data-drawn codebooks ("stress": every code in use) with the RVQ
+encoder's decision counters; every other workload (c1, c2 for r = 64..512,
+c3) with its tokens/s, roofline fraction and the oracle's tokens/s; the SPEL
+step (16 projectors [2048,512], and this boundary's projector); and the
+float64 oracle timed on the host cores (rank 0, N = 1 only).
 """
 import argparse
 import hashlib
@@ -107,40 +111,58 @@ def traffic_for(kernel):
 
 
 def cpu_baseline(x, budget_s=15.0):
-    """Time the float64 oracle's four codec calls on a token sample."""
+    """Time the float64 oracle's four codec calls on a token sample of
+    workload x, with its BLAS limited to the host cores this process may run
+    on (len(os.sched_getaffinity(0)))."""
     from oracle import codec as oc
+    from paper_2606_05484_amd import synth
+    cores = len(os.sched_getaffinity(0))
+    blas, ctl = "unknown", None
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            blas = "%s %s" % (info[0].get("internal_api", "?"), info[0].get("version", ""))
+        ctl = threadpool_limits(limits=cores, user_api="blas")
         threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     except Exception:
-        threads = len(os.sched_getaffinity(0))
-    from paper_2606_05484_amd import synth
-    f64 = lambda k, sel: synth.as_f64(x[k][sel], "bf16")
-    A, B = synth.as_f64(x["A"], "bf16"), synth.as_f64(x["B"], "bf16")
+        threads = None
+    dt = x["dtype"]
+    op = "bf16" if dt == "bf16" else "exact"
+    f64 = lambda k, sel: synth.as_f64(x[k][sel], dt)
+    A, B = synth.as_f64(x["A"], dt), synth.as_f64(x["B"], dt)
+    C = x["C"] if x["L"] else None
 
     def run(n):
         sel = slice(0, n)
         X, dXh, dZ = f64("X", sel), f64("dXhat", sel), f64("dZ", sel)
         ids = x["ids"][sel]
         t0 = time.perf_counter()
-        codes, _, _ = oc.encode(X, ids, x["U"], A, B, x["C"], operand="bf16")
-        oc.decode(codes, ids, x["U"], A, B, x["C"], operand="bf16")
-        oc.decode_bwd(dXh, codes, ids, x["U"], A, B, x["C"], operand="bf16")
-        oc.encode_bwd(dZ, X, ids, x["U"], A, B, operand="bf16")
+        enc = oc.encode(X, ids, x["U"], A, B, C, operand=op)
+        pay = enc[0] if C is not None else enc
+        oc.decode(pay, ids, x["U"], A, B, C, operand=op)
+        oc.decode_bwd(dXh, pay, ids, x["U"], A, B, C, operand=op)
+        oc.encode_bwd(dZ, X, ids, x["U"], A, B, operand=op)
         return time.perf_counter() - t0
 
-    # grow the token sample until one run takes a third of the budget; if the
-    # whole micro-batch is faster than that, repeat it until the budget is used
-    n = 512
-    dt = run(n)
-    while dt < budget_s / 3 and n < x["T"]:
-        n = min(x["T"], n * 4)
-        dt = run(n)
-    reps, total = 1, dt
-    while total < budget_s / 2 and n == x["T"]:
-        total += run(n)
-        reps += 1
-    return {"value": n * reps / total, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    try:
+        # grow the token sample until one run takes a third of the budget; if
+        # the whole micro-batch is faster than that, repeat it until the
+        # budget is used
+        n = min(512, x["T"])
+        dt_ = run(n)
+        while dt_ < budget_s / 3 and n < x["T"]:
+            n = min(x["T"], n * 4)
+            dt_ = run(n)
+        reps, total = 1, dt_
+        while total < budget_s / 2 and n == x["T"]:
+            total += run(n)
+            reps += 1
+    finally:
+        if ctl is not None:
+            ctl.unregister() if hasattr(ctl, "unregister") else None
+    return {"value": n * reps / total, "unit": "tokens/s", "cores": cores, "blas_threads": threads, "blas": blas,
+            "kind": "oracle",
             "sample": "%s%d of %d tokens of the same workload, float64 NumPy, the four codec calls, "
                       "%d run(s) in %.1f s" % ("" if n == x["T"] else "first ", n, x["T"], reps, total)}
 
@@ -229,7 +251,7 @@ def summarize(paths, write_traffic):
              "# from the rocprofv3 kernel trace of a bench.py run; each library dispatch is named by its",
              "# position in the repeated 4-call chain; bench.py's own HIP-event average beside it.", ""]
     disp = _dispatches(paths[1], "_kernel_trace.csv")
-    named = _chain_map(disp, order, bench["warmup"] + 2 * bench["steps"])
+    named = _chain_map(disp, order, len([x for x in disp if "mapl::" in x[1]]) // len(order))
     agg = {}
     for name, sym, e in named:
         row = e["row"]
@@ -297,14 +319,151 @@ def summarize(paths, write_traffic):
                 fh.write("%s %s %.0f\n" % (name, _src_sha(kernel_sources(name)), traffic[name]))
 
 
+def chain_counts(x):
+    """Per-call algorithmic (flops, bytes) of workload x (see per_call_counts)."""
+    es = 4 if x["dtype"] == "f32" else 2
+    T, d, r, k, L, K = (x[n] for n in ("T", "d", "r", "k", "L", "K"))
+    pay = (L * (1 if K <= 256 else 2)) if L else r * es
+    c = {
+        "encode": (2 * d * r + 2 * k * r + 2 * L * r * K, es * d + 4 + es * k + pay),
+        "decode": (2 * r * d + 2 * k * d, pay + 4 + es * k + es * d),
+        "decode_bwd": (4 * d * r, es * d + pay + es * r),
+        "encode_bwd": (4 * d * r + 2 * k * r, es * r + 2 * es * d + 4 + es * k),
+    }
+    return {n: (f * T, b * T) for n, (f, b) in c.items()}
+
+
+def roofline_of(x, ms):
+    """Chain roofline: sum over calls of max(F / peak, B / HBM) against the
+    measured ms per step (peak: bf16 or fp32 MFMA by the workload's type)."""
+    peak = PEAK_F32 if x["dtype"] == "f32" else PEAK_BF16
+    cc = chain_counts(x)
+    per = {n: max(f / peak, b / PEAK_HBM) for n, (f, b) in cc.items()}
+    bound = {n: ("mfma" if f / peak >= b / PEAK_HBM else "hbm") for n, (f, b) in cc.items()}
+    roof = sum(per.values())
+    return {"frac": roof / (ms * 1e-3), "roofline_us": roof * 1e6, "measured_us": ms * 1e3,
+            "flops": sum(f for f, _ in cc.values()), "bytes": sum(b for _, b in cc.values()),
+            "bound_per_call": bound}
+
+
+class Chain:
+    """Device buffers of one workload and its four-call chain (encode ->
+    decode -> decode_bwd -> encode_bwd, the decoder's dZ feeding the
+    encoder's backward as it would cross the pipeline)."""
+
+    def __init__(self, torch, mapl, x, C):
+        self.torch = torch
+        self.mapl = mapl
+        dt = x["dtype"]
+        tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+
+        def put(a):
+            a = np.ascontiguousarray(a)
+            if dt == "bf16":
+                return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+            return torch.from_numpy(a).cuda()
+
+        T, d, r, L, K = (x[n] for n in ("T", "d", "r", "L", "K"))
+        self.X, self.A, self.B, self.dXh = put(x["X"]), put(x["A"]), put(x["B"]), put(x["dXhat"])
+        self.U = torch.from_numpy(x["U"]).cuda()
+        self.ids = torch.from_numpy(x["ids"]).cuda()
+        self.C = torch.from_numpy(np.ascontiguousarray(C, dtype=np.float32)).cuda() if L else None
+        self.D = mapl.desc(T=T, d=d, r=r, V=x["V"], k=x["k"], L=L, K=K, x_dtype=dt)
+        self.ws = mapl.workspace(max(mapl.workspace_bytes(self.D, c) for c in range(4)))
+        if L:
+            self.payload = torch.empty((T, L), dtype=torch.uint8 if K <= 256 else torch.int16, device="cuda")
+        else:
+            self.payload = torch.empty((T, r), dtype=tdt, device="cuda")
+        self.Xh = torch.empty((T, d), dtype=tdt, device="cuda")
+        self.dZ = torch.empty((T, r), dtype=tdt, device="cuda")
+        self.dX = torch.empty((T, d), dtype=tdt, device="cuda")
+        self.dU = torch.empty((d, r), device="cuda")
+        self.T = T
+
+    def step(self, ev=None):
+        m, D = self.mapl, self.D
+        if ev: ev[0].record()
+        m.encode(D, self.X, self.ids, self.U, self.A, self.B, self.C, self.payload, self.ws)
+        if ev: ev[1].record()
+        m.decode(D, self.payload, self.ids, self.U, self.A, self.B, self.C, self.Xh, self.ws)
+        if ev: ev[2].record()
+        m.decode_bwd(D, self.dXh, self.payload, self.ids, self.U, self.A, self.B, self.C, self.dZ, self.dU, 0,
+                     self.ws)
+        if ev: ev[3].record()
+        m.encode_bwd(D, self.dZ, self.X, self.ids, self.U, self.A, self.B, self.dX, self.dU, 1, self.ws)
+        if ev: ev[4].record()
+
+    def capture(self):
+        """The chain captured once into a graph (its launches only: the
+        library records no memset and no synchronisation)."""
+        torch = self.torch
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.step()
+        torch.cuda.synchronize()
+        return g
+
+
+def time_steps(torch, run, warmup, steps):
+    """warmup untimed runs, then `steps` runs between two events (mean ms per
+    step over the block: the throughput figure), then `steps` more runs with
+    an event between consecutive runs (median ms per step)."""
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        run()
+    t1.record()
+    torch.cuda.synchronize()
+    mean = t0.elapsed_time(t1) / steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
+        run()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return mean, float(np.median(per))
+
+
+def library_stress_codebooks(torch, mapl, x, seed=104, n=8192):
+    """Data-drawn codebooks (every code in use) from the library's own
+    projection of the first n tokens: codeword 0 = 0, round 0's other
+    codewords are projected tokens, round 1's are 0.3 times projected
+    tokens.  Only the seeded choice of tokens is drawn here."""
+    n = min(n, x["T"])
+    sub = dict(x, T=n, X=x["X"][:n], ids=x["ids"][:n], dXhat=x["dXhat"][:n], L=0, K=0)
+    ch = Chain(torch, mapl, sub, np.zeros((0,)))
+    mapl.encode(ch.D, ch.X, ch.ids, ch.U, ch.A, ch.B, None, ch.payload, ch.ws)
+    torch.cuda.synchronize()
+    Z = ch.payload.float().cpu().numpy()
+    rng = np.random.default_rng(seed)
+    C = np.zeros((x["L"], x["K"], x["r"]), dtype=np.float32)
+    C[0, 1:] = Z[rng.choice(n, x["K"] - 1, replace=False)]
+    for l in range(1, x["L"]):
+        C[l, 1:] = 0.3 * Z[rng.choice(n, x["K"] - 1, replace=False)]
+    return C
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--stress", action="store_true", help="data-drawn codebooks (every code in use)")
-    ap.add_argument("--no-spel", action="store_true", help="skip the SPEL step timing")
+    ap.add_argument("--graph", action="store_true",
+                    help="headline from the chain replayed as one HIP graph (default: eager calls; both are "
+                         "reported)")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="only the c4 headline (no stress, per-config or SPEL blocks)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with one plain 256 MiB device copy (calibrates FETCH_SIZE / WRITE_SIZE counters)")
     ap.add_argument("--summarize", nargs="+", metavar="PATH",
@@ -326,74 +485,35 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    print("generating workload c4", file=sys.stderr, flush=True)
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    log("generating workload c4")
     x = synth.codec_inputs("c4")
     T, d, r, V, k, L, K = (x[n] for n in ("T", "d", "r", "V", "k", "L", "K"))
-    C = x["C"]
-    if args.stress:
-        from oracle import codec as oc
-        Z0 = oc.project(synth.as_f64(x["X"][:8192], "bf16"), x["ids"][:8192], x["U"],
-                        synth.as_f64(x["A"], "bf16"), synth.as_f64(x["B"], "bf16"), "ambient", "bf16")
-        rng = np.random.default_rng(104)
-        C = np.zeros_like(x["C"])
-        C[0, 1:] = Z0[rng.choice(8192, K - 1, replace=False)]
-        C[1, 1:] = 0.3 * Z0[rng.choice(8192, K - 1, replace=False)]
-    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
-    X, A, B, dXh = bf(x["X"]), bf(x["A"]), bf(x["B"]), bf(x["dXhat"])
-    U = torch.from_numpy(x["U"]).cuda()
-    ids = torch.from_numpy(x["ids"]).cuda()
-    Cg = torch.from_numpy(np.ascontiguousarray(C)).cuda()
-    D = mapl.desc(T=T, d=d, r=r, V=V, k=k, L=L, K=K)
-    ws = mapl.workspace(max(mapl.workspace_bytes(D, c) for c in range(4)))
-    codes = torch.empty((T, L), dtype=torch.int16, device="cuda")
-    Xh = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
-    dZ = torch.empty((T, r), dtype=torch.bfloat16, device="cuda")
-    dX = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
-    dU = torch.empty((d, r), device="cuda")
-
+    ch = Chain(torch, mapl, x, x["C"])
     calls = ["encode", "decode", "decode_bwd", "encode_bwd"]
 
-    def step(ev=None):
-        if ev: ev[0].record()
-        mapl.encode(D, X, ids, U, A, B, Cg, codes, ws)
-        if ev: ev[1].record()
-        mapl.decode(D, codes, ids, U, A, B, Cg, Xh, ws)
-        if ev: ev[2].record()
-        mapl.decode_bwd(D, dXh, codes, ids, U, A, B, Cg, dZ, dU, 0, ws)
-        if ev: ev[3].record()
-        mapl.encode_bwd(D, dZ, X, ids, U, A, B, dX, dU, 1, ws)
-        if ev: ev[4].record()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    print("timing %d steps" % args.steps, file=sys.stderr, flush=True)
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record()
-    for _ in range(args.steps):
-        step()
-    t1.record()
-    torch.cuda.synchronize()
-    ms = t0.elapsed_time(t1) / args.steps
+    # ---- the c4 headline: every c4 chain with the official codebooks runs
+    # first (eager, then graph replays, then the traced pass), so that a
+    # profiler can name the library's dispatches by position
+    log("timing %d eager steps" % args.steps)
+    eager_ms, eager_med = time_steps(torch, ch.step, args.warmup, args.steps)
+    log("capturing the chain and timing %d graph replays" % args.steps)
+    g = ch.capture()
+    graph_ms, graph_med = time_steps(torch, g.replay, args.warmup, args.steps)
+    ms, med = (graph_ms, graph_med) if args.graph else (eager_ms, eager_med)
     value = T / (ms * 1e-3)
 
-    # per-call times (events between calls) and per-kernel times (library trace)
+    # per-call times (events between calls) and per-kernel times (library
+    # trace: HIP events around each launch on its stream), eager
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     mapl.profile(True)
     for i in range(args.steps):
-        step(evs[i])
+        ch.step(evs[i])
     torch.cuda.synchronize()
     mapl.profile(False)
     prof = mapl.profile_report()
-    per_call = {c: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs])) * 1e3 for i, c in enumerate(calls)}
-
-    payload = L * 2
-    cc = per_call_counts(T, d, r, k, L, K, payload)
-    roof_calls = {n: max(f / PEAK_BF16, b / PEAK_HBM) for n, (f, b) in cc.items()}
-    roof_chain = sum(roof_calls.values())
-    Fsum, Bsum = sum(f for f, _ in cc.values()), sum(b for _, b in cc.values())
-    chain_frac = roof_chain / (ms * 1e-3)
+    per_call = {c: float(np.median([e[i].elapsed_time(e[i + 1]) for e in evs])) * 1e3 for i, c in enumerate(calls)}
+    chain_runs = 2 * args.warmup + 4 * args.steps + 2 + args.steps  # eager, capture warm-up, graph, traced
 
     kc = kernel_counts(T, d, r, k, L, K)
     kern = {n: (cnt, tot / cnt * 1e3) for n, (cnt, tot) in prof.items()}  # name -> (launches, avg us)
@@ -408,45 +528,7 @@ def main():
     roof["traffic"] = traffic_for(dom)
     roof["kernel"] = dom
     roof["avg_us"] = kern[dom][1]
-
-    # SPEL step: its own configuration (16 x [2048,512]) and this boundary's projector
-    def time_spel(P, dd, rr, reps):
-        st = synth.stiefel_inputs(None, seed=55, P=P, d=dd, r=rr, gscale=1e-3, lr=1e-2, beta=0.95, steps=1)
-        Ug, Gg, Mg = (torch.from_numpy(st[n]).cuda() for n in ("U", "G", "M"))
-        w = mapl.workspace(mapl.workspace_bytes(None, mapl.CALL_STIEFEL, P, dd, rr))
-        for _ in range(2):
-            mapl.stiefel_step(P, dd, rr, Ug, Gg, Mg, 1e-2, 0.95, 5, 7, w)
-        a, bb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        a.record()
-        for _ in range(reps):
-            mapl.stiefel_step(P, dd, rr, Ug, Gg, Mg, 1e-2, 0.95, 5, 7, w)
-        bb.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(bb) / reps
-
-    def spel_flops(P, dd, rr):
-        it = 4 * dd * rr * rr + 2 * rr ** 3
-        return P * (4 * dd * rr * rr + 12 * it)
-
-    spel, alg1 = None, None
-    if not args.no_spel:
-        spel_c5 = time_spel(16, 2048, 512, 5)
-        spel_b = time_spel(1, d, r, 10)
-        spel = {"config": "16 projectors [2048,512], PolarExpress 5 + 7 steps", "ms_per_step": spel_c5,
-                "tflops": spel_flops(16, 2048, 512) / (spel_c5 * 1e-3) / 1e12,
-                "roofline_frac_fp32": spel_flops(16, 2048, 512) / PEAK_F32 / (spel_c5 * 1e-3),
-                "boundary_projector_ms": spel_b}
-        amort = 128  # micro-batches per optimizer step: global batch 512 / micro-batch 4
-        alg1 = T / ((ms + spel_b / amort) * 1e-3)
-    calib = None
-    if args.calib_copy:
-        src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        calib = src.numel()
+    del g
 
     out = {
         "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -454,21 +536,113 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "1B-shaped boundary (c4): T=32768 tokens (16x2048), d=2048, r=256, "
                                "anchor k=128 over V=32000 (Zipf 1.1 ids), RVQ L=2 x K=1024, u16 codes, "
-                               "ambient anchor, enc+dec fwd+bwd per step" + (", data-drawn codebooks" if args.stress else ""),
+                               "ambient anchor, enc+dec fwd+bwd per step, %s" %
+                               ("the 4-call chain replayed as one HIP graph" if args.graph else "eager calls"),
                    "global_batch": T, "seq_len": 2048, "parallelism": "none (1 GPU)"},
         "roofline": roof,
-        "chain_roofline": {"frac": chain_frac, "roofline_us": roof_chain * 1e6, "measured_us": ms * 1e3,
-                           "flops": Fsum, "bytes": Bsum},
+        "median_ms_per_step": med,
+        "eager_ms_per_step": eager_ms, "eager_median_ms_per_step": eager_med,
+        "graph_ms_per_step": graph_ms, "graph_median_ms_per_step": graph_med,
+        "chain_roofline": roofline_of(x, ms),
         "per_call_us": per_call,
         "per_kernel_us": {n: round(v[1], 2) for n, v in sorted(kern.items())},
         "kernel_order": list(kern),
-        "spel": spel,
-        "alg1_tokens_per_s": alg1,
+        "c4_chain_runs": chain_runs,
     }
-    if calib:
-        out["calib_copy_bytes"] = calib
+
+    if not args.no_extra:
+        # ---- c4 with data-drawn codebooks: every code in use, so the encoder
+        # rescoring (and, where needed, second screening passes) run
+        log("c4 with data-drawn codebooks")
+        Cs = library_stress_codebooks(torch, mapl, x)
+        chs = Chain(torch, mapl, x, Cs)
+        s_ms, s_med = time_steps(torch, chs.step, args.warmup, args.steps)
+        # kernel times from an events-only traced pass, then the decision
+        # counters from a separate pass (counting adds atomics and a sync)
+        mapl.profile(1)
+        for i in range(10):
+            chs.step()
+        torch.cuda.synchronize()
+        mapl.profile(0)
+        sp = mapl.profile_report()
+        enc_us = sp["enc:gemm_rvq"][1] / sp["enc:gemm_rvq"][0] * 1e3 if "enc:gemm_rvq" in sp else None
+        mapl.profile(2)
+        for i in range(5):
+            chs.step()
+        torch.cuda.synchronize()
+        mapl.profile(0)
+        st = {n: v[0] for n, v in mapl.profile_report().items() if n.startswith("rvq:")}
+        out["stress"] = {
+            "codebooks": "codeword 0 = 0; round 0: projected tokens (the library's own L=0 encode of the first "
+                         "8192 tokens, seed 104); round 1: 0.3 x projected tokens",
+            "tokens_per_s": T / (s_ms * 1e-3), "ms_per_step": s_ms, "median_ms_per_step": s_med,
+            "workload": "as the headline, eager calls",
+            "chain_roofline_frac": roofline_of(x, s_ms)["frac"],
+            "enc_gemm_rvq_us": enc_us,
+            "encode_vs_headline": (enc_us / kern["enc:gemm_rvq"][1]) if enc_us and "enc:gemm_rvq" in kern else None,
+            "rvq_tokens_rescored_frac": st.get("rvq:tokens_rescored", 0) / (5.0 * T * L),
+            "rvq_candidates_per_rescored_token": st.get("rvq:candidates", 0) / max(1, st.get("rvq:tokens_rescored", 0)),
+            "rvq_second_pass_frac": st.get("rvq:second_pass_blocks", 0) / max(1, st.get("rvq:blocks", 0)),
+            "rvq_list_overflows": st.get("rvq:list_overflows", 0),
+        }
+        del chs
+
+        # ---- the other workloads: tokens/s and chain roofline (graph replay),
+        # the oracle beside each on the host
+        out["configs"] = {}
+        for name in ["c1", "c2_r64", "c2_r128", "c2_r256", "c2_r512", "c3"]:
+            log("workload", name)
+            xc = synth.codec_inputs(name)
+            cc = Chain(torch, mapl, xc, xc["C"])
+            c_ms, c_med = time_steps(torch, cc.step, args.warmup, args.steps)
+            gc = cc.capture()
+            g_ms, g_med = time_steps(torch, gc.replay, args.warmup, args.steps)
+            del gc
+            c_med = min(c_med, g_med)
+            rf = roofline_of(xc, c_med)
+            blk = {"T": xc["T"], "d": xc["d"], "r": xc["r"], "k": xc["k"], "L": xc["L"], "K": xc["K"],
+                   "dtype": xc["dtype"], "tokens_per_s": xc["T"] / (c_med * 1e-3), "median_ms_per_step": c_med,
+                   "mean_ms_per_step": c_ms, "graph_median_ms_per_step": g_med,
+                   "chain_roofline_frac": rf["frac"], "roofline_us": rf["roofline_us"],
+                   "bound_per_call": rf["bound_per_call"]}
+            if not args.no_cpu_baseline:
+                blk["cpu_baseline"] = cpu_baseline(xc, budget_s=4.0)
+            out["configs"][name] = blk
+            del cc
+
+        # ---- SPEL step: its own configuration (16 x [2048,512]) and this
+        # boundary's projector
+        def time_spel(P, dd, rr, reps):
+            stq = synth.stiefel_inputs(None, seed=55, P=P, d=dd, r=rr, gscale=1e-3, lr=1e-2, beta=0.95, steps=1)
+            Ug, Gg, Mg = (torch.from_numpy(stq[n]).cuda() for n in ("U", "G", "M"))
+            w = mapl.workspace(mapl.workspace_bytes(None, mapl.CALL_STIEFEL, P, dd, rr))
+            run = lambda: mapl.stiefel_step(P, dd, rr, Ug, Gg, Mg, 1e-2, 0.95, 5, 7, w)
+            return time_steps(torch, run, 2, reps)
+
+        def spel_flops(P, dd, rr):
+            it = 4 * dd * rr * rr + 2 * rr ** 3
+            return P * (4 * dd * rr * rr + 12 * it)
+
+        log("SPEL step")
+        spel_c5, spel_c5_med = time_spel(16, 2048, 512, 10)
+        spel_b, _ = time_spel(1, d, r, 20)
+        out["spel"] = {"config": "16 projectors [2048,512], PolarExpress 5 + 7 steps", "ms_per_step": spel_c5,
+                       "median_ms_per_step": spel_c5_med,
+                       "tflops": spel_flops(16, 2048, 512) / (spel_c5_med * 1e-3) / 1e12,
+                       "roofline_frac_fp32": spel_flops(16, 2048, 512) / PEAK_F32 / (spel_c5_med * 1e-3),
+                       "boundary_projector_ms": spel_b}
+        amort = 128  # micro-batches per optimizer step: global batch 512 / micro-batch 4
+        out["alg1_tokens_per_s"] = T / ((ms + spel_b / amort) * 1e-3)
+
+    if args.calib_copy:
+        src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calib_copy_bytes"] = src.numel()
     if not args.no_cpu_baseline:
-        print("timing the oracle on the host", file=sys.stderr, flush=True)
+        log("timing the oracle on the host")
         out["cpu_baseline"] = cpu_baseline(x)
     print(json.dumps(out), flush=True)
 
