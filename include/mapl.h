@@ -175,6 +175,24 @@ int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, const float* G,
                       float lr, float beta, int lmo_steps, int retract_steps, void* ws,
                       size_t ws_bytes, void* stream);
 
+/* mapl_encode without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, results and errors as mapl_encode;
+ * scratch comes from a static device array of MAPL_NOALLOC_SCRATCH_BYTES
+ * that the library holds on each GPU it runs on (the current device at the
+ * call) until the process ends.  Requests whose workspace
+ * (mapl_workspace_bytes(desc, MAPL_CALL_ENCODE)) exceeds it fail with
+ * MAPL_E_WORKSPACE before anything is enqueued; at r = 256 this is about
+ * 2.3 MiB for d = 2048, K = 1024, L = 2 at any T, while other ranks with
+ * L > 0 also hold Z0 (4 r bytes per token).  The call allocates nothing.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (other threads, other streams) race and must be serialised by the
+ * caller.  The first call on a device looks up the array's address there. */
+#define MAPL_NOALLOC_SCRATCH_BYTES (16u << 20)
+int mapl_encode_noalloc(const mapl_codec_desc* desc, const void* X, const int32_t* ids,
+                        const float* U, const void* A_s, const void* B_s, const float* C,
+                        void* payload, void* stream);
+
 /* Workspace bytes needed by `call` (enum mapl_call).  Codec calls read
  * `desc` and ignore P, d, r; MAPL_CALL_STIEFEL ignores `desc`.  Returns 0
  * for an invalid request (mapl_last_error() says why). */

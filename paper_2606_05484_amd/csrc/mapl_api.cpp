@@ -912,6 +912,53 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   return MAPL_OK;
 }
 
+// ------------------------------------------------------ allocation-free encode
+// Scratch of mapl_encode_noalloc: a file-scope device array, one copy per GPU
+// the library runs on, held until the process ends.  In host code the name
+// `scratch` is only a stand-in for the symbol; its device address on each GPU
+// comes from hipGetSymbolAddress, called once per device with that device
+// current, and only that address is ever handed to kernels.
+static __device__ __align__(256) unsigned char scratch[MAPL_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_for_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(MAPL_E_UNSUPPORTED, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(MAPL_E_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MAPL_OK;
+}
+}  // namespace
+
+extern "C" int mapl_encode_noalloc(const mapl_codec_desc* desc, const void* X, const int32_t* ids, const float* U,
+                                   const void* A_s, const void* B_s, const float* C, void* payload, void* stream) {
+  g_err.clear();
+  int st = check_desc(desc);
+  if (st) return st;
+  const size_t need = layout(*desc, MAPL_CALL_ENCODE).total;
+  if (need > (size_t)MAPL_NOALLOC_SCRATCH_BYTES)
+    return fail(MAPL_E_WORKSPACE,
+                "mapl_encode_noalloc: this request needs %zu bytes of scratch, the static scratch holds %zu "
+                "(use mapl_encode with a workspace)",
+                need, (size_t)MAPL_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((st = scratch_for_current_device(&ws))) return st;
+  return mapl_encode(desc, X, ids, U, A_s, B_s, C, payload, ws, (size_t)MAPL_NOALLOC_SCRATCH_BYTES, stream);
+}
+
 // ---------------------------------------------------------------- tracing API
 extern "C" int mapl_profile(int enable) {
   std::lock_guard<std::mutex> lk(g_prof_mu);

@@ -40,6 +40,7 @@ _lib = None
 _P = ctypes.c_void_p
 _SIG = {
     "mapl_encode": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [_P, ctypes.c_size_t, _P],
+    "mapl_encode_noalloc": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [_P],
     "mapl_decode": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [_P, ctypes.c_size_t, _P],
     "mapl_decode_bwd": [ctypes.POINTER(CodecDesc)] + [_P] * 9 + [ctypes.c_int, _P, ctypes.c_size_t, _P],
     "mapl_encode_bwd": [ctypes.POINTER(CodecDesc)] + [_P] * 8 + [ctypes.c_int, _P, ctypes.c_size_t, _P],
@@ -130,6 +131,15 @@ def encode(D, X, ids, U, A_s, B_s, C, payload, ws, ws_bytes=None, stream=None):
     wb = ws_bytes if ws_bytes is not None else (ws.numel() if ws is not None else 0)
     _check(lib().mapl_encode(ctypes.byref(D), _ptr(X), _ptr(ids), _ptr(U), _ptr(A_s), _ptr(B_s), _ptr(C),
                              _ptr(payload), _ptr(ws), wb, _stream(stream)))
+
+
+def encode_noalloc(D, X, ids, U, A_s, B_s, C, payload, stream=None):
+    """mapl_encode on the library's static device scratch (no workspace)."""
+    _check(lib().mapl_encode_noalloc(ctypes.byref(D), _ptr(X), _ptr(ids), _ptr(U), _ptr(A_s), _ptr(B_s), _ptr(C),
+                                     _ptr(payload), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 def decode(D, payload, ids, U, A_r, B_r, C, Xhat, ws, ws_bytes=None, stream=None):

@@ -144,3 +144,14 @@ def test_polar_table_matches_oracle_schedule():
         rows = np.array([[float(v) for v in r.split(",") if v.strip()] for r in re.findall(r"\{([^{}]*)\}", blk)])
         ref = np.array(ps.greedy_schedule(lo, rows.shape[0])[0])
         assert np.abs(rows - ref).max() <= 1e-12 * np.abs(ref).max()
+
+
+def test_noalloc_rejects_requests_beyond_its_scratch():
+    """mapl_encode_noalloc refuses, before touching any pointer or device,
+    a request whose workspace exceeds the static scratch (here the fp32 Z0 of
+    2^22 tokens at r = 128: 2 GiB)."""
+    D = mapl.desc(T=1 << 22, d=1024, r=128, V=100, k=16, L=2, K=256)
+    assert mapl.workspace_bytes(D, mapl.CALL_ENCODE) > mapl.NOALLOC_SCRATCH_BYTES
+    with pytest.raises(mapl.MaplError) as e:
+        mapl.encode_noalloc(D, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert e.value.status == -7 and "scratch" in str(e.value)
