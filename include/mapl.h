@@ -175,6 +175,25 @@ int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, const float* G,
                       float lr, float beta, int lmo_steps, int retract_steps, void* ws,
                       size_t ws_bytes, void* stream);
 
+/* Streaming codebook synchronisation (Sec. 3.5 "Codebook Synchronization",
+ * App. F): instead of the whole codebook, each micro-batch carries a random
+ * subset of its codewords (a 1/5 fraction per micro-batch in the paper's
+ * hyperparameter table), so sender and receiver copies stay identical up to
+ * a bounded staleness.  The subsets are the caller's: rows [L,n] int32 holds,
+ * per round l, the n codeword indices sent this micro-batch (a random
+ * partition of [0,K) into parts, one part per micro-batch, gives every
+ * codeword once per cycle).  Indices of one round must be distinct for
+ * unpack; indices outside [0,K) are skipped (pack writes a zero row).
+ *   pack   (sender):   buf[l][i][:] = C[l][rows[l][i]][:],  buf [L,n,r] fp32
+ *   unpack (receiver): C[l][rows[l][i]][:] = buf[l][i][:], other rows kept
+ * C is [L,K,r] fp32.  Requirements: 1 <= L <= 8, 1 <= K <= 65536,
+ * 4 <= r <= 1024 with r % 4 == 0, 0 <= n <= K; buf must not overlap C or
+ * rows.  Device pointers, 16-byte aligned; enqueued on `stream` only. */
+int mapl_codebook_pack(int32_t L, int32_t K, int64_t r, const float* C, const int32_t* rows,
+                       int32_t n, float* buf, void* stream);
+int mapl_codebook_unpack(int32_t L, int32_t K, int64_t r, const float* buf, const int32_t* rows,
+                         int32_t n, float* C, void* stream);
+
 /* mapl_encode without a workspace, for callers that cannot allocate device
  * memory (code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc).  Same arguments, results and errors as mapl_encode;

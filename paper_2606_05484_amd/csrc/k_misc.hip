@@ -190,6 +190,30 @@ __global__ __launch_bounds__(1024) void k_inf_norm_scales(const float* __restric
   }
 }
 
+// Streaming codebook synchronisation (Sec. 3.5): one wave per transmitted
+// codeword row, 16-byte accesses across the row.  pack: buf[l][i] =
+// C[l][rows[l][i]]; unpack: C[l][rows[l][i]] = buf[l][i].  Rows outside
+// [0, K) are skipped (pack writes zeros for them).
+__global__ void k_codebook_pack(const float* __restrict__ C, const int32_t* __restrict__ rows, int K, int r, int n,
+                                float* __restrict__ buf) {
+  const int i = blockIdx.x, l = blockIdx.y, lane = threadIdx.x;
+  const int row = rows[(int64_t)l * n + i];
+  const bool ok = (unsigned)row < (unsigned)K;
+  const float4* src = (const float4*)(C + ((int64_t)l * K + (ok ? row : 0)) * r);
+  float4* dst = (float4*)(buf + ((int64_t)l * n + i) * r);
+  for (int c = lane; c < r / 4; c += 64) dst[c] = ok ? src[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+__global__ void k_codebook_unpack(const float* __restrict__ buf, const int32_t* __restrict__ rows, int K, int r,
+                                  int n, float* __restrict__ C) {
+  const int i = blockIdx.x, l = blockIdx.y, lane = threadIdx.x;
+  const int row = rows[(int64_t)l * n + i];
+  if ((unsigned)row >= (unsigned)K) return;
+  const float4* src = (const float4*)(buf + ((int64_t)l * n + i) * r);
+  float4* dst = (float4*)(C + ((int64_t)l * K + row) * r);
+  for (int c = lane; c < r / 4; c += 64) dst[c] = src[c];
+}
+
 }  // namespace
 
 hipError_t launch_gather_rows_f32(const float* A, int k, const int32_t* ids, int V, int T, float* out,
@@ -251,6 +275,20 @@ hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* inv_nu, f
                                   hipStream_t s) {
   if (r > 1024) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_inf_norm_scales, dim3(P), dim3(1024), 0, s, S, r, inv_nu, inv_nu2, inv_nu4);
+  return hipGetLastError();
+}
+
+hipError_t launch_codebook_pack(const float* C, const int32_t* rows, int L, int K, int r, int n, float* buf,
+                                hipStream_t s) {
+  if (n <= 0 || L <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_codebook_pack, dim3(n, L), dim3(64), 0, s, C, rows, K, r, n, buf);
+  return hipGetLastError();
+}
+
+hipError_t launch_codebook_unpack(const float* buf, const int32_t* rows, int L, int K, int r, int n, float* C,
+                                  hipStream_t s) {
+  if (n <= 0 || L <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_codebook_unpack, dim3(n, L), dim3(64), 0, s, buf, rows, K, r, n, C);
   return hipGetLastError();
 }
 

@@ -192,6 +192,14 @@ hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64
 hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* inv_nu, float* inv_nu2,
                                   float* inv_nu4, hipStream_t s);
 
+// ---------------------------------------------------------------- codebook synchronisation
+// buf[l][i][:] = C[l][rows[l*n + i]][:] (zeros for rows outside [0, K)); r % 4 == 0.
+hipError_t launch_codebook_pack(const float* C, const int32_t* rows, int L, int K, int r, int n, float* buf,
+                                hipStream_t s);
+// C[l][rows[l*n + i]][:] = buf[l][i][:] (rows outside [0, K) skipped); r % 4 == 0.
+hipError_t launch_codebook_unpack(const float* buf, const int32_t* rows, int L, int K, int r, int n, float* C,
+                                  hipStream_t s);
+
 // ---------------------------------------------------------------- debug
 // flag[0] = 1 if any ids[t] is outside [0, V).
 hipError_t launch_check_ids(const int32_t* ids, int T, int64_t V, int* flag, hipStream_t s);

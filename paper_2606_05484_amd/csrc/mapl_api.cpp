@@ -912,6 +912,45 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   return MAPL_OK;
 }
 
+// ------------------------------------------------------ codebook synchronisation
+namespace {
+int check_sync(int32_t L, int32_t K, int64_t r, int32_t n) {
+  if (L < 1 || L > 8) return fail(MAPL_E_SHAPE, "codebook sync: need 1 <= L <= 8 (got %d)", L);
+  if (K < 1 || K > 65536) return fail(MAPL_E_SHAPE, "codebook sync: need 1 <= K <= 65536 (got %d)", K);
+  if (r < 4 || r > 1024 || r % 4) return fail(MAPL_E_SHAPE, "codebook sync: need 4 <= r <= 1024, r %% 4 == 0");
+  if (n < 0 || n > K) return fail(MAPL_E_SHAPE, "codebook sync: need 0 <= n <= K (got n=%d)", n);
+  return MAPL_OK;
+}
+}  // namespace
+
+extern "C" int mapl_codebook_pack(int32_t L, int32_t K, int64_t r, const float* C, const int32_t* rows, int32_t n,
+                                  float* buf, void* stream) {
+  g_err.clear();
+  int st = check_sync(L, K, r, n);
+  if (st) return st;
+  const size_t cb = (size_t)L * K * r * 4, bb = (size_t)L * n * r * 4, rb = (size_t)L * n * 4;
+  st = check_ptrs({{C, cb, "C"}, {rows, rb, "rows"}, {buf, bb, "buf"}}, {{buf, bb, "buf"}},
+                  {{C, cb, "C"}, {rows, rb, "rows"}});
+  if (st) return st;
+  hipStream_t s = (hipStream_t)stream;
+  LAUNCH("sync:pack", launch_codebook_pack(C, rows, L, K, (int)r, n, buf, s));
+  return MAPL_OK;
+}
+
+extern "C" int mapl_codebook_unpack(int32_t L, int32_t K, int64_t r, const float* buf, const int32_t* rows,
+                                    int32_t n, float* C, void* stream) {
+  g_err.clear();
+  int st = check_sync(L, K, r, n);
+  if (st) return st;
+  const size_t cb = (size_t)L * K * r * 4, bb = (size_t)L * n * r * 4, rb = (size_t)L * n * 4;
+  st = check_ptrs({{C, cb, "C"}, {rows, rb, "rows"}, {buf, bb, "buf"}}, {{C, cb, "C"}},
+                  {{buf, bb, "buf"}, {rows, rb, "rows"}});
+  if (st) return st;
+  hipStream_t s = (hipStream_t)stream;
+  LAUNCH("sync:unpack", launch_codebook_unpack(buf, rows, L, K, (int)r, n, C, s));
+  return MAPL_OK;
+}
+
 // ------------------------------------------------------ allocation-free encode
 // Scratch of mapl_encode_noalloc: a file-scope device array, one copy per GPU
 // the library runs on, held until the process ends.  In host code the name

@@ -41,6 +41,8 @@ _P = ctypes.c_void_p
 _SIG = {
     "mapl_encode": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [_P, ctypes.c_size_t, _P],
     "mapl_encode_noalloc": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [_P],
+    "mapl_codebook_pack": [ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, _P, _P, ctypes.c_int32, _P, _P],
+    "mapl_codebook_unpack": [ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, _P, _P, ctypes.c_int32, _P, _P],
     "mapl_decode": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [_P, ctypes.c_size_t, _P],
     "mapl_decode_bwd": [ctypes.POINTER(CodecDesc)] + [_P] * 9 + [ctypes.c_int, _P, ctypes.c_size_t, _P],
     "mapl_encode_bwd": [ctypes.POINTER(CodecDesc)] + [_P] * 8 + [ctypes.c_int, _P, ctypes.c_size_t, _P],
@@ -165,6 +167,16 @@ def stiefel_step(P, d, r, U, G, M, lr, beta, lmo_steps, retract_steps, ws, ws_by
     wb = ws_bytes if ws_bytes is not None else (ws.numel() if ws is not None else 0)
     _check(lib().mapl_stiefel_step(P, d, r, _ptr(U), _ptr(G), _ptr(M), lr, beta, lmo_steps, retract_steps,
                                    _ptr(ws), wb, _stream(stream)))
+
+
+def codebook_pack(L, K, r, C, rows, n, buf, stream=None):
+    """Sender side of the streaming codebook sync: buf[l, i] = C[l, rows[l, i]]."""
+    _check(lib().mapl_codebook_pack(L, K, r, _ptr(C), _ptr(rows), n, _ptr(buf), _stream(stream)))
+
+
+def codebook_unpack(L, K, r, buf, rows, n, C, stream=None):
+    """Receiver side: C[l, rows[l, i]] = buf[l, i]."""
+    _check(lib().mapl_codebook_unpack(L, K, r, _ptr(buf), _ptr(rows), n, _ptr(C), _stream(stream)))
 
 
 def profile(enable):
