@@ -146,6 +146,35 @@ int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, const void* 
                     const float* C, void* dZ, float* dU, int accumulate_dU, void* ws,
                     size_t ws_bytes, void* stream);
 
+/* mapl_decode_bwd with the returned gradient quantised (Sec. 3.5: the
+ * multi-codebook quantiser compresses "both forward activations and
+ * backward gradients").  Instead of writing dZ it residual-vector-quantises
+ * the r-dim gradient with its own codebooks:
+ *   dZ0 = dXhat U  (fp32 accumulation, not rounded; bf16 U~ on the bf16 path)
+ *   gcodes[t,l] = argmin_j ||R_l[t] - Cg[l,j]||^2, R_0 = dZ0,
+ *                 R_{l+1} = R_l - Cg[l, gcodes[t,l]]   (as mapl_encode)
+ *   dU (+)= exactly as mapl_decode_bwd.
+ * Cg [Lg,Kg,r] fp32; gcodes [T,Lg] of gcode_dtype (MAPL_U8 for Kg <= 256,
+ * MAPL_U16 otherwise).  1 <= Lg <= 8, 32 <= Kg <= 65536, Kg % 32 == 0; the
+ * bf16 path needs r in {64, 128, 256}.  Workspace:
+ * mapl_decode_bwd_q_workspace_bytes(desc, Lg, Kg).  The sending side turns
+ * gcodes back into the gradient with mapl_grad_dequantize and passes it to
+ * mapl_encode_bwd. */
+int mapl_decode_bwd_q(const mapl_codec_desc* desc, const void* dXhat, const void* payload,
+                      const int32_t* ids, const float* U, const void* A_r, const void* B_r,
+                      const float* C, int32_t Lg, int32_t Kg, int32_t gcode_dtype, const float* Cg,
+                      void* gcodes, float* dU, int accumulate_dU, void* ws, size_t ws_bytes,
+                      void* stream);
+size_t mapl_decode_bwd_q_workspace_bytes(const mapl_codec_desc* desc, int32_t Lg, int32_t Kg);
+
+/* The quantised gradient's reconstruction (progressive refinement of
+ * Sec. 3.5): dZ[t] = sum_l Cg[l, gcodes[t,l]], summed in fp32 and written as
+ * out_dtype (MAPL_BF16, round-to-nearest-even, or MAPL_F32) [T,r].
+ * 32 <= r <= 1024, r % 32 == 0; codes >= Kg are a caller error. */
+int mapl_grad_dequantize(int64_t T, int64_t r, int32_t Lg, int32_t Kg, int32_t gcode_dtype,
+                         const void* gcodes, const float* Cg, int32_t out_dtype, void* dZ,
+                         void* stream);
+
 /* Backward of Eq. 1; the quantiser is passed straight through (the gradient
  * of the codes' reconstruction is taken as the gradient of Z0).
  *   dX = dZ U^T                                    [T,d] of x_dtype

@@ -195,3 +195,20 @@ def encode_bwd(dZ, X, ids, U, A_s, B_s, anchor_space=AMBIENT, operand="exact"):
     if anchor_space == AMBIENT and A_s is not None and np.asarray(A_s).shape[1] > 0:
         Xr = X - anchor(A_s, ids) @ np.asarray(B_s, dtype=np.float64)
     return dX, Xr.T @ dZ
+
+
+def grad_quantize(dXhat, U, Cg, operand="exact"):
+    """Quantisation of the backward message (Sec. 3.5: the multi-codebook
+    quantiser compresses the backward gradients as well as the forward
+    activations).  The r-dim gradient that travels back across the boundary,
+    dZhat = dXhat U (the backward of Eq. 2), is residual-vector-quantised
+    over its own codebooks Cg [Lg,Kg,r] exactly as the activations are.
+    Returns (codes, gap, resid_sq) as rvq_encode."""
+    dZ0 = np.asarray(dXhat, dtype=np.float64) @ _projector(U, operand)
+    return rvq_encode(dZ0, Cg)
+
+
+def grad_dequantize(codes, Cg):
+    """The sending stage's reconstruction of the quantised gradient:
+    progressive refinement, sum_l Cg_l[codes[:, l]]."""
+    return rvq_decode(codes, Cg)

@@ -153,7 +153,15 @@ struct Layout {
 };
 
 
-Layout layout(const mapl_codec_desc& D, int call) {
+// Quantisation of the returned gradient (mapl_decode_bwd_q): its own RVQ
+// codebooks over the r-dim gradient.
+struct GradQ {
+  int L, K, code_bytes;
+  const float* C;
+  void* codes;
+};
+
+Layout layout(const mapl_codec_desc& D, int call, const GradQ* q = nullptr) {
   Layout Lo;
   Carve c;
   c.take(0);
@@ -185,6 +193,12 @@ Layout layout(const mapl_codec_desc& D, int call) {
         if (D.L > 0 || (!amb && k > 0)) Lo.ahat = c.take((size_t)T * r * 2);
         Lo.sp = plan_splits(T, (int)d, 0, (int)r);
         Lo.part = c.take((size_t)Lo.sp.splits * wgrad_row_offset((int)d) * r * 4);
+        if (q) {
+          if (!enc_rvq_fusable((int)r, q->L)) Lo.z0 = c.take((size_t)T * r * 4);
+          Lo.cb = c.take((size_t)q->L * q->K * rvq_cb_cols((int)r) * 2);
+          Lo.cn2 = c.take((size_t)rvq_meta_floats(q->L, q->K) * 4);
+          Lo.stats = c.take(32);
+        }
         break;
       case MAPL_CALL_ENCODE_BWD: {
         Lo.w2 = c.take((size_t)d * r * 2);
@@ -210,6 +224,7 @@ Layout layout(const mapl_codec_desc& D, int call) {
         if (k > 0) Lo.ga = c.take((size_t)T * k * 4);
         Lo.zh = c.take((size_t)T * r * 4);
         if (!amb && k > 0) Lo.z2 = c.take((size_t)T * r * 4);
+        if (q && call == MAPL_CALL_DECODE_BWD) Lo.z0 = c.take((size_t)T * r * 4);
         break;
       case MAPL_CALL_ENCODE_BWD:
         if (k > 0 && amb) {
@@ -567,10 +582,13 @@ extern "C" int mapl_decode(const mapl_codec_desc* desc, const void* payload, con
 }
 
 // ----------------------------------------------------------------- decode_bwd
-extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, const void* payload,
-                               const int32_t* ids, const float* U, const void* A_r, const void* B_r, const float* C,
-                               void* dZ, float* dU, int accumulate_dU, void* ws, size_t ws_bytes, void* stream) {
-  g_err.clear();
+namespace {
+// decode_bwd, and with q != null its gradient-quantising variant: the r-dim
+// gradient dXhat U is RVQ-encoded over q's codebooks into q->codes instead
+// of being written as dZ (dZ is then null).
+int decode_bwd_impl(const mapl_codec_desc* desc, const void* dXhat, const void* payload, const int32_t* ids,
+                    const float* U, const void* A_r, const void* B_r, const float* C, void* dZ, float* dU,
+                    int accumulate_dU, void* ws, size_t ws_bytes, void* stream, const GradQ* q) {
   int st = check_desc(desc);
   if (st) return st;
   const mapl_codec_desc& D = *desc;
@@ -582,19 +600,28 @@ extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, c
                    {ids, need_anchor ? (size_t)T * 4 : 0, "ids"}, {U, (size_t)d * r * 4, "U"},
                    {A_r, need_anchor ? (size_t)D.V * k * xe : 0, "A_r"},
                    {B_r, need_anchor ? (size_t)k * r * xe : 0, "B_r"},
-                   {C, D.L > 0 ? (size_t)D.L * D.K * r * 4 : 0, "C"}, {dZ, (size_t)T * r * xe, "dZ"},
+                   {C, D.L > 0 ? (size_t)D.L * D.K * r * 4 : 0, "C"}, {dZ, q ? 0 : (size_t)T * r * xe, "dZ"},
                    {dU, (size_t)d * r * 4, "dU"}},
-                  {{dZ, (size_t)T * r * xe, "dZ"}, {dU, (size_t)d * r * 4, "dU"}},
+                  {{dZ, q ? 0 : (size_t)T * r * xe, "dZ"}, {dU, (size_t)d * r * 4, "dU"}},
                   {{dXhat, (size_t)T * d * xe, "dXhat"}, {payload, payload_bytes(D), "payload"},
                    {ids, (size_t)T * 4, "ids"}, {U, (size_t)d * r * 4, "U"}, {A_r, (size_t)D.V * k * xe, "A_r"},
                    {B_r, (size_t)k * b_cols(D) * xe, "B_r"}, {C, (size_t)D.L * D.K * r * 4, "C"},
                    {ws, ws_bytes, "workspace"}});
   if (st) return st;
+  if (q) {
+    const size_t gb = (size_t)q->L * q->K * r * 4, cbn = (size_t)T * q->L * q->code_bytes;
+    st = check_ptrs({{q->C, gb, "Cg"}, {q->codes, cbn, "gcodes"}},
+                    {{q->codes, cbn, "gcodes"}},
+                    {{dXhat, (size_t)T * d * xe, "dXhat"}, {payload, payload_bytes(D), "payload"},
+                     {ids, (size_t)T * 4, "ids"}, {U, (size_t)d * r * 4, "U"}, {C, (size_t)D.L * D.K * r * 4, "C"},
+                     {q->C, gb, "Cg"}, {dU, (size_t)d * r * 4, "dU"}, {ws, ws_bytes, "workspace"}});
+    if (st) return st;
+  }
   if (dZ && dU) {
     const uintptr_t a0 = (uintptr_t)dZ, a1 = a0 + T * r * xe, b0 = (uintptr_t)dU, b1 = b0 + d * r * 4;
     if (a0 < b1 && b0 < a1) return fail(MAPL_E_ALIAS, "output dZ overlaps output dU");
   }
-  const Layout Lo = layout(D, MAPL_CALL_DECODE_BWD);
+  const Layout Lo = layout(D, MAPL_CALL_DECODE_BWD, q);
   if ((st = check_ws(ws, ws_bytes, Lo.total))) return st;
   hipStream_t s = (hipStream_t)stream;
   if (need_anchor && (st = run_id_check(ids, T, D.V, ws, Lo, s))) return st;
@@ -608,9 +635,12 @@ extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, c
     // one launch: Ut = U~^T and the second operand of dU (Zhat, plus the
     // coordinate anchor)
     bf16_t* Ut = at<bf16_t>(ws, Lo.w);
-    PrepJob jobs[2];
+    PrepJob jobs[3];
     int nj = 0;
     jobs[nj++] = prep_job_u(U, (int)d, (int)r, nullptr, 0, Ut, d);
+    bf16_t* Cbq = q ? at<bf16_t>(ws, Lo.cb) : nullptr;
+    float* metaq = q ? at<float>(ws, Lo.cn2) : nullptr;
+    if (q) jobs[nj++] = prep_job_codebook(q->C, q->L, q->K, (int)r, Cbq, metaq);
     const bf16_t* Q = (const bf16_t*)payload;
     if (D.L > 0 || need_anchor) {
       bf16_t* Ah = at<bf16_t>(ws, Lo.ahat);
@@ -627,8 +657,25 @@ extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, c
     g.A = (const bf16_t*)dXhat; g.lda = d; g.Ka = (int)d;
     g.W = Ut; g.ldw = d;
     g.M = (int)T; g.N = (int)r;
-    g.out = dZ; g.ldo = r; g.out_f32 = 0;
-    LAUNCH("dec_bwd:gemm_tn", launch_gemm_tn(g, s));
+    if (!q) {
+      g.out = dZ; g.ldo = r; g.out_f32 = 0;
+      LAUNCH("dec_bwd:gemm_tn", launch_gemm_tn(g, s));
+    } else {
+      // the gradient's RVQ, as the encoder's: fused with the GEMM at r = 256
+      RvqArgs a{};
+      a.Cb = Cbq; a.C = q->C; a.meta = metaq;
+      a.T = (int)T; a.r = (int)r; a.L = q->L; a.K = q->K;
+      a.codes = q->codes; a.code_bytes = q->code_bytes;
+      if (enc_rvq_fusable((int)r, q->L)) {
+        LAUNCH("dec_bwd_q:gemm_rvq", launch_enc_rvq(g, a, s));
+      } else {
+        float* Z0 = at<float>(ws, Lo.z0);
+        g.out = Z0; g.ldo = r; g.out_f32 = 1;
+        LAUNCH("dec_bwd_q:gemm_tn", launch_gemm_tn(g, s));
+        a.Z0 = Z0;
+        LAUNCH("dec_bwd_q:rvq", launch_rvq(a, s));
+      }
+    }
     WgradArgs w{};
     w.Pa = (const bf16_t*)dXhat; w.ldp = d; w.Ma = (int)d;
     w.Q = Q; w.ldq = r;
@@ -645,8 +692,11 @@ extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, c
     GemmF32Args g = gemm((int)T, (int)r, (int)d);
     g.A = dXhat; g.sAm = d; g.sAk = 1;
     g.B = U; g.sBk = r; g.sBn = 1;
-    g.C = dZ; g.sCm = r; g.sCn = 1;
+    g.C = q ? (void*)at<float>(ws, Lo.z0) : dZ; g.sCm = r; g.sCn = 1;
     LAUNCH("dec_bwd:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+    if (q)
+      LAUNCH("dec_bwd_q:rvq_f32", launch_rvq_f32(at<float>(ws, Lo.z0), q->C, (int)T, (int)r, q->L, q->K, q->codes,
+                                                 q->code_bytes, s));
   }
   const float* Zh = (const float*)payload;
   if (D.L > 0) {
@@ -673,6 +723,77 @@ extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, c
     if (accumulate_dU) { g.Cin = dU; g.sCinm = r; g.sCinn = 1; g.beta = 1.f; }
     g.C = dU; g.sCm = r; g.sCn = 1;
     LAUNCH("dec_bwd:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
+  }
+  return MAPL_OK;
+}
+}  // namespace
+
+extern "C" int mapl_decode_bwd(const mapl_codec_desc* desc, const void* dXhat, const void* payload,
+                               const int32_t* ids, const float* U, const void* A_r, const void* B_r, const float* C,
+                               void* dZ, float* dU, int accumulate_dU, void* ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  return decode_bwd_impl(desc, dXhat, payload, ids, U, A_r, B_r, C, dZ, dU, accumulate_dU, ws, ws_bytes, stream,
+                         nullptr);
+}
+
+namespace {
+int check_gradq(const mapl_codec_desc* desc, int32_t Lg, int32_t Kg, int32_t gcode_dtype) {
+  if (Lg < 1 || Lg > 8) return fail(MAPL_E_SHAPE, "gradient RVQ: need 1 <= Lg <= 8 (got %d)", Lg);
+  if (Kg < 32 || Kg > 65536 || Kg % 32) return fail(MAPL_E_SHAPE, "gradient RVQ: need 32 <= Kg <= 65536, Kg %% 32 == 0");
+  if (gcode_dtype == MAPL_U8) {
+    if (Kg > 256) return fail(MAPL_E_RANGE, "Kg=%d does not fit MAPL_U8 codes", Kg);
+  } else if (gcode_dtype != MAPL_U16) {
+    return fail(MAPL_E_DTYPE, "gcode_dtype must be MAPL_U8 or MAPL_U16 (got %d)", gcode_dtype);
+  }
+  if (desc && desc->x_dtype == MAPL_BF16 && desc->r != 64 && desc->r != 128 && desc->r != 256)
+    return fail(MAPL_E_UNSUPPORTED, "gradient RVQ on the bf16 path supports r in {64, 128, 256}");
+  return MAPL_OK;
+}
+}  // namespace
+
+extern "C" int mapl_decode_bwd_q(const mapl_codec_desc* desc, const void* dXhat, const void* payload,
+                                 const int32_t* ids, const float* U, const void* A_r, const void* B_r, const float* C,
+                                 int32_t Lg, int32_t Kg, int32_t gcode_dtype, const float* Cg, void* gcodes,
+                                 float* dU, int accumulate_dU, void* ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  int st = check_desc(desc);
+  if (st) return st;
+  if ((st = check_gradq(desc, Lg, Kg, gcode_dtype))) return st;
+  GradQ q{Lg, Kg, gcode_dtype == MAPL_U8 ? 1 : 2, Cg, gcodes};
+  return decode_bwd_impl(desc, dXhat, payload, ids, U, A_r, B_r, C, nullptr, dU, accumulate_dU, ws, ws_bytes,
+                         stream, &q);
+}
+
+extern "C" size_t mapl_decode_bwd_q_workspace_bytes(const mapl_codec_desc* desc, int32_t Lg, int32_t Kg) {
+  g_err.clear();
+  if (check_desc(desc) != MAPL_OK) return 0;
+  if (check_gradq(desc, Lg, Kg, Kg <= 256 ? MAPL_U8 : MAPL_U16) != MAPL_OK) return 0;
+  GradQ q{Lg, Kg, Kg <= 256 ? 1 : 2, nullptr, nullptr};
+  return layout(*desc, MAPL_CALL_DECODE_BWD, &q).total;
+}
+
+extern "C" int mapl_grad_dequantize(int64_t T, int64_t r, int32_t Lg, int32_t Kg, int32_t gcode_dtype,
+                                    const void* gcodes, const float* Cg, int32_t out_dtype, void* dZ, void* stream) {
+  g_err.clear();
+  int st = check_gradq(nullptr, Lg, Kg, gcode_dtype);
+  if (st) return st;
+  if (T < 0 || T >= ((int64_t)1 << 31)) return fail(MAPL_E_SHAPE, "T=%lld out of range", (long long)T);
+  if (r < 32 || r > 1024 || r % 32) return fail(MAPL_E_SHAPE, "r=%lld: need 32 <= r <= 1024, r %% 32 == 0", (long long)r);
+  if (out_dtype != MAPL_BF16 && out_dtype != MAPL_F32) return fail(MAPL_E_DTYPE, "out_dtype must be MAPL_BF16 or MAPL_F32");
+  const int cb = gcode_dtype == MAPL_U8 ? 1 : 2;
+  const size_t nc = (size_t)T * Lg * cb, ng = (size_t)Lg * Kg * r * 4, no = (size_t)T * r * esize(out_dtype);
+  st = check_ptrs({{gcodes, nc, "gcodes"}, {Cg, ng, "Cg"}, {dZ, no, "dZ"}}, {{dZ, no, "dZ"}},
+                  {{gcodes, nc, "gcodes"}, {Cg, ng, "Cg"}});
+  if (st) return st;
+  if (T == 0) return MAPL_OK;
+  hipStream_t s = (hipStream_t)stream;
+  if (out_dtype == MAPL_F32) {
+    LAUNCH("grad_dq:codes_sum_f32", launch_codes_sum_f32(gcodes, cb, Cg, (int)T, (int)r, Lg, Kg, (float*)dZ, s));
+  } else {
+    AssembleArgs a{};
+    a.codes = gcodes; a.code_bytes = cb; a.C = Cg; a.L = Lg; a.K = Kg;
+    a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = (bf16_t*)dZ;
+    LAUNCH("grad_dq:assemble", launch_assemble(a, s));
   }
   return MAPL_OK;
 }

@@ -46,6 +46,11 @@ _SIG = {
     "mapl_decode": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [_P, ctypes.c_size_t, _P],
     "mapl_decode_bwd": [ctypes.POINTER(CodecDesc)] + [_P] * 9 + [ctypes.c_int, _P, ctypes.c_size_t, _P],
     "mapl_encode_bwd": [ctypes.POINTER(CodecDesc)] + [_P] * 8 + [ctypes.c_int, _P, ctypes.c_size_t, _P],
+    "mapl_decode_bwd_q": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [ctypes.c_int32] * 3 + [_P] * 3 +
+                         [ctypes.c_int, _P, ctypes.c_size_t, _P],
+    "mapl_decode_bwd_q_workspace_bytes": [ctypes.POINTER(CodecDesc), ctypes.c_int32, ctypes.c_int32],
+    "mapl_grad_dequantize": [ctypes.c_int64, ctypes.c_int64] + [ctypes.c_int32] * 3 + [_P, _P, ctypes.c_int32,
+                                                                                        _P, _P],
     "mapl_stiefel_step": [ctypes.c_int64] * 3 + [_P] * 3 + [ctypes.c_float, ctypes.c_float, ctypes.c_int,
                                                             ctypes.c_int, _P, ctypes.c_size_t, _P],
     "mapl_workspace_bytes": [ctypes.POINTER(CodecDesc), ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
@@ -55,7 +60,8 @@ _SIG = {
     "mapl_profile": [ctypes.c_int],
     "mapl_profile_report": [ctypes.c_char_p, ctypes.c_size_t],
 }
-_RES = {"mapl_workspace_bytes": ctypes.c_size_t, "mapl_last_error": ctypes.c_char_p}
+_RES = {"mapl_workspace_bytes": ctypes.c_size_t, "mapl_decode_bwd_q_workspace_bytes": ctypes.c_size_t,
+        "mapl_last_error": ctypes.c_char_p}
 EXPORTS = tuple(_SIG)
 
 
@@ -155,6 +161,30 @@ def decode_bwd(D, dXhat, payload, ids, U, A_r, B_r, C, dZ, dU, accumulate_dU, ws
     _check(lib().mapl_decode_bwd(ctypes.byref(D), _ptr(dXhat), _ptr(payload), _ptr(ids), _ptr(U), _ptr(A_r),
                                  _ptr(B_r), _ptr(C), _ptr(dZ), _ptr(dU), int(accumulate_dU), _ptr(ws), wb,
                                  _stream(stream)))
+
+
+def decode_bwd_q(D, dXhat, payload, ids, U, A_r, B_r, C, Lg, Kg, Cg, gcodes, dU, accumulate_dU, ws,
+                 ws_bytes=None, stream=None, gcode_dtype=None):
+    """decode_bwd with the returned gradient RVQ-encoded into gcodes [T,Lg]."""
+    wb = ws_bytes if ws_bytes is not None else (ws.numel() if ws is not None else 0)
+    gdt = (U8 if Kg <= 256 else U16) if gcode_dtype is None else _DT.get(gcode_dtype, gcode_dtype)
+    _check(lib().mapl_decode_bwd_q(ctypes.byref(D), _ptr(dXhat), _ptr(payload), _ptr(ids), _ptr(U), _ptr(A_r),
+                                   _ptr(B_r), _ptr(C), Lg, Kg, gdt, _ptr(Cg), _ptr(gcodes), _ptr(dU),
+                                   int(accumulate_dU), _ptr(ws), wb, _stream(stream)))
+
+
+def decode_bwd_q_workspace_bytes(D, Lg, Kg):
+    n = lib().mapl_decode_bwd_q_workspace_bytes(ctypes.byref(D), Lg, Kg)
+    if n == 0 and last_error():
+        raise MaplError(-2, last_error())
+    return n
+
+
+def grad_dequantize(T, r, Lg, Kg, gcodes, Cg, dZ, out_dtype="bf16", stream=None, gcode_dtype=None):
+    """dZ[t] = sum_l Cg[l, gcodes[t, l]] as bf16 or fp32."""
+    gdt = (U8 if Kg <= 256 else U16) if gcode_dtype is None else _DT.get(gcode_dtype, gcode_dtype)
+    _check(lib().mapl_grad_dequantize(T, r, Lg, Kg, gdt, _ptr(gcodes), _ptr(Cg), _DT.get(out_dtype, out_dtype),
+                                      _ptr(dZ), _stream(stream)))
 
 
 def encode_bwd(D, dZ, X, ids, U, A_s, B_s, dX, dU, accumulate_dU, ws, ws_bytes=None, stream=None):

@@ -274,3 +274,20 @@ def oracle_payload(x, C=None):
         from oracle.precision import round_bf16
         return round_bf16(Z0)
     return ocodec.rvq_encode(Z0, Cn)[0]
+
+
+def grad_codebooks(x, Lg, Kg, seed):
+    """Gradient codebooks drawn like the stress codebooks, from the oracle's
+    own gradient rows dXhat U (codeword 0 = 0, the others residual rows plus
+    5 % noise), so every code is in use."""
+    rng = np.random.default_rng(seed)
+    R = f64(x, "dXhat") @ ocodec._projector(x["U"], operand(x))
+    T, r = R.shape
+    C = np.zeros((Lg, Kg, r), dtype=np.float32)
+    for l in range(Lg):
+        sig = np.sqrt(np.mean(R ** 2))
+        idx = rng.choice(T, Kg - 1, replace=False)
+        C[l, 1:] = (R[idx] + 0.05 * sig * rng.standard_normal((Kg - 1, r))).astype(np.float32)
+        codes, _, _ = ocodec.rvq_encode(R, C[l:l + 1].astype(np.float64))
+        R = R - C[l].astype(np.float64)[codes[:, 0]]
+    return C
