@@ -204,6 +204,32 @@ int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, const float* G,
                       float lr, float beta, int lmo_steps, int retract_steps, void* ws,
                       size_t ws_bytes, void* stream);
 
+/* Gradient of an anchor table (Sec. 3.2: E_small is trainable, Eq. 3; the
+ * sender's table enters Eq. 1, the receiver's Eq. 2).  Each token t gives a
+ * row g[t] of length k, and
+ *   dA[v] (+)= sum over the tokens t with ids[t] == v of g[t]      dA [V,k] fp32
+ * side = MAPL_SENDER (table A_s, dY = dZ [T,r], the gradient of Eq. 1's
+ * output; with RVQ it is the straight-through gradient):
+ *   g[t] = -dZ[t] (B_s U)^T   (ambient; on the bf16 path B_s U~ rounded to bf16
+ *                              as the encoder uses it)
+ *   g[t] = -dZ[t] B_s^T       (coord)
+ * side = MAPL_RECEIVER (table A_r):
+ *   g[t] = dXhat[t] B_r^T     (ambient, dY = dXhat [T,d])
+ *   g[t] = dZhat[t] B_r^T     (coord, dY = dZhat = dXhat U [T,r], e.g. the dZ
+ *                              output of mapl_decode_bwd)
+ * dY and B are of x_dtype; U is needed (fp32 [d,r]) only for the ambient
+ * sender.  The rows of one id are summed in a fixed order (tokens sorted
+ * stably by id, then in order), so repeated calls give identical bits;
+ * fp32 accumulation of fp32 rows.  accumulate = 0 overwrites all of dA
+ * (rows of absent ids become 0), 1 adds to it.  Requires k >= 1 and
+ * T <= 2^24; ids must lie in [0, V) (MAPL_DEBUG=1 checks them).
+ * Workspace: mapl_anchor_bwd_workspace_bytes(desc, side). */
+enum mapl_side { MAPL_SENDER = 0, MAPL_RECEIVER = 1 };
+int mapl_anchor_bwd(const mapl_codec_desc* desc, int side, const void* dY, const int32_t* ids,
+                    const float* U, const void* B, float* dA, int accumulate, void* ws,
+                    size_t ws_bytes, void* stream);
+size_t mapl_anchor_bwd_workspace_bytes(const mapl_codec_desc* desc, int side);
+
 /* Streaming codebook synchronisation (Sec. 3.5 "Codebook Synchronization",
  * App. F): instead of the whole codebook, each micro-batch carries a random
  * subset of its codewords (a 1/5 fraction per micro-batch in the paper's

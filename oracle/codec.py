@@ -212,3 +212,39 @@ def grad_dequantize(codes, Cg):
     """The sending stage's reconstruction of the quantised gradient:
     progressive refinement, sum_l Cg_l[codes[:, l]]."""
     return rvq_decode(codes, Cg)
+
+
+def anchor_grad(dY, ids, U, B, V, side="sender", anchor_space=AMBIENT, operand="exact"):
+    """Gradient of an anchor table E_small (trainable by Eq. 3), [V,k].
+
+    Every token t contributes a row g[t] to the table row ids[t]:
+      sender   (Eq. 1, dY = dZ, the gradient of the encoder's output):
+               g = -dZ (B U)^T  (ambient; B U rounded to bf16 when the
+               projector enters as bf16, as in project), g = -dZ B^T (coord)
+      receiver (Eq. 2): g = dXhat B^T (ambient, dY = dXhat),
+               g = dZhat B^T (coord, dY = dZhat = dXhat U)
+    and dA[v] = sum of g[t] over the tokens with ids[t] == v.
+    """
+    dY = np.asarray(dY, dtype=np.float64)
+    B = np.asarray(B, dtype=np.float64)
+    if side == "sender":
+        if anchor_space == AMBIENT:
+            Uo = _projector(U, operand)
+            BU = B @ Uo
+            if operand == "bf16":
+                BU = round_bf16(BU)
+            g = -dY @ BU.T
+        elif anchor_space == COORD:
+            g = -dY @ B.T
+        else:
+            raise ValueError(anchor_space)
+    elif side == "receiver":
+        g = dY @ B.T
+    else:
+        raise ValueError(side)
+    ids = np.asarray(ids)
+    if ids.size and (ids.min() < 0 or ids.max() >= V):
+        raise IndexError("token id out of range")
+    dA = np.zeros((V, B.shape[0]))
+    np.add.at(dA, ids, g)
+    return dA

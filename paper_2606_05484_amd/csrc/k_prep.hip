@@ -303,7 +303,11 @@ __device__ __forceinline__ void small_gemm_tile(int bx, int by, const PrepJob& j
     for (int e = 0; e < 4; ++e) {
       const int row = 4 * quad + e, col = lane & 15;
       const float v = ((acc[e] + part[0][row * 16 + col]) + part[1][row * 16 + col]) + part[2][row * 16 + col];
-      if (i0 + row < j.M) j.dst[(int64_t)(c0 + col) * j.ldd + j.off + i0 + row] = (bf16_t)f2bf(j.scale * v);
+      if (i0 + row < j.M) {
+        const int64_t o = j.dst_rows ? (int64_t)(i0 + row) * j.ldd + j.off + c0 + col
+                                     : (int64_t)(c0 + col) * j.ldd + j.off + i0 + row;
+        j.dst[o] = (bf16_t)f2bf(j.scale * v);
+      }
     }
   }
 }

@@ -123,9 +123,10 @@ struct PrepJob {
   AssembleArgs asm_args;
   // PJ_GATHER
   const bf16_t* A; int k; const int32_t* ids; int V, T; bf16_t* out;
-  // PJ_SMALL_GEMM: dst[c*ldd + off + i] = bf16(scale * sum_j P[i][j] bf16(Q(j, c))),
+  // PJ_SMALL_GEMM: dst[c*ldd + off + i] (dst_rows = 0) or dst[i*ldd + off + c]
+  // (dst_rows = 1) = bf16(scale * sum_j P[i][j] bf16(Q(j, c))),
   // Q(j, c) = Q[j*ldq + c] (qt = 0) or Q[c*ldq + j] (qt = 1)
-  const void* P; int64_t ldp; const float* Q; int64_t ldq; int qt, M, N, Kd;
+  const void* P; int64_t ldp; const float* Q; int64_t ldq; int qt, M, N, Kd, dst_rows;
 };
 constexpr int PREP_MAX_JOBS = 4;
 struct PrepBatch {
@@ -199,6 +200,26 @@ hipError_t launch_codebook_pack(const float* C, const int32_t* rows, int L, int 
 // C[l][rows[l*n + i]][:] = buf[l][i][:] (rows outside [0, K) skipped); r % 4 == 0.
 hipError_t launch_codebook_unpack(const float* buf, const int32_t* rows, int L, int K, int r, int n, float* C,
                                   hipStream_t s);
+
+// ---------------------------------------------------------------- anchor-table gradient
+// W[i][c] = B[i][c] (i < k), 0 for k <= i < kp; c < K; both row-major with K columns.
+hipError_t launch_pad_rows_bf16(const bf16_t* B, int k, int K, int kp, bf16_t* W, hipStream_t s);
+// Stable radix sort of (ids[i], i) by id over `passes` 8-bit digits; buffers of
+// n int32 each (k0/v0, k1/v1 ping-pong) and hist of 256 * radix_tiles(n) ints;
+// *skey / *sval receive the sorted ids and token indices.
+int radix_tiles(int n);
+hipError_t launch_sort_ids(const int32_t* ids, int n, int passes, int* hist, int32_t* k0, int32_t* v0, int32_t* k1,
+                           int32_t* v1, const int32_t** skey, const int32_t** sval, hipStream_t s);
+// dA[v] (+)= scale * sum of g[t] over the tokens t of id v, in sorted order
+// (sub-chunks of 64 positions, then their boundary pieces in order).
+struct AnchorSegArgs {
+  const float* g; int64_t ldg; int k;
+  const int32_t* skey; const int32_t* sval; int n;
+  float* dA; int V; int accumulate; float scale;  // rows of ids outside [0, V) are skipped
+  float* headp; float* tailp; int32_t* head_id; int32_t* head_thru; int32_t* tail_id; int nsub;
+};
+int anchor_sub_chunks(int n);
+hipError_t launch_anchor_segsum(const AnchorSegArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- debug
 // flag[0] = 1 if any ids[t] is outside [0, V).

@@ -1033,6 +1033,141 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   return MAPL_OK;
 }
 
+// ------------------------------------------------------ anchor-table gradient
+namespace {
+struct AnchorLayout {
+  size_t total = 0, w = 0, bu = 0, g = 0, k0 = 0, v0 = 0, k1 = 0, v1 = 0, hist = 0, headp = 0, tailp = 0, hid = 0,
+         hthru = 0, tid = 0;
+  int kp = 0, K = 0, passes = 1, nsub = 0;
+};
+
+constexpr int64_t kAnchorMaxT = (int64_t)1 << 24;
+
+int check_anchor_bwd(const mapl_codec_desc* desc, int side) {
+  int st = check_desc(desc);
+  if (st) return st;
+  if (side != MAPL_SENDER && side != MAPL_RECEIVER) return fail(MAPL_E_SHAPE, "side must be MAPL_SENDER or MAPL_RECEIVER");
+  if (desc->k < 1) return fail(MAPL_E_SHAPE, "anchor gradient needs k >= 1");
+  if (desc->T > kAnchorMaxT) return fail(MAPL_E_SHAPE, "anchor gradient: T=%lld above 2^24", (long long)desc->T);
+  return MAPL_OK;
+}
+
+AnchorLayout anchor_layout(const mapl_codec_desc& D, int side) {
+  AnchorLayout Lo;
+  Carve c;
+  const bool amb = D.anchor_space == MAPL_ANCHOR_AMBIENT;
+  const int64_t T = D.T;
+  Lo.K = (int)((side == MAPL_RECEIVER && amb) ? D.d : D.r);  // width of the incoming gradient
+  Lo.kp = (int)rup(D.k, 64);
+  if (D.x_dtype == MAPL_BF16) Lo.w = c.take((size_t)Lo.kp * Lo.K * 2);
+  else if (side == MAPL_SENDER && amb) Lo.bu = c.take((size_t)D.k * D.r * 4);
+  Lo.g = c.take((size_t)T * Lo.kp * 4);
+  Lo.k0 = c.take((size_t)T * 4);
+  Lo.v0 = c.take((size_t)T * 4);
+  Lo.k1 = c.take((size_t)T * 4);
+  Lo.v1 = c.take((size_t)T * 4);
+  Lo.hist = c.take((size_t)256 * radix_tiles((int)T) * 4);
+  Lo.nsub = anchor_sub_chunks((int)T);
+  Lo.headp = c.take((size_t)Lo.nsub * D.k * 4);
+  Lo.tailp = c.take((size_t)Lo.nsub * D.k * 4);
+  Lo.hid = c.take((size_t)Lo.nsub * 4);
+  Lo.hthru = c.take((size_t)Lo.nsub * 4);
+  Lo.tid = c.take((size_t)Lo.nsub * 4);
+  int bits = 0;
+  for (int64_t v = D.V - 1; v > 0; v >>= 1) ++bits;
+  Lo.passes = bits > 8 ? (bits + 7) / 8 : 1;
+  Lo.total = c.off;
+  return Lo;
+}
+}  // namespace
+
+extern "C" size_t mapl_anchor_bwd_workspace_bytes(const mapl_codec_desc* desc, int side) {
+  g_err.clear();
+  if (check_anchor_bwd(desc, side) != MAPL_OK) return 0;
+  return anchor_layout(*desc, side).total;
+}
+
+extern "C" int mapl_anchor_bwd(const mapl_codec_desc* desc, int side, const void* dY, const int32_t* ids,
+                               const float* U, const void* B, float* dA, int accumulate, void* ws, size_t ws_bytes,
+                               void* stream) {
+  g_err.clear();
+  int st = check_anchor_bwd(desc, side);
+  if (st) return st;
+  const mapl_codec_desc& D = *desc;
+  const int64_t T = D.T, d = D.d, r = D.r, k = D.k;
+  const size_t xe = esize(D.x_dtype);
+  const bool amb = D.anchor_space == MAPL_ANCHOR_AMBIENT;
+  const bool need_u = side == MAPL_SENDER && amb;
+  const AnchorLayout Lo = anchor_layout(D, side);
+  const size_t ny = (size_t)T * Lo.K * xe, na = (size_t)D.V * k * 4;
+  st = check_ptrs({{dY, ny, "dY"}, {ids, (size_t)T * 4, "ids"}, {U, need_u ? (size_t)d * r * 4 : 0, "U"},
+                   {B, (size_t)k * b_cols(D) * xe, "B"}, {dA, na, "dA"}},
+                  {{dA, na, "dA"}},
+                  {{dY, ny, "dY"}, {ids, (size_t)T * 4, "ids"}, {U, need_u ? (size_t)d * r * 4 : 0, "U"},
+                   {B, (size_t)k * b_cols(D) * xe, "B"}, {ws, ws_bytes, "workspace"}});
+  if (st) return st;
+  if ((st = check_ws(ws, ws_bytes, Lo.total))) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (!accumulate) LAUNCH("anchor_bwd:zero", launch_zero_bytes(dA, (int64_t)na, s));
+  if (T == 0) return MAPL_OK;
+  if (debug_ids()) {
+    Layout tmp;
+    tmp.flag = Lo.hid;  // the head-id slots are written later in the call
+    if ((st = run_id_check(ids, T, D.V, ws, tmp, s))) return st;
+  }
+  float* g = at<float>(ws, Lo.g);
+  // 1. per-token gradient rows g[t] (the sign of the sender's term is applied
+  //    in the reduction): sender  dZ (B_s U)^T (ambient) or dZ B_s^T (coord),
+  //    receiver dXhat B_r^T (ambient) or dZhat B_r^T (coord)
+  if (D.x_dtype == MAPL_BF16) {
+    bf16_t* W = at<bf16_t>(ws, Lo.w);
+    if (need_u) {
+      if (Lo.kp > k) LAUNCH("anchor_bwd:zero_w", launch_zero_bytes(W + k * r, (int64_t)(Lo.kp - k) * r * 2, s));
+      PrepJob j = prep_job_small_gemm((const bf16_t*)B, d, U, r, 0, (int)k, (int)r, (int)d, 1.f, W, r, 0);
+      j.dst_rows = 1;
+      LAUNCH("anchor_bwd:prep", launch_prep_batch(&j, 1, s));
+    } else {
+      LAUNCH("anchor_bwd:prep", launch_pad_rows_bf16((const bf16_t*)B, (int)k, Lo.K, Lo.kp, W, s));
+    }
+    TnArgs gg{};
+    gg.A = (const bf16_t*)dY; gg.lda = Lo.K; gg.Ka = Lo.K;
+    gg.W = W; gg.ldw = Lo.K;
+    gg.M = (int)T; gg.N = Lo.kp;
+    gg.out = g; gg.ldo = Lo.kp; gg.out_f32 = 1;
+    LAUNCH("anchor_bwd:gemm_tn", launch_gemm_tn(gg, s));
+  } else {
+    const float* Bk = (const float*)B;  // [k, K]
+    if (need_u) {
+      float* BU = at<float>(ws, Lo.bu);
+      GemmF32Args e = gemm((int)k, (int)r, (int)d);
+      e.A = B; e.sAm = d; e.sAk = 1;
+      e.B = U; e.sBk = r; e.sBn = 1;
+      e.C = BU; e.sCm = r; e.sCn = 1;
+      LAUNCH("anchor_bwd:gemm_f32", launch_gemm_f32(e, 0, 0, 0, s));
+      Bk = BU;
+    }
+    GemmF32Args e = gemm((int)T, (int)k, Lo.K);
+    e.A = dY; e.sAm = Lo.K; e.sAk = 1;
+    e.B = Bk; e.sBk = 1; e.sBn = Lo.K;
+    e.C = g; e.sCm = Lo.kp; e.sCn = 1;
+    LAUNCH("anchor_bwd:gemm_f32", launch_gemm_f32(e, 0, 0, 0, s));
+  }
+  // 2. tokens sorted by id (stable), 3. per-id sums in sorted order
+  const int32_t *skey = nullptr, *sval = nullptr;
+  LAUNCH("anchor_bwd:sort", launch_sort_ids(ids, (int)T, Lo.passes, at<int>(ws, Lo.hist), at<int32_t>(ws, Lo.k0),
+                                            at<int32_t>(ws, Lo.v0), at<int32_t>(ws, Lo.k1), at<int32_t>(ws, Lo.v1),
+                                            &skey, &sval, s));
+  AnchorSegArgs a{};
+  a.g = g; a.ldg = Lo.kp; a.k = (int)k;
+  a.skey = skey; a.sval = sval; a.n = (int)T;
+  a.dA = dA; a.V = (int)D.V; a.accumulate = accumulate ? 1 : 0; a.scale = side == MAPL_SENDER ? -1.f : 1.f;
+  a.headp = at<float>(ws, Lo.headp); a.tailp = at<float>(ws, Lo.tailp);
+  a.head_id = at<int32_t>(ws, Lo.hid); a.head_thru = at<int32_t>(ws, Lo.hthru); a.tail_id = at<int32_t>(ws, Lo.tid);
+  a.nsub = Lo.nsub;
+  LAUNCH("anchor_bwd:segsum", launch_anchor_segsum(a, s));
+  return MAPL_OK;
+}
+
 // ------------------------------------------------------ codebook synchronisation
 namespace {
 int check_sync(int32_t L, int32_t K, int64_t r, int32_t n) {

@@ -19,6 +19,7 @@ STATUS = {0: "MAPL_OK", -1: "MAPL_E_NULL", -2: "MAPL_E_SHAPE", -3: "MAPL_E_DTYPE
 F32, BF16, U8, U16 = 0, 1, 2, 3
 AMBIENT, COORD = 0, 1
 CALL_ENCODE, CALL_DECODE, CALL_DECODE_BWD, CALL_ENCODE_BWD, CALL_STIEFEL = range(5)
+SENDER, RECEIVER = 0, 1
 _DT = {"f32": F32, "bf16": BF16, "u8": U8, "u16": U16}
 _SPACE = {"ambient": AMBIENT, "coord": COORD}
 
@@ -49,6 +50,9 @@ _SIG = {
     "mapl_decode_bwd_q": [ctypes.POINTER(CodecDesc)] + [_P] * 7 + [ctypes.c_int32] * 3 + [_P] * 3 +
                          [ctypes.c_int, _P, ctypes.c_size_t, _P],
     "mapl_decode_bwd_q_workspace_bytes": [ctypes.POINTER(CodecDesc), ctypes.c_int32, ctypes.c_int32],
+    "mapl_anchor_bwd": [ctypes.POINTER(CodecDesc), ctypes.c_int] + [_P] * 5 + [ctypes.c_int, _P, ctypes.c_size_t,
+                                                                              _P],
+    "mapl_anchor_bwd_workspace_bytes": [ctypes.POINTER(CodecDesc), ctypes.c_int],
     "mapl_grad_dequantize": [ctypes.c_int64, ctypes.c_int64] + [ctypes.c_int32] * 3 + [_P, _P, ctypes.c_int32,
                                                                                         _P, _P],
     "mapl_stiefel_step": [ctypes.c_int64] * 3 + [_P] * 3 + [ctypes.c_float, ctypes.c_float, ctypes.c_int,
@@ -61,6 +65,7 @@ _SIG = {
     "mapl_profile_report": [ctypes.c_char_p, ctypes.c_size_t],
 }
 _RES = {"mapl_workspace_bytes": ctypes.c_size_t, "mapl_decode_bwd_q_workspace_bytes": ctypes.c_size_t,
+        "mapl_anchor_bwd_workspace_bytes": ctypes.c_size_t,
         "mapl_last_error": ctypes.c_char_p}
 EXPORTS = tuple(_SIG)
 
@@ -175,6 +180,20 @@ def decode_bwd_q(D, dXhat, payload, ids, U, A_r, B_r, C, Lg, Kg, Cg, gcodes, dU,
 
 def decode_bwd_q_workspace_bytes(D, Lg, Kg):
     n = lib().mapl_decode_bwd_q_workspace_bytes(ctypes.byref(D), Lg, Kg)
+    if n == 0 and last_error():
+        raise MaplError(-2, last_error())
+    return n
+
+
+def anchor_bwd(D, side, dY, ids, U, B, dA, accumulate, ws, ws_bytes=None, stream=None):
+    """Gradient of the sender's (side 0) or receiver's (side 1) anchor table."""
+    wb = ws_bytes if ws_bytes is not None else (ws.numel() if ws is not None else 0)
+    _check(lib().mapl_anchor_bwd(ctypes.byref(D), int(side), _ptr(dY), _ptr(ids), _ptr(U), _ptr(B), _ptr(dA),
+                                 int(accumulate), _ptr(ws), wb, _stream(stream)))
+
+
+def anchor_bwd_workspace_bytes(D, side):
+    n = lib().mapl_anchor_bwd_workspace_bytes(ctypes.byref(D), int(side))
     if n == 0 and last_error():
         raise MaplError(-2, last_error())
     return n
