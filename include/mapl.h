@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define MAPL_VERSION 1
+#define MAPL_VERSION 2
 
 enum mapl_status {
   MAPL_OK = 0,
@@ -100,6 +100,12 @@ enum mapl_call {
  *   x_dtype   MAPL_BF16 or MAPL_F32: X, Z, Xhat, dXhat, dZ, dX
  *   ab_dtype  element type of A and B; must equal x_dtype
  *   code_dtype MAPL_U8 (K <= 256) or MAPL_U16 (K <= 65536); ignored if L == 0
+ *   group_dim 0: whole r-dimensional codewords; 2: the coordinates split into
+ *      r/2 groups of two, each quantised on its own over the same two columns
+ *      of every codebook round (Sec. 3.5 "decomposed into G groups"; App. E:
+ *      group dimension 2, K = 256, R = 2).  Grouped codes are u8 [T, L, r/2]
+ *      (codes[(t*L + l)*(r/2) + g]); needs L >= 1, K <= 256, MAPL_U8, and
+ *      both element types are supported at any r above.
  *   On the bf16 path U is rounded to bf16 (round-to-nearest-even) where it
  *   enters the matrix units; accumulation is fp32.  On the fp32 path every
  *   operand stays fp32.
@@ -109,6 +115,7 @@ typedef struct mapl_codec_desc {
   int32_t anchor_space;
   int32_t L, K;
   int32_t x_dtype, ab_dtype, code_dtype;
+  int32_t group_dim;
 } mapl_codec_desc;
 
 /* Sender side, Eq. 1 (Alg. 1, "Project") followed by RVQ (Sec. 3.5).
@@ -120,13 +127,16 @@ typedef struct mapl_codec_desc {
  *           of code_dtype.  Distances are decided in fp32 from Z0 computed
  *           with fp32 accumulation (bf16 matrix-unit screening, then exact
  *           fp32 rescoring of every codeword that could be nearest).
+ *           group_dim 2: the same per group of two coordinates, codes
+ *           [T, L, r/2] u8, exact fp32 distances.
  *   C may be NULL when L == 0.  A_s/B_s may be NULL when k == 0. */
 int mapl_encode(const mapl_codec_desc* desc, const void* X, const int32_t* ids,
                 const float* U, const void* A_s, const void* B_s, const float* C,
                 void* payload, void* ws, size_t ws_bytes, void* stream);
 
 /* Receiver side, Eq. 2 (Alg. 1, "Reconstruct").
- *   Zhat = payload (L == 0) or sum_l C[l, codes[t,l]] (L > 0)
+ *   Zhat = payload (L == 0) or sum_l C[l, codes[t,l]] (L > 0; group_dim 2:
+ *          Zhat[t, 2g:2g+2] = sum_l C[l, codes[t,l,g], 2g:2g+2])
  *   Xhat[t] = Zhat[t] U^T + A_r[ids[t]] B_r       (ambient)
  *   Xhat[t] = (Zhat[t] + A_r[ids[t]] B_r) U^T     (coord)
  *   Xhat is [T,d] of x_dtype.  Codes >= K are a caller error. */

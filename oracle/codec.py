@@ -129,22 +129,30 @@ def rvq_decode(codes, C):
     return Zh
 
 
-def encode(X, ids, U, A_s, B_s, C=None, anchor_space=AMBIENT, operand="exact", direct=False):
+def encode(X, ids, U, A_s, B_s, C=None, anchor_space=AMBIENT, operand="exact", direct=False, group_dim=0):
     """Sender side of Alg. 1: Eq. 1, then RVQ if codebooks are given.
 
     Returns Z0 [T,r] when C is None or has no rounds, else
-    (codes, gap, resid_sq) from rvq_encode.
+    (codes, gap, resid_sq) from rvq_encode (group_dim 0: whole vectors) or
+    grouped_rvq_encode.
     """
     Z0 = project(X, ids, U, A_s, B_s, anchor_space, operand)
     if C is None or np.asarray(C).shape[0] == 0:
         return Z0
+    if group_dim:
+        return grouped_rvq_encode(Z0, C, group_dim)
     return rvq_encode(Z0, C, direct=direct)
 
 
 def coords(payload, C=None):
-    """The receiver's coordinates Zhat: the payload itself, or the RVQ sum."""
+    """The receiver's coordinates Zhat: the payload itself, or the RVQ sum
+    (whole-vector codes [T,L], or grouped codes [T,L,G] whose group size is
+    r / G)."""
     if C is None or np.asarray(C).shape[0] == 0:
         return np.asarray(payload, dtype=np.float64)
+    payload = np.asarray(payload)
+    if payload.ndim == 3:
+        return grouped_rvq_decode(payload, C, np.asarray(C).shape[2] // payload.shape[2])
     return rvq_decode(payload, C)
 
 
@@ -248,3 +256,48 @@ def anchor_grad(dY, ids, U, B, V, side="sender", anchor_space=AMBIENT, operand="
     dA = np.zeros((V, B.shape[0]))
     np.add.at(dA, ids, g)
     return dA
+
+
+def grouped_rvq_encode(Z0, C, group_dim):
+    """Residual vector quantisation with the coordinates decomposed into
+    groups (Sec. 3.5; App. E: group dimension 2).  The r coordinates split
+    into r / group_dim groups of group_dim consecutive coordinates; group i
+    is quantised on its own, over the same group_dim columns of every
+    codebook (the per-stage codebook C_p in R^{r x K} read as r / group_dim
+    stacked codebooks of K group_dim-dimensional codewords), round after
+    round as rvq_encode does for whole vectors.
+
+    The near-tie measure of a group's round is its top-2 gap relative to the
+    group's unquantised energy ||Z0_g||^2 (not to the round's own residual):
+    two-coordinate groups shrink their residual by orders of magnitude per
+    round, so late rounds decide on residuals whose size approaches the
+    rounding of Z0 itself, and a gap is only meaningful against the scale at
+    which Z0 was computed.
+
+    Returns (codes [T,L,G], gap [T,L,G], resid_sq [T,L+1,G])."""
+    Z0 = np.asarray(Z0, dtype=np.float64)
+    C = np.asarray(C, dtype=np.float64)
+    T, r = Z0.shape
+    L = C.shape[0]
+    G = r // group_dim
+    codes = np.zeros((T, L, G), dtype=np.int64)
+    gap = np.zeros((T, L, G))
+    resid_sq = np.zeros((T, L + 1, G))
+    for g in range(G):
+        cols = slice(g * group_dim, (g + 1) * group_dim)
+        codes[:, :, g], gap[:, :, g], resid_sq[:, :, g] = rvq_encode(Z0[:, cols], C[:, :, cols])
+    # rvq_encode's gap is relative to each round's residual; rescale to ||Z0_g||^2
+    gap = gap * resid_sq[:, :L, :] / np.maximum(resid_sq[:, :1, :], 1e-300)
+    return codes, gap, resid_sq
+
+
+def grouped_rvq_decode(codes, C, group_dim):
+    """Zhat[:, group g] = sum_l C_l[codes[:, l, g], group g's columns]."""
+    C = np.asarray(C, dtype=np.float64)
+    codes = np.asarray(codes)
+    T, L, G = codes.shape
+    Zh = np.zeros((T, C.shape[2]))
+    for g in range(G):
+        cols = slice(g * group_dim, (g + 1) * group_dim)
+        Zh[:, cols] = rvq_decode(codes[:, :, g], C[:, :, cols])
+    return Zh

@@ -20,7 +20,7 @@ LIB = os.path.join(HERE, "libmapl.so")
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["k_gemm_bf16.hip", "k_gemm_f32.hip", "k_wgrad.hip", "k_rvq.hip", "k_prep.hip", "k_misc.hip",
-           "k_anchor.hip", "mapl_api.cpp"]
+           "k_anchor.hip", "k_grvq.hip", "mapl_api.cpp"]
 FLAGS = ["--offload-arch=%s" % ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include")]

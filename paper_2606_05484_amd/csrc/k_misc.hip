@@ -59,15 +59,17 @@ __global__ void k_rvq_f32(const float* __restrict__ Z0, const float* __restrict_
   }
 }
 
+// gdim 2: grouped codes [T, L, r/2] (u8), column c takes group c / 2's code.
 __global__ void k_codes_sum_f32(const void* __restrict__ codes, int code_bytes, const float* __restrict__ C,
-                                int T, int r, int L, int K, float* __restrict__ Zhat) {
+                                int T, int r, int L, int K, int gdim, float* __restrict__ Zhat) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= (int64_t)T * r) return;
   const int t = (int)(i / r), c = (int)(i % r);
   float v = 0.f;
   for (int l = 0; l < L; ++l) {
-    int code = code_bytes == 1 ? ((const uint8_t*)codes)[(int64_t)t * L + l]
-                               : ((const uint16_t*)codes)[(int64_t)t * L + l];
+    int code = gdim == 2 ? ((const uint8_t*)codes)[((int64_t)t * L + l) * (r / 2) + c / 2]
+               : code_bytes == 1 ? ((const uint8_t*)codes)[(int64_t)t * L + l]
+                                 : ((const uint16_t*)codes)[(int64_t)t * L + l];
     code = code < K ? code : K - 1;
     v += C[((int64_t)l * K + code) * r + c];
   }
@@ -233,11 +235,11 @@ hipError_t launch_rvq_f32(const float* Z0, const float* C, int T, int r, int L, 
 }
 
 hipError_t launch_codes_sum_f32(const void* codes, int code_bytes, const float* C, int T, int r, int L, int K,
-                                float* Zhat, hipStream_t s) {
+                                float* Zhat, hipStream_t s, int gdim) {
   const int64_t n = (int64_t)T * r;
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_codes_sum_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, codes, code_bytes, C,
-                     T, r, L, K, Zhat);
+                     T, r, L, K, gdim, Zhat);
   return hipGetLastError();
 }
 

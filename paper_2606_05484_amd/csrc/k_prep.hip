@@ -108,6 +108,30 @@ __device__ __forceinline__ void assemble_block(int bx, const AssembleArgs& a) {
       const uint32_t w[4] = {z.x, z.y, z.z, z.w};
 #pragma unroll
       for (int q = 0; q < 4; ++q) { v[2 * q] = bf2f(w[q] & 0xFFFFu); v[2 * q + 1] = bf2f(w[q] >> 16); }
+    } else if (a.gdim == 2) {
+      // grouped codes [T, L, r/2]: columns c0 .. c0 + 7 are groups
+      // c0/2 .. c0/2 + 3, four code bytes per round in one load
+      constexpr int LMAX = 8;
+      const int G = a.r / 2;
+      uint32_t cw4[LMAX];
+#pragma unroll
+      for (int l = 0; l < LMAX; ++l)
+        if (l < a.L) cw4[l] = *(const uint32_t*)((const uint8_t*)a.codes + ((int64_t)t * a.L + l) * G + c0 / 2);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = 0.f;
+#pragma unroll
+      for (int l = 0; l < LMAX; ++l) {
+        if (l < a.L) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            int c = (int)((cw4[l] >> (8 * q)) & 255u);
+            c = c < a.K ? c : a.K - 1;
+            const float2 p = *(const float2*)(a.C + ((int64_t)l * a.K + c) * a.r + c0 + 2 * q);
+            v[2 * q] += p.x;
+            v[2 * q + 1] += p.y;
+          }
+        }
+      }
     } else {
       // all codes, then all codeword rows, then the sum in stage order: the
       // loads of every stage are in flight together (L <= 8)
@@ -421,7 +445,7 @@ PrepJob prep_job_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float
 PrepJob prep_job_assemble(const AssembleArgs& a) {
   PrepJob j{};
   j.asm_args = a;
-  if (a.L >= 1 && a.L <= 2 && a.A == nullptr && a.Bc == nullptr && a.ldo == a.r) {
+  if (a.L >= 1 && a.L <= 2 && a.A == nullptr && a.Bc == nullptr && a.ldo == a.r && a.gdim == 0) {
     j.kind = PJ_ASSEMBLE_SUM;
     j.blocks = a.T > 0 ? (int)(((int64_t)(a.T + 3) / 4 * (a.r / 8) + 255) / 256) : 0;
   } else {

@@ -104,6 +104,7 @@ struct AssembleArgs {
   const int32_t* ids; int V;
   int T, r; int64_t ldo;
   bf16_t* out;
+  int gdim;                          // 2: grouped u8 codes [T, L, r/2] (group dimension 2)
 };
 hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s);
 
@@ -170,9 +171,15 @@ hipError_t launch_gather_rows_f32(const float* A, int k, const int32_t* ids, int
 // fp32 residual quantisation with exact fp32 distances over all K.
 hipError_t launch_rvq_f32(const float* Z0, const float* C, int T, int r, int L, int K, void* codes,
                           int code_bytes, hipStream_t s);
-// Zhat[t] = sum_l C[l][codes[t,l]] (fp32).
+// Zhat[t] = sum_l C[l][codes[t,l]] (fp32); gdim 2: grouped u8 codes [T,L,r/2],
+// Zhat[t][2g:2g+2] = sum_l C[l][codes[t,l,g]][2g:2g+2].
 hipError_t launch_codes_sum_f32(const void* codes, int code_bytes, const float* C, int T, int r, int L,
-                                int K, float* Zhat, hipStream_t s);
+                                int K, float* Zhat, hipStream_t s, int gdim = 0);
+// Grouped RVQ (group dimension 2): codes[t][l][g] (u8) = the nearest 2-D codeword
+// C[l][j][2g:2g+2] to the group's residual, exact fp32 distances, lowest index
+// on ties; Z0 [T,r] fp32.  Needs grvq_supported(r, L, K).
+hipError_t launch_grvq(const float* Z0, const float* C, int T, int r, int L, int K, uint8_t* codes, hipStream_t s);
+bool grvq_supported(int r, int L, int K);
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s);
 
 // ---------------------------------------------------------------- Stiefel step helpers

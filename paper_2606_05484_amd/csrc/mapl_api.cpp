@@ -153,6 +153,8 @@ struct Layout {
 };
 
 
+bool grouped(const mapl_codec_desc& D);
+
 // Quantisation of the returned gradient (mapl_decode_bwd_q): its own RVQ
 // codebooks over the r-dim gradient.
 struct GradQ {
@@ -175,7 +177,9 @@ Layout layout(const mapl_codec_desc& D, int call, const GradQ* q = nullptr) {
       case MAPL_CALL_ENCODE:
         Lo.kw = d + Lo.kp;
         Lo.w = c.take((size_t)r * Lo.kw * 2);
-        if (D.L > 0) {
+        if (grouped(D)) {
+          Lo.z0 = c.take((size_t)T * r * 4);  // fp32 Z0 for the grouped quantiser
+        } else if (D.L > 0) {
           // fp32 Z0 between the projection and the RVQ, unless one launch does both
           if (!enc_rvq_fusable((int)r, D.L)) Lo.z0 = c.take((size_t)T * r * 4);
           Lo.cb = c.take((size_t)D.L * D.K * rvq_cb_cols((int)r) * 2);
@@ -266,9 +270,18 @@ int check_desc(const mapl_codec_desc* D) {
     } else if (D->code_dtype != MAPL_U16) {
       return fail(MAPL_E_DTYPE, "code_dtype must be MAPL_U8 or MAPL_U16 (got %d)", D->code_dtype);
     }
-    if (D->x_dtype == MAPL_BF16 && D->r != 64 && D->r != 128 && D->r != 256)
+    if (D->group_dim == 2) {
+      if (D->K > 256 || D->code_dtype != MAPL_U8)
+        return fail(MAPL_E_RANGE, "grouped RVQ (group_dim 2) needs K <= 256 and MAPL_U8 codes");
+      if (!grvq_supported((int)D->r, D->L, D->K))
+        return fail(MAPL_E_UNSUPPORTED, "grouped RVQ: r=%lld, L=%d, K=%d not supported", (long long)D->r, D->L, D->K);
+    } else if (D->x_dtype == MAPL_BF16 && D->r != 64 && D->r != 128 && D->r != 256) {
       return fail(MAPL_E_UNSUPPORTED, "RVQ on the bf16 path supports r in {64, 128, 256} (got %lld)", (long long)D->r);
+    }
   }
+  if (D->group_dim != 0 && D->group_dim != 2)
+    return fail(MAPL_E_SHAPE, "group_dim must be 0 (whole vectors) or 2 (got %d)", D->group_dim);
+  if (D->group_dim == 2 && D->L == 0) return fail(MAPL_E_SHAPE, "group_dim 2 needs RVQ stages (L >= 1)");
   return MAPL_OK;
 }
 
@@ -328,7 +341,9 @@ template <typename P>
 inline P* at(void* ws, size_t off) { return (P*)((char*)ws + off); }
 
 size_t code_bytes(const mapl_codec_desc& D) { return D.code_dtype == MAPL_U8 ? 1 : 2; }
+bool grouped(const mapl_codec_desc& D) { return D.L > 0 && D.group_dim == 2; }
 size_t payload_bytes(const mapl_codec_desc& D) {
+  if (grouped(D)) return (size_t)D.T * D.L * (D.r / 2);
   return D.L == 0 ? (size_t)D.T * D.r * esize(D.x_dtype) : (size_t)D.T * D.L * code_bytes(D);
 }
 size_t b_cols(const mapl_codec_desc& D) { return D.anchor_space == MAPL_ANCHOR_AMBIENT ? D.d : D.r; }
@@ -407,7 +422,7 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
       else
         jobs[nj++] = prep_job_transpose(B_s, 0, (int)k, (int)r, r, -1.f, Wt, Lo.kw, (int)d);
     }
-    if (D.L > 0) jobs[nj++] = prep_job_codebook(C, D.L, D.K, (int)r, Cb, meta);
+    if (D.L > 0 && !grouped(D)) jobs[nj++] = prep_job_codebook(C, D.L, D.K, (int)r, Cb, meta);
     LAUNCH("enc:prep", launch_prep_batch(jobs, nj, s));
     TnArgs g{};
     g.A = (const bf16_t*)X; g.lda = d; g.Ka = (int)d;
@@ -417,6 +432,13 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
     if (D.L == 0) {
       g.out = payload; g.ldo = r; g.out_f32 = 0;
       LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
+      return MAPL_OK;
+    }
+    if (grouped(D)) {
+      float* Z0 = at<float>(ws, Lo.z0);
+      g.out = Z0; g.ldo = r; g.out_f32 = 1;
+      LAUNCH("enc:gemm_tn", launch_gemm_tn(g, s));
+      LAUNCH("enc:grvq", launch_grvq(Z0, C, (int)T, (int)r, D.L, D.K, (uint8_t*)payload, s));
       return MAPL_OK;
     }
     RvqArgs a{};
@@ -479,7 +501,10 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
     g.alpha = -1.f; g.beta = 1.f;
     LAUNCH("enc:gemm_f32", launch_gemm_f32(g, 0, 0, 0, s));
   }
-  if (D.L > 0) LAUNCH("enc:rvq_f32", launch_rvq_f32(out, C, (int)T, (int)r, D.L, D.K, payload, cbytes, s));
+  if (grouped(D))
+    LAUNCH("enc:grvq", launch_grvq(out, C, (int)T, (int)r, D.L, D.K, (uint8_t*)payload, s));
+  else if (D.L > 0)
+    LAUNCH("enc:rvq_f32", launch_rvq_f32(out, C, (int)T, (int)r, D.L, D.K, payload, cbytes, s));
   return MAPL_OK;
 }
 
@@ -529,7 +554,7 @@ extern "C" int mapl_decode(const mapl_codec_desc* desc, const void* payload, con
       bf16_t* Ah = at<bf16_t>(ws, Lo.ahat);
       AssembleArgs a{};
       a.codes = payload; a.code_bytes = cbytes; a.C = C; a.L = D.L; a.K = D.K;
-      a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah;
+      a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah; a.gdim = grouped(D) ? 2 : 0;
       jobs[nj++] = prep_job_assemble(a);
       Aop = Ah;
     }
@@ -548,7 +573,7 @@ extern "C" int mapl_decode(const mapl_codec_desc* desc, const void* payload, con
   const float* Zh = (const float*)payload;
   if (D.L > 0) {
     float* z = at<float>(ws, Lo.zh);
-    LAUNCH("dec:codes_sum_f32", launch_codes_sum_f32(payload, cbytes, C, (int)T, (int)r, D.L, D.K, z, s));
+    LAUNCH("dec:codes_sum_f32", launch_codes_sum_f32(payload, cbytes, C, (int)T, (int)r, D.L, D.K, z, s, grouped(D) ? 2 : 0));
     Zh = z;
   }
   float* a = k > 0 ? at<float>(ws, Lo.ga) : nullptr;
@@ -648,7 +673,7 @@ int decode_bwd_impl(const mapl_codec_desc* desc, const void* dXhat, const void* 
       a.Zp = D.L == 0 ? (const bf16_t*)payload : nullptr;
       a.codes = payload; a.code_bytes = cbytes; a.C = C; a.L = D.L; a.K = D.K;
       if (need_anchor) { a.A = (const bf16_t*)A_r; a.k = (int)k; a.Bc = (const bf16_t*)B_r; a.ids = ids; a.V = (int)D.V; }
-      a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah;
+      a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah; a.gdim = grouped(D) ? 2 : 0;
       jobs[nj++] = prep_job_assemble(a);
       Q = Ah;
     }
@@ -701,7 +726,7 @@ int decode_bwd_impl(const mapl_codec_desc* desc, const void* dXhat, const void* 
   const float* Zh = (const float*)payload;
   if (D.L > 0) {
     float* z = at<float>(ws, Lo.zh);
-    LAUNCH("dec_bwd:codes_sum_f32", launch_codes_sum_f32(payload, cbytes, C, (int)T, (int)r, D.L, D.K, z, s));
+    LAUNCH("dec_bwd:codes_sum_f32", launch_codes_sum_f32(payload, cbytes, C, (int)T, (int)r, D.L, D.K, z, s, grouped(D) ? 2 : 0));
     Zh = z;
   }
   if (need_anchor) {

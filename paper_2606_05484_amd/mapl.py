@@ -34,7 +34,7 @@ class CodecDesc(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int64), ("d", ctypes.c_int64), ("r", ctypes.c_int64), ("V", ctypes.c_int64),
                 ("k", ctypes.c_int64), ("anchor_space", ctypes.c_int32), ("L", ctypes.c_int32),
                 ("K", ctypes.c_int32), ("x_dtype", ctypes.c_int32), ("ab_dtype", ctypes.c_int32),
-                ("code_dtype", ctypes.c_int32)]
+                ("code_dtype", ctypes.c_int32), ("group_dim", ctypes.c_int32)]
 
 
 _lib = None
@@ -111,19 +111,21 @@ def _stream(stream):
     return stream.cuda_stream
 
 
-def desc(T, d, r, V=0, k=0, L=0, K=0, x_dtype="bf16", anchor_space="ambient", code_dtype=None):
+def desc(T, d, r, V=0, k=0, L=0, K=0, x_dtype="bf16", anchor_space="ambient", code_dtype=None, group_dim=0):
     """Build a mapl_codec_desc; code_dtype defaults to u8 for K <= 256, else u16."""
     if code_dtype is None:
         code_dtype = "u8" if K <= 256 else "u16"
     dt = _DT[x_dtype] if isinstance(x_dtype, str) else x_dtype
     return CodecDesc(T, d, r, V, k, _SPACE[anchor_space] if isinstance(anchor_space, str) else anchor_space,
-                     L, K, dt, dt, _DT[code_dtype] if isinstance(code_dtype, str) else code_dtype)
+                     L, K, dt, dt, _DT[code_dtype] if isinstance(code_dtype, str) else code_dtype, group_dim)
 
 
 def payload_bytes_per_token(D):
     """Bytes that cross the pipeline link per token (ids excluded)."""
     if D.L == 0:
         return D.r * (4 if D.x_dtype == F32 else 2)
+    if D.group_dim == 2:
+        return D.L * (D.r // 2)
     return D.L * (1 if D.code_dtype == U8 else 2)
 
 

@@ -12,6 +12,8 @@ for 150M, d = 2048 for 1B, vocabulary 32000, micro-batches of 4 x 2048 tokens):
             T=8192,  d=1024, r=.., V=32000, k=64,  L=0,         bf16
   c3        T=8192,  d=1024, r=128, V=32000, k=16,  L=4, K=256,  bf16, u8 codes
   c4        T=32768, d=2048, r=256, V=32000, k=128, L=2, K=1024, bf16, u16 codes
+  c6        T=8192,  d=1024, r=256, V=32000, k=64,  L=2, K=256,  bf16, grouped RVQ
+            (group dimension 2: u8 codes [T, 2, 128], 256 bytes per token)
   c5        16 projectors U_p [2048,512] fp32, G_p = 1e-3 N(0,1)
 
 Recipe (PCG64 ``numpy.random.default_rng(seed)``, draws in this order):
@@ -50,11 +52,15 @@ PRESETS = {
     "c4": dict(T=32768, d=2048, r=256, V=32000, k=128, L=2, K=1024, dtype=BF16, alpha=0.7,
                n_out=16, cb_sigma=None, gscale=1.0, lr=1e-2),
 }
+# the paper's own VQ setting (App. E; Table 1's MAPL+VQ rows at 150M): r = 256,
+# two-coordinate groups, K = 256, R = 2 rounds -> 256 bytes per token
+PRESETS["c6"] = dict(T=8192, d=1024, r=256, V=32000, k=64, L=2, K=256, dtype=BF16, alpha=0.8, n_out=4,
+                     cb_sigma=None, gscale=1.0, lr=1e-2, group_dim=2)
 for _r in (64, 128, 256, 512):
     PRESETS["c2_r%d" % _r] = dict(T=8192, d=1024, r=_r, V=32000, k=64, L=0, K=0, dtype=BF16,
                                   alpha=0.8, n_out=4, cb_sigma=None, gscale=1.0, lr=1e-2)
 
-SEEDS = {"c1": 1, "c2_r64": 2, "c2_r128": 2, "c2_r256": 2, "c2_r512": 2, "c3": 3, "c4": 4, "c5": 5}
+SEEDS = {"c1": 1, "c2_r64": 2, "c2_r128": 2, "c2_r256": 2, "c2_r512": 2, "c3": 3, "c4": 4, "c5": 5, "c6": 6}
 
 STIEFEL_PRESETS = {
     "c1": dict(P=1, d=256, r=32, gscale=1.0, lr=1e-2, beta=0.95, steps=1),
@@ -152,7 +158,8 @@ def codec_inputs(name=None, seed=None, anchor_space="ambient", chunk=4096, ancho
     return dict(name=name, seed=seed, T=T, d=d, r=r, V=V, k=k, L=L, K=K, dtype=dt,
                 anchor_space=anchor_space, X=X, U=U, A=_store(A32, dt), B=_store(B32, dt),
                 ids=ids, C=C, dXhat=dXhat, dZ=dZ, G=G, cb_sigma=float(sigma),
-                code_dtype=("u8" if K <= 256 else "u16"), lr=float(cfg.get("lr", 1e-2)), anchor=anchor)
+                code_dtype=("u8" if K <= 256 else "u16"), lr=float(cfg.get("lr", 1e-2)), anchor=anchor,
+                group_dim=int(cfg.get("group_dim", 0)))
 
 
 def stiefel_inputs(name=None, seed=None, **over):

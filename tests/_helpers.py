@@ -56,7 +56,8 @@ def descr(x, L=None, K=None):
     L = x["L"] if L is None else L
     K = x["K"] if K is None else K
     return mapl.desc(T=x["T"], d=x["d"], r=x["r"], V=x["V"], k=x["k"], L=L, K=K, x_dtype=x["dtype"],
-                     anchor_space=x["anchor_space"], code_dtype=None if L else "u8")
+                     anchor_space=x["anchor_space"], code_dtype=None if L else "u8",
+                     group_dim=x.get("group_dim", 0) if L else 0)
 
 
 class Dev:
@@ -82,6 +83,8 @@ def run_encode(x, D, g, payload=None):
     if payload is None:
         if D.L == 0:
             payload = t.full((x["T"], x["r"]), float("nan"), dtype=g.tdt, device="cuda")
+        elif D.group_dim == 2:
+            payload = t.full((x["T"], D.L, x["r"] // 2), 255, dtype=t.uint8, device="cuda")
         else:
             payload = t.full((x["T"], D.L), -1 if D.code_dtype == mapl.U16 else 255,
                              dtype=t.int16 if D.code_dtype == mapl.U16 else t.uint8, device="cuda")
@@ -98,9 +101,19 @@ def codes_np(payload, D):
 
 
 def compare_codes(gpu_codes, ref_codes, gap):
-    """Returns (n_mismatch_nonexempt, n_exempt).  A token is exempt when any
-    round has an oracle top-2 gap under TIE_GAP; for the rest every round
-    must match."""
+    """Returns (n_mismatch_nonexempt, n_exempt).  Whole-vector codes [T, L]:
+    a token is exempt when any round has an oracle top-2 gap under TIE_GAP;
+    for the rest every round must match.  Grouped codes [T, L, G] (gap
+    relative to the group's unquantised energy): each (token, group) is
+    compared round by round up to its first near-tie round, every decision
+    before it must match; n_exempt counts the decisions not compared."""
+    if gpu_codes.ndim == 3:
+        L = ref_codes.shape[1]
+        near = gap < TIE_GAP
+        first = np.where(near.any(axis=1), near.argmax(axis=1), L)  # [T, G]
+        compared = np.arange(L)[None, :, None] < first[:, None, :]
+        bad = int(((gpu_codes != ref_codes) & compared).sum())
+        return bad, int((~compared).sum())
     exempt = (gap < TIE_GAP).any(axis=1)
     bad = (gpu_codes != ref_codes).any(axis=1) & ~exempt
     return int(bad.sum()), int(exempt.sum())
@@ -219,9 +232,10 @@ def check_chain(x, res, C=None, rx=None):
         print("Z rel err", e)
         assert e <= tol(x)
     else:
-        codes_ref, gap, _ = ocodec.rvq_encode(ref["Z0"], Cn)
+        gd = x.get("group_dim", 0)
+        codes_ref, gap, _ = (ocodec.grouped_rvq_encode(ref["Z0"], Cn, gd) if gd else ocodec.rvq_encode(ref["Z0"], Cn))
         bad, ex = compare_codes(cg, codes_ref, gap)
-        print("codes: mismatched non-exempt", bad, "exempt", ex, "of", x["T"])
+        print("codes: mismatched non-exempt", bad, "exempt", ex, "of", cg.size if gd else x["T"])
         assert bad == 0
     e = rel_fro(res["Xh"], ref["Xh"])
     print("Xhat rel err", e)
@@ -290,4 +304,22 @@ def grad_codebooks(x, Lg, Kg, seed):
         C[l, 1:] = (R[idx] + 0.05 * sig * rng.standard_normal((Kg - 1, r))).astype(np.float32)
         codes, _, _ = ocodec.rvq_encode(R, C[l:l + 1].astype(np.float64))
         R = R - C[l].astype(np.float64)[codes[:, 0]]
+    return C
+
+
+def grouped_stress_codebooks(x, seed):
+    """Stress codebooks for grouped RVQ: codeword rows drawn from the oracle's
+    residual rows plus 5 % noise (codeword 0 = 0), the residual updated group
+    by group after each round."""
+    gd = x["group_dim"]
+    rng = np.random.default_rng(seed)
+    R = ocodec.project(f64(x, "X"), x["ids"], x["U"], f64(x, "A"), f64(x, "B"), x["anchor_space"], operand(x))
+    L, K, r, T = x["L"], x["K"], x["r"], x["T"]
+    C = np.zeros((L, K, r), dtype=np.float32)
+    for l in range(L):
+        sig = np.sqrt(np.mean(R ** 2))
+        idx = rng.choice(T, K - 1, replace=False)
+        C[l, 1:] = (R[idx] + 0.05 * sig * rng.standard_normal((K - 1, r))).astype(np.float32)
+        codes, _, _ = ocodec.grouped_rvq_encode(R, C[l:l + 1].astype(np.float64), gd)
+        R = R - ocodec.grouped_rvq_decode(codes, C[l:l + 1].astype(np.float64), gd)
     return C

@@ -27,12 +27,12 @@ def test_exports_every_declared_symbol():
     assert set(declared) == set(mapl.EXPORTS)
     for name in declared:
         assert hasattr(L, name), name
-    assert L.mapl_version() == 1
+    assert L.mapl_version() == 2
 
 
 def test_desc_layout_matches_header():
-    # two int64 groups then six int32: 5*8 + 6*4 = 64 bytes, no padding
-    assert ctypes.sizeof(mapl.CodecDesc) == 64
+    # five int64 then seven int32: 5*8 + 7*4 = 68 bytes, padded to 72 (int64 alignment)
+    assert ctypes.sizeof(mapl.CodecDesc) == 72
 
 
 def _enc(D, **kw):
@@ -128,6 +128,10 @@ def test_payload_bytes_against_paper(tmp_path):
     for row in g["uncompressed_bf16"]:
         D = mapl.desc(T=1, d=row["d"], r=row["d"] if row["d"] <= 1024 else 1024, L=0)
         assert 2 * row["d"] == row["bytes"]
+    # the paper's VQ setting (Table 1's MAPL+VQ rows, App. E): 256 bytes per token
+    for row in g["mapl_vq"]:
+        D = mapl.desc(T=1, d=row["d"], r=row["r"], L=row["R"], K=row["K"], group_dim=row["group_dim"])
+        assert mapl.payload_bytes_per_token(D) == row["bytes"]
     # the build's RVQ payloads: L stages of u8 / u16 codes
     assert mapl.payload_bytes_per_token(mapl.desc(T=1, d=1024, r=128, L=4, K=256)) == 4
     assert mapl.payload_bytes_per_token(mapl.desc(T=1, d=2048, r=256, L=2, K=1024)) == 4
