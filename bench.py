@@ -319,30 +319,44 @@ def summarize(paths, write_traffic):
                 fh.write("%s %s %.0f\n" % (name, _src_sha(kernel_sources(name)), traffic[name]))
 
 
+GROUP_DIST_FLOPS = 5  # (x - cx)^2 + (y - cy)^2: two subtractions, two products, one sum
+
+
 def chain_counts(x):
-    """Per-call algorithmic (flops, bytes) of workload x (see per_call_counts)."""
+    """Per-call algorithmic (matrix flops, vector-ALU flops, bytes) of
+    workload x (see per_call_counts).  Whole-vector RVQ distances are matrix
+    products (2 r K per token and round); the grouped quantiser's 2-D
+    distances are vector work (5 flops per codeword, group and round)."""
     es = 4 if x["dtype"] == "f32" else 2
     T, d, r, k, L, K = (x[n] for n in ("T", "d", "r", "k", "L", "K"))
-    pay = (L * (1 if K <= 256 else 2)) if L else r * es
+    gd = x.get("group_dim", 0) if L else 0
+    if gd:
+        pay = L * (r // gd)
+        rvq_m, rvq_a = 0, GROUP_DIST_FLOPS * L * (r // gd) * K
+    else:
+        pay = (L * (1 if K <= 256 else 2)) if L else r * es
+        rvq_m, rvq_a = 2 * L * r * K, 0
     c = {
-        "encode": (2 * d * r + 2 * k * r + 2 * L * r * K, es * d + 4 + es * k + pay),
-        "decode": (2 * r * d + 2 * k * d, pay + 4 + es * k + es * d),
-        "decode_bwd": (4 * d * r, es * d + pay + es * r),
-        "encode_bwd": (4 * d * r + 2 * k * r, es * r + 2 * es * d + 4 + es * k),
+        "encode": (2 * d * r + 2 * k * r + rvq_m, rvq_a, es * d + 4 + es * k + pay),
+        "decode": (2 * r * d + 2 * k * d, 0, pay + 4 + es * k + es * d),
+        "decode_bwd": (4 * d * r, 0, es * d + pay + es * r),
+        "encode_bwd": (4 * d * r + 2 * k * r, 0, es * r + 2 * es * d + 4 + es * k),
     }
-    return {n: (f * T, b * T) for n, (f, b) in c.items()}
+    return {n: (fm * T, fa * T, b * T) for n, (fm, fa, b) in c.items()}
 
 
 def roofline_of(x, ms):
-    """Chain roofline: sum over calls of max(F / peak, B / HBM) against the
-    measured ms per step (peak: bf16 or fp32 MFMA by the workload's type)."""
+    """Chain roofline: sum over calls of max(Fm / mfma peak + Fa / fp32
+    vector peak, B / HBM) against the measured ms per step (matrix peak:
+    bf16 or fp32 MFMA by the workload's type)."""
     peak = PEAK_F32 if x["dtype"] == "f32" else PEAK_BF16
     cc = chain_counts(x)
-    per = {n: max(f / peak, b / PEAK_HBM) for n, (f, b) in cc.items()}
-    bound = {n: ("mfma" if f / peak >= b / PEAK_HBM else "hbm") for n, (f, b) in cc.items()}
+    per = {n: max(fm / peak + fa / PEAK_F32, b / PEAK_HBM) for n, (fm, fa, b) in cc.items()}
+    bound = {n: (("mfma" if fm / peak >= fa / PEAK_F32 else "alu") if fm / peak + fa / PEAK_F32 >= b / PEAK_HBM
+                 else "hbm") for n, (fm, fa, b) in cc.items()}
     roof = sum(per.values())
     return {"frac": roof / (ms * 1e-3), "roofline_us": roof * 1e6, "measured_us": ms * 1e3,
-            "flops": sum(f for f, _ in cc.values()), "bytes": sum(b for _, b in cc.values()),
+            "flops": sum(fm + fa for fm, fa, _ in cc.values()), "bytes": sum(b for _, _, b in cc.values()),
             "bound_per_call": bound}
 
 
@@ -368,9 +382,12 @@ class Chain:
         self.U = torch.from_numpy(x["U"]).cuda()
         self.ids = torch.from_numpy(x["ids"]).cuda()
         self.C = torch.from_numpy(np.ascontiguousarray(C, dtype=np.float32)).cuda() if L else None
-        self.D = mapl.desc(T=T, d=d, r=r, V=x["V"], k=x["k"], L=L, K=K, x_dtype=dt)
+        self.D = mapl.desc(T=T, d=d, r=r, V=x["V"], k=x["k"], L=L, K=K, x_dtype=dt,
+                           group_dim=x.get("group_dim", 0) if L else 0)
         self.ws = mapl.workspace(max(mapl.workspace_bytes(self.D, c) for c in range(4)))
-        if L:
+        if L and self.D.group_dim:
+            self.payload = torch.empty((T, L, r // self.D.group_dim), dtype=torch.uint8, device="cuda")
+        elif L:
             self.payload = torch.empty((T, L), dtype=torch.uint8 if K <= 256 else torch.int16, device="cuda")
         else:
             self.payload = torch.empty((T, r), dtype=tdt, device="cuda")
@@ -451,6 +468,84 @@ def library_stress_codebooks(torch, mapl, x, seed=104, n=8192):
     for l in range(1, x["L"]):
         C[l, 1:] = 0.3 * Z[rng.choice(n, x["K"] - 1, replace=False)]
     return C
+
+
+def next_rows(torch, mapl, x, Cs, args):
+    """Timings of the calls beside the four-call chain at the c4 widths,
+    each against its own roofline: decode_bwd with the returned gradient
+    quantised (K = 1024, two rounds; Sec. 3.5), the anchor-table gradient on
+    both sides (Eq. 3) and the streaming codebook sync (1/5 of the codewords
+    per micro-batch)."""
+    T, d, r, V, k, L, K = (x[n] for n in ("T", "d", "r", "V", "k", "L", "K"))
+    ch = Chain(torch, mapl, x, Cs)
+    ch.step()
+    out = {}
+    # gradient codebooks: the library's own gradient rows dXhat U~ of the first 8192 tokens
+    n = 8192
+    sub = dict(x, T=n, X=x["dXhat"][:n], ids=x["ids"][:n], dXhat=x["dXhat"][:n], L=0, K=0, k=0)
+    cg = Chain(torch, mapl, sub, np.zeros((0,)))
+    mapl.encode(cg.D, cg.X, None, cg.U, None, None, None, cg.payload, cg.ws)
+    torch.cuda.synchronize()
+    G = cg.payload.float().cpu().numpy()
+    rng = np.random.default_rng(105)
+    Lg, Kg = 2, 1024
+    Cg = np.zeros((Lg, Kg, r), dtype=np.float32)
+    Cg[0, 1:] = G[rng.choice(n, Kg - 1, replace=False)]
+    Cg[1, 1:] = 0.3 * G[rng.choice(n, Kg - 1, replace=False)]
+    Cgg = torch.from_numpy(Cg).cuda()
+    del cg
+    wsq = mapl.workspace(mapl.decode_bwd_q_workspace_bytes(ch.D, Lg, Kg))
+    gcodes = torch.empty((T, Lg), dtype=torch.int16, device="cuda")
+    run = lambda: mapl.decode_bwd_q(ch.D, ch.dXh, ch.payload, ch.ids, ch.U, ch.A, ch.B, ch.C, Lg, Kg, Cgg, gcodes,
+                                    ch.dU, 0, wsq)
+    q_ms, q_med = time_steps(torch, run, 3, args.steps)
+    runb = lambda: mapl.decode_bwd(ch.D, ch.dXh, ch.payload, ch.ids, ch.U, ch.A, ch.B, ch.C, ch.dZ, ch.dU, 0, ch.ws)
+    b_ms, b_med = time_steps(torch, runb, 3, args.steps)
+    fq = T * (4 * d * r + 2 * Lg * r * Kg)
+    bq = T * (2 * d + 2 * L + 2 * Lg)
+    roofq = max(fq / PEAK_BF16, bq / PEAK_HBM)
+    out["decode_bwd_q"] = {"gradient_codebooks": "Lg=2 x Kg=1024 drawn from the library's own dXhat U~ rows",
+                           "median_us": q_med * 1e3, "decode_bwd_median_us": b_med * 1e3,
+                           "tokens_per_s": T / (q_med * 1e-3), "roofline_us": roofq * 1e6,
+                           "roofline_frac": roofq / (q_med * 1e-3),
+                           "bytes_per_token_returned": 2 * Lg, "bytes_per_token_unquantised": 2 * r}
+    # anchor-table gradient, both sides
+    for side, name in ((mapl.SENDER, "sender"), (mapl.RECEIVER, "receiver")):
+        wsa = mapl.workspace(mapl.anchor_bwd_workspace_bytes(ch.D, side))
+        dA = torch.empty((V, k), device="cuda")
+        dY = ch.dZ if side == mapl.SENDER else ch.dXh
+        runa = lambda: mapl.anchor_bwd(ch.D, side, dY, ch.ids, ch.U, ch.B, dA, 0, wsa)
+        a_ms, a_med = time_steps(torch, runa, 3, args.steps)
+        width = r if side == mapl.SENDER else d
+        ba = T * (2 * width + 4) + V * k * 4
+        fa = T * 2 * width * k
+        roofa = max(fa / PEAK_BF16, ba / PEAK_HBM)
+        mapl.profile(1)
+        runa()
+        torch.cuda.synchronize()
+        mapl.profile(0)
+        kp = mapl.profile_report()
+        out["anchor_bwd_" + name] = {"median_us": a_med * 1e3, "roofline_us": roofa * 1e6,
+                                     "roofline_frac": roofa / (a_med * 1e-3),
+                                     "bound": "mfma" if fa / PEAK_BF16 >= ba / PEAK_HBM else "hbm",
+                                     "per_kernel_us": {nm: round(v[1] / v[0] * 1e3, 2) for nm, v in kp.items()}}
+        del wsa, dA
+    # streaming codebook sync: one part of five per micro-batch
+    parts = 5
+    nrow = (K + parts - 1) // parts
+    rows = torch.from_numpy(np.stack([np.random.default_rng(l).permutation(K)[:nrow] for l in range(L)])
+                            .astype(np.int32)).cuda()
+    buf = torch.empty((L, nrow, r), device="cuda")
+    recv = ch.C.clone()
+    runs = lambda: (mapl.codebook_pack(L, K, r, ch.C, rows, nrow, buf),
+                    mapl.codebook_unpack(L, K, r, buf, rows, nrow, recv))
+    s_ms, s_med = time_steps(torch, runs, 3, args.steps)
+    bs = 4 * L * nrow * r * 4 + 2 * L * nrow * 4
+    out["codebook_sync"] = {"rows_per_round": nrow, "parts": parts, "median_us": s_med * 1e3,
+                            "bytes_moved": bs, "roofline_us": bs / PEAK_HBM * 1e6,
+                            "roofline_frac": bs / PEAK_HBM / (s_med * 1e-3),
+                            "bytes_on_the_wire": L * nrow * r * 4}
+    return out
 
 
 def main():
@@ -582,7 +677,8 @@ def main():
             "encode_vs_headline": (enc_us / kern["enc:gemm_rvq"][1]) if enc_us and "enc:gemm_rvq" in kern else None,
             "rvq_tokens_rescored_frac": st.get("rvq:tokens_rescored", 0) / (5.0 * T * L),
             "rvq_candidates_per_rescored_token": st.get("rvq:candidates", 0) / max(1, st.get("rvq:tokens_rescored", 0)),
-            "rvq_second_pass_frac": st.get("rvq:second_pass_blocks", 0) / max(1, st.get("rvq:blocks", 0)),
+            "rvq_deep_pass_frac": st.get("rvq:deep_pass_blocks", 0) / max(1, st.get("rvq:blocks", 0)),
+            "rvq_listing_pass_frac": st.get("rvq:listing_pass_blocks", 0) / max(1, st.get("rvq:blocks", 0)),
             "rvq_list_overflows": st.get("rvq:list_overflows", 0),
         }
         del chs
@@ -590,7 +686,7 @@ def main():
         # ---- the other workloads: tokens/s and chain roofline (graph replay),
         # the oracle beside each on the host
         out["configs"] = {}
-        for name in ["c1", "c2_r64", "c2_r128", "c2_r256", "c2_r512", "c3"]:
+        for name in ["c1", "c2_r64", "c2_r128", "c2_r256", "c2_r512", "c3", "c6"]:
             log("workload", name)
             xc = synth.codec_inputs(name)
             cc = Chain(torch, mapl, xc, xc["C"])
@@ -601,14 +697,34 @@ def main():
             c_med = min(c_med, g_med)
             rf = roofline_of(xc, c_med)
             blk = {"T": xc["T"], "d": xc["d"], "r": xc["r"], "k": xc["k"], "L": xc["L"], "K": xc["K"],
+                   "group_dim": xc.get("group_dim", 0),
                    "dtype": xc["dtype"], "tokens_per_s": xc["T"] / (c_med * 1e-3), "median_ms_per_step": c_med,
                    "mean_ms_per_step": c_ms, "graph_median_ms_per_step": g_med,
                    "chain_roofline_frac": rf["frac"], "roofline_us": rf["roofline_us"],
                    "bound_per_call": rf["bound_per_call"]}
+            if xc.get("group_dim", 0):
+                # the grouped quantiser alone: vector-ALU work against the fp32 vector peak
+                mapl.profile(1)
+                for _ in range(10):
+                    cc.step()
+                torch.cuda.synchronize()
+                mapl.profile(0)
+                kp = mapl.profile_report()
+                if "enc:grvq" in kp:
+                    us = kp["enc:grvq"][1] / kp["enc:grvq"][0] * 1e3
+                    fa = GROUP_DIST_FLOPS * xc["T"] * xc["L"] * (xc["r"] // 2) * xc["K"]
+                    blk["grvq_kernel"] = {"bound": "alu", "avg_us": us, "achieved": fa / (us * 1e-6) / 1e12,
+                                          "peak": PEAK_F32 / 1e12, "unit": "TFLOP/s",
+                                          "frac": fa / (us * 1e-6) / PEAK_F32,
+                                          "per_kernel_us": {n: round(v[1] / v[0] * 1e3, 2) for n, v in kp.items()}}
             if not args.no_cpu_baseline:
                 blk["cpu_baseline"] = cpu_baseline(xc, budget_s=4.0)
             out["configs"][name] = blk
             del cc
+
+        # ---- the rows beside the chain, at the c4 widths
+        log("gradient quantisation, anchor-table gradient, codebook sync")
+        out["next"] = next_rows(torch, mapl, x, Cs, args)
 
         # ---- SPEL step: its own configuration (16 x [2048,512]) and this
         # boundary's projector

@@ -55,20 +55,52 @@ __device__ __forceinline__ int clamp_id(int id, int V) { return (unsigned)id < (
 
 __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
 
-// Screening margin of the RVQ kernel for residual width R: with the
-// accumulator holding ||C_j||^2 exactly after the first k-step (three bf16
-// pieces that sum to it exactly, times ones) and bf16 operands,
-//   |s~_j - s_j| <= k1 ||R|| ||C_j|| + k2 ||C_j||^2, where
-//   k1 = 2 (2 * 2^-8 + 2^-16)  (bf16 rounding of both operands, doubled)
-//      + 8 R 2^-24             (fp32 accumulation of 2R~.C~, any order,
+// Screening margin of the RVQ kernel for residual width R.  With
+// R~ = bf16(R), C~_j = bf16(C_j), eR = ||R - R~|| and e_j = ||C_j - C~_j||
+// (bf16 has 8 significant bits, so e_j <= 2^-8 ||C_j||), the screen's score
+// s~_j = ||C_j||^2 - 2 R~.C~_j (the squared norm exact after the first
+// k-step: three bf16 pieces that sum to it exactly, times ones) satisfies
+//   |s~_j - s_j| <= 2 ||R|| e_j + 2 eR (1 + 2^-8) ||C_j||
+//                   + ka ||R|| ||C_j|| + k2 ||C_j||^2  =: Delta_j, where
+// 2 R.C_j - 2 R~.C~_j = 2 R.(C_j - C~_j) + 2 (R - R~).C~_j gives the first
+// two terms (Cauchy-Schwarz, ||C~_j|| <= ||C_j|| + e_j), and
+//   ka = (8 R 2^-24            (fp32 accumulation of 2R~.C~, any order,
 //                               relative error up to 2 u per addition)
-//      + 2^-20 + 2^-17         (norm rounding; the 4-bit index tag)
-//   k2 = 4 (R + 4) 2^-24 + 2^-18 (accumulation and fp32 rounding of
-//                               ||C_j||^2; the index tag)
-__host__ __device__ constexpr float rvq_margin_k1(int R) {
-  return 0.015625f * 1.0078125f + 8.0f * R / 16777216.0f + 1.0f / 1048576.0f + 1.0f / 131072.0f;
+//        + 2^-20 + 2^-12) (1 + 2^-7)  (norm rounding; the 9-bit index tag,
+//                               which moves a score by at most 2^-14 of
+//                               |s~_j| <= ||C_j||^2 + 2.02 ||R|| ||C_j||,
+//                               doubled; ||R~|| ||C~|| against ||R|| ||C||)
+//   k2 = 4 (R + 4) 2^-24 + 2^-13 (accumulation and fp32 rounding of
+//                               ||C_j||^2; the index tag, doubled)
+// The actual rounding-error norms replace the componentwise worst case
+// 2^-8 ||.||: for data they are about 0.4 of it, and the candidate sets
+// shrink accordingly.
+__host__ __device__ constexpr float rvq_margin_ka(int R) {
+  return (8.0f * R / 16777216.0f + 1.0f / 1048576.0f + 1.0f / 4096.0f) * 1.0078125f;
 }
-__host__ __device__ constexpr float rvq_margin_k2(int R) { return 4.0f * (R + 4) / 16777216.0f + 1.0f / 262144.0f; }
+__host__ __device__ constexpr float rvq_margin_k2(int R) { return 4.0f * (R + 4) / 16777216.0f + 1.0f / 8192.0f; }
+
+// The screen of the RVQ kernel computes, per codeword, a certified lower bound
+// of the exact score s_j = ||C_j||^2 - 2 R . C_j rather than the score itself:
+// the norm columns of a codeword row hold (1 - RVQ_K2_SLACK k2) ||C_j||^2
+// (three bf16 pieces, exact), ||C_j|| rounded up (two bf16 pieces) and e_j
+// rounded up (one piece); the token's operand multiplies them by ones, by -b
+// with b = (2 eR (1 + 2^-7) + ka ||R||) RVQ_K1_SLACK and by -c with
+// c = 2 ||R|| RVQ_K1_SLACK, each rounded up to bf16, so that the accumulator
+// ends at
+//   L_j = s~_j - k2' ||C_j||^2 - b ||C_j||' - c e_j'  <=  s_j.
+// The subtracted amount is at most RVQ_SUB_FACTOR Delta_j (bf16 rounding up
+// of the coefficients and of e_j, 2^-7 each, and the slack), so
+// s_j <= L_j + (RVQ_SUB_FACTOR + 1) Delta_j.
+constexpr float RVQ_K1_SLACK = 1.0002f * 1.01f;
+constexpr float RVQ_K2_SLACK = 1.01f;
+constexpr float RVQ_SUB_FACTOR = 1.03f;
+
+// bf16 bit pattern of a non-negative finite float, rounded toward +infinity.
+__device__ __forceinline__ uint32_t bf16_up(float f) {
+  const uint32_t b = __float_as_uint(f);
+  return (b >> 16) + ((b & 0xFFFFu) ? 1u : 0u);
+}
 
 // Wave-wide reductions (wave64) through LDS-free cross-lane shuffles.
 __device__ __forceinline__ float wave_sum(float v) {

@@ -18,9 +18,9 @@ namespace mapl {
 
 namespace {
 
-constexpr int GQ_THREADS = 256, GQ_TOK = 256, GQ_KMAX = 256, GQ_LDS_FLOATS = 16384;  // 64 KiB
+constexpr int GQ_THREADS = 256, GQ_TOK = 128, GQ_KMAX = 256, GQ_LDS_FLOATS = 16384;  // 64 KiB at most
 
-template <int GPW>  // groups per wave
+template <int GPW>  // groups per wave, searched side by side (independent chains)
 __global__ __launch_bounds__(GQ_THREADS) void k_grvq(const float* __restrict__ Z0, const float* __restrict__ C,
                                                      int T, int r, int L, int K, uint8_t* __restrict__ codes) {
   extern __shared__ float cb[];  // [L][GW][K][2]
@@ -41,30 +41,41 @@ __global__ __launch_bounds__(GQ_THREADS) void k_grvq(const float* __restrict__ Z
     uint32_t word[8];  // codes of this wave's groups, per round (GPW <= 4 bytes each)
 #pragma unroll
     for (int l = 0; l < 8; ++l) word[l] = 0;
+    float2 R[GPW];
 #pragma unroll
-    for (int q = 0; q < GPW; ++q) {
-      const int gi = wave * GPW + q, g = g0 + gi;
-      float2 R = valid ? *(const float2*)(Z0 + (int64_t)t * r + 2 * g) : make_float2(0.f, 0.f);
-      for (int l = 0; l < L; ++l) {
-        const float* cl = cb + ((int64_t)l * GW + gi) * K * 2;
-        float best = INFINITY;
-        int bj = 0;
-        for (int j = 0; j < K; j += 2) {
-          const float4 c2 = *(const float4*)(cl + 2 * j);  // codewords j, j + 1 (broadcast)
-          float dx = R.x - c2.x, dy = R.y - c2.y;
+    for (int q = 0; q < GPW; ++q)
+      R[q] = valid ? *(const float2*)(Z0 + (int64_t)t * r + 2 * (g0 + wave * GPW + q)) : make_float2(0.f, 0.f);
+    for (int l = 0; l < L; ++l) {
+      const float* cl[GPW];
+      float best[GPW];
+      int bj[GPW];
+#pragma unroll
+      for (int q = 0; q < GPW; ++q) {
+        cl[q] = cb + ((int64_t)l * GW + wave * GPW + q) * K * 2;
+        best[q] = INFINITY;
+        bj[q] = 0;
+      }
+      for (int j = 0; j < K; j += 2) {
+#pragma unroll
+        for (int q = 0; q < GPW; ++q) {
+          const float4 c2 = *(const float4*)(cl[q] + 2 * j);  // codewords j, j + 1 (broadcast)
+          float dx = R[q].x - c2.x, dy = R[q].y - c2.y;
           float dd = fmaf(dy, dy, dx * dx);
-          if (dd < best) { best = dd; bj = j; }
-          dx = R.x - c2.z;
-          dy = R.y - c2.w;
+          if (dd < best[q]) { best[q] = dd; bj[q] = j; }
+          dx = R[q].x - c2.z;
+          dy = R[q].y - c2.w;
           dd = fmaf(dy, dy, dx * dx);
-          if (dd < best) { best = dd; bj = j + 1; }
+          if (dd < best[q]) { best[q] = dd; bj[q] = j + 1; }
         }
-        const float2 w = *(const float2*)(cl + 2 * bj);
-        R.x -= w.x;
-        R.y -= w.y;
+      }
+#pragma unroll
+      for (int q = 0; q < GPW; ++q) {
+        const float2 w = *(const float2*)(cl[q] + 2 * bj[q]);
+        R[q].x -= w.x;
+        R[q].y -= w.y;
 #pragma unroll
         for (int ll = 0; ll < 8; ++ll)
-          if (ll == l) word[ll] |= (uint32_t)bj << (8 * q);
+          if (ll == l) word[ll] |= (uint32_t)bj[q] << (8 * q);
       }
     }
     if (valid) {
@@ -85,7 +96,7 @@ __global__ __launch_bounds__(GQ_THREADS) void k_grvq(const float* __restrict__ Z
 
 // Groups per workgroup so that L rounds of K two-float codewords fit the LDS.
 static int grvq_groups_per_wg(int L, int K, int G) {
-  for (int gw = 16; gw >= 4; gw /= 2)
+  for (int gw = 8; gw >= 4; gw /= 2)
     if ((int64_t)L * K * gw * 2 <= GQ_LDS_FLOATS && G % gw == 0) return gw;
   return 0;
 }

@@ -59,11 +59,11 @@ __device__ __forceinline__ void transpose_tile(int bx, int by, const void* __res
 }
 
 // One wave per (stage, codeword slot of a 64-codeword chunk): the bf16 copy
-// with the squared norm appended as three bf16 pieces (rows of r + 16), and
-// the fp32 squared norm, laid out per chunk as 64 consecutive floats.  The
-// pieces: hi = bf16(s), mid = bf16(s - hi), lo = bf16(s - hi - mid); each
-// difference is exact in fp32 and an fp32 value has 24 significant bits, so
-// hi + mid + lo = s exactly, in any order of addition.
+// with the norm columns of the RVQ screen appended (rows of r + 16), and the
+// fp32 squared norm, laid out per chunk as 64 consecutive floats.  A squared
+// norm x is stored as hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi -
+// mid); each difference is exact in fp32 and an fp32 value has 24
+// significant bits, so hi + mid + lo = x exactly, in any order of addition.
 __device__ __forceinline__ void prep_codebook_block(int bx, const float* __restrict__ C, int L, int K, int r,
                                                     bf16_t* __restrict__ Cb, float* __restrict__ meta) {
   const int nch = (K + 63) / 64;
@@ -72,24 +72,53 @@ __device__ __forceinline__ void prep_codebook_block(int bx, const float* __restr
   const int l = w / (nch * 64), slot = w % (nch * 64);
   const int j = slot;  // codeword index within stage l
   const int cols = rvq_cb_cols(r);
-  float s = 0.f;
+  float s = 0.f, es = 0.f;
   if (j < K) {
     const float* row = C + ((int64_t)l * K + j) * r;
     for (int c = lane; c < r; c += 64) {
       const float v = row[c];
       s += v * v;
-      Cb[((int64_t)l * K + j) * cols + c] = (bf16_t)f2bf(v);
+      const uint32_t vb = f2bf(v);
+      const float d = v - bf2f(vb);  // the rounding error, exact in fp32
+      es += d * d;
+      Cb[((int64_t)l * K + j) * cols + c] = (bf16_t)vb;
     }
   }
   s = wave_sum(s);
+  es = wave_sum(es);
+  // ||C_j - bf16(C_j)|| rounded up: es carries at most r ulps of accumulation error
+  const float eu = sqrtf(es) * (1.0f + 1.0f / 32768.0f);
   if (j < K && lane < 16) {
-    const uint32_t hi = f2bf(s);
-    const float r1 = s - bf2f(hi);
+    // columns r .. r+2: the reduced norm n' = s - 1.01 k2 s in three pieces
+    // (each difference exact in fp32, so they sum to n' exactly); columns
+    // r+3, r+4: ||C_j|| rounded up, c_hi + c_lo >= sqrt(s) (1 + 2^-15), which
+    // bounds the norm of the fp32 codeword above (s carries at most r ulps
+    // of accumulation error); r+5: the rounding-error norm, rounded up to
+    // bf16; the rest zero
+    const float np = s - s * (RVQ_K2_SLACK * rvq_margin_k2(r));
+    const uint32_t hi = f2bf(np);
+    const float r1 = np - bf2f(hi);
     const uint32_t mid = f2bf(r1);
     const uint32_t lo = f2bf(r1 - bf2f(mid));
-    Cb[((int64_t)l * K + j) * cols + r + lane] = (bf16_t)(lane == 0 ? hi : lane == 1 ? mid : lane == 2 ? lo : 0u);
+    const float cu = sqrtf(s) * (1.0f + 1.0f / 32768.0f);
+    const uint32_t chi = f2bf(cu);
+    const float cr = cu - bf2f(chi);
+    // toward +infinity: up for a positive remainder, magnitude truncated for a negative one
+    const uint32_t clo = cr > 0.f ? bf16_up(cr) : (__float_as_uint(cr) >> 16);
+    uint32_t v = 0u;
+    if (lane == 0) v = hi;
+    if (lane == 1) v = mid;
+    if (lane == 2) v = lo;
+    if (lane == 3) v = chi;
+    if (lane == 4) v = clo;
+    if (lane == 5) v = bf16_up(eu);
+    Cb[((int64_t)l * K + j) * cols + r + lane] = (bf16_t)v;
   }
-  if (lane == 0) meta[((int64_t)l * nch + j / 64) * 64 + (j % 64)] = s;
+  if (lane == 0) {
+    const int64_t m = ((int64_t)l * nch + j / 64) * 64 + (j % 64);
+    meta[m] = s;
+    meta[(int64_t)L * nch * 64 + m] = eu;
+  }
 }
 
 // One thread per (token, 8 columns): 16 B stores, independent gathers.

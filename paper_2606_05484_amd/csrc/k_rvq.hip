@@ -3,27 +3,33 @@
 // current residual R_l and subtracts it.  Ties go to the lowest index.
 //
 // Decision procedure (exact with respect to the fp32 residual):
-//   screen  s~_j = ||C_j||^2 - 2 R~ . C~_j on the bf16 matrix units with
-//           R~ = bf16(R), C~ = bf16(C): the first k-step of every tile
-//           multiplies three extra codeword columns (||C_j||^2 split into
-//           three bf16 pieces that sum to it exactly) by ones, so the
-//           accumulator holds ||C_j||^2 (fp32, exact) before the products
-//           with the second operand bf16(-2R) = -2 R~ (exact) follow.  The
-//           true s_j = ||C_j||^2 - 2 R.C_j differs from s~_j by at most
-//           Delta = k1 ||R|| max_j||C_j|| + k2 max_j||C_j||^2 (bf16 rounding
-//           of both operands, fp32 accumulation and norms, the index tag
-//           below; constants inflated, see rvq_margin_k1/k2), one margin per
-//           token and round.
-//   tag     the low 4 mantissa bits of s~_j are replaced by the codeword's
-//           slot among the 16 scores a lane sees per tile, so a plain float
-//           min also yields the position; the tile is tracked separately.
-//   pass 1  per lane: smallest tagged score m1 (and its tile) and the
-//           second smallest m2 (v_med3); the nearest codeword lies in
-//           {j : s~_j <= m1 + 2 Delta}; if m2 exceeds that bound the set
-//           is a single codeword and the decision is final.
-//   pass 2  (only when a token of the workgroup is ambiguous) re-screens
-//           and lists every candidate; the candidates are rescored exactly
-//           in fp32 as sum_c (R_c - C_jc)^2.
+//   screen  on the bf16 matrix units with R~ = bf16(R), C~ = bf16(C), the
+//           first k-step of every tile multiplying the codeword's norm
+//           columns by the token's norm operand, so the accumulator ends at
+//           a certified lower bound of the exact score s_j = ||C_j||^2 -
+//           2 R.C_j:  L_j = s~_j - Delta'_j,  s~_j = ||C_j||^2 - 2 R~.C~_j,
+//           where Delta'_j >= Delta_j bounds |s~_j - s_j| from the actual
+//           bf16 rounding-error norms of the token's residual and of the
+//           codeword, fp32 accumulation and norms, and the index tag below
+//           (see rvq_margin_ka/k2 and the norm columns in common.hpp): the
+//           margin is each codeword's own, not the codebook's largest.
+//   tag     the low 9 mantissa bits of L_j hold the codeword's tile (mod 32)
+//           and slot among the 16 scores a lane sees per tile, so a plain
+//           float min / med3 also yields the position (the codeword itself
+//           for K <= 1024).
+//   pass 1  per lane: the two smallest keys (tagged with the slot only).
+//           The nearest codeword j* satisfies L_j* <= s_j* <= s_j1 <= U =
+//           L_j1 + (1 + 1.03) Delta_j1 for the smallest key j1, so it is
+//           among {j : L_j <= U}: a single codeword when the token's second
+//           key exceeds U (final).
+//   pass 2  (only in a workgroup with an open token, K <= 1024) re-screens
+//           keeping the six smallest keys per lane, tagged with tile and
+//           slot so each names its codeword; when both halves' sixth keys
+//           exceed U the candidates are among the kept keys and are
+//           rescored exactly in fp32 by the token's two lanes.
+//   pass 3  (only when a token is still open) re-screens and lists every
+//           candidate; they are rescored exactly in fp32 as
+//           sum_c (R_c - C_jc)^2.
 // The fp32 residual stays in registers across rounds, updated as
 // R_{l+1} = R_l - C_l[code_l]; the rescoring reads it from there (through a
 // per-wave LDS row), so screening and rescoring see the same R.
@@ -76,8 +82,22 @@ __device__ __forceinline__ int load_code(const void* codes, int cb, int64_t idx)
 // Row of a 32-codeword tile held by accumulator slot e of a lane in `half`.
 __device__ __forceinline__ int rq_row(int e, int half) { return 8 * (e >> 2) + 4 * half + (e & 3); }
 
-__device__ __forceinline__ float rq_tag(float s, int e) {
+// A score tagged in its low 9 mantissa bits with its tile mod 32 (bits 4..8)
+// and its slot among the lane's 16 scores of the tile (bits 0..3): a plain
+// float min / med3 then also carries the position, and with the lane's half
+// (K <= 1024) the key names its codeword.  te = ((tile & 31) << 4) | slot is
+// uniform across the wave, so the tag costs one vector operation.
+__device__ __forceinline__ float rq_tag(float s, uint32_t te) {
+  return __uint_as_float((__float_as_uint(s) & ~511u) | te);
+}
+// The lean form: the slot alone (inline constants, one operation); the tile
+// of the smallest key is tracked beside the fold.
+__device__ __forceinline__ float rq_tag_slot(float s, int e) {
   return __uint_as_float((__float_as_uint(s) & ~15u) | (uint32_t)e);
+}
+__device__ __forceinline__ int rq_tag_index(float key, int half) {
+  const uint32_t b = __float_as_uint(key);
+  return (int)((b >> 4) & 31u) * 32 + rq_row((int)(b & 15u), half);
 }
 
 // Per-workgroup LDS of the rounds besides the three codebook stages.
@@ -85,7 +105,6 @@ struct RqSmall {
   int cand_cnt[RQ_TOK];
   uint16_t cand[RQ_TOK][RQ_CAP];
   int amb_s[RQ_TOK];
-  float red_s[4];
 };
 
 // The L rounds for the workgroup's 128 tokens (blockIdx.x), given each
@@ -104,7 +123,6 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
   auto& cand_cnt = sm.cand_cnt;
   auto& cand = sm.cand;
   auto& amb_s = sm.amb_s;
-  auto& red_s = sm.red_s;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
   const int tl = wave * 32 + (lane & 31);  // token within the workgroup
@@ -141,45 +159,44 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
                                                    : RQ_OOB,
                                                0, 0, 0);
   };
-  // this thread's share of the largest ||C_j||^2 of round l (zero past K)
-  auto n2share = [&](int l) {
-    const float* n2g = a.meta + (int64_t)l * nchunks * 64;
-    float m = 0.f;
-    for (int j = tid; j < nchunks * 64; j += RQ_THREADS) m = fmaxf(m, n2g[j]);
-    return m;
-  };
-
-  // A round's first two chunks and its norm maxima are requested before the
-  // previous round's residual update, so their latencies overlap.
+  // A round's first two chunks are requested before the previous round's
+  // residual update, so their latencies overlap.
   issue_l(0, 0, s0);
   issue_l(0, 1, s1);
-  float n2next = n2share(0);
 
   // res: fp32 residual of the lane's token, R_{l+1} = R_l - C_l[code_l]
   for (int l = 0; l < a.L; ++l) {
     auto issue = [&](int q, bf16_t* sc) { issue_l(l, q, sc); };
 
-    float n2max = n2next;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) n2max = fmaxf(n2max, __shfl_xor(n2max, o, WAVE));
-    if (lane == 0) red_s[wave] = n2max;
-
-    // bf16(-2 R_l) in B-fragment layout and ||R_l||^2 from the fp32 residual
+    // bf16(-2 R_l) in B-fragment layout, ||R_l||^2 and ||R_l - bf16(R_l)||^2
+    // from the fp32 residual (-2 bf16(v) = bf16(-2 v), and v - bf16(v) is
+    // exact in fp32)
     uint4 rb[NK16];
-    float rn2 = 0.f;
+    float rn2 = 0.f, er2 = 0.f;
 #pragma unroll
     for (int s = 0; s < NK16; ++s) {
       const float* v = res[s];
+      uint32_t w[4];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) rn2 += v[e] * v[e];
-      rb[s] = make_uint4(pack_bf2(-2.f * v[0], -2.f * v[1]), pack_bf2(-2.f * v[2], -2.f * v[3]),
-                         pack_bf2(-2.f * v[4], -2.f * v[5]), pack_bf2(-2.f * v[6], -2.f * v[7]));
+      for (int e = 0; e < 4; ++e) {
+        w[e] = pack_bf2(-2.f * v[2 * e], -2.f * v[2 * e + 1]);
+        const float d0 = fmaf(0.5f, __uint_as_float(w[e] << 16), v[2 * e]);
+        const float d1 = fmaf(0.5f, __uint_as_float(w[e] & 0xFFFF0000u), v[2 * e + 1]);
+        rn2 = fmaf(v[2 * e], v[2 * e], rn2);
+        rn2 = fmaf(v[2 * e + 1], v[2 * e + 1], rn2);
+        er2 = fmaf(d0, d0, er2);
+        er2 = fmaf(d1, d1, er2);
+      }
+      rb[s] = make_uint4(w[0], w[1], w[2], w[3]);
     }
     rn2 += __shfl_xor(rn2, 32, WAVE);
-    __syncthreads();  // red_s
-    n2max = fmaxf(fmaxf(red_s[0], red_s[1]), fmaxf(red_s[2], red_s[3]));
-    const float delta =
-        rvq_margin_k1(R) * sqrtf(rn2) * sqrtf(n2max) * 1.0002f + rvq_margin_k2(R) * n2max + 1e-30f;
+    er2 += __shfl_xor(er2, 32, WAVE);
+    // norms rounded up (each sum carries at most R ulps of accumulation error)
+    const float rnorm = sqrtf(rn2) * (1.0f + 1.0f / 32768.0f);
+    const float enorm = sqrtf(er2) * (1.0f + 1.0f / 32768.0f);
+    // the margin's coefficient of ||C_j|| (b) and of e_j (c)
+    const float bco = 2.0f * enorm * 1.0078125f + rvq_margin_ka(R) * rnorm;
+    const float cco = 2.0f * rnorm;
 
     // One screening pass over all chunks.  Per 32-codeword tile the fold
     // callbacks see begin(), score(acc, tile, e) for e = 0..15, end(tile).
@@ -196,8 +213,14 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
     // one fragment read per product.
     constexpr int P = NK16 + 1;
     constexpr int FPS = (16 + P - 1) / P;  // scores folded per product step
-    // second operand of the norm step: ones in k = 0..2 of the block
-    const uint4 rbn = half == 0 ? make_uint4(0x3F803F80u, 0x00003F80u, 0u, 0u) : make_uint4(0u, 0u, 0u, 0u);
+    // second operand of the norm step: ones in k = 0..2 (the reduced norm's
+    // pieces), -b in k = 3, 4 (times the norm's pieces) and -c in k = 5
+    // (times the rounding-error norm) of the block: the screen yields the
+    // lower bound L_j of each codeword's score
+    const uint32_t bbits = bf16_up(bco * RVQ_K1_SLACK) | 0x8000u;
+    const uint32_t cbits = bf16_up(cco * RVQ_K1_SLACK) | 0x8000u;
+    const uint4 rbn = half == 0 ? make_uint4(0x3F803F80u, 0x3F80u | (bbits << 16), bbits | (cbits << 16), 0u)
+                                : make_uint4(0u, 0u, 0u, 0u);
     auto pass = [&](auto&& fbegin, auto&& fscore, auto&& fend, bool first) {
       if (!first) {
         issue(0, s0);
@@ -290,29 +313,124 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       fold_all(pend, pend_tile);
     };
 
-    // ---- pass 1: smallest and second-smallest tagged score per lane
-    float m1 = INFINITY, m2 = INFINITY, m1_in = INFINITY;
-    int tile1 = 0;
-    pass([&]() { m1_in = m1; },
-         [&](const f32x16_t& acc, int, auto ec) {
-           constexpr int E = decltype(ec)::value;
-           const float key = rq_tag(acc[E], E);
-           m2 = __builtin_amdgcn_fmed3f(m1, m2, key);
-           m1 = __builtin_amdgcn_fmed3f(m1, key, -3.40282347e38f);  // min for finite keys
-         },
-         [&](int tile) { tile1 = m1 < m1_in ? tile : tile1; }, true);
-    int j1 = tile1 * 32 + rq_row((int)(__float_as_uint(m1) & 15u), half);
+    // Decision.  Each key is a lower bound L_j of its codeword's exact score
+    // (the screen subtracts that codeword's own error bound), and s_j1 <= U =
+    // L_j1 + (RVQ_SUB_FACTOR + 1) Delta_j1 for the smallest key j1 (of equal
+    // keys, half 0's), so only codewords with L_j <= U can be nearest.
+    //  pass 1 (every workgroup): final when the token's second key exceeds U;
+    //  pass 2 (workgroups with an open token, K <= 1024): the six smallest
+    //    keys per lane, tagged to name their codewords; when both halves'
+    //    sixth keys exceed U the candidates are the kept keys <= U, rescored
+    //    exactly;
+    //  pass 3 (tokens still open): every candidate listed and rescored.
+    const float* n2l = a.meta + (int64_t)l * nchunks * 64;
+    const float* e2l = n2l + (int64_t)a.L * nchunks * 64;
+    auto margin = [&](int j) {  // Delta_j, rounded up
+      const int jj = min(max(j, 0), nchunks * 64 - 1);
+      const float n2 = n2l[jj];
+      return (cco * e2l[jj] + bco * (sqrtf(n2) * (1.0f + 1.0f / 32768.0f)) + rvq_margin_k2(R) * n2) * 1.0002f +
+             1e-30f;
+    };
+    // ---- pass 1: the two smallest keys per lane
+    int j1;
+    bool fin;
+    float thr;
     {
-      const float o_m1 = __shfl_xor(m1, 32, WAVE);
-      const float o_m2 = __shfl_xor(m2, 32, WAVE);
-      const int o_j1 = __shfl_xor(j1, 32, WAVE);
-      const float nm2 = fminf(fmaxf(m1, o_m1), fminf(m2, o_m2));
-      if (o_m1 < m1 || (o_m1 == m1 && o_j1 < j1)) j1 = o_j1;
-      m1 = fminf(m1, o_m1);
-      m2 = nm2;
+      float m1 = INFINITY, m2 = INFINITY, m1_in = INFINITY;
+      int tile1 = 0;
+      pass([&]() { m1_in = m1; },
+           [&](const f32x16_t& acc, int, auto ec) {
+             constexpr int E = decltype(ec)::value;
+             const float key = rq_tag_slot(acc[E], E);
+             m2 = __builtin_amdgcn_fmed3f(m1, m2, key);
+             m1 = __builtin_amdgcn_fmed3f(m1, key, -3.40282347e38f);  // min for finite keys
+           },
+           [&](int tile) { tile1 = m1 < m1_in ? tile : tile1; }, true);
+      const float o1 = __shfl_xor(m1, 32, WAVE), o2 = __shfl_xor(m2, 32, WAVE);
+      const int own_j1 = tile1 * 32 + rq_row((int)(__float_as_uint(m1) & 15u), half);
+      const int o_j1 = __shfl_xor(own_j1, 32, WAVE);
+      j1 = (m1 < o1 || (m1 == o1 && half == 0)) ? own_j1 : o_j1;
+      const float k1 = fminf(m1, o1);
+      const float k2 = fminf(fmaxf(m1, o1), fminf(m2, o2));
+      thr = k1 + (RVQ_SUB_FACTOR + 1.0f) * margin(j1);
+      fin = !valid || k2 > thr;
     }
-    const float thr = m1 + 2.0002f * delta;
-    const bool amb = valid && !(m2 > thr);
+    const bool names = a.K <= 1024;
+    const int any_open = __syncthreads_or(fin ? 0 : 1);
+    bool multi = false;
+    if (any_open && names) {
+      // ---- pass 2: the six smallest keys per lane, tagged with tile and slot
+      float m1 = INFINITY, m2 = INFINITY, m3 = INFINITY, m4 = INFINITY, m5 = INFINITY, m6 = INFINITY;
+      pass([&]() {},
+           [&](const f32x16_t& acc, int tile, auto ec) {
+             constexpr int E = decltype(ec)::value;
+             const float key = rq_tag(acc[E], ((uint32_t)(tile & 31) << 4) | (uint32_t)E);
+             m6 = __builtin_amdgcn_fmed3f(m5, m6, key);
+             m5 = __builtin_amdgcn_fmed3f(m4, m5, key);
+             m4 = __builtin_amdgcn_fmed3f(m3, m4, key);
+             m3 = __builtin_amdgcn_fmed3f(m2, m3, key);
+             m2 = __builtin_amdgcn_fmed3f(m1, m2, key);
+             m1 = __builtin_amdgcn_fmed3f(m1, key, -3.40282347e38f);
+           },
+           [&](int) {}, false);
+      const float o1 = __shfl_xor(m1, 32, WAVE), o2 = __shfl_xor(m2, 32, WAVE);
+      const float o3 = __shfl_xor(m3, 32, WAVE), o4 = __shfl_xor(m4, 32, WAVE);
+      const float o5 = __shfl_xor(m5, 32, WAVE), o6 = __shfl_xor(m6, 32, WAVE);
+      const bool own_first = m1 < o1 || (m1 == o1 && half == 0);
+      const int jd = rq_tag_index(own_first ? m1 : o1, own_first ? half : half ^ 1);
+      const float Ud = fminf(m1, o1) + (RVQ_SUB_FACTOR + 1.0f) * margin(jd);
+      if (!fin) thr = Ud;
+      multi = !fin && m6 > Ud && o6 > Ud;
+      if (__any(multi)) {
+        // exact fp32 rescoring over the kept keys, half 0's then half 1's,
+        // each lane summing its half of the residual (in registers), halves added
+        float best = INFINITY;
+        int bj = 0x7fffffff, ncand = 0;
+        static_for<0, 12>([&](auto ic) {
+          constexpr int I = decltype(ic)::value, P = I % 6;
+          const bool from_own = (I < 6) == (half == 0);
+          const float mine = P == 0 ? m1 : P == 1 ? m2 : P == 2 ? m3 : P == 3 ? m4 : P == 4 ? m5 : m6;
+          const float theirs = P == 0 ? o1 : P == 1 ? o2 : P == 2 ? o3 : P == 3 ? o4 : P == 4 ? o5 : o6;
+          const float key = from_own ? mine : theirs;
+          const int j = rq_tag_index(key, I / 6);
+          const bool cand = multi && (unsigned)j < (unsigned)a.K && key <= Ud;
+          float dpart = 0.f;
+          if (cand) {
+            const float* cw = a.C + ((int64_t)l * a.K + j) * R + 8 * half;
+#pragma unroll
+            for (int s = 0; s < NK16; ++s) {
+              const float4 p0 = *(const float4*)(cw + 16 * s), p1 = *(const float4*)(cw + 16 * s + 4);
+              const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float u = res[s][e] - pv[e];
+                dpart = fmaf(u, u, dpart);
+              }
+            }
+          }
+          const float dd = dpart + __shfl_xor(dpart, 32, WAVE);
+          if (cand) {
+            ++ncand;
+            if (dd < best || (dd == best && j < bj)) {
+              best = dd;
+              bj = j;
+            }
+          }
+        });
+        if (multi && ncand > 0) j1 = bj;
+        if (a.stats) {
+          const int nm = __popcll(__ballot(multi && half == 0));
+          int nc = multi && half == 0 ? ncand : 0;
+#pragma unroll
+          for (int o = 32; o > 0; o >>= 1) nc += __shfl_xor(nc, o, WAVE);
+          if (lane == 0 && nm) {
+            atomicAdd(&a.stats[0], nm);
+            atomicAdd(&a.stats[1], nc);
+          }
+        }
+      }
+    }
+    const bool amb = !fin && !multi;  // pass 3: a full candidate listing
     if (half == 0) {
       amb_s[tl] = amb ? 1 : 0;
       cand_cnt[tl] = 0;
@@ -320,16 +438,17 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
     const int any_amb = __syncthreads_or(amb ? 1 : 0);
     if (a.stats && tid == 0) {
       atomicAdd(&a.stats[4], 1);
-      if (any_amb) atomicAdd(&a.stats[3], 1);
+      if (any_open && names) atomicAdd(&a.stats[3], 1);
+      if (any_amb) atomicAdd(&a.stats[5], 1);
     }
 
     int jstar = j1;
     if (any_amb) {
-      // ---- pass 2: list every candidate of the ambiguous tokens
+      // ---- pass 3: list every candidate of the open tokens
       pass([&]() {},
            [&](const f32x16_t& acc, int tile, auto ec) {
              constexpr int E = decltype(ec)::value;
-             if (amb && tile >= 0 && rq_tag(acc[E], E) <= thr) {
+             if (amb && tile >= 0 && rq_tag(acc[E], ((uint32_t)(tile & 31) << 4) | (uint32_t)E) <= thr) {
                const int idx = atomicAdd(&cand_cnt[tl], 1);
                if (idx < RQ_CAP) cand[tl][idx] = (uint16_t)(tile * 32 + rq_row(E, half));
              }
@@ -405,7 +524,6 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       // rescoring's), so stages 0 and 1 are free
       issue_l(l + 1, 0, s0);
       issue_l(l + 1, 1, s1);
-      n2next = n2share(l + 1);
       const float* cw = a.C + ((int64_t)l * a.K + jstar) * R + 8 * half;
 #pragma unroll
       for (int s = 0; s < NK16; ++s) {
@@ -422,9 +540,9 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       else
         ((uint16_t*)a.codes)[(int64_t)t * a.L + l] = (uint16_t)jstar;
     }
-    // no barrier: the next round's shared state (red_s, and amb_s, cand_cnt,
-    // cand and rvs, which only the token's own wave touches) is written
-    // after barriers that every wave reaches only once done with this round
+    // no barrier: the next round's shared state (amb_s, cand_cnt, cand and
+    // rvs, which only the token's own wave touches) is written after
+    // barriers that every wave reaches only once done with this round
   }
 }
 

@@ -84,10 +84,12 @@ hipError_t launch_transpose_into(const void* src, int src_f32, int rows, int col
 // Screening copy of the codebooks, rows of rvq_cb_cols(r) = r + 16 bf16:
 // Cb[l][j][0:r] = bf16(C[l][j]), Cb[l][j][r:r+3] = hi, mid, lo with
 // hi + mid + lo = ||C_j||^2 exactly (fp32 split into three bf16 pieces),
-// Cb[l][j][r+3:r+16] = 0.  meta[l][chunk][64]: ||C_j||^2 in fp32 per
-// 64-codeword chunk (zero past K).
+// Cb[l][j][r+3:r+5] = ||C_j|| rounded up (two pieces), Cb[l][j][r+5] =
+// ||C_j - bf16(C_j)|| rounded up, Cb[l][j][r+6:r+16] = 0.  meta[0][l][chunk][64]:
+// ||C_j||^2 in fp32 per 64-codeword chunk, meta[1][l][chunk][64]:
+// ||C_j - bf16(C_j)|| rounded up (zero past K).
 hipError_t launch_prep_codebook(const float* C, int L, int K, int r, bf16_t* Cb, float* meta, hipStream_t s);
-inline int64_t rvq_meta_floats(int L, int K) { return (int64_t)L * ((K + 63) / 64) * 64; }
+inline int64_t rvq_meta_floats(int L, int K) { return 2 * (int64_t)L * ((K + 63) / 64) * 64; }
 __host__ __device__ constexpr int rvq_cb_cols(int r) { return r + 16; }
 
 // ---------------------------------------------------------------- receiver-side operand
@@ -150,12 +152,13 @@ struct RvqArgs {
   const float* Z0;     // [T,r] fp32 unquantised coordinates
   const bf16_t* Cb;    // [L,K,r+16] bf16 screening copy with the split norms (rvq_cb_cols)
   const float* C;      // [L,K,r] fp32 codebooks
-  const float* meta;   // [L][ceil(K/64)][64]: ||C_j||^2 (rvq_meta_floats)
+  const float* meta;   // [2][L][ceil(K/64)][64]: ||C_j||^2, ||C_j - bf16(C_j)|| (rvq_meta_floats)
   int T, r, L, K;
   void* codes; int code_bytes;  // [T,L]
   int* stats;          // [8] optional counters, may be null: tokens rescored, their candidates,
-                       // candidate-list overflows, (workgroup, round) pairs with a second
-                       // screening pass, (workgroup, round) pairs in total
+                       // candidate-list overflows, (workgroup, round) pairs with the deep
+                       // second pass, (workgroup, round) pairs in total, pairs with the
+                       // listing pass
 };
 hipError_t launch_rvq(const RvqArgs& a, hipStream_t s);
 // The encoder in one launch: Z0 = [X | a] W as launch_gemm_tn computes it

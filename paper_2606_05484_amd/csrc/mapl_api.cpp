@@ -72,9 +72,10 @@ struct ProfRec {
 std::mutex g_prof_mu;
 bool g_prof = false;
 bool g_prof_rvq = false;      // mapl_profile(2): also collect the RVQ decision counters
-long long g_rvq_stats[5] = {0, 0, 0, 0, 0};
-const char* const kRvqStatNames[5] = {"rvq:tokens_rescored", "rvq:candidates", "rvq:list_overflows",
-                                      "rvq:second_pass_blocks", "rvq:blocks"};
+constexpr int kRvqStats = 6;
+long long g_rvq_stats[kRvqStats] = {0, 0, 0, 0, 0, 0};
+const char* const kRvqStatNames[kRvqStats] = {"rvq:tokens_rescored", "rvq:candidates", "rvq:list_overflows",
+                                              "rvq:deep_pass_blocks", "rvq:blocks", "rvq:listing_pass_blocks"};
 std::vector<ProfRec> g_prof_recs;
 std::vector<hipEvent_t> g_prof_pool;
 
@@ -466,7 +467,7 @@ extern "C" int mapl_encode(const mapl_codec_desc* desc, const void* X, const int
       MAPL_HIP(hipMemcpyAsync(h, a.stats, sizeof h, hipMemcpyDeviceToHost, s));
       MAPL_HIP(hipStreamSynchronize(s));
       std::lock_guard<std::mutex> lk(g_prof_mu);
-      for (int i = 0; i < 5; ++i) g_rvq_stats[i] += h[i];
+      for (int i = 0; i < kRvqStats; ++i) g_rvq_stats[i] += h[i];
     }
     return MAPL_OK;
   }
@@ -1289,11 +1290,11 @@ extern "C" int mapl_profile(int enable) {
 
 extern "C" int mapl_profile_report(char* buf, size_t bytes) {
   std::vector<ProfRec> recs;
-  long long rvq[5];
+  long long rvq[kRvqStats];
   {
     std::lock_guard<std::mutex> lk(g_prof_mu);
     recs.swap(g_prof_recs);
-    for (int i = 0; i < 5; ++i) {
+    for (int i = 0; i < kRvqStats; ++i) {
       rvq[i] = g_rvq_stats[i];
       g_rvq_stats[i] = 0;
     }
@@ -1331,7 +1332,7 @@ extern "C" int mapl_profile_report(char* buf, size_t bytes) {
     outs += line;
   }
   if (rvq[4] > 0)
-    for (int i = 0; i < 5; ++i) {
+    for (int i = 0; i < kRvqStats; ++i) {
       snprintf(line, sizeof line, "%s %lld 0\n", kRvqStatNames[i], rvq[i]);
       outs += line;
     }
