@@ -677,8 +677,7 @@ def main():
             "encode_vs_headline": (enc_us / kern["enc:gemm_rvq"][1]) if enc_us and "enc:gemm_rvq" in kern else None,
             "rvq_tokens_rescored_frac": st.get("rvq:tokens_rescored", 0) / (5.0 * T * L),
             "rvq_candidates_per_rescored_token": st.get("rvq:candidates", 0) / max(1, st.get("rvq:tokens_rescored", 0)),
-            "rvq_deep_pass_frac": st.get("rvq:deep_pass_blocks", 0) / max(1, st.get("rvq:blocks", 0)),
-            "rvq_listing_pass_frac": st.get("rvq:listing_pass_blocks", 0) / max(1, st.get("rvq:blocks", 0)),
+            "rvq_second_pass_frac": st.get("rvq:second_pass_blocks", 0) / max(1, st.get("rvq:blocks", 0)),
             "rvq_list_overflows": st.get("rvq:list_overflows", 0),
         }
         del chs

@@ -298,9 +298,9 @@ int mapl_version(void);
  * per kernel, in the order of each name's first launch (names are
  * "<call>:<kernel>"), followed, after RVQ counting, by lines "name count 0"
  * for rvq:tokens_rescored, rvq:candidates (summed over rescored tokens),
- * rvq:list_overflows, rvq:deep_pass_blocks, rvq:blocks and
- * rvq:listing_pass_blocks ((workgroup, round) pairs with the deep second
- * screening pass, in total, and with the candidate-listing pass), into buf
+ * rvq:list_overflows, rvq:second_pass_blocks and rvq:blocks ((workgroup,
+ * round) pairs with the second, candidate-listing screen, and in total),
+ * into buf
  * (NUL-terminated, at most `bytes` bytes), and forgets the records.  Not for
  * use under stream capture.  Returns MAPL_OK, MAPL_E_HIP if an event could
  * not be resolved, or MAPL_E_WORKSPACE if buf was too small (the text is

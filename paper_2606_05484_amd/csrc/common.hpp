@@ -66,10 +66,11 @@ __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 
 // two terms (Cauchy-Schwarz, ||C~_j|| <= ||C_j|| + e_j), and
 //   ka = (8 R 2^-24            (fp32 accumulation of 2R~.C~, any order,
 //                               relative error up to 2 u per addition)
-//        + 2^-20 + 2^-12) (1 + 2^-7)  (norm rounding; the 9-bit index tag,
-//                               which moves a score by at most 2^-14 of
-//                               |s~_j| <= ||C_j||^2 + 2.02 ||R|| ||C_j||,
-//                               doubled; ||R~|| ||C~|| against ||R|| ||C||)
+//        + 2^-20 + 2^-12) (1 + 2^-7)  (norm rounding; an index tag in up
+//                               to 9 low mantissa bits, which moves a score
+//                               by at most 2^-14 of |s~_j| <= ||C_j||^2 +
+//                               2.02 ||R|| ||C_j||, doubled; ||R~|| ||C~||
+//                               against ||R|| ||C||)
 //   k2 = 4 (R + 4) 2^-24 + 2^-13 (accumulation and fp32 rounding of
 //                               ||C_j||^2; the index tag, doubled)
 // The actual rounding-error norms replace the componentwise worst case

@@ -13,26 +13,23 @@
 //           codeword, fp32 accumulation and norms, and the index tag below
 //           (see rvq_margin_ka/k2 and the norm columns in common.hpp): the
 //           margin is each codeword's own, not the codebook's largest.
-//   tag     the low 9 mantissa bits of L_j hold the codeword's tile (mod 32)
-//           and slot among the 16 scores a lane sees per tile, so a plain
-//           float min / med3 also yields the position (the codeword itself
-//           for K <= 1024).
-//   pass 1  per lane: the two smallest keys (tagged with the slot only).
-//           The nearest codeword j* satisfies L_j* <= s_j* <= s_j1 <= U =
-//           L_j1 + (1 + 1.03) Delta_j1 for the smallest key j1, so it is
-//           among {j : L_j <= U}: a single codeword when the token's second
-//           key exceeds U (final).
-//   pass 2  (only in a workgroup with an open token, K <= 1024) re-screens
-//           keeping the six smallest keys per lane, tagged with tile and
-//           slot so each names its codeword; when both halves' sixth keys
-//           exceed U the candidates are among the kept keys and are
-//           rescored exactly in fp32 by the token's two lanes.
-//   pass 3  (only when a token is still open) re-screens and lists every
-//           candidate; they are rescored exactly in fp32 as
-//           sum_c (R_c - C_jc)^2.
+//   tag     the low 4 mantissa bits of L_j hold its slot among the 16
+//           scores a lane sees per tile, so a plain float min / med3 also
+//           yields the position; the tile of the smallest is tracked per
+//           tile.
+//   pass 1  per lane: the two smallest keys.  The nearest codeword j*
+//           satisfies L_j* <= s_j* <= s_j1 <= U = L_j1 + (1 + 1.03) Delta_j1
+//           for the smallest key j1, so it is among {j : L_j <= U}: a
+//           single codeword when the token's second key exceeds U (final).
+//   pass 2  (only in a workgroup with a token not final) re-screens and
+//           lists every codeword with L_j <= U of those tokens.
+//   rescore the listed candidates exactly in fp32 as sum_c (R_c - C_jc)^2:
+//           per wave a batch of up to 8 open tokens, their residual rows
+//           staged in LDS, 8 (token, codeword) pairs per step with coalesced
+//           codeword rows and one cross-lane reduction for all 8.
 // The fp32 residual stays in registers across rounds, updated as
-// R_{l+1} = R_l - C_l[code_l]; the rescoring reads it from there (through a
-// per-wave LDS row), so screening and rescoring see the same R.
+// R_{l+1} = R_l - C_l[code_l]; the rescoring reads it from there (through
+// LDS rows), so screening and rescoring see the same R.
 //
 // Layout: a workgroup of 4 waves owns 128 tokens, 32 per wave.  A wave keeps
 // its tokens' bf16(-2R) as the B operand of v_mfma_f32_32x32x16_bf16 in
@@ -82,22 +79,12 @@ __device__ __forceinline__ int load_code(const void* codes, int cb, int64_t idx)
 // Row of a 32-codeword tile held by accumulator slot e of a lane in `half`.
 __device__ __forceinline__ int rq_row(int e, int half) { return 8 * (e >> 2) + 4 * half + (e & 3); }
 
-// A score tagged in its low 9 mantissa bits with its tile mod 32 (bits 4..8)
-// and its slot among the lane's 16 scores of the tile (bits 0..3): a plain
-// float min / med3 then also carries the position, and with the lane's half
-// (K <= 1024) the key names its codeword.  te = ((tile & 31) << 4) | slot is
-// uniform across the wave, so the tag costs one vector operation.
-__device__ __forceinline__ float rq_tag(float s, uint32_t te) {
-  return __uint_as_float((__float_as_uint(s) & ~511u) | te);
-}
-// The lean form: the slot alone (inline constants, one operation); the tile
-// of the smallest key is tracked beside the fold.
+// A score tagged in its low 4 mantissa bits with its slot among the lane's
+// 16 scores of a tile (inline constants, one operation): a plain float min /
+// med3 then also carries the slot.  The tag moves a score by less than
+// 2^-19 of its magnitude, inside the margin's allowance for it.
 __device__ __forceinline__ float rq_tag_slot(float s, int e) {
   return __uint_as_float((__float_as_uint(s) & ~15u) | (uint32_t)e);
-}
-__device__ __forceinline__ int rq_tag_index(float key, int half) {
-  const uint32_t b = __float_as_uint(key);
-  return (int)((b >> 4) & 31u) * 32 + rq_row((int)(b & 15u), half);
 }
 
 // Per-workgroup LDS of the rounds besides the three codebook stages.
@@ -105,18 +92,19 @@ struct RqSmall {
   int cand_cnt[RQ_TOK];
   uint16_t cand[RQ_TOK][RQ_CAP];
   int amb_s[RQ_TOK];
+  int dec[4][8];  // per wave: the decisions of a rescoring batch
 };
 
 // The L rounds for the workgroup's 128 tokens (blockIdx.x), given each
 // lane's fp32 residual R_0 = Z0 (columns 16 s + 8 (lane / 32) + 0..7 of
 // token 32 wave + lane % 32; zeros past T).  s0, s1, s2: three stage
 // buffers of at least sizeof(RqStage<R>) bytes, each its own __shared__
-// object; rvs: 4 R floats of LDS (one token's residual per wave while it is
-// rescored).  No load may be in flight on entry and the workgroup must have
-// passed a barrier after its last use of the buffers.
+// object (stage 2 also holds the residuals of the tokens being rescored).
+// No load may be in flight on entry and the workgroup must have passed a
+// barrier after its last use of the buffers.
 template <int R>
 __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t* s1, bf16_t* s2, RqSmall& sm,
-                                           float* rvs, float (&res)[R / 16][8]) {
+                                           float (&res)[R / 16][8]) {
   constexpr int NK16 = R / 16;                     // k-steps of the coordinates
   constexpr int CPR = (R + 16) / 8;                // 16 B chunks per codeword row
   constexpr int LOADS = rq_blocks<R>();            // DMA blocks per wave per stage
@@ -317,12 +305,10 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
     // (the screen subtracts that codeword's own error bound), and s_j1 <= U =
     // L_j1 + (RVQ_SUB_FACTOR + 1) Delta_j1 for the smallest key j1 (of equal
     // keys, half 0's), so only codewords with L_j <= U can be nearest.
-    //  pass 1 (every workgroup): final when the token's second key exceeds U;
-    //  pass 2 (workgroups with an open token, K <= 1024): the six smallest
-    //    keys per lane, tagged to name their codewords; when both halves'
-    //    sixth keys exceed U the candidates are the kept keys <= U, rescored
-    //    exactly;
-    //  pass 3 (tokens still open): every candidate listed and rescored.
+    //  pass 1: per lane the two smallest keys and the position of the
+    //    first; a token is final when its second key exceeds U;
+    //  pass 2 (only in a workgroup with an open token): every key <= U of
+    //    the open tokens listed; the candidates are rescored exactly in fp32.
     const float* n2l = a.meta + (int64_t)l * nchunks * 64;
     const float* e2l = n2l + (int64_t)a.L * nchunks * 64;
     auto margin = [&](int j) {  // Delta_j, rounded up
@@ -331,10 +317,11 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       return (cco * e2l[jj] + bco * (sqrtf(n2) * (1.0f + 1.0f / 32768.0f)) + rvq_margin_k2(R) * n2) * 1.0002f +
              1e-30f;
     };
-    // ---- pass 1: the two smallest keys per lane
+    // ---- pass 1: the two smallest keys per lane (slot tags) and the tile
+    // of the smallest
     int j1;
-    bool fin;
     float thr;
+    bool open;  // not final: the token's candidates are listed by pass 2
     {
       float m1 = INFINITY, m2 = INFINITY, m1_in = INFINITY;
       int tile1 = 0;
@@ -350,173 +337,206 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       const int own_j1 = tile1 * 32 + rq_row((int)(__float_as_uint(m1) & 15u), half);
       const int o_j1 = __shfl_xor(own_j1, 32, WAVE);
       j1 = (m1 < o1 || (m1 == o1 && half == 0)) ? own_j1 : o_j1;
-      const float k1 = fminf(m1, o1);
       const float k2 = fminf(fmaxf(m1, o1), fminf(m2, o2));
-      thr = k1 + (RVQ_SUB_FACTOR + 1.0f) * margin(j1);
-      fin = !valid || k2 > thr;
+      thr = fminf(m1, o1) + (RVQ_SUB_FACTOR + 1.0f) * margin(j1);
+      open = valid && !(k2 > thr);
+      if (half == 0) cand_cnt[tl] = 0;
     }
-    const bool names = a.K <= 1024;
-    const int any_open = __syncthreads_or(fin ? 0 : 1);
-    bool multi = false;
-    if (any_open && names) {
-      // ---- pass 2: the six smallest keys per lane, tagged with tile and slot
-      float m1 = INFINITY, m2 = INFINITY, m3 = INFINITY, m4 = INFINITY, m5 = INFINITY, m6 = INFINITY;
-      pass([&]() {},
-           [&](const f32x16_t& acc, int tile, auto ec) {
-             constexpr int E = decltype(ec)::value;
-             const float key = rq_tag(acc[E], ((uint32_t)(tile & 31) << 4) | (uint32_t)E);
-             m6 = __builtin_amdgcn_fmed3f(m5, m6, key);
-             m5 = __builtin_amdgcn_fmed3f(m4, m5, key);
-             m4 = __builtin_amdgcn_fmed3f(m3, m4, key);
-             m3 = __builtin_amdgcn_fmed3f(m2, m3, key);
-             m2 = __builtin_amdgcn_fmed3f(m1, m2, key);
-             m1 = __builtin_amdgcn_fmed3f(m1, key, -3.40282347e38f);
-           },
-           [&](int) {}, false);
-      const float o1 = __shfl_xor(m1, 32, WAVE), o2 = __shfl_xor(m2, 32, WAVE);
-      const float o3 = __shfl_xor(m3, 32, WAVE), o4 = __shfl_xor(m4, 32, WAVE);
-      const float o5 = __shfl_xor(m5, 32, WAVE), o6 = __shfl_xor(m6, 32, WAVE);
-      const bool own_first = m1 < o1 || (m1 == o1 && half == 0);
-      const int jd = rq_tag_index(own_first ? m1 : o1, own_first ? half : half ^ 1);
-      const float Ud = fminf(m1, o1) + (RVQ_SUB_FACTOR + 1.0f) * margin(jd);
-      if (!fin) thr = Ud;
-      multi = !fin && m6 > Ud && o6 > Ud;
-      if (__any(multi)) {
-        // exact fp32 rescoring over the kept keys, half 0's then half 1's,
-        // each lane summing its half of the residual (in registers), halves added
-        float best = INFINITY;
-        int bj = 0x7fffffff, ncand = 0;
-        static_for<0, 12>([&](auto ic) {
-          constexpr int I = decltype(ic)::value, P = I % 6;
-          const bool from_own = (I < 6) == (half == 0);
-          const float mine = P == 0 ? m1 : P == 1 ? m2 : P == 2 ? m3 : P == 3 ? m4 : P == 4 ? m5 : m6;
-          const float theirs = P == 0 ? o1 : P == 1 ? o2 : P == 2 ? o3 : P == 3 ? o4 : P == 4 ? o5 : o6;
-          const float key = from_own ? mine : theirs;
-          const int j = rq_tag_index(key, I / 6);
-          const bool cand = multi && (unsigned)j < (unsigned)a.K && key <= Ud;
-          float dpart = 0.f;
-          if (cand) {
-            const float* cw = a.C + ((int64_t)l * a.K + j) * R + 8 * half;
-#pragma unroll
-            for (int s = 0; s < NK16; ++s) {
-              const float4 p0 = *(const float4*)(cw + 16 * s), p1 = *(const float4*)(cw + 16 * s + 4);
-              const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                const float u = res[s][e] - pv[e];
-                dpart = fmaf(u, u, dpart);
-              }
-            }
-          }
-          const float dd = dpart + __shfl_xor(dpart, 32, WAVE);
-          if (cand) {
-            ++ncand;
-            if (dd < best || (dd == best && j < bj)) {
-              best = dd;
-              bj = j;
-            }
-          }
-        });
-        if (multi && ncand > 0) j1 = bj;
-        if (a.stats) {
-          const int nm = __popcll(__ballot(multi && half == 0));
-          int nc = multi && half == 0 ? ncand : 0;
-#pragma unroll
-          for (int o = 32; o > 0; o >>= 1) nc += __shfl_xor(nc, o, WAVE);
-          if (lane == 0 && nm) {
-            atomicAdd(&a.stats[0], nm);
-            atomicAdd(&a.stats[1], nc);
-          }
-        }
-      }
-    }
-    const bool amb = !fin && !multi;  // pass 3: a full candidate listing
-    if (half == 0) {
-      amb_s[tl] = amb ? 1 : 0;
-      cand_cnt[tl] = 0;
-    }
-    const int any_amb = __syncthreads_or(amb ? 1 : 0);
+    const int any_open = __syncthreads_or(open ? 1 : 0);
     if (a.stats && tid == 0) {
       atomicAdd(&a.stats[4], 1);
-      if (any_open && names) atomicAdd(&a.stats[3], 1);
-      if (any_amb) atomicAdd(&a.stats[5], 1);
+      if (any_open) atomicAdd(&a.stats[3], 1);
     }
 
     int jstar = j1;
-    if (any_amb) {
-      // ---- pass 3: list every candidate of the open tokens
-      pass([&]() {},
-           [&](const f32x16_t& acc, int tile, auto ec) {
+    if (any_open) {
+      // ---- pass 2: list every key <= U of the open tokens (a per-tile hit
+      // mask, flushed once per tile)
+      const float lthr = open ? thr : -INFINITY;
+      uint32_t hit = 0;
+      pass([&]() { hit = 0; },
+           [&](const f32x16_t& acc, int, auto ec) {
              constexpr int E = decltype(ec)::value;
-             if (amb && tile >= 0 && rq_tag(acc[E], ((uint32_t)(tile & 31) << 4) | (uint32_t)E) <= thr) {
-               const int idx = atomicAdd(&cand_cnt[tl], 1);
-               if (idx < RQ_CAP) cand[tl][idx] = (uint16_t)(tile * 32 + rq_row(E, half));
+             hit |= acc[E] <= lthr ? (1u << E) : 0u;
+           },
+           [&](int tile) {
+             if (hit && tile >= 0) {
+               for (uint32_t h = hit; h; h &= h - 1u) {
+                 const int e = __builtin_ctz(h);
+                 const int idx = atomicAdd(&cand_cnt[tl], 1);
+                 if (idx < RQ_CAP) cand[tl][idx] = (uint16_t)(tile * 32 + rq_row(e, half));
+               }
              }
            },
-           [&](int) {}, false);
-      // ---- exact fp32 rescoring, one wave per token of its own 32
-      for (int u = 0; u < 32; ++u) {
-        const int tu = wave * 32 + u;
-        if (!amb_s[tu]) continue;  // wave-uniform
-        // the token's residual R_l, from the registers of its two lanes
-        constexpr int PER = (R + 63) / 64;
-        float* rw = rvs + wave * R;
-        if ((lane & 31) == u) {
+           false);
+      __syncthreads();  // stage 2 (read last by the pass) is free for the rescoring
+      // ---- exact fp32 rescoring of the open tokens, wave by wave (each wave
+      // its own 32), a batch of up to 8 tokens at a time: their residuals go
+      // to the wave's share of stage 2, their (token, codeword) pairs are
+      // listed one per lane, and the wave scores G = 8 pairs per step, each
+      // lane holding R / 64 coordinates of a pair (coalesced codeword rows),
+      // with one reduction for all G pairs.  A list that overflowed stands
+      // for every codeword of the round.
+      constexpr int PER = R / 64, NB = 8, G = 8;
+      static_assert(NB * R * 4 <= CBLK * 1024, "a batch of residuals fits the wave's share of a stage");
+      static_assert(NB * RQ_CAP <= 128, "two pairs per lane");
+      float* stg = reinterpret_cast<float*>(s2) + wave * (CBLK * 256);
+      const float* Cl = a.C + (int64_t)l * a.K * R;
+      uint32_t pend = (uint32_t)__ballot(half == 0 && open);
+      const int u_own = lane & 31;
+      int* dec = sm.dec[wave];
+      // lane of the full sum of pair g after the reduction below
+      auto glane = [](int g) { return 32 * (g >> 2) + 16 * ((g >> 1) & 1) + 8 * (g & 1); };
+      while (pend) {  // wave-uniform
+        uint32_t rest = pend;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) rest &= rest - 1u;
+        const uint32_t bm = pend & ~rest;
+        pend = rest;
+        const int nb = __popc(bm);
+        const bool mine = (bm >> u_own) & 1u;
+        const int slot = __popc(bm & ((1u << u_own) - 1u));
+        if (mine) {
+          float* rw = stg + slot * R + 8 * half;
 #pragma unroll
           for (int s = 0; s < NK16; ++s) {
-            *(float4*)(rw + 16 * s + 8 * half) = make_float4(res[s][0], res[s][1], res[s][2], res[s][3]);
-            *(float4*)(rw + 16 * s + 8 * half + 4) = make_float4(res[s][4], res[s][5], res[s][6], res[s][7]);
+            *(float4*)(rw + 16 * s) = make_float4(res[s][0], res[s][1], res[s][2], res[s][3]);
+            *(float4*)(rw + 16 * s + 4) = make_float4(res[s][4], res[s][5], res[s][6], res[s][7]);
           }
         }
+        // lane i < nb: the token of batch slot i and its list length
+        int tok = 0, cnt = 0;
+        if (lane < nb) {
+          uint32_t m = bm;
+          for (int i = 0; i < lane; ++i) m &= m - 1u;
+          tok = wave * 32 + __builtin_ctz(m);
+          cnt = cand_cnt[tok];
+        }
+        // the slots' first pairs (scalar): listed pairs only, overflowed
+        // lists apart
+        int bs[NB];
+        int npairs = 0;
+        uint32_t ovm = 0;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          const int ci = __builtin_amdgcn_readlane(cnt, i);
+          bs[i] = npairs;
+          if (i < nb && ci > RQ_CAP) ovm |= 1u << i;
+          npairs += (i < nb && ci <= RQ_CAP) ? ci : 0;
+        }
+        // pair p = lane + 64 h: (slot << 16) | codeword
+        uint32_t pj[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int p = lane + 64 * h;
+          int sl = 0, b0 = 0;
+#pragma unroll
+          for (int i = 1; i < NB; ++i)
+            if (i < nb && p >= bs[i]) {
+              sl = i;
+              b0 = bs[i];
+            }
+          const int tk = __shfl(tok, sl, WAVE);
+          pj[h] = p < npairs ? ((uint32_t)sl << 16) | (uint32_t)cand[tk][p - b0] : 0xFFFFFFFFu;
+        }
+        float best = INFINITY;
+        int bj = 0x7fffffff;
+        float cv[G][PER];
+        int sg[G], jg[G];
+        // request the rows of G pairs given by pair(g) = (slot, codeword),
+        // slot -1 for none
+        auto load = [&](auto&& pair) {
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            pair(g, sg[g], jg[g]);
+            const int jl = sg[g] >= 0 ? jg[g] : 0;
+            const float* src = Cl + (int64_t)jl * R + PER * lane;
+            if constexpr (PER == 4) {
+              const float4 v = *(const float4*)src;
+              cv[g][0] = v.x; cv[g][1] = v.y; cv[g][2] = v.z; cv[g][3] = v.w;
+            } else if constexpr (PER == 2) {
+              const float2 v = *(const float2*)src;
+              cv[g][0] = v.x; cv[g][1] = v.y;
+            } else {
+              cv[g][0] = *src;
+            }
+          }
+        };
+        // score the requested pairs and keep each slot's best (lane = slot),
+        // ties to the lower index
+        auto score = [&]() {
+          float v8[G];
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            const float* rsrc = stg + (sg[g] >= 0 ? sg[g] : 0) * R + PER * lane;
+            float d = 0.f;
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+              const float df = rsrc[e] - cv[g][e];
+              d = fmaf(df, df, d);
+            }
+            v8[g] = d;
+          }
+          // all G sums at once: the steps over lane bits 5, 4, 3 halve the
+          // values a lane holds, then bits 2, 1, 0 finish the single one
+          float w4[4], w2[2];
+          const int b5 = (lane >> 5) & 1, b4 = (lane >> 4) & 1, b3 = (lane >> 3) & 1;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) w4[t] = (b5 ? v8[4 + t] : v8[t]) + __shfl_xor(b5 ? v8[t] : v8[4 + t], 32, WAVE);
+#pragma unroll
+          for (int t = 0; t < 2; ++t) w2[t] = (b4 ? w4[2 + t] : w4[t]) + __shfl_xor(b4 ? w4[t] : w4[2 + t], 16, WAVE);
+          float y = (b3 ? w2[1] : w2[0]) + __shfl_xor(b3 ? w2[0] : w2[1], 8, WAVE);
+          y += __shfl_xor(y, 4, WAVE);
+          y += __shfl_xor(y, 2, WAVE);
+          y += __shfl_xor(y, 1, WAVE);
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            const float dg = __shfl(y, glane(g), WAVE);
+            if (sg[g] >= 0 && lane == sg[g] && (dg < best || (dg == best && jg[g] < bj))) {
+              best = dg;
+              bj = jg[g];
+            }
+          }
+        };
+        auto listed = [&](int p0) {
+          return [&, p0](int g, int& sl, int& j) {
+            const int p = p0 + g;
+            const uint32_t e = p < 64 ? (uint32_t)__builtin_amdgcn_readlane((int)pj[0], p & 63)
+                                      : (uint32_t)__builtin_amdgcn_readlane((int)pj[1], p & 63);
+            const bool ok = p < npairs && (int)(e & 0xFFFFu) < a.K;
+            sl = ok ? (int)(e >> 16) : -1;
+            j = (int)(e & 0xFFFFu);
+          };
+        };
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        float rv[PER];
-#pragma unroll
-        for (int p = 0; p < PER; ++p) {
-          const int c = lane + 64 * p;
-          rv[p] = c < R ? rw[c] : 0.f;
+        for (int p0 = 0; p0 < npairs; p0 += G) {  // wave-uniform
+          load(listed(p0));
+          score();
         }
-        const float* Cl = a.C + (int64_t)l * a.K * R;
-        auto dist = [&](int j) {
-          float s = 0.f;
-#pragma unroll
-          for (int p = 0; p < PER; ++p) {
-            const int c = lane + 64 * p;
-            if (c < R) {
-              const float df = rv[p] - Cl[(int64_t)j * R + c];
-              s = fmaf(df, df, s);
-            }
-          }
-          return wave_sum(s);
-        };
-        const int cnt = cand_cnt[tu];
-        float best = INFINITY;
-        int bj = 0x7fffffff;
-        if (cnt <= RQ_CAP) {
-          for (int q = 0; q < cnt; ++q) {
-            const int j = cand[tu][q];
-            const float dd = dist(j);
-            if (dd < best || (dd == best && j < bj)) { best = dd; bj = j; }
-          }
-        } else {
-          for (int j = 0; j < a.K; ++j) {
-            const float dd = dist(j);
-            if (dd < best) { best = dd; bj = j; }
+        for (uint32_t ov = ovm; ov; ov &= ov - 1u) {  // overflowed lists: every codeword
+          const int si = __builtin_ctz(ov);
+          for (int q0 = 0; q0 < a.K; q0 += G) {
+            load([&](int g, int& sl, int& j) {
+              j = q0 + g;
+              sl = j < a.K ? si : -1;
+            });
+            score();
           }
         }
-        if (bj >= a.K) bj = 0;  // only reachable with non-finite inputs
-        if (lane == 0) {
-          cand_cnt[tu] = bj;  // reuse as the decision slot
-          if (a.stats) {
-            atomicAdd(&a.stats[0], 1);
-            atomicAdd(&a.stats[1], cnt);
-            if (cnt > RQ_CAP) atomicAdd(&a.stats[2], 1);
-          }
+        if (lane < nb) dec[lane] = bj < a.K ? bj : 0;  // bj >= K only with non-finite inputs
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (mine) jstar = dec[slot];
+        if (a.stats && lane == 0) {
+          atomicAdd(&a.stats[0], nb);
+          atomicAdd(&a.stats[1], npairs);
+          if (ovm) atomicAdd(&a.stats[2], __popc(ovm));
         }
+        __builtin_amdgcn_wave_barrier();  // dec and the staging rows are reused by the next batch
       }
-      __syncthreads();
-      if (amb) jstar = cand_cnt[tl];
     }
     if (jstar < 0 || jstar >= a.K) jstar = 0;  // only reachable with non-finite inputs
     if (l + 1 < a.L) {
@@ -540,9 +560,10 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       else
         ((uint16_t*)a.codes)[(int64_t)t * a.L + l] = (uint16_t)jstar;
     }
-    // no barrier: the next round's shared state (amb_s, cand_cnt, cand and
-    // rvs, which only the token's own wave touches) is written after
-    // barriers that every wave reaches only once done with this round
+    // no barrier: the next round's shared state (amb_s, cand_cnt and cand;
+    // dec and the staging rows, which only the token's own wave touches) is
+    // written after barriers that every wave reaches only once done with
+    // this round
   }
 }
 
@@ -553,7 +574,6 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
   __shared__ __attribute__((aligned(1024))) RqStage<R> S1;
   __shared__ __attribute__((aligned(1024))) RqStage<R> S2;
   __shared__ RqSmall sm;
-  __shared__ __attribute__((aligned(16))) float rvs[4 * R];
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int t = blockIdx.x * RQ_TOK + (threadIdx.x >> 6) * 32 + (lane & 31);
   float res[R / 16][8];
@@ -568,7 +588,7 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
     res[s][0] = z0.x; res[s][1] = z0.y; res[s][2] = z0.z; res[s][3] = z0.w;
     res[s][4] = z1.x; res[s][5] = z1.y; res[s][6] = z1.z; res[s][7] = z1.w;
   }
-  rvq_rounds<R>(a, S0.c, S1.c, S2.c, sm, rvs, res);
+  rvq_rounds<R>(a, S0.c, S1.c, S2.c, sm, res);
 #endif
 }
 
@@ -581,6 +601,7 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
 // the RVQ's codebook stages.
 constexpr int FU_R = 256;
 static_assert(sizeof(RqStage<FU_R>) <= sizeof(TnSmem<FU_R>), "RVQ stages fit the GEMM stages");
+static_assert(sizeof(RqStage<FU_R>) <= (GM + FU_R) * GK * sizeof(bf16_t), "RVQ stage 2 fits the third GEMM stage");
 static_assert(GM == RQ_TOK, "one token block");
 
 template <bool FULLK>
@@ -592,7 +613,6 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
   __shared__ __attribute__((aligned(1024))) TnSmem<R> S1;
   __shared__ __attribute__((aligned(1024))) bf16_t S2buf[(GM + R) * GK];
   __shared__ RqSmall sm;
-  __shared__ __attribute__((aligned(16))) float rvs[4 * R];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
   constexpr int ROWS = (int)(sizeof(TnSmem<R>) / 1024);  // 1 KiB fp32 rows per stage buffer
   static_assert(3 * ROWS >= GM, "the tile fits the stage buffers");
@@ -653,7 +673,7 @@ __global__ __launch_bounds__(RQ_THREADS) __attribute__((amdgpu_waves_per_eu(1, 1
     }
   }
   __syncthreads();  // the stages are free for the codebook
-  rvq_rounds<R>(a, S0.a, S1.a, S2buf, sm, rvs, res);
+  rvq_rounds<R>(a, S0.a, S1.a, S2buf, sm, res);
 #endif
 }
 

@@ -156,9 +156,8 @@ struct RvqArgs {
   int T, r, L, K;
   void* codes; int code_bytes;  // [T,L]
   int* stats;          // [8] optional counters, may be null: tokens rescored, their candidates,
-                       // candidate-list overflows, (workgroup, round) pairs with the deep
-                       // second pass, (workgroup, round) pairs in total, pairs with the
-                       // listing pass
+                       // candidate-list overflows, (workgroup, round) pairs with the second
+                       // (listing) pass, (workgroup, round) pairs in total
 };
 hipError_t launch_rvq(const RvqArgs& a, hipStream_t s);
 // The encoder in one launch: Z0 = [X | a] W as launch_gemm_tn computes it

@@ -72,10 +72,10 @@ struct ProfRec {
 std::mutex g_prof_mu;
 bool g_prof = false;
 bool g_prof_rvq = false;      // mapl_profile(2): also collect the RVQ decision counters
-constexpr int kRvqStats = 6;
-long long g_rvq_stats[kRvqStats] = {0, 0, 0, 0, 0, 0};
+constexpr int kRvqStats = 5;
+long long g_rvq_stats[kRvqStats] = {0, 0, 0, 0, 0};
 const char* const kRvqStatNames[kRvqStats] = {"rvq:tokens_rescored", "rvq:candidates", "rvq:list_overflows",
-                                              "rvq:deep_pass_blocks", "rvq:blocks", "rvq:listing_pass_blocks"};
+                                              "rvq:second_pass_blocks", "rvq:blocks"};
 std::vector<ProfRec> g_prof_recs;
 std::vector<hipEvent_t> g_prof_pool;
 
