@@ -8,7 +8,9 @@
 //   2. a segmented sum over the sorted order in 64-position sub-chunks, one
 //      wave each, walking its positions in order; a segment that crosses a
 //      sub-chunk boundary leaves its pieces in per-sub-chunk slots;
-//   3. a fix-up that adds those pieces in sub-chunk order.
+//   3. a fix-up, one workgroup per segment that crosses sub-chunks, adding
+//      its pieces in a fixed order (four interleaved wave sums, then the
+//      waves in order).
 // Zipf-distributed ids make a few rows very long (id 0 takes about a seventh
 // of the tokens); the sub-chunk split keeps every wave's share at 64 rows.
 #include "common.hpp"
@@ -18,8 +20,8 @@ namespace mapl {
 
 namespace {
 
-constexpr int RS_THREADS = 256, RS_TILE = 2048, RS_ROUNDS = RS_TILE / RS_THREADS;
-constexpr int SEG = 64, SEG_COLS = 8, SEG_BATCH = 8;  // positions per sub-chunk; k <= 512; rows in flight
+constexpr int RS_THREADS = 256, RS_TILE = 512, RS_ROUNDS = RS_TILE / RS_THREADS;
+constexpr int SEG = 64;  // sorted positions per sub-chunk
 
 // W[i][c] = B[i][c] for i < k, c < K, zero for the padding rows k <= i < kp.
 __global__ void k_pad_rows_bf16(const bf16_t* __restrict__ B, int k, int K, int kp, bf16_t* __restrict__ W) {
@@ -45,27 +47,49 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const int32_t* __rest
 }
 
 // Exclusive scan, in place, of m counts (digit-major: all tiles of digit 0,
-// then digit 1, ...), by one block.
+// then digit 1, ...), by one block: chunks of 8192 counts move through LDS
+// with coalesced loads and stores, each thread scans 8 consecutive counts,
+// the 1024 thread sums are scanned in LDS, and a carry links the chunks.
 __global__ __launch_bounds__(1024) void k_radix_scan(int* __restrict__ hist, int m) {
+  constexpr int PER = 8, CH = 1024 * PER;
+  __shared__ int buf[CH];
   __shared__ int part[1024];
   const int tid = threadIdx.x;
-  const int per = (m + 1023) / 1024;
-  const int b0 = min(m, tid * per), b1 = min(m, b0 + per);
-  int sum = 0;
-  for (int i = b0; i < b1; ++i) sum += hist[i];
-  part[tid] = sum;
-  __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {
-    const int v = tid >= o ? part[tid - o] : 0;
+  int carry = 0;
+  for (int base = 0; base < m; base += CH) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int i = base + j * 1024 + tid;
+      buf[j * 1024 + tid] = i < m ? hist[i] : 0;
+    }
     __syncthreads();
-    part[tid] += v;
+    int sum = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) sum += buf[tid * PER + j];
+    part[tid] = sum;
     __syncthreads();
-  }
-  int run = tid ? part[tid - 1] : 0;
-  for (int i = b0; i < b1; ++i) {
-    const int c = hist[i];
-    hist[i] = run;
-    run += c;
+    for (int o = 1; o < 1024; o <<= 1) {
+      const int v = tid >= o ? part[tid - o] : 0;
+      __syncthreads();
+      part[tid] += v;
+      __syncthreads();
+    }
+    int run = carry + (tid ? part[tid - 1] : 0);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int c = buf[tid * PER + j];
+      buf[tid * PER + j] = run;
+      run += c;
+    }
+    const int total = part[1023];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int i = base + j * 1024 + tid;
+      if (i < m) hist[i] = buf[j * 1024 + tid];
+    }
+    carry += total;
+    __syncthreads();  // buf and part are reused by the next chunk
   }
 }
 
@@ -116,10 +140,12 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(const int32_t* __r
   }
 }
 
-__device__ __forceinline__ void seg_store(float* __restrict__ row, const float (&acc)[SEG_COLS], int k, int lane,
+// row[c] (+)= scale acc[q] for the lane's columns c = lane + 64 q < k
+template <int NC>
+__device__ __forceinline__ void seg_store(float* __restrict__ row, const float (&acc)[NC], int k, int lane,
                                           float scale, int add) {
 #pragma unroll
-  for (int q = 0; q < SEG_COLS; ++q) {
+  for (int q = 0; q < NC; ++q) {
     const int c = lane + 64 * q;
     if (c < k) row[c] = add ? row[c] + scale * acc[q] : scale * acc[q];
   }
@@ -130,7 +156,10 @@ __device__ __forceinline__ void seg_store(float* __restrict__ row, const float (
 // sub-chunk is written to dA, a piece that continues from the previous
 // sub-chunk goes to the head slot (flagged when it also continues into the
 // next), a piece that starts here and continues goes to the tail slot.
+// NC columns per lane (k <= 64 NC); 64 / NC rows are requested at a time.
+template <int NC>
 __global__ __launch_bounds__(256) void k_seg_partial(AnchorSegArgs a) {
+  constexpr int BR = 64 / NC;
   const int lane = threadIdx.x & 63;
   const int s = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (s >= a.nsub) return;  // wave-uniform
@@ -143,82 +172,127 @@ __global__ __launch_bounds__(256) void k_seg_partial(AnchorSegArgs a) {
     a.head_thru[s] = 0;
     a.tail_id[s] = -1;
   }
-  float acc[SEG_COLS];
+  float acc[NC];
 #pragma unroll
-  for (int q = 0; q < SEG_COLS; ++q) acc[q] = 0.f;
+  for (int q = 0; q < NC; ++q) acc[q] = 0.f;
   int pstart = p0;
-  for (int pb = p0; pb < p1; pb += SEG_BATCH) {
+  for (int pb = p0; pb < p1; pb += BR) {
     // the batch's ids, tokens and rows are requested before any is summed
-    int id[SEG_BATCH], t[SEG_BATCH];
-    float v[SEG_BATCH][SEG_COLS];
+    int id[BR], t[BR];
+    float v[BR][NC];
 #pragma unroll
-    for (int u = 0; u < SEG_BATCH; ++u) {
+    for (int u = 0; u < BR; ++u) {
       const int p = min(pb + u, p1 - 1);
       id[u] = a.skey[p];
       t[u] = a.sval[p];
     }
 #pragma unroll
-    for (int u = 0; u < SEG_BATCH; ++u) {
+    for (int u = 0; u < BR; ++u) {
       const float* gr = a.g + (int64_t)t[u] * a.ldg;
 #pragma unroll
-      for (int q = 0; q < SEG_COLS; ++q) {
+      for (int q = 0; q < NC; ++q) {
         const int c = lane + 64 * q;
         v[u][q] = c < a.k ? gr[c] : 0.f;
       }
     }
 #pragma unroll
-    for (int u = 0; u < SEG_BATCH; ++u) {
+    for (int u = 0; u < BR; ++u) {
       const int p = pb + u;
       if (p >= p1) break;
 #pragma unroll
-      for (int q = 0; q < SEG_COLS; ++q) acc[q] += v[u][q];
-      const int nid = p + 1 < p1 ? (u + 1 < SEG_BATCH ? id[u + 1] : a.skey[p + 1]) : next_id;
+      for (int q = 0; q < NC; ++q) acc[q] += v[u][q];
+      const int nid = p + 1 < p1 ? (u + 1 < BR ? id[u + 1] : a.skey[p + 1]) : next_id;
       if (nid == id[u] && p + 1 < p1) continue;  // the segment goes on inside the sub-chunk
       const bool before = pstart == p0 && prev_id == id[u];
       const bool after = p + 1 == p1 && next_id == id[u];
       if (!before && !after) {
         if ((unsigned)id[u] < (unsigned)a.V)  // an id outside [0, V) is a caller error: skipped
-          seg_store(a.dA + (int64_t)id[u] * a.k, acc, a.k, lane, a.scale, a.accumulate);
+          seg_store<NC>(a.dA + (int64_t)id[u] * a.k, acc, a.k, lane, a.scale, a.accumulate);
       } else if (before) {
-        seg_store(a.headp + (int64_t)s * a.k, acc, a.k, lane, 1.f, 0);
+        seg_store<NC>(a.headp + (int64_t)s * a.k, acc, a.k, lane, 1.f, 0);
         if (lane == 0) {
           a.head_id[s] = id[u];
           a.head_thru[s] = after ? 1 : 0;
         }
       } else {
-        seg_store(a.tailp + (int64_t)s * a.k, acc, a.k, lane, 1.f, 0);
+        seg_store<NC>(a.tailp + (int64_t)s * a.k, acc, a.k, lane, 1.f, 0);
         if (lane == 0) a.tail_id[s] = id[u];
       }
 #pragma unroll
-      for (int q = 0; q < SEG_COLS; ++q) acc[q] = 0.f;
+      for (int q = 0; q < NC; ++q) acc[q] = 0.f;
       pstart = p + 1;
     }
   }
 }
 
-// Segments that cross sub-chunk boundaries: the sub-chunk where one starts
-// adds the head pieces of the following sub-chunks in order.
+// Segments that cross sub-chunk boundaries, one workgroup per sub-chunk s
+// whose tail piece starts one: its head pieces are those of sub-chunks
+// s+1 .. e, e the first that does not continue further.  Wave w sums the
+// pieces s+1+w, s+5+w, ... in order (eight requested at a time); the sum is
+// tail + wave 0 + wave 1 + wave 2 + wave 3, a fixed order.
+template <int NC>
 __global__ __launch_bounds__(256) void k_seg_fixup(AnchorSegArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int s = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (s >= a.nsub) return;
+  constexpr int FB = 8;
+  __shared__ float part[4][64 * NC];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int s = blockIdx.x;
   const int id = a.tail_id[s];
-  if (id < 0 || id >= a.V) return;
-  float acc[SEG_COLS];
-#pragma unroll
-  for (int q = 0; q < SEG_COLS; ++q) {
-    const int c = lane + 64 * q;
-    acc[q] = c < a.k ? a.tailp[(int64_t)s * a.k + c] : 0.f;
-  }
-  for (int s2 = s + 1; s2 < a.nsub; ++s2) {
-#pragma unroll
-    for (int q = 0; q < SEG_COLS; ++q) {
-      const int c = lane + 64 * q;
-      if (c < a.k) acc[q] += a.headp[(int64_t)s2 * a.k + c];
+  if (id < 0 || id >= a.V) return;  // workgroup-uniform
+  // e: the first head piece after s that ends the segment (exists: a tail
+  // piece continues into sub-chunk s + 1, and the last sub-chunk's head
+  // piece never continues)
+  int e = a.nsub - 1;
+  for (int b = s + 1; b < a.nsub; b += 64) {
+    const int i = b + lane;
+    const uint64_t m = __ballot(i < a.nsub && a.head_thru[i] == 0);
+    if (m) {
+      e = b + __builtin_ctzll(m);
+      break;
     }
-    if (!a.head_thru[s2]) break;
   }
-  seg_store(a.dA + (int64_t)id * a.k, acc, a.k, lane, a.scale, a.accumulate);
+  float acc[NC];
+#pragma unroll
+  for (int q = 0; q < NC; ++q) acc[q] = 0.f;
+  for (int b = s + 1 + wave; b <= e; b += 4 * FB) {
+    float v[FB][NC];
+#pragma unroll
+    for (int u = 0; u < FB; ++u) {
+      const int s2 = min(b + 4 * u, e);
+#pragma unroll
+      for (int q = 0; q < NC; ++q) {
+        const int c = lane + 64 * q;
+        v[u][q] = c < a.k ? a.headp[(int64_t)s2 * a.k + c] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < FB; ++u)
+      if (b + 4 * u <= e) {
+#pragma unroll
+        for (int q = 0; q < NC; ++q) acc[q] += v[u][q];
+      }
+  }
+#pragma unroll
+  for (int q = 0; q < NC; ++q) part[wave][lane + 64 * q] = acc[q];
+  __syncthreads();
+  if (wave != 0) return;
+  float tot[NC];
+#pragma unroll
+  for (int q = 0; q < NC; ++q) {
+    const int c = lane + 64 * q;
+    float x = c < a.k ? a.tailp[(int64_t)s * a.k + c] : 0.f;
+    x += part[0][c];
+    x += part[1][c];
+    x += part[2][c];
+    x += part[3][c];
+    tot[q] = x;
+  }
+  seg_store<NC>(a.dA + (int64_t)id * a.k, tot, a.k, lane, a.scale, a.accumulate);
+}
+
+template <int NC>
+void launch_segsum_nc(const AnchorSegArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_seg_partial<NC>, dim3((a.nsub + 3) / 4), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_seg_fixup<NC>, dim3(a.nsub), dim3(256), 0, s, a);
 }
 
 }  // namespace
@@ -256,10 +330,16 @@ hipError_t launch_sort_ids(const int32_t* ids, int n, int passes, int* hist, int
 
 hipError_t launch_anchor_segsum(const AnchorSegArgs& a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
-  if (a.k > 64 * SEG_COLS) return hipErrorInvalidValue;
-  const int blocks = (a.nsub + 3) / 4;
-  hipLaunchKernelGGL(k_seg_partial, dim3(blocks), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_seg_fixup, dim3(blocks), dim3(256), 0, s, a);
+  if (a.k <= 64)
+    launch_segsum_nc<1>(a, s);
+  else if (a.k <= 128)
+    launch_segsum_nc<2>(a, s);
+  else if (a.k <= 256)
+    launch_segsum_nc<4>(a, s);
+  else if (a.k <= 512)
+    launch_segsum_nc<8>(a, s);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
