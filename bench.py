@@ -738,13 +738,21 @@ def main():
             it = 4 * dd * rr * rr + 2 * rr ** 3
             return P * (4 * dd * rr * rr + 12 * it)
 
+        def spel_roofline_s(P, dd, rr):
+            """Eq. 4 and the 7 retraction steps on the fp32 matrix units; the
+            5 LMO steps as split-bf16 products (three bf16 products per
+            flop) on the bf16 matrix units."""
+            it = 4 * dd * rr * rr + 2 * rr ** 3
+            return P * (4 * dd * rr * rr + 7 * it) / PEAK_F32 + P * 5 * it * 3 / PEAK_BF16
+
         log("SPEL step")
         spel_c5, spel_c5_med = time_spel(16, 2048, 512, 10)
         spel_b, _ = time_spel(1, d, r, 20)
         out["spel"] = {"config": "16 projectors [2048,512], PolarExpress 5 + 7 steps", "ms_per_step": spel_c5,
                        "median_ms_per_step": spel_c5_med,
                        "tflops": spel_flops(16, 2048, 512) / (spel_c5_med * 1e-3) / 1e12,
-                       "roofline_frac_fp32": spel_flops(16, 2048, 512) / PEAK_F32 / (spel_c5_med * 1e-3),
+                       "roofline_ms": spel_roofline_s(16, 2048, 512) * 1e3,
+                       "roofline_frac": spel_roofline_s(16, 2048, 512) / (spel_c5_med * 1e-3),
                        "boundary_projector_ms": spel_b}
         amort = 128  # micro-batches per optimizer step: global batch 512 / micro-batch 4
         out["alg1_tokens_per_s"] = T / ((ms + spel_b / amort) * 1e-3)

@@ -195,8 +195,8 @@ int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, const void* X,
                     void* dX, float* dU, int accumulate_dU, void* ws, size_t ws_bytes,
                     void* stream);
 
-/* SPEL step (Sec. 3.3, Eqs. 4-7) on P independent projectors, all fp32,
- * arrays [P,d,r]:
+/* SPEL step (Sec. 3.3, Eqs. 4-7) on P independent projectors, fp32 arrays
+ * [P,d,r]:
  *   g_R = G - U sym(U^T G)                     (Eq. 4, sym(S) = (S+S^T)/2)
  *   M   = beta M + (1 - beta) g_R              (Eq. 5, in place)
  *   D   = PolarExpress_{lmo_steps}(M / (||M||_F + 1e-7))          (Eq. 6)
@@ -207,7 +207,11 @@ int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, const void* X,
  *         |Y^T Y| (an upper bound of sigma_max(Y)^2)                (Eq. 7)
  * PolarExpress step: X <- a X + X (b S + c S^2), S = X^T X, with the greedy
  * minimax odd-quintic schedule designed for singular values in [1e-3, 1]
- * (LMO) and [0.5, 1] (retraction).  Requirements: 1 <= P, 32 <= r <= d,
+ * (LMO) and [0.5, 1] (retraction).  Every product is fp32 except those of
+ * the LMO's iterations, which multiply split-bf16 operands (each fp32 value
+ * as bf16 hi + bf16 lo, three products, fp32 accumulation: about 3e-5
+ * relative error in the direction D; the retraction and U stay fp32).
+ * Requirements: 1 <= P, 32 <= r <= d,
  * r multiple of 32, d multiple of 32, r <= 1024, 1 <= lmo_steps,
  * retract_steps <= 16.  The retraction is accurate while lr*||D||_2 <= 1/3. */
 int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, const float* G, float* M,

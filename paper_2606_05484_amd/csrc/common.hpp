@@ -192,6 +192,39 @@ __device__ __forceinline__ void reg_pin(u32x4 (&v)[N]) {
   for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
 }
 
+// Chunk swizzle of token-major tiles: chunk c of row t is stored at
+// c ^ wg_sw(t, cpr); it stays inside the row for every cpr >= 8.
+__device__ __forceinline__ int wg_sw(int row, int cpr) { return (4 * (row & 3)) & (cpr - 1); }
+
+// Transposed fragment read from a token-major LDS tile (rows = tokens,
+// `cpr` 16 B chunks per row, swizzled by wg_sw).  ds_read_b64_tr_b16 gives
+// lane i of each 16-lane group element (i & 3) of the 8 B read by lane
+// 4j + (i >> 2), j = 0..3; pointing lane 4j + q at token t0 + j, columns
+// 4q..4q+3 hands lane i column i of tokens t0..t0+3.  Two reads build the
+// MFMA fragment: 8 consecutive tokens of column col0 + lane % 32, tokens
+// 8 (lane / 32) .. +7 of the 16-token k-step.
+//
+// The reads are issued as inline asm (a kernel that fills LDS by
+// direct-to-LDS loads would otherwise drain all of those first); the caller
+// completes them with lds_wait() on the fragments.
+__device__ __forceinline__ u32x4 tr_frag(const bf16_t* tile, int cpr, int k0, int col0, int lane) {
+  const int g = lane >> 4, sidx = lane & 15, j = sidx >> 2, q = sidx & 3;
+  const int col = col0 + 16 * (g & 1) + 4 * q;
+  typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+  u32x2 h0, h1;
+  {
+    const int row = k0 + 8 * (g >> 1) + j;
+    const int pc = (col >> 3) ^ wg_sw(row, cpr);
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(h0) : "v"(lds_addr(tile + row * cpr * 8 + pc * 8 + (col & 7))) : "memory");
+  }
+  {
+    const int row = k0 + 8 * (g >> 1) + 4 + j;
+    const int pc = (col >> 3) ^ wg_sw(row, cpr);
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(h1) : "v"(lds_addr(tile + row * cpr * 8 + pc * 8 + (col & 7))) : "memory");
+  }
+  return u32x4{h0.x, h0.y, h1.x, h1.y};
+}
+
 // Compile-time loop: f(std::integral_constant<int, I>) for I = B .. E-1.
 template <int B, int E, typename F>
 __device__ __forceinline__ void static_for(F&& f) {

@@ -122,6 +122,41 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32(GemmF32Args g) {
 // m' = m ^ 4 ((k / 2) % 8) for the k-contiguous A.
 constexpr int GV_BM = 128, GV_BN = 128, GV_BK = 32;
 
+// Tile coordinates and batch entry of a workgroup.  Workgroups are handed to
+// the 8 XCDs round-robin by linear id, each XCD with its own L2; when the
+// batch count is a multiple of 8, linear id w is given to batch entry
+// b = (w % 8) + 8 j and tile t (w / 8 = j T + t, T tiles per entry), so that
+// all tiles of one entry run on one XCD and share its L2 (its operands are
+// read once from HBM instead of once per XCD).  Otherwise the grid's
+// (x, y, z).  With sym_upper the tiles are those on or above the diagonal of
+// an nt x nt tile grid, row by row.
+__device__ __forceinline__ void gv_tile(const GemmF32Args& g, int& bm, int& bn, int& b) {
+  const int ntm = (g.M + 127) / 128, ntn = (g.N + 127) / 128;
+  const int T = g.sym_upper ? ntm * (ntm + 1) / 2 : ntm * ntn;
+  int t;
+  if (g.batch % 8 == 0) {
+    const int w = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const int q = w >> 3;
+    b = (w & 7) + 8 * (q / T);
+    t = q % T;
+  } else {
+    b = blockIdx.z;
+    t = blockIdx.x + gridDim.x * blockIdx.y;
+  }
+  if (g.sym_upper) {
+    int row = 0;
+    while (t >= ntm - row) {
+      t -= ntm - row;
+      ++row;
+    }
+    bm = row;
+    bn = row + t;
+  } else {
+    bm = t % ntm;
+    bn = t / ntm;
+  }
+}
+
 // Operand loads are raw buffer loads (out-of-range offsets read zero) into
 // registers that are converted to fp32 only when the stage is written to LDS,
 // so nothing waits for the loads before the products of the current stage.
@@ -160,8 +195,9 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
   __shared__ __attribute__((aligned(16))) float Bs[2][GV_BK / 2][GV_BN][2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, 64 x 64 each
-  const int b = blockIdx.z;
-  const int m0 = blockIdx.x * GV_BM, n0 = blockIdx.y * GV_BN;
+  int tbm, tbn, b;
+  gv_tile(g, tbm, tbn, b);
+  const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
   // the host guarantees that each operand's extent fits 31-bit byte offsets
   const __amdgpu_buffer_rsrc_t rA =
       gv_rsrc((const TA*)g.A + b * g.sAb,
@@ -282,10 +318,179 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
           float v = alpha * acc[i][j][e];
           if (Cin && beta != 0.f) v += beta * Cin[m * g.sCinm + n * g.sCinn];
           if (m == n) v += g.diag;
-          if constexpr (sizeof(TO) == 4)
+          if constexpr (sizeof(TO) == 4) {
             C[m * g.sCm + n * g.sCn] = v;
-          else
+            if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = v;
+          } else {
             C[m * g.sCm + n * g.sCn] = (TO)f2bf(v);
+            if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = (TO)f2bf(v);
+          }
+        }
+      }
+}
+
+// Split-bf16 variant of the aligned fp32 GEMM (fp32 operands and output):
+// every operand element x is held as hi = bf16(x) and lo = bf16(x - hi)
+// (round to nearest even; x - hi - lo is below 2^-16 |x|), and each product
+// is taken as hi.hi + hi.lo + lo.hi on the bf16 matrix units
+// (v_mfma_f32_32x32x16_bf16, fp32 accumulation), dropping lo.lo: about
+// 2^-15 relative error per product term, at five times the fp32 MFMA rate.
+// Same tiling as k_gemm_f32v (128 x 128, K staged 32 at a time, 16-byte
+// loads into registers one stage ahead, two LDS buffers).  Hi and lo pieces
+// live apart in LDS, each operand in the layout its loads give:
+//  - a k-contiguous A as [row][k], rows 80 bytes apart (an odd number of
+//    16 B chunks: consecutive rows' 16-byte accesses hit distinct bank
+//    groups), fragments read as 8 consecutive k of one row per lane;
+//  - B and an m-contiguous A as [k][row] (k-major, 128 rows = 16 chunks per
+//    k, chunk-swizzled by wg_sw), written 8 bytes per lane along the row and
+//    read with transposing LDS reads (tr_frag).
+constexpr int GX_LD = GV_BK + 8;  // bf16 per row of a [row][k] tile
+constexpr int GX_CPR = GV_BM / 8;  // 16-byte chunks per k of a [k][row] tile
+
+template <bool AK>
+__global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
+  // [row][k] tiles (k-contiguous A) or [k][row] tiles (the rest), per buffer and piece
+  constexpr int A_ELEMS = AK ? GV_BM * GX_LD : GV_BK * GV_BM;
+  __shared__ __attribute__((aligned(16))) bf16_t Ah[2][A_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t Al[2][A_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t Bh[2][GV_BK * GV_BN];
+  __shared__ __attribute__((aligned(16))) bf16_t Bl[2][GV_BK * GV_BN];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, 64 x 64 each
+  int tbm, tbn, b;
+  gv_tile(g, tbm, tbn, b);
+  const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
+  const __amdgpu_buffer_rsrc_t rA =
+      gv_rsrc((const float*)g.A + b * g.sAb,
+              (AK ? (int64_t)(g.M - 1) * g.sAm + g.K : (int64_t)(g.K - 1) * g.sAk + g.M) * 4);
+  const __amdgpu_buffer_rsrc_t rB = gv_rsrc((const float*)g.B + b * g.sBb, ((int64_t)(g.K - 1) * g.sBk + g.N) * 4);
+  typedef Raw4<float>::type raw_t;
+  raw_t ra[4], rb[4];
+  // B (and an m-contiguous A): thread t loads rows 4 (t % 32) + 0..3 at
+  // k = 4 (t / 32) + 0..3, one 16-byte piece per k; a k-contiguous A: row
+  // t / 2, k = 16 (t % 2) + 0..15
+  auto load = [&](int k0) {
+    const int kb = k0 + 4 * (tid >> 5), c = 4 * (tid & 31);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const int k = kb + h;
+      rb[h] = Raw4<float>::load(rB, (k < g.K && n0 + c < g.N) ? (uint32_t)(((int64_t)k * g.sBk + n0 + c) * 4) : GV_OOB);
+      if constexpr (!AK)
+        ra[h] = Raw4<float>::load(rA, (k < g.K && m0 + c < g.M) ? (uint32_t)(((int64_t)k * g.sAk + m0 + c) * 4) : GV_OOB);
+    }
+    if constexpr (AK) {
+      const int m = m0 + (tid >> 1), k = k0 + 16 * (tid & 1);
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        ra[h] = Raw4<float>::load(rA, (m < g.M && k + 4 * h < g.K) ? (uint32_t)(((int64_t)m * g.sAm + k + 4 * h) * 4)
+                                                                    : GV_OOB);
+    }
+  };
+  // hi and lo bf16 pieces of two floats, packed
+  auto split2 = [](float x, float y, uint32_t& hi, uint32_t& lo) {
+    hi = pack_bf2(x, y);
+    lo = pack_bf2(x - __uint_as_float(hi << 16), y - __uint_as_float(hi & 0xFFFF0000u));
+  };
+  // 4 consecutive rows at 4 consecutive k (v[h]: k = h) into a [k][row] tile
+  auto put_kmajor = [&](bf16_t* H, bf16_t* Lo, const raw_t (&v)[4], int row0, int kk) {
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const int k = kk + h;
+      const int off = k * GX_CPR * 8 + (((row0 >> 3) ^ wg_sw(k, GX_CPR)) << 3) + (row0 & 7);
+      uint32_t h0, l0, h1, l1;
+      split2(__uint_as_float(v[h][0]), __uint_as_float(v[h][1]), h0, l0);
+      split2(__uint_as_float(v[h][2]), __uint_as_float(v[h][3]), h1, l1);
+      *(uint2*)(H + off) = make_uint2(h0, h1);
+      *(uint2*)(Lo + off) = make_uint2(l0, l1);
+    }
+  };
+  auto store = [&](int buf) {
+    const int kk = 4 * (tid >> 5), c = 4 * (tid & 31);
+    put_kmajor(Bh[buf], Bl[buf], rb, c, kk);
+    if constexpr (!AK) {
+      put_kmajor(Ah[buf], Al[buf], ra, c, kk);
+    } else {
+      const int m = tid >> 1, k = 16 * (tid & 1);
+      uint32_t hv[8], lv[8];
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        split2(__uint_as_float(ra[h][0]), __uint_as_float(ra[h][1]), hv[2 * h], lv[2 * h]);
+        split2(__uint_as_float(ra[h][2]), __uint_as_float(ra[h][3]), hv[2 * h + 1], lv[2 * h + 1]);
+      }
+      bf16_t* H = Ah[buf] + m * GX_LD + k;
+      bf16_t* Lo = Al[buf] + m * GX_LD + k;
+      *(uint4*)H = make_uint4(hv[0], hv[1], hv[2], hv[3]);
+      *(uint4*)(H + 8) = make_uint4(hv[4], hv[5], hv[6], hv[7]);
+      *(uint4*)Lo = make_uint4(lv[0], lv[1], lv[2], lv[3]);
+      *(uint4*)(Lo + 8) = make_uint4(lv[4], lv[5], lv[6], lv[7]);
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+
+  const int nk = (g.K + GV_BK - 1) / GV_BK;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int it = 0; it < nk; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < nk) load((it + 1) * GV_BK);
+#pragma unroll
+    for (int ks = 0; ks < GV_BK / 16; ++ks) {
+      u32x4 f[8];  // ah0 ah1 al0 al1 bh0 bh1 bl0 bl1
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        if constexpr (AK) {
+          const int row = wm * 64 + i * 32 + (lane & 31), kc = 16 * ks + 8 * (lane >> 5);
+          f[i] = *(const u32x4*)(Ah[buf] + row * GX_LD + kc);
+          f[2 + i] = *(const u32x4*)(Al[buf] + row * GX_LD + kc);
+        } else {
+          f[i] = tr_frag(Ah[buf], GX_CPR, 16 * ks, wm * 64 + i * 32, lane);
+          f[2 + i] = tr_frag(Al[buf], GX_CPR, 16 * ks, wm * 64 + i * 32, lane);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        f[4 + j] = tr_frag(Bh[buf], GX_CPR, 16 * ks, wn * 64 + j * 32, lane);
+        f[6 + j] = tr_frag(Bl[buf], GX_CPR, 16 * ks, wn * 64 + j * 32, lane);
+      }
+      lds_wait(f);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = mfma32x32x16(as_uint4(f[2 + i]), as_uint4(f[4 + j]), acc[i][j]);
+          acc[i][j] = mfma32x32x16(as_uint4(f[i]), as_uint4(f[6 + j]), acc[i][j]);
+          acc[i][j] = mfma32x32x16(as_uint4(f[i]), as_uint4(f[4 + j]), acc[i][j]);
+        }
+    }
+    // the other buffer was last read in the previous stage, before the barrier
+    if (it + 1 < nk) store(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
+  const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
+  const float* Cin = g.Cin ? g.Cin + b * g.sCinb : nullptr;
+  float* C = (float*)g.C + b * g.sCb;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        int m = m0 + wm * 64 + i * 32 + acc_row(e, lane);
+        int n = n0 + wn * 64 + j * 32 + (lane & 31);
+        if (m < g.M && n < g.N) {
+          float v = alpha * acc[i][j][e];
+          if (Cin && beta != 0.f) v += beta * Cin[m * g.sCinm + n * g.sCinn];
+          if (m == n) v += g.diag;
+          C[m * g.sCm + n * g.sCn] = v;
+          if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = v;
         }
       }
 }
@@ -311,8 +516,19 @@ int gemm_f32_vec_mode(const GemmF32Args& g, int ta, int tb) {
 hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return hipSuccess;
   const int vm = gemm_f32_vec_mode(g, ta, tb);
+  if (g.sym_upper && (vm < 0 || g.M != g.N || g.Cin)) return hipErrorInvalidValue;
+  const int ntm = (g.M + GV_BM - 1) / GV_BM;
+  const dim3 vgrid = g.sym_upper ? dim3(ntm * (ntm + 1) / 2, 1, g.batch)
+                                 : dim3(ntm, (g.N + GV_BN - 1) / GV_BN, g.batch);
+  if (g.split_bf16 && vm >= 0 && ta == 0 && tb == 0 && to == 0) {
+    if (vm)
+      hipLaunchKernelGGL((k_gemm_x3<true>), vgrid, dim3(GF_THREADS), 0, s, g);
+    else
+      hipLaunchKernelGGL((k_gemm_x3<false>), vgrid, dim3(GF_THREADS), 0, s, g);
+    return hipGetLastError();
+  }
   if (vm >= 0) {
-    dim3 grid((g.M + GV_BM - 1) / GV_BM, (g.N + GV_BN - 1) / GV_BN, g.batch);
+    const dim3 grid = vgrid;
 #define MAPL_GV(TA_, TB_, TO_)                                                                        \
   do {                                                                                                \
     if (vm)                                                                                           \

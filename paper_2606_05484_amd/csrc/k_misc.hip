@@ -152,44 +152,51 @@ __global__ void k_axpy(const float* __restrict__ U, const float* __restrict__ D,
   if (i < n) Y[i] = U[i] - lr * D[i];
 }
 
-// One block of 16 waves per projector: nu2 = max_i sum_j |S_ij|.  A wave
-// reads whole rows (lane + 64 q), four rows at a time, so the loads are
-// coalesced and several rows are in flight; r <= 1024.
-__global__ __launch_bounds__(1024) void k_inf_norm_scales(const float* __restrict__ S, int r, float* inv_nu,
-                                                          float* inv_nu2, float* inv_nu4) {
-  __shared__ float red[16];
-  const int p = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// nu2 = max_i sum_j |S_ij| per projector, in two launches: blocks of four
+// waves take 64 rows each (a wave 16 rows, four at a time with every load of
+// the four rows issued before the sums) and write their row maximum; one
+// thread per projector then takes the maximum over its blocks.  r <= 1024.
+__global__ __launch_bounds__(256) void k_inf_norm_partial(const float* __restrict__ S, int r,
+                                                          float* __restrict__ part) {
+  __shared__ float red[4];
+  constexpr int RB = 4, QMAX = 16;
+  const int p = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float* Sp = S + (int64_t)p * r * r;
-  constexpr int RB = 4, QMAX = 16;  // rows per batch; 64-column groups (r <= 1024)
   const int nq = (r + 63) / 64;
   float m = 0.f;
-  for (int i0 = wave * RB; i0 < r; i0 += 16 * RB) {
-    float part[RB];
+  for (int i0 = blockIdx.x * 64 + wave * 16; i0 < min(r, blockIdx.x * 64 + wave * 16 + 16); i0 += RB) {
+    float v[RB][QMAX];
+#pragma unroll
+    for (int u = 0; u < RB; ++u)
+#pragma unroll
+      for (int q = 0; q < QMAX; ++q) {
+        const int i = i0 + u, c = lane + 64 * q;
+        v[u][q] = (q < nq && i < r && c < r) ? Sp[(int64_t)i * r + c] : 0.f;
+      }
 #pragma unroll
     for (int u = 0; u < RB; ++u) {
-      part[u] = 0.f;
-      const int i = i0 + u;
-      if (i < r) {
+      float sum = 0.f;
 #pragma unroll
-        for (int q = 0; q < QMAX; ++q) {
-          const int c = lane + 64 * q;
-          if (q < nq && c < r) part[u] += fabsf(Sp[(int64_t)i * r + c]);
-        }
-      }
+      for (int q = 0; q < QMAX; ++q) sum += fabsf(v[u][q]);
+      m = fmaxf(m, wave_sum(sum));
     }
-#pragma unroll
-    for (int u = 0; u < RB; ++u) m = fmaxf(m, wave_sum(part[u]));
   }
   if (lane == 0) red[wave] = m;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    float nu2 = red[0];
-    for (int w = 1; w < 16; ++w) nu2 = fmaxf(nu2, red[w]);
-    const float in2 = 1.f / nu2;
-    inv_nu2[p] = in2;
-    inv_nu4[p] = in2 * in2;
-    inv_nu[p] = sqrtf(in2);
-  }
+  if (threadIdx.x == 0)
+    part[(int64_t)p * gridDim.x + blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+__global__ void k_inf_norm_final(const float* __restrict__ part, int nb, int P, float* inv_nu, float* inv_nu2,
+                                 float* inv_nu4) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= P) return;
+  float nu2 = 0.f;
+  for (int j = 0; j < nb; ++j) nu2 = fmaxf(nu2, part[(int64_t)p * nb + j]);
+  const float in2 = 1.f / nu2;
+  inv_nu2[p] = in2;
+  inv_nu4[p] = in2 * in2;
+  inv_nu[p] = sqrtf(in2);
 }
 
 // Streaming codebook synchronisation (Sec. 3.5): one wave per transmitted
@@ -273,10 +280,12 @@ hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64
   return hipGetLastError();
 }
 
-hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* inv_nu, float* inv_nu2, float* inv_nu4,
-                                  hipStream_t s) {
+hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* part, float* inv_nu, float* inv_nu2,
+                                  float* inv_nu4, hipStream_t s) {
   if (r > 1024) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_inf_norm_scales, dim3(P), dim3(1024), 0, s, S, r, inv_nu, inv_nu2, inv_nu4);
+  const int nb = (r + 63) / 64;
+  hipLaunchKernelGGL(k_inf_norm_partial, dim3(nb, P), dim3(256), 0, s, S, r, part);
+  hipLaunchKernelGGL(k_inf_norm_final, dim3((P + 255) / 256), dim3(256), 0, s, part, nb, P, inv_nu, inv_nu2, inv_nu4);
   return hipGetLastError();
 }
 

@@ -38,6 +38,9 @@ struct GemmF32Args {
   float alpha, beta;
   const float* alpha_ptr; const float* beta_ptr;
   float diag;  // added to every element with m == n after the scaling
+  int split_bf16;  // fp32 operands and output, aligned: products as split-bf16 (hi.hi + hi.lo + lo.hi)
+  int sym_upper;   // C = A B known symmetric (B = A^T, M == N, no Cin): only tiles on or above the
+                   // diagonal are computed, each off-diagonal one also written mirrored (aligned case)
 };
 hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStream_t s);
 
@@ -198,8 +201,8 @@ hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, fl
 // Y = U - lr D.
 hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64_t n, hipStream_t s);
 // For S [P][r][r]: nu2 = max_i sum_j |S_ij|; inv_nu = 1/sqrt(nu2), inv_nu2 = 1/nu2,
-// inv_nu4 = 1/nu2^2.
-hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* inv_nu, float* inv_nu2,
+// inv_nu4 = 1/nu2^2; part: P * ceil(r / 64) floats of scratch.
+hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* part, float* inv_nu, float* inv_nu2,
                                   float* inv_nu4, hipStream_t s);
 
 // ---------------------------------------------------------------- codebook synchronisation

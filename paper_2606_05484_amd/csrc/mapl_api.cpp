@@ -967,8 +967,12 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   float* scale = sc, *scale2 = sc + P, *inv_nu = sc + 2 * P, *inv_nu2 = sc + 3 * P, *inv_nu4 = sc + 4 * P;
   const int64_t n = d * r, rr = r * r;
 
-  auto gram = [&](const float* X, const float* aptr) {  // S = X^T X (times aptr)
+  // x3: the products as split-bf16 (hi.hi + hi.lo + lo.hi, about 2^-15
+  // relative per term) on the bf16 matrix units; the LMO's direction only
+  auto gram = [&](const float* X, const float* aptr, bool x3) {  // S = X^T X (times aptr)
     GemmF32Args g = gemm((int)r, (int)r, (int)d);
+    g.split_bf16 = x3;
+    g.sym_upper = 1;  // X^T X: the tiles above the diagonal, mirrored
     g.batch = (int)P;
     g.A = X; g.sAm = 1; g.sAk = r; g.sAb = n;
     g.B = X; g.sBk = r; g.sBn = 1; g.sBb = n;
@@ -976,8 +980,9 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.alpha_ptr = aptr;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr) {  // Qm = a I + b S + c S S
+  auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr, bool x3) {  // Qm = a I + b S + c S S
     GemmF32Args g = gemm((int)r, (int)r, (int)r);
+    g.split_bf16 = x3;
     g.batch = (int)P;
     g.A = S; g.sAm = r; g.sAk = 1; g.sAb = rr;
     g.B = S; g.sBk = r; g.sBn = 1; g.sBb = rr;
@@ -987,8 +992,9 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.alpha_ptr = aptr; g.beta_ptr = bptr;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  auto apply = [&](const float* X, float* Xo, const float* sptr) {  // Xo = s X Qm
+  auto apply = [&](const float* X, float* Xo, const float* sptr, bool x3) {  // Xo = s X Qm
     GemmF32Args g = gemm((int)d, (int)r, (int)r);
+    g.split_bf16 = x3;
     g.batch = (int)P;
     g.A = X; g.sAm = r; g.sAk = 1; g.sAb = n;
     g.B = Qm; g.sBk = r; g.sBn = 1; g.sBb = rr;
@@ -1024,17 +1030,18 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   LAUNCH("stiefel:momentum", launch_momentum(M, X0, G, n, (int)P, beta, partial, nblk, s));
   LAUNCH("stiefel:fro_scale", launch_fro_scale(partial, nblk, (int)P, 1e-7f, 1.0f / 1048576.0f, scale, scale2, s));
 
-  // Eq. 6: D = PE(M / (||M|| + eps))
+  // Eq. 6: D = PE(M / (||M|| + eps)), products in split-bf16 (the direction
+  // carries about 3e-5 relative error; the retraction below stays fp32)
   const float* Xin = M;
   float* bufs[2] = {X0, X1};
   int cur = 0;
   for (int i = 0; i < lmo_steps; ++i) {
     const double a = kLmoCoef[i][0], b = kLmoCoef[i][1], cc = kLmoCoef[i][2];
     const bool first = i == 0;
-    LAUNCH("stiefel:gram", gram(Xin, first ? scale2 : nullptr));
-    LAUNCH("stiefel:poly", poly(a, b, cc, nullptr, nullptr));
+    LAUNCH("stiefel:lmo_gram", gram(Xin, first ? scale2 : nullptr, true));
+    LAUNCH("stiefel:lmo_poly", poly(a, b, cc, nullptr, nullptr, true));
     float* Xo = bufs[cur];
-    LAUNCH("stiefel:apply", apply(Xin, Xo, first ? scale : nullptr));
+    LAUNCH("stiefel:lmo_apply", apply(Xin, Xo, first ? scale : nullptr, true));
     Xin = Xo;
     cur ^= 1;
   }
@@ -1043,16 +1050,17 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   LAUNCH("stiefel:axpy", launch_axpy(U, Xin, lr, Y, P * n, s));
   cur ^= 1;
   // Eq. 7: U = PE(Y / nu), nu^2 = max row sum |Y^T Y|
-  LAUNCH("stiefel:gram", gram(Y, nullptr));
-  LAUNCH("stiefel:inf_norm_scales", launch_inf_norm_scales(S, (int)P, (int)r, inv_nu, inv_nu2, inv_nu4, s));
+  LAUNCH("stiefel:gram", gram(Y, nullptr, false));
+  // (the momentum's norm partials are consumed by now; their buffer takes the row maxima)
+  LAUNCH("stiefel:inf_norm_scales", launch_inf_norm_scales(S, (int)P, (int)r, partial, inv_nu, inv_nu2, inv_nu4, s));
   Xin = Y;
   for (int i = 0; i < retract_steps; ++i) {
     const double a = kRetractCoef[i][0], b = kRetractCoef[i][1], cc = kRetractCoef[i][2];
     const bool first = i == 0;
-    if (!first) LAUNCH("stiefel:gram", gram(Xin, nullptr));
-    LAUNCH("stiefel:poly", poly(a, b, cc, first ? inv_nu4 : nullptr, first ? inv_nu2 : nullptr));
+    if (!first) LAUNCH("stiefel:gram", gram(Xin, nullptr, false));
+    LAUNCH("stiefel:poly", poly(a, b, cc, first ? inv_nu4 : nullptr, first ? inv_nu2 : nullptr, false));
     float* Xo = (i == retract_steps - 1) ? U : bufs[cur];
-    LAUNCH("stiefel:apply", apply(Xin, Xo, first ? inv_nu : nullptr));
+    LAUNCH("stiefel:apply", apply(Xin, Xo, first ? inv_nu : nullptr, false));
     Xin = Xo;
     cur ^= 1;
   }
