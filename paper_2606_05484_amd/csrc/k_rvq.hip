@@ -21,8 +21,11 @@
 //           satisfies L_j* <= s_j* <= s_j1 <= U = L_j1 + (1 + 1.03) Delta_j1
 //           for the smallest key j1, so it is among {j : L_j <= U}: a
 //           single codeword when the token's second key exceeds U (final).
-//   pass 2  (only in a workgroup with a token not final) re-screens and
-//           lists every codeword with L_j <= U of those tokens.
+//   pass 2  (only in a workgroup with a token not final) lists every
+//           codeword with L_j <= U of those tokens: their B operands are
+//           compacted into 32-token tiles in LDS, and each wave screens a
+//           quarter of the codeword tiles against them, codebook fragments
+//           read straight from the L2-resident screening copy.
 //   rescore the listed candidates exactly in fp32 as sum_c (R_c - C_jc)^2:
 //           per wave a batch of up to 8 open tokens, their residual rows
 //           staged in LDS, 8 (token, codeword) pairs per step with coalesced
@@ -91,8 +94,10 @@ __device__ __forceinline__ float rq_tag_slot(float s, int e) {
 struct RqSmall {
   int cand_cnt[RQ_TOK];
   uint16_t cand[RQ_TOK][RQ_CAP];
-  int amb_s[RQ_TOK];
-  int dec[4][8];  // per wave: the decisions of a rescoring batch
+  float cthr[RQ_TOK];  // the open tokens, compacted: threshold U and token index
+  int cmap[RQ_TOK];
+  int wcnt[4];         // open tokens per wave
+  int dec[4][8];       // per wave: the decisions of a rescoring batch
 };
 
 // The L rounds for the workgroup's 128 tokens (blockIdx.x), given each
@@ -110,7 +115,6 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
   constexpr int LOADS = rq_blocks<R>();            // DMA blocks per wave per stage
   auto& cand_cnt = sm.cand_cnt;
   auto& cand = sm.cand;
-  auto& amb_s = sm.amb_s;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
   const int tl = wave * 32 + (lane & 31);  // token within the workgroup
@@ -308,7 +312,8 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
     //  pass 1: per lane the two smallest keys and the position of the
     //    first; a token is final when its second key exceeds U;
     //  pass 2 (only in a workgroup with an open token): every key <= U of
-    //    the open tokens listed; the candidates are rescored exactly in fp32.
+    //    the open tokens listed (the open tokens compacted); the candidates
+    //    are rescored exactly in fp32.
     const float* n2l = a.meta + (int64_t)l * nchunks * 64;
     const float* e2l = n2l + (int64_t)a.L * nchunks * 64;
     auto margin = [&](int j) {  // Delta_j, rounded up
@@ -350,26 +355,97 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
 
     int jstar = j1;
     if (any_open) {
-      // ---- pass 2: list every key <= U of the open tokens (a per-tile hit
-      // mask, flushed once per tile)
-      const float lthr = open ? thr : -INFINITY;
-      uint32_t hit = 0;
-      pass([&]() { hit = 0; },
-           [&](const f32x16_t& acc, int, auto ec) {
-             constexpr int E = decltype(ec)::value;
-             hit |= acc[E] <= lthr ? (1u << E) : 0u;
-           },
-           [&](int tile) {
-             if (hit && tile >= 0) {
-               for (uint32_t h = hit; h; h &= h - 1u) {
-                 const int e = __builtin_ctz(h);
-                 const int idx = atomicAdd(&cand_cnt[tl], 1);
-                 if (idx < RQ_CAP) cand[tl][idx] = (uint16_t)(tile * 32 + rq_row(e, half));
-               }
-             }
-           },
-           false);
-      __syncthreads();  // stage 2 (read last by the pass) is free for the rescoring
+      // ---- pass 2: list every key <= U of the open tokens.  The open
+      // tokens are compacted: each writes its MFMA B operand (the 17 k-steps
+      // of bf16(-2R) and the norm operand, 16 B per lane half and k-step) to
+      // a row of stages 0 and 1 (free until the next round's loads), its
+      // threshold and index to a table; then every wave takes 32 compacted
+      // tokens at a time against its quarter of the codeword tiles, the
+      // codebook fragments read straight from the (L2-resident) screening
+      // copy, with no LDS staging and no barrier between waves.
+      constexpr int TB = (R + 16) * 2;                        // bytes of a compacted row
+      constexpr int CAP0 = (int)(sizeof(RqStage<R>) / TB);     // rows in stage 0
+      static_assert(2 * CAP0 >= RQ_TOK, "stages 0 and 1 hold every token's row");
+      auto crow = [&](int c) -> char* {
+        return c < CAP0 ? (char*)s0 + (int64_t)c * TB : (char*)s1 + (int64_t)(c - CAP0) * TB;
+      };
+      {
+        const uint64_t ob = __ballot(half == 0 && open);
+        if (lane == 0) sm.wcnt[wave] = __popcll(ob);
+        __syncthreads();
+        int base = 0;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) base += w < wave ? sm.wcnt[w] : 0;
+        if (open) {
+          const int c = base + __popcll(ob & ((1ull << (lane & 31)) - 1ull));
+          char* rw = crow(c) + 16 * half;
+#pragma unroll
+          for (int s = 0; s < NK16; ++s) *(uint4*)(rw + 32 * s) = rb[s];
+          *(uint4*)(rw + 32 * NK16) = rbn;
+          if (half == 0) {
+            sm.cthr[c] = thr;
+            sm.cmap[c] = tl;
+          }
+        }
+        __syncthreads();
+      }
+      const int n_open = (sm.wcnt[0] + sm.wcnt[1]) + (sm.wcnt[2] + sm.wcnt[3]);
+      const __amdgpu_buffer_rsrc_t rcb =
+          rq_rsrc(a.Cb + (int64_t)l * a.K * (R + 16), (uint64_t)a.K * (R + 16) * 2);
+      const int ntiles = a.K / 32;  // K % 32 == 0
+      for (int ct = 0; ct * 32 < n_open; ++ct) {  // workgroup-uniform
+        const int c = ct * 32 + (lane & 31);
+        const bool cv = c < n_open;
+        const int cc = cv ? c : n_open - 1;
+        uint4 bq[NK16 + 1];  // [0]: the norm step, [1 + s]: k-step s
+        {
+          const char* rr = crow(cc) + 16 * half;
+          bq[0] = *(const uint4*)(rr + 32 * NK16);
+#pragma unroll
+          for (int s = 0; s < NK16; ++s) bq[1 + s] = *(const uint4*)(rr + 32 * s);
+        }
+        const float cthr = cv ? sm.cthr[cc] : -INFINITY;
+        const int ctl = sm.cmap[cc];
+        // codeword tiles q = wave, wave + 4, ...; the next tile's fragments
+        // are requested before the products of the current one
+        constexpr int PF = NK16 + 1;  // the whole next tile
+        auto frag = [&](int q, int p) -> uint4 {
+          // row q * 32 + lane % 32; 16-byte chunk 2 s + half for k-step s =
+          // p - 1, the norm columns (chunk 2 NK16 + half) for p = 0
+          const uint32_t off = (uint32_t)(q * 32 + (lane & 31)) * (uint32_t)TB + 16u * (uint32_t)half +
+                               32u * (uint32_t)(p == 0 ? NK16 : p - 1);
+          const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rcb, off, 0, 0);
+          return make_uint4(v[0], v[1], v[2], v[3]);
+        };
+        uint4 pre[PF];
+        if (wave < ntiles) {
+#pragma unroll
+          for (int p = 0; p < PF; ++p) pre[p] = frag(wave, p);
+        }
+        for (int q = wave; q < ntiles; q += 4) {  // wave-uniform
+          uint4 af[NK16 + 1];
+#pragma unroll
+          for (int p = 0; p < PF; ++p) af[p] = pre[p];
+#pragma unroll
+          for (int p = PF; p <= NK16; ++p) af[p] = frag(q, p);
+          if (q + 4 < ntiles) {
+#pragma unroll
+            for (int p = 0; p < PF; ++p) pre[p] = frag(q + 4, p);
+          }
+          f32x16_t acc = f32x16_t{};
+#pragma unroll
+          for (int p = 0; p <= NK16; ++p) acc = mfma32x32x16(af[p], bq[p], acc);
+          uint32_t hit = 0;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) hit |= acc[e] <= cthr ? (1u << e) : 0u;
+          for (uint32_t h = hit; h; h &= h - 1u) {
+            const int e = __builtin_ctz(h);
+            const int idx = atomicAdd(&cand_cnt[ctl], 1);
+            if (idx < RQ_CAP) cand[ctl][idx] = (uint16_t)(q * 32 + rq_row(e, half));
+          }
+        }
+      }
+      __syncthreads();  // every list is complete, stages 0 and 1 are read
       // ---- exact fp32 rescoring of the open tokens, wave by wave (each wave
       // its own 32), a batch of up to 8 tokens at a time: their residuals go
       // to the wave's share of stage 2, their (token, codeword) pairs are
@@ -560,7 +636,8 @@ __device__ __forceinline__ void rvq_rounds(const RvqArgs& a, bf16_t* s0, bf16_t*
       else
         ((uint16_t*)a.codes)[(int64_t)t * a.L + l] = (uint16_t)jstar;
     }
-    // no barrier: the next round's shared state (amb_s, cand_cnt and cand;
+    // no barrier: the next round's shared state (cand_cnt, cand, the
+    // compacted tokens' table;
     // dec and the staging rows, which only the token's own wave touches) is
     // written after barriers that every wave reaches only once done with
     // this round
