@@ -307,6 +307,42 @@ def test_rvq_candidate_overflow_full_rescan(d, r):
 
 
 @pytest.mark.parametrize("r", [64, 128, 256])
+def test_rvq_every_token_undecided(r):
+    """Every token of every workgroup undecided after the first pass, and
+    every candidate list overflowing: each round's codebook is four distinct
+    codewords repeated (C[l, j] = C[l, j % 4], K = 128), so each token's
+    nearest row has 31 bitwise-identical copies, an exact tie that the lowest
+    index breaks.  The second pass then lists all 128 tokens of a workgroup
+    (four compacted tiles) and the rescoring falls back to the full codebook
+    for each.  Codes must be the lowest index of the nearest distinct
+    codeword; tokens whose two nearest distinct codewords nearly tie are
+    exempt, as everywhere."""
+    x = _x(None, seed=21, **dict(SMALL, T=300, d=512, r=r, k=16, L=2, K=128))
+    Z0 = ocodec.project(f64(x, "X"), x["ids"], x["U"], f64(x, "A"), f64(x, "B"), "ambient", "bf16")
+    rng = np.random.default_rng(5)
+    sig = float(np.sqrt(np.mean(Z0 ** 2)))
+    base = np.zeros((2, 4, r), dtype=np.float32)
+    base[0, 1:] = (Z0[rng.choice(300, 3, replace=False)] + 0.05 * sig * rng.standard_normal((3, r))).astype(np.float32)
+    base[1, 1:] = (0.3 * sig * rng.standard_normal((3, r))).astype(np.float32)
+    C = np.stack([np.tile(base[l], (32, 1)) for l in range(2)])
+    assert C.shape == (2, 128, r) and np.array_equal(C[:, 4], C[:, 0])
+    codes_ref, _, _ = ocodec.rvq_encode(Z0, C)          # lowest index among the copies
+    codes_4, gap4, _ = ocodec.rvq_encode(Z0, base)      # the near-tie measure among distinct rows
+    assert np.array_equal(codes_ref, codes_4)
+    D = descr(x)
+    g = Dev(x, C)
+    mapl.profile(2)
+    cg = codes_np(run_encode(x, D, g), D)
+    st = mapl.profile_report()
+    mapl.profile(0)
+    bad, ex = compare_codes(cg, codes_ref, gap4)
+    ovf = st.get("rvq:list_overflows", (0, 0))[0]
+    print("every token undecided, r=%d: mismatched %d exempt %d list overflows %d" % (r, bad, ex, ovf))
+    assert bad == 0
+    assert ovf == 2 * 300  # every (token, round) list overflowed into the full rescan
+
+
+@pytest.mark.parametrize("r", [64, 128, 256])
 def test_short_k_many_tiles(r):
     """Decode and encode_bwd at d=2048 with enough tokens (8192 + a ragged
     77) that each workgroup walks several output tiles: the K depths
