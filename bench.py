@@ -190,18 +190,18 @@ def _chain_map(disp, order, chains):
     timed and profiled steps; the SPEL timing follows them) by its position."""
     lib = [x for x in disp if "mapl::" in x[1]]
     n = len(order)
-    if n == 0 or len(lib) < n * chains:
-        raise SystemExit("summarize: %d library dispatches, fewer than %d chains of %d" % (len(lib), chains, n))
-    lib = lib[:n * chains]
-    named = []
-    for i, (did, sym, e) in enumerate(lib):
-        named.append((order[i % n], sym, e))
-    # every position must always be the same kernel symbol
-    for j in range(n):
-        syms = {named[i][1] for i in range(j, len(named), n)}
-        if len(syms) != 1:
-            raise SystemExit("summarize: chain position %d (%s) maps to several kernels" % (j, order[j]))
-    return named
+    # the chains may follow a few set-up dispatches (e.g. the data-drawn
+    # codebooks' projection): the first offset at which every chain position
+    # is always the same kernel symbol
+    for off in range(0, 8):
+        body = lib[off:]
+        m = min(chains, len(body) // n) if n else 0
+        if m < 1:
+            break
+        body = body[:n * m]
+        if all(len({body[i][1] for i in range(j, len(body), n)}) == 1 for j in range(n)):
+            return [(order[i % n], sym, e) for i, (did, sym, e) in enumerate(body)]
+    raise SystemExit("summarize: no offset maps the %d library dispatches onto chains of %d" % (len(lib), n))
 
 
 def _short(sym):
@@ -548,6 +548,28 @@ def next_rows(torch, mapl, x, Cs, args):
     return out
 
 
+def spel_step_timing(torch, mapl, synth, P, dd, rr, reps):
+    """(mean, median) ms of one SPEL step on P projectors [dd, rr] (seed 55)."""
+    stq = synth.stiefel_inputs(None, seed=55, P=P, d=dd, r=rr, gscale=1e-3, lr=1e-2, beta=0.95, steps=1)
+    Ug, Gg, Mg = (torch.from_numpy(stq[n]).cuda() for n in ("U", "G", "M"))
+    w = mapl.workspace(mapl.workspace_bytes(None, mapl.CALL_STIEFEL, P, dd, rr))
+    run = lambda: mapl.stiefel_step(P, dd, rr, Ug, Gg, Mg, 1e-2, 0.95, 5, 7, w)
+    return time_steps(torch, run, 2, reps)
+
+
+def spel_flops(P, dd, rr):
+    it = 4 * dd * rr * rr + 2 * rr ** 3
+    return P * (4 * dd * rr * rr + 12 * it)
+
+
+def spel_roofline_s(P, dd, rr):
+    """Eq. 4 and the 7 retraction steps on the fp32 matrix units; the 5 LMO
+    steps as split-bf16 products (three bf16 products per flop) on the bf16
+    matrix units."""
+    it = 4 * dd * rr * rr + 2 * rr ** 3
+    return P * (4 * dd * rr * rr + 7 * it) / PEAK_F32 + P * 5 * it * 3 / PEAK_BF16
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -559,6 +581,11 @@ def main():
                          "reported)")
     ap.add_argument("--no-extra", action="store_true",
                     help="only the c4 headline (no stress, per-config or SPEL blocks)")
+    ap.add_argument("--spel-only", action="store_true",
+                    help="only the SPEL step (16 projectors [2048,512]): one JSON line, for profiling")
+    ap.add_argument("--codebooks", choices=("official", "stress"), default="official",
+                    help="codebooks of the headline chain: the workload's own (default), or data-drawn ones "
+                         "(every code in use; for profiling the RVQ's second pass and rescoring)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with one plain 256 MiB device copy (calibrates FETCH_SIZE / WRITE_SIZE counters)")
     ap.add_argument("--summarize", nargs="+", metavar="PATH",
@@ -581,10 +608,18 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    if args.spel_only:
+        ms_, med_ = spel_step_timing(torch, mapl, synth, 16, 2048, 512, args.steps)
+        print(json.dumps({"config": "SPEL step, 16 projectors [2048,512], PolarExpress 5 + 7 steps",
+                          "ms_per_step": ms_, "median_ms_per_step": med_,
+                          "roofline_ms": spel_roofline_s(16, 2048, 512) * 1e3,
+                          "roofline_frac": spel_roofline_s(16, 2048, 512) / (med_ * 1e-3)}))
+        return
     log("generating workload c4")
     x = synth.codec_inputs("c4")
     T, d, r, V, k, L, K = (x[n] for n in ("T", "d", "r", "V", "k", "L", "K"))
-    ch = Chain(torch, mapl, x, x["C"])
+    C_head = x["C"] if args.codebooks == "official" else library_stress_codebooks(torch, mapl, x)
+    ch = Chain(torch, mapl, x, C_head)
     calls = ["encode", "decode", "decode_bwd", "encode_bwd"]
 
     # ---- the c4 headline: every c4 chain with the official codebooks runs
@@ -631,8 +666,9 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "1B-shaped boundary (c4): T=32768 tokens (16x2048), d=2048, r=256, "
                                "anchor k=128 over V=32000 (Zipf 1.1 ids), RVQ L=2 x K=1024, u16 codes, "
-                               "ambient anchor, enc+dec fwd+bwd per step, %s" %
-                               ("the 4-call chain replayed as one HIP graph" if args.graph else "eager calls"),
+                               "ambient anchor, enc+dec fwd+bwd per step, %s%s" %
+                               ("the 4-call chain replayed as one HIP graph" if args.graph else "eager calls",
+                                "" if args.codebooks == "official" else ", data-drawn codebooks"),
                    "global_batch": T, "seq_len": 2048, "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "median_ms_per_step": med,
@@ -727,27 +763,9 @@ def main():
 
         # ---- SPEL step: its own configuration (16 x [2048,512]) and this
         # boundary's projector
-        def time_spel(P, dd, rr, reps):
-            stq = synth.stiefel_inputs(None, seed=55, P=P, d=dd, r=rr, gscale=1e-3, lr=1e-2, beta=0.95, steps=1)
-            Ug, Gg, Mg = (torch.from_numpy(stq[n]).cuda() for n in ("U", "G", "M"))
-            w = mapl.workspace(mapl.workspace_bytes(None, mapl.CALL_STIEFEL, P, dd, rr))
-            run = lambda: mapl.stiefel_step(P, dd, rr, Ug, Gg, Mg, 1e-2, 0.95, 5, 7, w)
-            return time_steps(torch, run, 2, reps)
-
-        def spel_flops(P, dd, rr):
-            it = 4 * dd * rr * rr + 2 * rr ** 3
-            return P * (4 * dd * rr * rr + 12 * it)
-
-        def spel_roofline_s(P, dd, rr):
-            """Eq. 4 and the 7 retraction steps on the fp32 matrix units; the
-            5 LMO steps as split-bf16 products (three bf16 products per
-            flop) on the bf16 matrix units."""
-            it = 4 * dd * rr * rr + 2 * rr ** 3
-            return P * (4 * dd * rr * rr + 7 * it) / PEAK_F32 + P * 5 * it * 3 / PEAK_BF16
-
         log("SPEL step")
-        spel_c5, spel_c5_med = time_spel(16, 2048, 512, 10)
-        spel_b, _ = time_spel(1, d, r, 20)
+        spel_c5, spel_c5_med = spel_step_timing(torch, mapl, synth, 16, 2048, 512, 10)
+        spel_b, _ = spel_step_timing(torch, mapl, synth, 1, d, r, 20)
         out["spel"] = {"config": "16 projectors [2048,512], PolarExpress 5 + 7 steps", "ms_per_step": spel_c5,
                        "median_ms_per_step": spel_c5_med,
                        "tflops": spel_flops(16, 2048, 512) / (spel_c5_med * 1e-3) / 1e12,
