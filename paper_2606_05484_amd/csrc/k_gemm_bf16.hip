@@ -58,41 +58,88 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 #endif
 }
 
-// Short-K, write-heavy products with bf16 output (decode: K = r + k,
-// encode_bwd: K = r; N = d), walked over many output tiles per 128-token
-// block: 128 x 128 tiles, each of the 4 waves owning 32 token rows and all
-// 128 columns.  A wave loads the token fragments of its rows for the whole
-// K (up to 6 stages) once, straight from memory into registers in the
-// matrix unit's operand layout (16 B per lane and fragment: token row
-// l % 32, k 8 (l / 32) .. +7 of a 16-wide k-step; anchor rows gathered by
-// id), so the token operand uses no LDS; W streams through a three-deep
-// ring of 16 KiB stages.  48 KiB of LDS and at most 216 registers per lane
-// let two workgroups share a CU, so one's output stores overlap the
-// other's products.  Epilogue: as tn_epilogue, for 32-row waves.
+// Short-K, write-heavy products with bf16 output (decode: K = r + k <= 384,
+// encode_bwd: K = r; N = d).  A workgroup of 4 waves owns a 256-token block
+// and walks a run of 128-column output tiles; each wave owns 64 token rows
+// (two 32-row fragments) x all 128 columns, so every W fragment read from
+// LDS feeds two matrix products (half the LDS bytes per product of a 32-row
+// wave).  A wave loads its token fragments for the whole K once, straight
+// from memory into registers in the matrix unit's operand layout (16 B per
+// lane and fragment; anchor rows gathered by id).  W streams through a ring
+// of NSW 16 KiB stages filled by buffer_load ... lds, D = NSW - 1 stages
+// ahead; the stage-ready wait and barrier sit after the third k-step of the
+// stage before, so the first fragments of every stage are read while the
+// last products of the previous one run.  The 128 accumulator registers per
+// lane take one wave per SIMD.
+//
+// Output: at the end of a tile each wave packs its 64 x 128 block to bf16
+// (the cross-half swap of tn_epilogue) into a wave-private 16 KiB LDS area
+// as 128 B row segments; the 16 row-segment stores (8 rows x 128 B each)
+// are then spread over the first k-steps of the next tile, one LDS read and
+// one range-checked buffer store at a time, so the output leaves while the
+// matrix units work instead of in a burst that stalls them (rows past the
+// last token are dropped by the hardware; the last tile's stores drain
+// after the loop).  Every wave issues the same memory operations in the same
+// order every tile -- the first tile's stores go to an out-of-range offset,
+// DMA past the last stage reads zeros into a slot nobody reads -- so each
+// stage wait is a fixed vmcnt count, computed below from that order.
+constexpr int SH_BM = 256, SH_BN = 128;
+
 template <int KS>
-__global__ __launch_bounds__(GTHREADS, 2) void k_gemm_tn_short(TnArgs g, int ntiles_per_wg) {
+struct ShortPlan {
+  static constexpr int KSTEP = GK / 16, KST = KS * KSTEP, D = KS < 4 ? KS : 4, NSW = D + 1, WBLK = 4, NCH = 16;
+  // row-segment stores issued at the end of k-step q of a tile
+  static constexpr int st(int q) { return (NCH * (q + 1)) / KST - (NCH * q) / KST; }
+  static constexpr int st0(int q) { return (NCH * q) / KST; }  // first chunk stored at k-step q
+  // memory operations issued after the last DMA block of stage s + 1 up to
+  // the wait for it in stage s (after k-step 2's DMA): per k-step one DMA
+  // block then its stores; the prologue issues the DMA of stages 0 .. D-1
+  static constexpr int wait_n(int ksi, bool first) {
+    const int s = (first ? 0 : KS) + ksi, y = s + 1;
+    int n = 0, g0 = 0;
+    if (y < D) {
+      n += WBLK * (D - 1 - y);
+    } else {
+      const int gy = 4 * (y - D) + 3;
+      n += st(gy % KST);
+      g0 = gy + 1;
+    }
+    for (int gq = g0; gq < 4 * s + 2; ++gq) n += 1 + st(gq % KST);
+    return n + 1;
+  }
+};
+
+template <int KS>
+__global__ __launch_bounds__(GTHREADS, 1) void k_gemm_tn_short(TnArgs g, int ntiles_per_wg) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int BN = 128, NSW = 3, FN = BN / 32, KSTEP = GK / 16, KST = KS * KSTEP;
-  constexpr int WBLK = BN / 8 / 4;  // W: 1 KiB blocks per wave per stage
-  __shared__ __attribute__((aligned(1024))) bf16_t SW[NSW][BN * GK];
+  using P = ShortPlan<KS>;
+  constexpr int BN = SH_BN, FM = 2, FN = BN / 32, KSTEP = P::KSTEP, KST = P::KST, D = P::D, NSW = P::NSW;
+  constexpr int WBLK = P::WBLK;
+  static_assert(WBLK == BN / 8 / 4 && WBLK == KSTEP, "one 1 KiB DMA block per wave and k-step");
+  static_assert(KST >= 8, "at most two stores per k-step");
+  constexpr uint32_t WSTG = BN * GK * 2;
+  constexpr int COLS = 64, CPR = COLS / 8, STGB = 64 * BN * 2;  // per-wave staging: 64 rows x 128 columns
+  __shared__ __attribute__((aligned(1024))) bf16_t SW[NSW * BN * GK + 4 * STGB / 2];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int m0 = blockIdx.x * GM;
+  const int m0 = blockIdx.x * SH_BM;
   const int nt0 = blockIdx.y * ntiles_per_wg;
   const int ntiles = min(ntiles_per_wg, g.N / BN - nt0);
   const int total = ntiles * KS;
 
-  const int mrows = min(GM, g.M - m0);
-  const __amdgpu_buffer_rsrc_t ra = rsrc(g.A + (int64_t)m0 * g.lda, (uint64_t)(mrows > 0 ? mrows : 0) * g.lda * 2);
+  const int mrows = min(SH_BM, g.M - m0);
+  const __amdgpu_buffer_rsrc_t ra = rsrc(g.A + (int64_t)m0 * g.lda, (uint64_t)mrows * g.lda * 2);
   const __amdgpu_buffer_rsrc_t rt = rsrc(g.T, g.T ? (uint64_t)g.V * g.ldt * 2 : 0);
   const __amdgpu_buffer_rsrc_t rw = rsrc(g.W, (uint64_t)g.N * g.ldw * 2);
+  const __amdgpu_buffer_rsrc_t ro = rsrc((bf16_t*)g.out + (int64_t)m0 * g.ldo, (uint64_t)mrows * g.ldo * 2);
 
-  // token fragments of rows 32 wave .. +31; rows past the last token read zeros
-  u32x4 afr[KST];
-  {
-    const int row = wave * 32 + (lane & 31);
-    const bool in = m0 + row < g.M;
+  // token fragments of rows 64 wave + 32 i .. +31; rows past the last token read zeros
+  u32x4 afr[FM][KST];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int row = wave * 64 + i * 32 + (lane & 31);
+    const bool in = row < mrows;
     const uint32_t ch = 16u * (uint32_t)(lane >> 5);
     const uint32_t aoff = in ? (uint32_t)row * (uint32_t)g.lda * 2u + ch : OOB;
     const uint32_t toff =
@@ -100,160 +147,185 @@ __global__ __launch_bounds__(GTHREADS, 2) void k_gemm_tn_short(TnArgs g, int nti
 #pragma unroll
     for (int q = 0; q < KST; ++q) {
       const int kc = q * 16;
-      if (kc < g.Ka)
-        afr[q] = __builtin_amdgcn_raw_buffer_load_b128(ra, aoff, kc * 2, 0);
-      else
-        afr[q] = __builtin_amdgcn_raw_buffer_load_b128(rt, toff, (kc - g.Ka) * 2, 0);
+      const bool in_a = kc < g.Ka;
+      afr[i][q] = __builtin_amdgcn_raw_buffer_load_b128(in_a ? ra : rt, in_a ? aoff : toff,
+                                                        in_a ? kc * 2 : (kc - g.Ka) * 2, 0);
     }
   }
 
-  const int lrow = lane >> 3;
-  const uint32_t lchp[2] = {(uint32_t)((lane & 7) ^ (lane >> 4)), (uint32_t)((lane & 7) ^ (4 + (lane >> 4)))};
+  // W stage s (tile s / KS, k 64 (s % KS) ..) goes to ring slot s % NSW as
+  // 128 B rows, 16 B chunks swizzled by ((row >> 1) & 7); block j of a wave
+  // covers rows 8 (4 wave + j) .. +7
   uint32_t w_off[WBLK];
+  {
+    const int lrow = lane >> 3;
+    const uint32_t lchp[2] = {(uint32_t)((lane & 7) ^ (lane >> 4)), (uint32_t)((lane & 7) ^ (4 + (lane >> 4)))};
 #pragma unroll
-  for (int j = 0; j < WBLK; ++j) {
-    const int row = 8 * (wave * WBLK + j) + lrow;
-    w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lchp[j & 1];
-  }
-  int pl_ks = 0, pl_nt = nt0, pl_s = 0;
-  struct WPlan {
-    bf16_t* sw;
-    int soff;
-    bool live;
-  };
-  auto plan_next = [&](bf16_t* sw) {
-    WPlan p;
-    p.sw = sw;
-    const int ks = __builtin_amdgcn_readfirstlane(pl_ks), nt = __builtin_amdgcn_readfirstlane(pl_nt);
-    p.live = __builtin_amdgcn_readfirstlane(pl_s) < total;
-    ++pl_s;
-    if (++pl_ks == KS) {
-      pl_ks = 0;
-      ++pl_nt;
+    for (int j = 0; j < WBLK; ++j) {
+      const int row = 8 * (wave * WBLK + j) + lrow;
+      w_off[j] = (uint32_t)row * (uint32_t)g.ldw * 2u + 16u * lchp[j & 1];
     }
-    p.soff = (int)((uint32_t)nt * BN * (uint32_t)g.ldw * 2u + (uint32_t)(ks * GK) * 2u);
-    return p;
+  }
+  const uint32_t ntile_bytes = (uint32_t)BN * (uint32_t)g.ldw * 2u;
+  // the DMA cursor: the stage it fills next, its ring slot, its byte offset in W
+  int d_stage = 0, d_slot = 0, d_ks = 0;
+  uint32_t d_off = (uint32_t)nt0 * ntile_bytes;
+  auto dma_block = [&](int j) {
+    const bool live = d_stage < total;
+    bf16_t* dst = SW + d_slot * (BN * GK) + (wave * WBLK + j) * 512;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)dst, 16, live ? w_off[j] : OOB, (int)d_off, 0, 0);
   };
-  auto issue_range = [&](const WPlan& p, auto b0c, auto b1c) {
-    if (!p.live) return;
-    static_for<decltype(b0c)::value, decltype(b1c)::value>([&](auto jc) {
-      constexpr int J = decltype(jc)::value;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(p.sw + (wave * WBLK + J) * 512), 16, w_off[J], p.soff, 0,
-                                               0);
-    });
+  auto dma_next = [&]() {
+    ++d_stage;
+    d_slot = d_slot + 1 == NSW ? 0 : d_slot + 1;
+    if (++d_ks == KS) {
+      d_ks = 0;
+      d_off += ntile_bytes - (uint32_t)((KS - 1) * GK * 2);
+    } else {
+      d_off += GK * 2;
+    }
   };
-
-  f32x16_t acc[FN];
 #pragma unroll
-  for (int j = 0; j < FN; ++j) acc[j] = f32x16_t{};
+  for (int s = 0; s < D; ++s) {
+#pragma unroll
+    for (int j = 0; j < WBLK; ++j) dma_block(j);
+    dma_next();
+  }
+  // the token fragments land here, not inside the stage loop
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int q = 0; q < KST; ++q) asm volatile("" : "+v"(afr[i][q]));
+
   uint32_t koff[KSTEP];
 #pragma unroll
   for (int kk = 0; kk < KSTEP; ++kk) koff[kk] = tn_koff(kk, lane);
-  constexpr int PER = (WBLK + KSTEP - 1) / KSTEP;
-  constexpr uint32_t WSTG = BN * GK * 2;
-  const uint32_t swb = lds_addr(&SW[0][0]);
-  auto wbuf = [&](int u) { return (bf16_t*)&SW[0][0] + u * (BN * GK); };
+  const uint32_t swb = lds_addr(SW);
+  const uint32_t stg = swb + NSW * WSTG + wave * STGB;
+  const int half = lane >> 5;
+  // staging chunk c (block b = c / 4 = 2 i + h, 32 rows x 64 columns; part
+  // q = c % 4): lane l reads row (l + 64 q) / 8, 16 B chunk (l + 64 q) % 8
+  auto chunk_lds = [&](int c) {
+    const int cc = lane + 64 * (c & 3), row = cc / CPR, chn = cc % CPR;
+    return stg + (c >> 2) * (32 * COLS * 2) + row * COLS * 2 + 16 * (chn ^ ((row >> 1) & (CPR - 1)));
+  };
+  auto chunk_out = [&](int c, int nt) {
+    const int cc = lane + 64 * (c & 3), row = cc / CPR, chn = cc % CPR;
+    const int i = c >> 3, h = (c >> 2) & 1;
+    return (uint32_t)(wave * 64 + i * 32 + row) * (uint32_t)g.ldo * 2u +
+           (uint32_t)(nt * BN + h * COLS + chn * 8) * 2u;
+  };
 
-  issue_range(plan_next(wbuf(0)), std::integral_constant<int, 0>{}, std::integral_constant<int, WBLK>{});
-  issue_range(plan_next(wbuf(1)), std::integral_constant<int, 0>{}, std::integral_constant<int, WBLK>{});
-  // wait for the token fragments here, not inside the tile loop
+  f32x16_t acc[FM][FN];
 #pragma unroll
-  for (int q = 0; q < KST; ++q) asm volatile("" : "+v"(afr[q]));
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16_t{};
 
-  int s = 0, u = 0;
+  u32x4 fr[2][FN];
+  auto wload = [&](uint32_t slot_base, int kk, u32x4 (&f)[FN]) {
+    const uint32_t b = slot_base + koff[kk];
+    static_for<0, FN>([&](auto jc) {
+      constexpr int J = decltype(jc)::value;
+      f[J] = lds_read_b128<J * 32 * GK * 2>(b);
+    });
+  };
+  // stage 0 ready: the DMA of stages 1 .. D-1 may still be in flight
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WBLK * (D - 1)) : "memory");
+  __builtin_amdgcn_s_barrier();
+  wload(swb, 0, fr[0]);
+  lds_wait(fr[0]);
+
+  int c_slot = 0;  // ring slot of the stage being consumed
   for (int tile = 0; tile < ntiles; ++tile) {
+    // the previous tile's output, stored during this tile's first k-steps
+    // (the first tile's stores go nowhere)
+    const int pnt = nt0 + tile - 1;
+    const bool pout = tile > 0;
     static_for<0, KS>([&](auto ksc) {
       constexpr int KSI = decltype(ksc)::value;
-      if (s + 1 < total)
-        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WBLK) : "memory");
-      else
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __builtin_amdgcn_s_barrier();
-      const int un = u == 0 ? NSW - 1 : u - 1;
-      const WPlan nx = plan_next(wbuf(un));
-      const uint32_t bw = swb + u * WSTG;
-      u32x4 fr[2][FN];
-      auto load = [&](int kk, u32x4 (&f)[FN]) {
-        static_for<0, FN>([&](auto jc) {
-          constexpr int J = decltype(jc)::value;
-          f[J] = lds_read_b128<J * 32 * GK * 2>(bw + koff[kk]);
-        });
-      };
-      load(0, fr[0]);
-      lds_wait(fr[0]);
+      const uint32_t bw = swb + (uint32_t)c_slot * WSTG;
+      const int n_slot = c_slot + 1 == NSW ? 0 : c_slot + 1;
       static_for<0, KSTEP>([&](auto kkc) {
         constexpr int KK = decltype(kkc)::value, CB = KK & 1;
-        if constexpr (KK + 1 < KSTEP) load(KK + 1, fr[CB ^ 1]);
+        constexpr int Q = KSI * KSTEP + KK, NS = P::st(Q), C0 = P::st0(Q);
+        // the next k-step's W fragments (the next stage's first, after the barrier below)
+        if constexpr (KK + 1 < KSTEP) wload(bw, KK + 1, fr[CB ^ 1]);
+        if constexpr (KK + 1 == KSTEP) wload(swb + (uint32_t)n_slot * WSTG, 0, fr[CB ^ 1]);
+        u32x4 sv[NS > 0 ? NS : 1];
+        static_for<0, NS>([&](auto uc) {
+          constexpr int U = decltype(uc)::value;
+          sv[U] = lds_read_b128(chunk_lds(C0 + U));
+        });
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[j] = mfma32x32x16(as_uint4(fr[CB][j]), as_uint4(afr[KSI * KSTEP + KK]), acc[j]);
-        constexpr int B0 = KK * PER < WBLK ? KK * PER : WBLK;
-        constexpr int B1 = (KK + 1) * PER < WBLK ? (KK + 1) * PER : WBLK;
-        issue_range(nx, std::integral_constant<int, B0>{}, std::integral_constant<int, B1>{});
-        if constexpr (KK + 1 < KSTEP) lds_wait(fr[CB ^ 1]);
+#pragma unroll
+          for (int i = 0; i < FM; ++i) acc[i][j] = mfma32x32x16(as_uint4(fr[CB][j]), as_uint4(afr[i][Q]), acc[i][j]);
+        dma_block(KK);
+        lds_wait(fr[CB ^ 1]);
+        if constexpr (KK == KSTEP - 2) {
+          // stage s + 1 ready (the count of later operations is fixed by the
+          // issue order), and every wave is done with stage s - 1's slot,
+          // which the DMA refills from the next k-step on
+          if (tile == 0)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(P::wait_n(KSI, true)) : "memory");
+          else
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(P::wait_n(KSI, false)) : "memory");
+          __builtin_amdgcn_s_barrier();
+        }
+        static_for<0, NS>([&](auto uc) {
+          constexpr int U = decltype(uc)::value;
+          __builtin_amdgcn_raw_buffer_store_b128(sv[U], ro, pout ? chunk_out(C0 + U, pnt) : OOB, 0, 0);
+        });
       });
-      ++s;
-      if (KSI + 1 < KS) u = u + 1 == NSW ? 0 : u + 1;
+      dma_next();
+      c_slot = n_slot;
     });
 
-    // epilogue through the W buffer the tile's last step consumed: per half
-    // of the columns, each wave stages its 32 x 64 block (4 KiB) and stores
-    // full 128 B row segments
-    __builtin_amdgcn_s_barrier();  // every wave is done reading it
-    {
-      constexpr int COLS = 64, CPR = COLS / 8;
-      const int half = lane >> 5;
-      const uint32_t stg = swb + u * WSTG + wave * (32 * COLS * 2);
-      const int nt = nt0 + tile;
+    // this tile's output into the staging area (its previous contents were
+    // all read by the stores above)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const f32x16_t& c = acc[h * 2 + jj];
-          uint32_t p[8];
+      for (int j = 0; j < FN; ++j) {
+        const f32x16_t& c = acc[i][j];
+        uint32_t p[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) p[e] = pack_bf2(c[2 * e], c[2 * e + 1]);
+        for (int e = 0; e < 8; ++e) p[e] = pack_bf2(c[2 * e], c[2 * e + 1]);
 #pragma unroll
-          for (int q = 0; q < 2; ++q)
+        for (int q = 0; q < 2; ++q)
 #pragma unroll
-            for (int w = 0; w < 2; ++w) {
-              const auto sw2 = __builtin_amdgcn_permlane32_swap(p[4 * q + w], p[4 * q + 2 + w], false, false);
-              p[4 * q + w] = sw2[0];
-              p[4 * q + 2 + w] = sw2[1];
-            }
-          const int row = lane & 31;
-#pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            const int chn = jj * 4 + 2 * q + half;
-            lds_write_b128(stg + row * COLS * 2 + 16 * (chn ^ ((row >> 1) & (CPR - 1))),
-                           u32x4{p[4 * q], p[4 * q + 1], p[4 * q + 2], p[4 * q + 3]});
+          for (int w = 0; w < 2; ++w) {
+            const auto sw2 = __builtin_amdgcn_permlane32_swap(p[4 * q + w], p[4 * q + 2 + w], false, false);
+            p[4 * q + w] = sw2[0];
+            p[4 * q + 2 + w] = sw2[1];
           }
-        }
-        u32x4 v[4];
+        const int row = lane & 31, h = j >> 1, jj = j & 1;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int c = lane + 64 * q;
-          const int row = c / CPR, chn = c % CPR;
-          v[q] = lds_read_b128(stg + row * COLS * 2 + 16 * (chn ^ ((row >> 1) & (CPR - 1))));
+        for (int q = 0; q < 2; ++q) {
+          const int chn = jj * 4 + 2 * q + half;
+          lds_write_b128(stg + (2 * i + h) * (32 * COLS * 2) + row * COLS * 2 + 16 * (chn ^ ((row >> 1) & (CPR - 1))),
+                         u32x4{p[4 * q], p[4 * q + 1], p[4 * q + 2], p[4 * q + 3]});
         }
-        lds_wait(v);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int c = lane + 64 * q;
-          const int row = c / CPR, chn = c % CPR;
-          const int t = m0 + wave * 32 + row;
-          if (t < g.M)
-            *(uint4*)((bf16_t*)g.out + (int64_t)t * g.ldo + nt * BN + h * COLS + chn * 8) = as_uint4(v[q]);
-        }
+        acc[i][j] = f32x16_t{};
       }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) acc[j] = f32x16_t{};
-    }
-    u = u + 1 == NSW ? 0 : u + 1;
   }
+  // the last tile's output
+  {
+    u32x4 v[8];
+#pragma unroll
+    for (int h8 = 0; h8 < 2; ++h8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = lds_read_b128(chunk_lds(8 * h8 + u));
+      lds_wait(v);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        __builtin_amdgcn_raw_buffer_store_b128(v[u], ro, chunk_out(8 * h8 + u, nt0 + ntiles - 1), 0, 0);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // and the zero-filling DMA past the last stage
 #endif
 }
-
 
 template <int BN, int NS>
 hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
@@ -266,27 +338,6 @@ hipError_t launch_bn(const TnArgs& g, hipStream_t s) {
   int per = 1;
   while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) * zs >= 256) per *= 2;
   dim3 grid(mt, (nt + per - 1) / per, zs);
-  // a short K (2 to 6 stages) walked over many tiles with bf16 output
-  // (decode, encode_bwd): token operand in registers, read once, 128-wide
-  // tiles, two workgroups per CU; each workgroup walks per2 tiles and the
-  // grid fills two workgroups per CU
-  const int KS = (g.Ka + g.Kg) / GK;
-  if constexpr (BN == 256) {
-    const int nt2 = g.N / 128;
-    int per2 = 1;
-    while (per2 < nt2 && (int64_t)mt * ((nt2 + per2 * 2 - 1) / (per2 * 2)) >= 512) per2 *= 2;
-    if (!g.out_f32 && fullk && g.kz == 0 && per2 >= 2 && KS >= 2 && KS <= 6) {
-      dim3 grid2(mt, (nt2 + per2 - 1) / per2, 1);
-      switch (KS) {
-        case 2: hipLaunchKernelGGL((k_gemm_tn_short<2>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
-        case 3: hipLaunchKernelGGL((k_gemm_tn_short<3>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
-        case 4: hipLaunchKernelGGL((k_gemm_tn_short<4>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
-        case 5: hipLaunchKernelGGL((k_gemm_tn_short<5>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
-        default: hipLaunchKernelGGL((k_gemm_tn_short<6>), grid2, dim3(GTHREADS), 0, s, g, per2); break;
-      }
-      return hipGetLastError();
-    }
-  }
   if (fullk)
     hipLaunchKernelGGL((k_gemm_tn<BN, NS, true>), grid, dim3(GTHREADS), 0, s, g, per);
   else
@@ -309,6 +360,27 @@ hipError_t launch_ns(const TnArgs& g, hipStream_t s) {
 hipError_t launch_gemm_tn(const TnArgs& g, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
   if (g.kz > 0 && (g.kz % GK != 0 || g.Ka % g.kz != 0 || g.Kg != 0)) return hipErrorInvalidValue;
+  // a short K (2 to 6 stages) walked over several 128-column tiles with bf16
+  // output (decode, encode_bwd): one 256-token workgroup per CU, each walking
+  // per tiles, as long as every workgroup gets at least two
+  const int ks = (g.Ka + g.Kg) / GK;
+  if (!g.out_f32 && g.kz == 0 && g.Ka % GK == 0 && g.Kg % GK == 0 && g.Ka + g.Kg <= g.ldw && g.N % SH_BN == 0 &&
+      ks >= 2 && ks <= 6) {
+    const int mt = (g.M + SH_BM - 1) / SH_BM, nt = g.N / SH_BN;
+    int per = 1;
+    while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) >= 256) per *= 2;
+    if (per >= 2) {
+      const dim3 grid(mt, (nt + per - 1) / per);
+      switch (ks) {
+        case 2: hipLaunchKernelGGL((k_gemm_tn_short<2>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        case 3: hipLaunchKernelGGL((k_gemm_tn_short<3>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        case 4: hipLaunchKernelGGL((k_gemm_tn_short<4>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        case 5: hipLaunchKernelGGL((k_gemm_tn_short<5>), grid, dim3(GTHREADS), 0, s, g, per); break;
+        default: hipLaunchKernelGGL((k_gemm_tn_short<6>), grid, dim3(GTHREADS), 0, s, g, per); break;
+      }
+      return hipGetLastError();
+    }
+  }
   if (g.N % 256 == 0) return launch_ns<256>(g, s);
   if (g.N % 128 == 0) return launch_ns<128>(g, s);
   if (g.N % 64 == 0) return launch_ns<64>(g, s);
