@@ -136,20 +136,69 @@ __global__ __launch_bounds__(GTHREADS, 1) void k_gemm_tn_short(TnArgs g, int nti
 
   // token fragments of rows 64 wave + 32 i .. +31; rows past the last token read zeros
   u32x4 afr[FM][KST];
+  if (!g.codes) {
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int row = wave * 64 + i * 32 + (lane & 31);
-    const bool in = row < mrows;
-    const uint32_t ch = 16u * (uint32_t)(lane >> 5);
-    const uint32_t aoff = in ? (uint32_t)row * (uint32_t)g.lda * 2u + ch : OOB;
-    const uint32_t toff =
-        in && g.Kg > 0 ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + ch : OOB;
+    for (int i = 0; i < FM; ++i) {
+      const int row = wave * 64 + i * 32 + (lane & 31);
+      const bool in = row < mrows;
+      const uint32_t ch = 16u * (uint32_t)(lane >> 5);
+      const uint32_t aoff = in ? (uint32_t)row * (uint32_t)g.lda * 2u + ch : OOB;
+      const uint32_t toff =
+          in && g.Kg > 0 ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + ch : OOB;
 #pragma unroll
-    for (int q = 0; q < KST; ++q) {
-      const int kc = q * 16;
-      const bool in_a = kc < g.Ka;
-      afr[i][q] = __builtin_amdgcn_raw_buffer_load_b128(in_a ? ra : rt, in_a ? aoff : toff,
-                                                        in_a ? kc * 2 : (kc - g.Ka) * 2, 0);
+      for (int q = 0; q < KST; ++q) {
+        const int kc = q * 16;
+        const bool in_a = kc < g.Ka;
+        afr[i][q] = __builtin_amdgcn_raw_buffer_load_b128(in_a ? ra : rt, in_a ? aoff : toff,
+                                                          in_a ? kc * 2 : (kc - g.Ka) * 2, 0);
+      }
+    }
+  } else {
+    // the first Ka columns gathered from the codebooks: lane (row, half)
+    // sums the 8 fp32 values k0 .. k0+7 (k0 = 16 q + 8 half) of its row's
+    // codewords, l = 0 then 1, and rounds the sums to bf16
+    const __amdgpu_buffer_rsrc_t rc = rsrc(g.C, (uint64_t)g.L * g.K * g.Ka * 4);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wave * 64 + i * 32 + (lane & 31);
+      const bool in = row < mrows;
+      const uint32_t ch = 16u * (uint32_t)(lane >> 5);
+      uint32_t cw[2];
+#pragma unroll
+      for (int l = 0; l < 2; ++l) {
+        cw[l] = OOB;
+        if (in && l < g.L) {
+          const int64_t e = (int64_t)(m0 + row) * g.L + l;
+          const int c = g.code_bytes == 1 ? ((const uint8_t*)g.codes)[e] : ((const uint16_t*)g.codes)[e];
+          cw[l] = (uint32_t)(l * g.K + (c < g.K ? c : g.K - 1)) * (uint32_t)g.Ka * 4u + 2u * ch;
+        }
+      }
+      const uint32_t toff =
+          in && g.Kg > 0 ? (uint32_t)clamp_id(g.ids[m0 + row], g.V) * (uint32_t)g.ldt * 2u + ch : OOB;
+#pragma unroll
+      for (int q = 0; q < KST; ++q) {
+        const int kc = q * 16;
+        if (kc < g.Ka) {
+          const u32x4 a0 = __builtin_amdgcn_raw_buffer_load_b128(rc, cw[0], kc * 4, 0);
+          const u32x4 a1 = __builtin_amdgcn_raw_buffer_load_b128(rc, cw[0], kc * 4 + 16, 0);
+          const u32x4 b0 = __builtin_amdgcn_raw_buffer_load_b128(rc, cw[1], kc * 4, 0);
+          const u32x4 b1 = __builtin_amdgcn_raw_buffer_load_b128(rc, cw[1], kc * 4 + 16, 0);
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = 0.f + __uint_as_float(a0[e]);
+            v[4 + e] = 0.f + __uint_as_float(a1[e]);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] += __uint_as_float(b0[e]);
+            v[4 + e] += __uint_as_float(b1[e]);
+          }
+          afr[i][q] = u32x4{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])};
+        } else {
+          afr[i][q] = __builtin_amdgcn_raw_buffer_load_b128(rt, toff, (kc - g.Ka) * 2, 0);
+        }
+      }
     }
   }
 
@@ -357,19 +406,35 @@ hipError_t launch_ns(const TnArgs& g, hipStream_t s) {
 
 }  // namespace
 
+// Tiles per workgroup of the short-K kernel for g, or 0 where it does not
+// apply: bf16 output, 2 to 6 full stages, N a multiple of 128, and at least
+// two tiles per workgroup with one 256-token workgroup per CU.
+static int short_per(const TnArgs& g) {
+  const int ks = (g.Ka + g.Kg) / GK;
+  if (g.M <= 0 || g.out_f32 || g.kz != 0 || g.Ka % GK || g.Kg % GK || g.Ka + g.Kg > g.ldw || g.N % SH_BN ||
+      ks < 2 || ks > 6)
+    return 0;
+  if (g.codes && (g.L < 1 || g.L > 2 || !g.C || g.K < 1 || (g.code_bytes != 1 && g.code_bytes != 2))) return 0;
+  const int mt = (g.M + SH_BM - 1) / SH_BM, nt = g.N / SH_BN;
+  int per = 1;
+  while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) >= 256) per *= 2;
+  return per >= 2 ? per : 0;
+}
+
+bool gemm_tn_gathers(const TnArgs& g) { return short_per(g) >= 2; }
+
 hipError_t launch_gemm_tn(const TnArgs& g, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
   if (g.kz > 0 && (g.kz % GK != 0 || g.Ka % g.kz != 0 || g.Kg != 0)) return hipErrorInvalidValue;
+  const int per = short_per(g);
+  if (g.codes && per < 2) return hipErrorInvalidValue;
   // a short K (2 to 6 stages) walked over several 128-column tiles with bf16
   // output (decode, encode_bwd): one 256-token workgroup per CU, each walking
   // per tiles, as long as every workgroup gets at least two
-  const int ks = (g.Ka + g.Kg) / GK;
-  if (!g.out_f32 && g.kz == 0 && g.Ka % GK == 0 && g.Kg % GK == 0 && g.Ka + g.Kg <= g.ldw && g.N % SH_BN == 0 &&
-      ks >= 2 && ks <= 6) {
-    const int mt = (g.M + SH_BM - 1) / SH_BM, nt = g.N / SH_BN;
-    int per = 1;
-    while (per < nt && (int64_t)mt * ((nt + per * 2 - 1) / (per * 2)) >= 256) per *= 2;
+  {
+    const int ks = (g.Ka + g.Kg) / GK;
     if (per >= 2) {
+      const int mt = (g.M + SH_BM - 1) / SH_BM, nt = g.N / SH_BN;
       const dim3 grid(mt, (nt + per - 1) / per);
       switch (ks) {
         case 2: hipLaunchKernelGGL((k_gemm_tn_short<2>), grid, dim3(GTHREADS), 0, s, g, per); break;

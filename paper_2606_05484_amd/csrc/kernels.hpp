@@ -16,6 +16,11 @@ typedef uint16_t bf16_t;
 // Split-K: with kz > 0 (and Kg == 0) grid z-slice s covers columns
 // [s*kz, (s+1)*kz) of A and W and writes its own fp32 partial at out + s*out_z.
 // out_accum (fp32 output only) adds to the existing output instead of storing.
+// With codes != null the first Ka columns of the token operand are not read
+// from A but gathered: sum_{l<L} C[l][codes[t][l]][c] (C fp32 [L][K][Ka],
+// codes [M][L] of code_bytes each, clamped to K-1, L <= 2), summed in fp32
+// in l order from 0 and rounded once to bf16 -- the decoder's Zhat.  Only
+// the short-K kernel takes it: gemm_tn_gathers() says whether g does.
 struct TnArgs {
   const bf16_t* A; int64_t lda;
   const bf16_t* T; int64_t ldt; const int32_t* ids; int Kg; int V;  // ids clamped to [0,V)
@@ -23,8 +28,10 @@ struct TnArgs {
   int M, N, Ka;
   void* out; int64_t ldo; int out_f32;
   int kz; int64_t out_z; int out_accum;
+  const void* codes; int code_bytes; const float* C; int L; int K;
 };
 hipError_t launch_gemm_tn(const TnArgs& g, hipStream_t s);
+bool gemm_tn_gathers(const TnArgs& g);
 
 // ---------------------------------------------------------------- fp32 GEMM
 // C[b](m,n) = alpha_b sum_k A[b](m,k) B[b](k,n) + beta_b Cin[b](m,n)

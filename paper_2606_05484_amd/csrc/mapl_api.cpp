@@ -5,7 +5,8 @@
 //   encode      prep U~^T | B_s U~ (ambient) -> Z0 = [X | a_s] [U~ ; -(B_s U~)]^T
 //               (one token-major GEMM, anchors gathered in flight) -> bf16 Z
 //               (L = 0) or fp32 Z0 -> RVQ screen/rescore -> codes
-//   decode      prep [U~ | B_r^T] -> Zhat (payload, or codebook gather-sum)
+//   decode      prep [U~ | B_r^T] (and Zhat's codebook gather-sum where the
+//               product cannot gather the codewords itself)
 //               -> Xhat = [Zhat | a_r] [U~ | B_r^T]^T
 //   decode_bwd  dZ = dXhat U~;  dU (+)= dXhat^T Zhat  (split over tokens,
 //               fixed-order reduction)
@@ -550,22 +551,28 @@ extern "C" int mapl_decode(const mapl_codec_desc* desc, const void* payload, con
         jobs[nj++] = prep_job_small_gemm((const bf16_t*)B_r, r, U, r, 1, (int)k, (int)d, (int)r, 1.f, W2, Lo.kw,
                                          (int)r);
     }
-    const bf16_t* Aop = (const bf16_t*)payload;
-    if (D.L > 0) {
-      bf16_t* Ah = at<bf16_t>(ws, Lo.ahat);
-      AssembleArgs a{};
-      a.codes = payload; a.code_bytes = cbytes; a.C = C; a.L = D.L; a.K = D.K;
-      a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah; a.gdim = grouped(D) ? 2 : 0;
-      jobs[nj++] = prep_job_assemble(a);
-      Aop = Ah;
-    }
-    LAUNCH("dec:prep", launch_prep_batch(jobs, nj, s));
     TnArgs g{};
-    g.A = Aop; g.lda = r; g.Ka = (int)r;
+    g.A = (const bf16_t*)payload; g.lda = r; g.Ka = (int)r;
     g.T = (const bf16_t*)A_r; g.ldt = k; g.ids = ids; g.Kg = (int)k; g.V = (int)D.V;
     g.W = W2; g.ldw = Lo.kw;
     g.M = (int)T; g.N = (int)d;
     g.out = Xhat; g.ldo = d; g.out_f32 = 0;
+    if (D.L > 0) {
+      // Zhat: gathered by code inside the product's token-operand load where
+      // the short-K kernel runs it (whole-vector codewords, L <= 2), else
+      // assembled in the preparation launch
+      g.codes = payload; g.code_bytes = cbytes; g.C = C; g.L = D.L; g.K = D.K;
+      if (grouped(D) || !gemm_tn_gathers(g)) {
+        g.codes = nullptr;
+        bf16_t* Ah = at<bf16_t>(ws, Lo.ahat);
+        AssembleArgs a{};
+        a.codes = payload; a.code_bytes = cbytes; a.C = C; a.L = D.L; a.K = D.K;
+        a.T = (int)T; a.r = (int)r; a.ldo = r; a.out = Ah; a.gdim = grouped(D) ? 2 : 0;
+        jobs[nj++] = prep_job_assemble(a);
+        g.A = Ah;
+      }
+    }
+    LAUNCH("dec:prep", launch_prep_batch(jobs, nj, s));
     LAUNCH("dec:gemm_tn", launch_gemm_tn(g, s));
     return MAPL_OK;
   }

@@ -10,7 +10,7 @@ import pytest
 from oracle import codec as ocodec
 from paper_2606_05484_amd import mapl, synth
 from _helpers import (BF16_TOL, F32_TOL, Dev, chain as _chain, check_chain as _check_chain, codes_np,
-                      compare_codes, descr, f64, host_f64, operand, oracle_encode, rel_fro, run_encode,
+                      compare_codes, descr, dev, f64, host_f64, operand, oracle_encode, rel_fro, run_encode,
                       stress_codebooks, tol, torch)
 
 pytestmark = pytest.mark.gpu
@@ -350,6 +350,49 @@ def test_short_k_many_tiles(r):
     register-resident token operand, besides the benchmark's 384 and 256."""
     x = _x("c4", T=8192 + 77, r=r, k=64, L=0, K=0)
     _check_chain(x, _chain(x))
+
+
+@pytest.mark.parametrize("k", [0, 64])
+@pytest.mark.parametrize("L,K", [(1, 256), (2, 256), (2, 1024)])
+def test_decode_gathers_codewords_bit_exact(L, K, k):
+    """Where the decoder's product walks several output tiles per workgroup
+    (here 8192 + 77 tokens at d = 2048) it gathers the codewords by code
+    inside its token-operand load instead of reading an assembled Zhat.
+    With U = [I_r ; 0] and B_r rows = unit vectors e_{r+i}, Xhat[:, :r] must
+    equal bf16(sum_l C_l[code_l]) (fp32 sum in l order, rounded once) and
+    Xhat[:, r:r+k] must equal A_r[ids], bit for bit; u8 and u16 codes, one
+    and two rounds, codes 0 and K-1 included, a ragged last block."""
+    t = torch()
+    T, d, r, V = 8192 + 77, 2048, 256, 3000
+    print("decode codeword gather", L, K, k, flush=True)
+    rng = np.random.default_rng(1000 + 10 * L + K + k)
+    C = rng.standard_normal((L, K, r)).astype(np.float32)
+    codes = rng.integers(0, K, size=(T, L))
+    codes[:5] = K - 1
+    codes[5:9] = 0
+    cdt = np.uint8 if K <= 256 else np.uint16
+    U = np.zeros((d, r), dtype=np.float32)
+    U[:r, :r] = np.eye(r)
+    A = synth.f32_to_bf16_bits(rng.standard_normal((V, max(k, 1))).astype(np.float32))[:, :k]
+    ids = synth.zipf_ids(rng, V, T)
+    B = np.zeros((k, d), dtype=np.float32)
+    B[np.arange(k), r + np.arange(k)] = 1.0
+    D = mapl.desc(T=T, d=d, r=r, V=V, k=k, L=L, K=K)
+    payload = t.from_numpy(codes.astype(cdt).astype(np.int16 if cdt == np.uint16 else np.uint8)).cuda()
+    Xh = t.full((T, d), float("nan"), dtype=t.bfloat16, device="cuda")
+    ws = mapl.workspace(mapl.workspace_bytes(D, mapl.CALL_DECODE))
+    mapl.decode(D, payload, dev(ids, "i32") if k else None, dev(U, "f32"), dev(A, "bf16") if k else None,
+                dev(synth.f32_to_bf16_bits(B), "bf16") if k else None, t.from_numpy(C).cuda(), Xh, ws)
+    t.cuda.synchronize()
+    zsum = np.zeros((T, r), dtype=np.float32)
+    for l in range(L):
+        zsum = (zsum + C[l][codes[:, l]]).astype(np.float32)
+    want = synth.f32_to_bf16_bits(zsum)
+    got = Xh.view(t.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got[:, :r], want), int((got[:, :r] != want).sum())
+    if k:
+        assert np.array_equal(got[:, r:r + k], A[ids])
+    assert (host_f64(Xh)[:, r + k:] == 0).all()
 
 
 @pytest.mark.slow
