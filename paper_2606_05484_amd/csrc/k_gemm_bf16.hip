@@ -30,6 +30,7 @@
 // 16 B row segments and staged through LDS into full 128 B row writes.  Buffer resources bound every
 // operand: lanes past the last token row, past Kg or past ldw read zeros.
 #include "tn_gemm.hpp"
+#include "short_plan.hpp"
 
 namespace mapl {
 
@@ -86,33 +87,10 @@ __global__ __launch_bounds__(GTHREADS) void k_gemm_tn(TnArgs g, int ntiles_per_w
 constexpr int SH_BM = 256, SH_BN = 128;
 
 template <int KS>
-struct ShortPlan {
-  static constexpr int KSTEP = GK / 16, KST = KS * KSTEP, D = KS < 4 ? KS : 4, NSW = D + 1, WBLK = 4, NCH = 16;
-  // row-segment stores issued at the end of k-step q of a tile
-  static constexpr int st(int q) { return (NCH * (q + 1)) / KST - (NCH * q) / KST; }
-  static constexpr int st0(int q) { return (NCH * q) / KST; }  // first chunk stored at k-step q
-  // memory operations issued after the last DMA block of stage s + 1 up to
-  // the wait for it in stage s (after k-step 2's DMA): per k-step one DMA
-  // block then its stores; the prologue issues the DMA of stages 0 .. D-1
-  static constexpr int wait_n(int ksi, bool first) {
-    const int s = (first ? 0 : KS) + ksi, y = s + 1;
-    int n = 0, g0 = 0;
-    if (y < D) {
-      n += WBLK * (D - 1 - y);
-    } else {
-      const int gy = 4 * (y - D) + 3;
-      n += st(gy % KST);
-      g0 = gy + 1;
-    }
-    for (int gq = g0; gq < 4 * s + 2; ++gq) n += 1 + st(gq % KST);
-    return n + 1;
-  }
-};
-
-template <int KS>
 __global__ __launch_bounds__(GTHREADS, 1) void k_gemm_tn_short(TnArgs g, int ntiles_per_wg) {
 #if defined(__HIP_DEVICE_COMPILE__)
   using P = ShortPlan<KS>;
+  static_assert(P::KSTEP == GK / 16, "64-deep stages");
   constexpr int BN = SH_BN, FM = 2, FN = BN / 32, KSTEP = P::KSTEP, KST = P::KST, D = P::D, NSW = P::NSW;
   constexpr int WBLK = P::WBLK;
   static_assert(WBLK == BN / 8 / 4 && WBLK == KSTEP, "one 1 KiB DMA block per wave and k-step");
