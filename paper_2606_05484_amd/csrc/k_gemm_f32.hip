@@ -157,6 +157,53 @@ __device__ __forceinline__ void gv_tile(const GemmF32Args& g, int& bm, int& bn, 
   }
 }
 
+// Stream-K split of a symmetric product (sym_upper with a partial
+// workspace): the (tile, k-stage) units, tile after tile (batch entries
+// outermost), are dealt out in equal runs of U to one workgroup per CU, the
+// runs of each XCD contiguous so that its workgroups share operands in its
+// L2.  A run covers the end of one tile and the start of the next; each
+// (tile, workgroup) piece of accumulators goes to its own fp32 slot, and
+// k_gemm_sk_fix sums a tile's pieces in K order (bitwise reproducible) and
+// applies the epilogue.  Without the split, 160 tiles of the c5 Gram products
+// would leave 96 of the 256 CUs idle.
+__device__ __forceinline__ void sk_tile(int t, int M, int& b, int& bm, int& bn) {
+  const int ntm = (M + 127) / 128, Tb = ntm * (ntm + 1) / 2;
+  b = t / Tb;
+  int tl = t % Tb, row = 0;
+  while (tl >= ntm - row) {
+    tl -= ntm - row;
+    ++row;
+  }
+  bm = row;
+  bn = row + tl;
+}
+
+template <typename F>
+__device__ __forceinline__ void sk_run(const GemmF32Args& g, F&& products, int tid) {
+  const SkPlan p = gemm_f32_sk_plan(g.M, g.K, g.batch);
+  const int w = blockIdx.x;
+  const int v = p.nwg % 8 == 0 ? (w & 7) * (p.nwg >> 3) + (w >> 3) : w;
+  const int64_t total = (int64_t)p.T * p.nk;
+  const int64_t u1 = min((int64_t)(v + 1) * p.U, total);
+  for (int64_t u = (int64_t)v * p.U; u < u1;) {
+    const int t = (int)(u / p.nk), ks0 = (int)(u % p.nk);
+    const int ks1 = (int)min((int64_t)p.nk, ks0 + (u1 - u));
+    const int piece = v - (int)(((int64_t)t * p.nk) / p.U);
+    int b, bm, bn;
+    sk_tile(t, g.M, b, bm, bn);
+    f32x16_t acc[2][2];
+    products(b, bm, bn, ks0, ks1, acc);
+    float* slot = g.sk_part + ((int64_t)t * p.maxp + piece) * (128 * 128);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) slot[((i * 2 + j) * 16 + e) * 256 + tid] = acc[i][j][e];
+    u += ks1 - ks0;
+  }
+}
+
 // Operand loads are raw buffer loads (out-of-range offsets read zero) into
 // registers that are converted to fp32 only when the stage is written to LDS,
 // so nothing waits for the loads before the products of the current stage.
@@ -195,8 +242,9 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
   __shared__ __attribute__((aligned(16))) float Bs[2][GV_BK / 2][GV_BN][2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, 64 x 64 each
-  int tbm, tbn, b;
-  gv_tile(g, tbm, tbn, b);
+  const int nk = (g.K + GV_BK - 1) / GV_BK;
+  // the products of tile (tbm, tbn) of batch entry b over k-stages [ks0, ks1)
+  auto products = [&](int b, int tbm, int tbn, int ks0, int ks1, f32x16_t (&acc)[2][2]) {
   const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
   // the host guarantees that each operand's extent fits 31-bit byte offsets
   const __amdgpu_buffer_rsrc_t rA =
@@ -269,19 +317,17 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
     }
   };
 
-  f32x16_t acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
 
-  const int nk = (g.K + GV_BK - 1) / GV_BK;
-  load(0);
+  load(ks0 * GV_BK);
   store(0);
   __syncthreads();
-  for (int it = 0; it < nk; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < nk) load((it + 1) * GV_BK);
+  for (int it = ks0; it < ks1; ++it) {
+    const int buf = (it - ks0) & 1;
+    if (it + 1 < ks1) load((it + 1) * GV_BK);
 #pragma unroll
     for (int kp = 0; kp < GV_BK / 2; ++kp) {
       float a[2], bb[2];
@@ -298,9 +344,20 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
         for (int j = 0; j < 2; ++j) acc[i][j] = mfma32x32x2f32(a[i], bb[j], acc[i][j]);
     }
     // the other buffer was last read in the previous stage, before the barrier
-    if (it + 1 < nk) store(buf ^ 1);
+    if (it + 1 < ks1) store(buf ^ 1);
     __syncthreads();
   }
+  };
+
+  if (g.sk_part) {
+    sk_run(g, products, tid);
+    return;
+  }
+  int tbm, tbn, b;
+  gv_tile(g, tbm, tbn, b);
+  const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
+  f32x16_t acc[2][2];
+  products(b, tbm, tbn, 0, nk, acc);
 
   const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
   const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
@@ -357,8 +414,9 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
   __shared__ __attribute__((aligned(16))) bf16_t Bl[2][GV_BK * GV_BN];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, 64 x 64 each
-  int tbm, tbn, b;
-  gv_tile(g, tbm, tbn, b);
+  const int nk = (g.K + GV_BK - 1) / GV_BK;
+  // the products of tile (tbm, tbn) of batch entry b over k-stages [ks0, ks1)
+  auto products = [&](int b, int tbm, int tbn, int ks0, int ks1, f32x16_t (&acc)[2][2]) {
   const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
   const __amdgpu_buffer_rsrc_t rA =
       gv_rsrc((const float*)g.A + b * g.sAb,
@@ -426,19 +484,17 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
     }
   };
 
-  f32x16_t acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
 
-  const int nk = (g.K + GV_BK - 1) / GV_BK;
-  load(0);
+  load(ks0 * GV_BK);
   store(0);
   __syncthreads();
-  for (int it = 0; it < nk; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < nk) load((it + 1) * GV_BK);
+  for (int it = ks0; it < ks1; ++it) {
+    const int buf = (it - ks0) & 1;
+    if (it + 1 < ks1) load((it + 1) * GV_BK);
 #pragma unroll
     for (int ks = 0; ks < GV_BK / 16; ++ks) {
       u32x4 f[8];  // ah0 ah1 al0 al1 bh0 bh1 bl0 bl1
@@ -469,9 +525,20 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
         }
     }
     // the other buffer was last read in the previous stage, before the barrier
-    if (it + 1 < nk) store(buf ^ 1);
+    if (it + 1 < ks1) store(buf ^ 1);
     __syncthreads();
   }
+  };
+
+  if (g.sk_part) {
+    sk_run(g, products, tid);
+    return;
+  }
+  int tbm, tbn, b;
+  gv_tile(g, tbm, tbn, b);
+  const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
+  f32x16_t acc[2][2];
+  products(b, tbm, tbn, 0, nk, acc);
 
   const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
   const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
@@ -491,6 +558,47 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
           if (m == n) v += g.diag;
           C[m * g.sCm + n * g.sCn] = v;
           if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = v;
+        }
+      }
+}
+
+// The stream-K fix-up: one workgroup per tile sums the tile's pieces in
+// piece (= K) order and applies the epilogue of the one-launch kernels
+// (scaling, diagonal, the mirrored write of an off-diagonal tile).
+__global__ __launch_bounds__(GF_THREADS) void k_gemm_sk_fix(GemmF32Args g) {
+  const SkPlan p = gemm_f32_sk_plan(g.M, g.K, g.batch);
+  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int pf = (int)(((int64_t)t * p.nk) / p.U), pl = (int)(((int64_t)(t + 1) * p.nk - 1) / p.U);
+  const float* slot = g.sk_part + (int64_t)t * p.maxp * (128 * 128);
+  float v[64];
+#pragma unroll
+  for (int q = 0; q < 64; ++q) v[q] = slot[q * 256 + tid];
+  for (int pc = 1; pc <= pl - pf; ++pc) {
+    float w[64];
+#pragma unroll
+    for (int q = 0; q < 64; ++q) w[q] = slot[(int64_t)pc * (128 * 128) + q * 256 + tid];
+#pragma unroll
+    for (int q = 0; q < 64; ++q) v[q] += w[q];
+  }
+  int b, bm, bn;
+  sk_tile(t, g.M, b, bm, bn);
+  const int m0 = bm * GV_BM, n0 = bn * GV_BN;
+  const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
+  float* C = (float*)g.C + b * g.sCb;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = m0 + wm * 64 + i * 32 + acc_row(e, lane);
+        const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+        if (m < g.M && n < g.N) {
+          float x = alpha * v[(i * 2 + j) * 16 + e];
+          if (m == n) x += g.diag;
+          C[m * g.sCm + n * g.sCn] = x;
+          if (bm != bn) C[n * g.sCm + m * g.sCn] = x;
         }
       }
 }
@@ -517,15 +625,23 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return hipSuccess;
   const int vm = gemm_f32_vec_mode(g, ta, tb);
   if (g.sym_upper && (vm < 0 || g.M != g.N || g.Cin)) return hipErrorInvalidValue;
+  if (g.sk_part && !(g.sym_upper && ta == 0 && tb == 0 && to == 0)) return hipErrorInvalidValue;
   const int ntm = (g.M + GV_BM - 1) / GV_BM;
-  const dim3 vgrid = g.sym_upper ? dim3(ntm * (ntm + 1) / 2, 1, g.batch)
-                                 : dim3(ntm, (g.N + GV_BN - 1) / GV_BN, g.batch);
+  const dim3 vgrid = g.sk_part      ? dim3(gemm_f32_sk_plan(g.M, g.K, g.batch).nwg)
+                     : g.sym_upper ? dim3(ntm * (ntm + 1) / 2, 1, g.batch)
+                                   : dim3(ntm, (g.N + GV_BN - 1) / GV_BN, g.batch);
+  auto sk_fix = [&]() {
+    if (!g.sk_part) return hipGetLastError();
+    hipLaunchKernelGGL(k_gemm_sk_fix, dim3(gemm_f32_sk_plan(g.M, g.K, g.batch).T), dim3(GF_THREADS), 0, s, g);
+    return hipGetLastError();
+  };
   if (g.split_bf16 && vm >= 0 && ta == 0 && tb == 0 && to == 0) {
     if (vm)
       hipLaunchKernelGGL((k_gemm_x3<true>), vgrid, dim3(GF_THREADS), 0, s, g);
     else
       hipLaunchKernelGGL((k_gemm_x3<false>), vgrid, dim3(GF_THREADS), 0, s, g);
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    return e != hipSuccess ? e : sk_fix();
   }
   if (vm >= 0) {
     const dim3 grid = vgrid;
@@ -546,8 +662,10 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
     else if (ta == 0 && tb == 1 && to == 1) MAPL_GV(float, bf16_t, bf16_t);
     else return hipErrorInvalidValue;
 #undef MAPL_GV
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    return e != hipSuccess ? e : sk_fix();
   }
+  if (g.sk_part) return hipErrorInvalidValue;
   dim3 grid((g.M + GF_BM - 1) / GF_BM, (g.N + GF_BN - 1) / GF_BN, g.batch);
   dim3 block(GF_THREADS);
 #define MAPL_GF(TA_, TB_, TO_) hipLaunchKernelGGL((k_gemm_f32<TA_, TB_, TO_>), grid, block, 0, s, g)

@@ -48,8 +48,35 @@ struct GemmF32Args {
   int split_bf16;  // fp32 operands and output, aligned: products as split-bf16 (hi.hi + hi.lo + lo.hi)
   int sym_upper;   // C = A B known symmetric (B = A^T, M == N, no Cin): only tiles on or above the
                    // diagonal are computed, each off-diagonal one also written mirrored (aligned case)
+  float* sk_part;  // sym_upper, fp32 operands and output: with this workspace (gemm_f32_sk_bytes)
+                   // the tiles' K ranges are split evenly over one workgroup per CU (stream-K) and
+                   // a second launch sums each tile's pieces in K order
 };
 hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStream_t s);
+
+// Stream-K plan of a symmetric product (M x M output, upper 128 x 128 tiles
+// of batch entries, K in 32-deep stages): T tiles, nk stages each, runs of U
+// consecutive (tile, stage) units per workgroup over nwg workgroups, at most
+// maxp pieces per tile.
+struct SkPlan {
+  int T, nk, U, maxp, nwg;
+};
+constexpr int SK_WORKGROUPS = 256;  // one per compute unit of an MI355X
+__host__ __device__ inline SkPlan gemm_f32_sk_plan(int M, int K, int batch) {
+  SkPlan p;
+  const int ntm = (M + 127) / 128;
+  p.T = ntm * (ntm + 1) / 2 * batch;
+  p.nk = (K + 31) / 32;
+  const long long total = (long long)p.T * p.nk;
+  p.U = (int)((total + SK_WORKGROUPS - 1) / SK_WORKGROUPS);
+  p.nwg = (int)((total + p.U - 1) / p.U);
+  p.maxp = (p.nk - 1) / p.U + 2;
+  return p;
+}
+inline size_t gemm_f32_sk_bytes(int M, int K, int batch) {
+  const SkPlan p = gemm_f32_sk_plan(M, K, batch);
+  return (size_t)p.T * p.maxp * 128 * 128 * 4;
+}
 
 // ---------------------------------------------------------------- weight gradient
 // part[s][m][n] = sum over tokens t of split s of P[t,m] Q[t,n], where

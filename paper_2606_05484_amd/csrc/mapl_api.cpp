@@ -122,6 +122,14 @@ struct Carve {
   }
 };
 
+// The Stiefel step's Gram products X^T X ([r, r] upper tiles over K = d)
+// take the stream-K split where they have fewer tiles than the chip has CUs
+// and K is long enough for the split to pay for its fix-up launch.
+bool gram_stream_k(int P, int d, int r) {
+  const SkPlan p = gemm_f32_sk_plan(r, d, P);
+  return p.T < SK_WORKGROUPS && p.nk >= 16;
+}
+
 struct SplitPlan {
   int splits, tps;
 };
@@ -371,6 +379,7 @@ extern "C" size_t mapl_workspace_bytes(const mapl_codec_desc* desc, int call, in
     c.take((size_t)P * d * r * 4);   // X1
     c.take((size_t)P * 2048 * 4);    // partial sums of M^2 and G^2
     c.take((size_t)P * 8 * 4);       // scalars
+    if (gram_stream_k((int)P, (int)d, (int)r)) c.take(gemm_f32_sk_bytes((int)r, (int)d, (int)P));  // Gram pieces
     return c.off;
   }
   if (call < MAPL_CALL_ENCODE || call > MAPL_CALL_ENCODE_BWD) {
@@ -971,6 +980,9 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   float* X1 = at<float>(ws, c.take((size_t)P * d * r * 4));
   float* partial = at<float>(ws, c.take((size_t)P * 2048 * 4));
   float* sc = at<float>(ws, c.take((size_t)P * 8 * 4));
+  float* skp = gram_stream_k((int)P, (int)d, (int)r)
+                   ? at<float>(ws, c.take(gemm_f32_sk_bytes((int)r, (int)d, (int)P)))
+                   : nullptr;
   float* scale = sc, *scale2 = sc + P, *inv_nu = sc + 2 * P, *inv_nu2 = sc + 3 * P, *inv_nu4 = sc + 4 * P;
   const int64_t n = d * r, rr = r * r;
 
@@ -985,6 +997,7 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.B = X; g.sBk = r; g.sBn = 1; g.sBb = n;
     g.C = S; g.sCm = r; g.sCn = 1; g.sCb = rr;
     g.alpha_ptr = aptr;
+    g.sk_part = skp;  // split over one workgroup per CU where the upper tiles are fewer
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
   auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr, bool x3) {  // Qm = a I + b S + c S S

@@ -103,11 +103,14 @@ def test_symmetric_gradient_moves_little():
     assert _orth_err(Un) <= 1e-5
 
 
-@pytest.mark.parametrize("P,d,r", [(1, 256, 256), (3, 96, 32), (1, 1024, 1024)], ids=["square", "odd", "r1024"])
+@pytest.mark.parametrize("P,d,r", [(1, 256, 256), (3, 96, 32), (1, 1024, 1024), (5, 640, 160)],
+                         ids=["square", "odd", "r1024", "split_gram"])
 def test_step_at_shape_limits(P, d, r):
     """Square projectors (r = d: the Stiefel manifold is the orthogonal
     group), widths that are multiples of 32 but not of 64 or 128 with several
-    projectors, and the largest rank, against the iteration-matched oracle."""
+    projectors, the largest rank, and a shape whose Gram products take the
+    stream-K split with a partial 128-row tile and up to 11 pieces per tile,
+    against the iteration-matched oracle."""
     st = synth.stiefel_inputs(None, seed=60 + r, P=P, d=d, r=r, gscale=1.0, lr=1e-2, beta=0.95, steps=1)
     U, G, M = st["U"], st["G"], st["M"]
     Un, Mn = _gpu_step(U, G, M, st["lr"], st["beta"])
