@@ -81,15 +81,33 @@ __global__ void k_copy_f32(const float* __restrict__ src, float* __restrict__ ds
   if (i < n) dst[i] = src[i];
 }
 
-__global__ void k_symmetrize(float* S, int r) {
+// S <- (S + S^T) / 2 per projector: one block per pair of 32 x 32 tiles
+// (ta, tb), ta <= tb (row by row), both read and written in rows through LDS;
+// element (a, b) and its mirror get the same 0.5 (S[a][b] + S[b][a]).
+__global__ __launch_bounds__(256) void k_symmetrize(float* S, int r) {
+  __shared__ float A[32][33], B[32][33];
   float* Sp = S + (int64_t)blockIdx.y * r * r;
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)r * r) return;
-  const int a = (int)(i / r), b = (int)(i % r);
-  if (a < b) {
-    const float v = 0.5f * (Sp[(int64_t)a * r + b] + Sp[(int64_t)b * r + a]);
-    Sp[(int64_t)a * r + b] = v;
-    Sp[(int64_t)b * r + a] = v;
+  const int nt = (r + 31) / 32;
+  int t = blockIdx.x, ta = 0;
+  while (t >= nt - ta) {
+    t -= nt - ta;
+    ++ta;
+  }
+  const int tb = ta + t;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 8 rows of 32 per pass
+  const int a0 = 32 * ta, b0 = 32 * tb;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = ty + 8 * u;
+    A[i][tx] = (a0 + i < r && b0 + tx < r) ? Sp[(int64_t)(a0 + i) * r + b0 + tx] : 0.f;
+    B[i][tx] = (b0 + i < r && a0 + tx < r) ? Sp[(int64_t)(b0 + i) * r + a0 + tx] : 0.f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = ty + 8 * u;
+    if (a0 + i < r && b0 + tx < r) Sp[(int64_t)(a0 + i) * r + b0 + tx] = 0.5f * (A[i][tx] + B[tx][i]);
+    if (ta != tb && b0 + i < r && a0 + tx < r) Sp[(int64_t)(b0 + i) * r + a0 + tx] = 0.5f * (A[tx][i] + B[i][tx]);
   }
 }
 
@@ -153,9 +171,9 @@ __global__ void k_axpy(const float* __restrict__ U, const float* __restrict__ D,
 }
 
 // nu2 = max_i sum_j |S_ij| per projector, in two launches: blocks of four
-// waves take 64 rows each (a wave 16 rows, four at a time with every load of
-// the four rows issued before the sums) and write their row maximum; one
-// thread per projector then takes the maximum over its blocks.  r <= 1024.
+// waves take 16 rows each (a wave 4 rows, every load of the four rows issued
+// before the sums: one round of loads per wave) and write their row maximum;
+// one thread per projector then takes the maximum over its blocks.  r <= 1024.
 __global__ __launch_bounds__(256) void k_inf_norm_partial(const float* __restrict__ S, int r,
                                                           float* __restrict__ part) {
   __shared__ float red[4];
@@ -164,7 +182,7 @@ __global__ __launch_bounds__(256) void k_inf_norm_partial(const float* __restric
   const float* Sp = S + (int64_t)p * r * r;
   const int nq = (r + 63) / 64;
   float m = 0.f;
-  for (int i0 = blockIdx.x * 64 + wave * 16; i0 < min(r, blockIdx.x * 64 + wave * 16 + 16); i0 += RB) {
+  for (int i0 = blockIdx.x * 16 + wave * RB; i0 < min(r, blockIdx.x * 16 + wave * RB + RB); i0 += RB) {
     float v[RB][QMAX];
 #pragma unroll
     for (int u = 0; u < RB; ++u)
@@ -257,8 +275,8 @@ hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t 
 }
 
 hipError_t launch_symmetrize(float* S, int P, int r, hipStream_t s) {
-  const int64_t n = (int64_t)r * r;
-  hipLaunchKernelGGL(k_symmetrize, dim3((unsigned)((n + 255) / 256), P), dim3(256), 0, s, S, r);
+  const int nt = (r + 31) / 32;
+  hipLaunchKernelGGL(k_symmetrize, dim3((unsigned)(nt * (nt + 1) / 2), P), dim3(256), 0, s, S, r);
   return hipGetLastError();
 }
 
@@ -283,7 +301,7 @@ hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64
 hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* part, float* inv_nu, float* inv_nu2,
                                   float* inv_nu4, hipStream_t s) {
   if (r > 1024) return hipErrorInvalidValue;
-  const int nb = (r + 63) / 64;
+  const int nb = (r + 15) / 16;  // 16 rows per block, 4 per wave
   hipLaunchKernelGGL(k_inf_norm_partial, dim3(nb, P), dim3(256), 0, s, S, r, part);
   hipLaunchKernelGGL(k_inf_norm_final, dim3((P + 255) / 256), dim3(256), 0, s, part, nb, P, inv_nu, inv_nu2, inv_nu4);
   return hipGetLastError();
