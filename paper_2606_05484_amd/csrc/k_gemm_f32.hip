@@ -562,28 +562,30 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
       }
 }
 
-// The stream-K fix-up: one workgroup per tile sums the tile's pieces in
-// piece (= K) order and applies the epilogue of the one-launch kernels
-// (scaling, diagonal, the mirrored write of an off-diagonal tile).
-__global__ __launch_bounds__(GF_THREADS) void k_gemm_sk_fix(GemmF32Args g) {
+// The stream-K fix-up: one single-wave workgroup per (tile, wave quarter)
+// sums that quarter's pieces in piece (= K) order and applies the epilogue
+// of the one-launch kernels (scaling, diagonal); an off-diagonal tile's
+// mirror is written through a 64 x 64 LDS transpose, in whole rows.
+__global__ __launch_bounds__(64) void k_gemm_sk_fix(GemmF32Args g) {
+  __shared__ float L[64][65];
   const SkPlan p = gemm_f32_sk_plan(g.M, g.K, g.batch);
-  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = blockIdx.x >> 2, wave = blockIdx.x & 3, lane = threadIdx.x;
   const int wm = wave >> 1, wn = wave & 1;
   const int pf = (int)(((int64_t)t * p.nk) / p.U), pl = (int)(((int64_t)(t + 1) * p.nk - 1) / p.U);
-  const float* slot = g.sk_part + (int64_t)t * p.maxp * (128 * 128);
+  const float* slot = g.sk_part + (int64_t)t * p.maxp * (128 * 128) + 64 * wave + lane;
   float v[64];
 #pragma unroll
-  for (int q = 0; q < 64; ++q) v[q] = slot[q * 256 + tid];
+  for (int q = 0; q < 64; ++q) v[q] = slot[q * 256];
   for (int pc = 1; pc <= pl - pf; ++pc) {
     float w[64];
 #pragma unroll
-    for (int q = 0; q < 64; ++q) w[q] = slot[(int64_t)pc * (128 * 128) + q * 256 + tid];
+    for (int q = 0; q < 64; ++q) w[q] = slot[(int64_t)pc * (128 * 128) + q * 256];
 #pragma unroll
     for (int q = 0; q < 64; ++q) v[q] += w[q];
   }
   int b, bm, bn;
   sk_tile(t, g.M, b, bm, bn);
-  const int m0 = bm * GV_BM, n0 = bn * GV_BN;
+  const int mb = bm * GV_BM + wm * 64, nb = bn * GV_BN + wn * 64;
   const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
   float* C = (float*)g.C + b * g.sCb;
 #pragma unroll
@@ -592,15 +594,17 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_sk_fix(GemmF32Args g) {
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int m = m0 + wm * 64 + i * 32 + acc_row(e, lane);
-        const int n = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (m < g.M && n < g.N) {
-          float x = alpha * v[(i * 2 + j) * 16 + e];
-          if (m == n) x += g.diag;
-          C[m * g.sCm + n * g.sCn] = x;
-          if (bm != bn) C[n * g.sCm + m * g.sCn] = x;
-        }
+        const int mm = i * 32 + acc_row(e, lane), nn = j * 32 + (lane & 31);
+        float x = alpha * v[(i * 2 + j) * 16 + e];
+        if (mb + mm == nb + nn) x += g.diag;
+        if (mb + mm < g.M && nb + nn < g.N) C[(mb + mm) * g.sCm + (nb + nn) * g.sCn] = x;
+        L[mm][nn] = x;
       }
+  if (bm == bn) return;  // a diagonal tile has no mirror (uniform over the workgroup)
+  __syncthreads();
+  // mirror: C[nb + nn][mb + lane] = L[lane][nn], one 64-float row per step
+  for (int nn = 0; nn < 64; ++nn)
+    if (nb + nn < g.N && mb + lane < g.M) C[(nb + nn) * g.sCm + (mb + lane) * g.sCn] = L[lane][nn];
 }
 
 // The aligned case of the pipelined kernel: returns 0 (A m-contiguous), 1
@@ -632,7 +636,7 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
                                    : dim3(ntm, (g.N + GV_BN - 1) / GV_BN, g.batch);
   auto sk_fix = [&]() {
     if (!g.sk_part) return hipGetLastError();
-    hipLaunchKernelGGL(k_gemm_sk_fix, dim3(gemm_f32_sk_plan(g.M, g.K, g.batch).T), dim3(GF_THREADS), 0, s, g);
+    hipLaunchKernelGGL(k_gemm_sk_fix, dim3(4 * gemm_f32_sk_plan(g.M, g.K, g.batch).T), dim3(64), 0, s, g);
     return hipGetLastError();
   };
   if (g.split_bf16 && vm >= 0 && ta == 0 && tb == 0 && to == 0) {
