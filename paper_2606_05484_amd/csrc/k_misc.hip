@@ -164,12 +164,6 @@ __global__ void k_fro_scale(const float* __restrict__ partial, int nblk, int P, 
   }
 }
 
-__global__ void k_axpy(const float* __restrict__ U, const float* __restrict__ D, float lr, float* __restrict__ Y,
-                       int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) Y[i] = U[i] - lr * D[i];
-}
-
 // nu2 = max_i sum_j |S_ij| per projector, in two launches: blocks of four
 // waves take 16 rows each (a wave 4 rows, every load of the four rows issued
 // before the sums: one round of loads per wave) and write their row maximum;
@@ -289,12 +283,6 @@ hipError_t launch_momentum(float* M, const float* gR, const float* G, int64_t n,
 hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float zero_rel, float* scale,
                             float* scale2, hipStream_t s) {
   hipLaunchKernelGGL(k_fro_scale, dim3(P), dim3(64), 0, s, partial, nblk, P, eps, zero_rel, scale, scale2);
-  return hipGetLastError();
-}
-
-hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64_t n, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_axpy, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, U, D, lr, Y, n);
   return hipGetLastError();
 }
 

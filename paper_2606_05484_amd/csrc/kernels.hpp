@@ -232,8 +232,6 @@ hipError_t launch_momentum(float* M, const float* gR, const float* G, int64_t n,
 // ||M_p|| <= zero_rel ||G_p|| (norms from launch_momentum's partials).
 hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float zero_rel, float* scale,
                             float* scale2, hipStream_t s);
-// Y = U - lr D.
-hipError_t launch_axpy(const float* U, const float* D, float lr, float* Y, int64_t n, hipStream_t s);
 // For S [P][r][r]: nu2 = max_i sum_j |S_ij|; inv_nu = 1/sqrt(nu2), inv_nu2 = 1/nu2,
 // inv_nu4 = 1/nu2^2; part: P * ceil(r / 64) floats of scratch.
 hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* part, float* inv_nu, float* inv_nu2,

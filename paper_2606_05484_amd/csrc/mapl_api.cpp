@@ -1012,7 +1012,9 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.alpha_ptr = aptr; g.beta_ptr = bptr;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  auto apply = [&](const float* X, float* Xo, const float* sptr, bool x3) {  // Xo = s X Qm
+  // Xo = s X Qm, or with Yin: Xo = Yin - lr s X Qm (the LMO's last product
+  // and Eq. 7's argument U - lr D in one launch)
+  auto apply = [&](const float* X, float* Xo, const float* sptr, bool x3, const float* Yin = nullptr) {
     GemmF32Args g = gemm((int)d, (int)r, (int)r);
     g.split_bf16 = x3;
     g.batch = (int)P;
@@ -1020,6 +1022,10 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.B = Qm; g.sBk = r; g.sBn = 1; g.sBb = rr;
     g.C = Xo; g.sCm = r; g.sCn = 1; g.sCb = n;
     g.alpha_ptr = sptr;
+    if (Yin) {
+      g.Cin = Yin; g.sCinm = r; g.sCinn = 1; g.sCinb = n; g.beta = 1.f;
+      g.alpha = -lr;
+    }
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
 
@@ -1057,18 +1063,16 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   int cur = 0;
   for (int i = 0; i < lmo_steps; ++i) {
     const double a = kLmoCoef[i][0], b = kLmoCoef[i][1], cc = kLmoCoef[i][2];
-    const bool first = i == 0;
+    const bool first = i == 0, last = i == lmo_steps - 1;
     LAUNCH("stiefel:lmo_gram", gram(Xin, first ? scale2 : nullptr, true));
     LAUNCH("stiefel:lmo_poly", poly(a, b, cc, nullptr, nullptr, true));
     float* Xo = bufs[cur];
-    LAUNCH("stiefel:lmo_apply", apply(Xin, Xo, first ? scale : nullptr, true));
+    // the last product writes Y = U - lr D directly (D itself is not kept)
+    LAUNCH("stiefel:lmo_apply", apply(Xin, Xo, first ? scale : nullptr, true, last ? U : nullptr));
     Xin = Xo;
     cur ^= 1;
   }
-  // Y = U - lr D
-  float* Y = bufs[cur];
-  LAUNCH("stiefel:axpy", launch_axpy(U, Xin, lr, Y, P * n, s));
-  cur ^= 1;
+  float* Y = (float*)Xin;
   // Eq. 7: U = PE(Y / nu), nu^2 = max row sum |Y^T Y|
   LAUNCH("stiefel:gram", gram(Y, nullptr, false));
   // (the momentum's norm partials are consumed by now; their buffer takes the row maxima)
