@@ -563,11 +563,15 @@ def spel_flops(P, dd, rr):
 
 
 def spel_roofline_s(P, dd, rr):
-    """Eq. 4 and the 7 retraction steps on the fp32 matrix units; the 5 LMO
-    steps as split-bf16 products (three bf16 products per flop) on the bf16
-    matrix units."""
+    """Eq. 4's two products and the retraction's first Gram product (the one
+    that fixes nu) on the fp32 matrix units; every other product as a split
+    product (three 16-bit products per flop: bf16 pieces in the 5 LMO steps,
+    fp16 pieces in the 7 retraction steps) on the 16-bit matrix units, whose
+    dense fp16 and bf16 peaks are equal."""
     it = 4 * dd * rr * rr + 2 * rr ** 3
-    return P * (4 * dd * rr * rr + 7 * it) / PEAK_F32 + P * 5 * it * 3 / PEAK_BF16
+    f32 = 4 * dd * rr * rr + 2 * dd * rr * rr
+    split = 12 * it - 2 * dd * rr * rr
+    return P * f32 / PEAK_F32 + P * split * 3 / PEAK_BF16
 
 
 def main():

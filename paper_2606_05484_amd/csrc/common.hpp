@@ -35,6 +35,14 @@ __device__ __forceinline__ f32x16_t mfma32x32x16(const uint4& a, const uint4& b,
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, c, 0, 0, 0);
 }
 
+// 32x32x16 fp16 MFMA, fp32 accumulate; same lane layout as mfma32x32x16.
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8_t;
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ f32x16_t mfma32x32x16h(const uint4& a, const uint4& b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c,
+                                                0, 0, 0);
+}
+
 // 16x16x32 bf16 MFMA, fp32 accumulate.
 // Lane l holds A[m = l%16][k = 8(l/16) .. +7] and B[k = 8(l/16) .. +7][n = l%16];
 // accumulator j of lane l is D[m = 4(l/16) + j][n = l%16].

@@ -386,12 +386,25 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
       }
 }
 
-// Split-bf16 variant of the aligned fp32 GEMM (fp32 operands and output):
-// every operand element x is held as hi = bf16(x) and lo = bf16(x - hi)
-// (round to nearest even; x - hi - lo is below 2^-16 |x|), and each product
-// is taken as hi.hi + hi.lo + lo.hi on the bf16 matrix units
-// (v_mfma_f32_32x32x16_bf16, fp32 accumulation), dropping lo.lo: about
-// 2^-15 relative error per product term, at five times the fp32 MFMA rate.
+// Split variants of the aligned fp32 GEMM (fp32 operands and output): every
+// operand element x is held as two 16-bit pieces hi + lo, and each product
+// is taken as hi.hi + hi.lo + lo.hi on the 16-bit matrix units (fp32
+// accumulation), dropping lo.lo, at five times the fp32 MFMA rate:
+//  - F16 = false: hi = bf16(x), lo = bf16(x - hi) (round to nearest even;
+//    x - hi - lo is below 2^-16 |x|): about 2^-15 relative error per
+//    product term, over fp32's whole exponent range;
+//  - F16 = true: the split of Ootomo and Yokota (2022) on fp16 pieces, with
+//    a power-of-two prescale instead of their scaled low piece:
+//    y = 2^8 x, hi = fp16(y), lo = fp16(y - hi) (both round to nearest
+//    even, subnormals kept), products on v_mfma_f32_32x32x16_f16 and the
+//    sums scaled by 2^-16 (exact).  An operand may carry a per-batch factor
+//    (pre_a, pre_b) taken into the prescale, so the product is of the
+//    scaled operands.  hi + lo holds y to 22 bits where lo is
+//    normal (|x| >= 2^-11) and to an absolute 2^-33 below that, so each
+//    product term carries about 2^-21 relative error: fp32's accuracy for
+//    the sums over K of a few thousand.  The (scaled) operands must satisfy
+//    |x| < 255 (hi stays finite); callers use it only where a norm bound
+//    holds.
 // Same tiling as k_gemm_f32v (128 x 128, K staged 32 at a time, 16-byte
 // loads into registers one stage ahead, two LDS buffers).  Hi and lo pieces
 // live apart in LDS, each operand in the layout its loads give:
@@ -404,7 +417,7 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
 constexpr int GX_LD = GV_BK + 8;  // bf16 per row of a [row][k] tile
 constexpr int GX_CPR = GV_BM / 8;  // 16-byte chunks per k of a [k][row] tile
 
-template <bool AK>
+template <bool AK, bool F16>
 __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
   // [row][k] tiles (k-contiguous A) or [k][row] tiles (the rest), per buffer and piece
   constexpr int A_ELEMS = AK ? GV_BM * GX_LD : GV_BK * GV_BM;
@@ -444,36 +457,50 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
                                                                     : GV_OOB);
     }
   };
-  // hi and lo bf16 pieces of two floats, packed
-  auto split2 = [](float x, float y, uint32_t& hi, uint32_t& lo) {
-    hi = pack_bf2(x, y);
-    lo = pack_bf2(x - __uint_as_float(hi << 16), y - __uint_as_float(hi & 0xFFFF0000u));
+  // the fp16 split's prescale: 2^8 times the operand's factor for this batch entry
+  const float sa = F16 ? 256.f * (g.pre_a ? g.pre_a[b] : 1.f) : 1.f;
+  const float sb = F16 ? 256.f * (g.pre_b ? g.pre_b[b] : 1.f) : 1.f;
+  // hi and lo pieces of two floats, packed
+  auto split2 = [](float x, float y, uint32_t& hi, uint32_t& lo, float sc) {
+    if constexpr (F16) {
+      const f32x2_t v = (f32x2_t){x, y} * sc;
+      const f16x2_t h = __builtin_convertvector(v, f16x2_t);
+      hi = __builtin_bit_cast(uint32_t, h);
+      lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(v - __builtin_convertvector(h, f32x2_t), f16x2_t));
+    } else {
+      hi = pack_bf2(x, y);
+      lo = pack_bf2(x - __uint_as_float(hi << 16), y - __uint_as_float(hi & 0xFFFF0000u));
+    }
+  };
+  auto mma = [](const u32x4& a, const u32x4& b, f32x16_t c) {
+    if constexpr (F16) return mfma32x32x16h(as_uint4(a), as_uint4(b), c);
+    else return mfma32x32x16(as_uint4(a), as_uint4(b), c);
   };
   // 4 consecutive rows at 4 consecutive k (v[h]: k = h) into a [k][row] tile
-  auto put_kmajor = [&](bf16_t* H, bf16_t* Lo, const raw_t (&v)[4], int row0, int kk) {
+  auto put_kmajor = [&](bf16_t* H, bf16_t* Lo, const raw_t (&v)[4], int row0, int kk, float sc) {
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
       const int k = kk + h;
       const int off = k * GX_CPR * 8 + (((row0 >> 3) ^ wg_sw(k, GX_CPR)) << 3) + (row0 & 7);
       uint32_t h0, l0, h1, l1;
-      split2(__uint_as_float(v[h][0]), __uint_as_float(v[h][1]), h0, l0);
-      split2(__uint_as_float(v[h][2]), __uint_as_float(v[h][3]), h1, l1);
+      split2(__uint_as_float(v[h][0]), __uint_as_float(v[h][1]), h0, l0, sc);
+      split2(__uint_as_float(v[h][2]), __uint_as_float(v[h][3]), h1, l1, sc);
       *(uint2*)(H + off) = make_uint2(h0, h1);
       *(uint2*)(Lo + off) = make_uint2(l0, l1);
     }
   };
   auto store = [&](int buf) {
     const int kk = 4 * (tid >> 5), c = 4 * (tid & 31);
-    put_kmajor(Bh[buf], Bl[buf], rb, c, kk);
+    put_kmajor(Bh[buf], Bl[buf], rb, c, kk, sb);
     if constexpr (!AK) {
-      put_kmajor(Ah[buf], Al[buf], ra, c, kk);
+      put_kmajor(Ah[buf], Al[buf], ra, c, kk, sa);
     } else {
       const int m = tid >> 1, k = 16 * (tid & 1);
       uint32_t hv[8], lv[8];
 #pragma unroll
       for (int h = 0; h < 4; ++h) {
-        split2(__uint_as_float(ra[h][0]), __uint_as_float(ra[h][1]), hv[2 * h], lv[2 * h]);
-        split2(__uint_as_float(ra[h][2]), __uint_as_float(ra[h][3]), hv[2 * h + 1], lv[2 * h + 1]);
+        split2(__uint_as_float(ra[h][0]), __uint_as_float(ra[h][1]), hv[2 * h], lv[2 * h], sa);
+        split2(__uint_as_float(ra[h][2]), __uint_as_float(ra[h][3]), hv[2 * h + 1], lv[2 * h + 1], sa);
       }
       bf16_t* H = Ah[buf] + m * GX_LD + k;
       bf16_t* Lo = Al[buf] + m * GX_LD + k;
@@ -519,14 +546,20 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          acc[i][j] = mfma32x32x16(as_uint4(f[2 + i]), as_uint4(f[4 + j]), acc[i][j]);
-          acc[i][j] = mfma32x32x16(as_uint4(f[i]), as_uint4(f[6 + j]), acc[i][j]);
-          acc[i][j] = mfma32x32x16(as_uint4(f[i]), as_uint4(f[4 + j]), acc[i][j]);
+          acc[i][j] = mma(f[2 + i], f[4 + j], acc[i][j]);
+          acc[i][j] = mma(f[i], f[6 + j], acc[i][j]);
+          acc[i][j] = mma(f[i], f[4 + j], acc[i][j]);
         }
     }
     // the other buffer was last read in the previous stage, before the barrier
     if (it + 1 < ks1) store(buf ^ 1);
     __syncthreads();
+  }
+  if constexpr (F16) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] *= 1.f / 65536.f;
   }
   };
 
@@ -629,6 +662,8 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return hipSuccess;
   const int vm = gemm_f32_vec_mode(g, ta, tb);
   if (g.sym_upper && (vm < 0 || g.M != g.N || g.Cin)) return hipErrorInvalidValue;
+  if (g.split < 0 || g.split > GEMM_SPLIT_F16) return hipErrorInvalidValue;
+  if ((g.pre_a || g.pre_b) && g.split != GEMM_SPLIT_F16) return hipErrorInvalidValue;
   if (g.sk_part && !(g.sym_upper && ta == 0 && tb == 0 && to == 0)) return hipErrorInvalidValue;
   const int ntm = (g.M + GV_BM - 1) / GV_BM;
   const dim3 vgrid = g.sk_part      ? dim3(gemm_f32_sk_plan(g.M, g.K, g.batch).nwg)
@@ -639,11 +674,13 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
     hipLaunchKernelGGL(k_gemm_sk_fix, dim3(4 * gemm_f32_sk_plan(g.M, g.K, g.batch).T), dim3(64), 0, s, g);
     return hipGetLastError();
   };
-  if (g.split_bf16 && vm >= 0 && ta == 0 && tb == 0 && to == 0) {
-    if (vm)
-      hipLaunchKernelGGL((k_gemm_x3<true>), vgrid, dim3(GF_THREADS), 0, s, g);
-    else
-      hipLaunchKernelGGL((k_gemm_x3<false>), vgrid, dim3(GF_THREADS), 0, s, g);
+  if (g.split && (vm < 0 || ta || tb || to)) return hipErrorInvalidValue;
+  if (g.split == GEMM_SPLIT_BF16 || g.split == GEMM_SPLIT_F16) {
+    const bool h = g.split == GEMM_SPLIT_F16;
+    if (vm && h) hipLaunchKernelGGL((k_gemm_x3<true, true>), vgrid, dim3(GF_THREADS), 0, s, g);
+    else if (vm) hipLaunchKernelGGL((k_gemm_x3<true, false>), vgrid, dim3(GF_THREADS), 0, s, g);
+    else if (h) hipLaunchKernelGGL((k_gemm_x3<false, true>), vgrid, dim3(GF_THREADS), 0, s, g);
+    else hipLaunchKernelGGL((k_gemm_x3<false, false>), vgrid, dim3(GF_THREADS), 0, s, g);
     const hipError_t e = hipGetLastError();
     return e != hipSuccess ? e : sk_fix();
   }

@@ -199,15 +199,13 @@ __global__ __launch_bounds__(256) void k_inf_norm_partial(const float* __restric
     part[(int64_t)p * gridDim.x + blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
 }
 
-__global__ void k_inf_norm_final(const float* __restrict__ part, int nb, int P, float* inv_nu, float* inv_nu2,
-                                 float* inv_nu4) {
+__global__ void k_inf_norm_final(const float* __restrict__ part, int nb, int P, float* inv_nu, float* inv_nu2) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= P) return;
   float nu2 = 0.f;
   for (int j = 0; j < nb; ++j) nu2 = fmaxf(nu2, part[(int64_t)p * nb + j]);
   const float in2 = 1.f / nu2;
   inv_nu2[p] = in2;
-  inv_nu4[p] = in2 * in2;
   inv_nu[p] = sqrtf(in2);
 }
 
@@ -287,11 +285,11 @@ hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, fl
 }
 
 hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* part, float* inv_nu, float* inv_nu2,
-                                  float* inv_nu4, hipStream_t s) {
+                                  hipStream_t s) {
   if (r > 1024) return hipErrorInvalidValue;
   const int nb = (r + 15) / 16;  // 16 rows per block, 4 per wave
   hipLaunchKernelGGL(k_inf_norm_partial, dim3(nb, P), dim3(256), 0, s, S, r, part);
-  hipLaunchKernelGGL(k_inf_norm_final, dim3((P + 255) / 256), dim3(256), 0, s, part, nb, P, inv_nu, inv_nu2, inv_nu4);
+  hipLaunchKernelGGL(k_inf_norm_final, dim3((P + 255) / 256), dim3(256), 0, s, part, nb, P, inv_nu, inv_nu2);
   return hipGetLastError();
 }
 

@@ -983,14 +983,20 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   float* skp = gram_stream_k((int)P, (int)d, (int)r)
                    ? at<float>(ws, c.take(gemm_f32_sk_bytes((int)r, (int)d, (int)P)))
                    : nullptr;
-  float* scale = sc, *scale2 = sc + P, *inv_nu = sc + 2 * P, *inv_nu2 = sc + 3 * P, *inv_nu4 = sc + 4 * P;
+  float* scale = sc, *scale2 = sc + P, *inv_nu = sc + 2 * P, *inv_nu2 = sc + 3 * P;
   const int64_t n = d * r, rr = r * r;
 
-  // x3: the products as split-bf16 (hi.hi + hi.lo + lo.hi, about 2^-15
-  // relative per term) on the bf16 matrix units; the LMO's direction only
-  auto gram = [&](const float* X, const float* aptr, bool x3) {  // S = X^T X (times aptr)
+  // split: the products from 16-bit pieces (hi.hi + hi.lo + lo.hi) on the
+  // 16-bit matrix units.  GEMM_SPLIT_BF16 (about 2^-15 relative per term,
+  // any exponent) carries the LMO's direction; GEMM_SPLIT_F16 (fp32's
+  // accuracy, |operands| < 255) the retraction, whose iterates have
+  // spectral norm at most about 1.03: X0 = Y / nu has norm <= 1 (its first
+  // step takes Y and S = Y^T Y scaled by 1/nu and 1/nu^2 inside the split)
+  // and each PolarExpress quintic maps [0, 1.03] into [0, 1.03], so every
+  // entry of X, S = X^T X and a + b S + c S^2 stays below 5.
+  auto gram = [&](const float* X, const float* aptr, int split) {  // S = X^T X (times aptr)
     GemmF32Args g = gemm((int)r, (int)r, (int)d);
-    g.split_bf16 = x3;
+    g.split = split;
     g.sym_upper = 1;  // X^T X: the tiles above the diagonal, mirrored
     g.batch = (int)P;
     g.A = X; g.sAm = 1; g.sAk = r; g.sAb = n;
@@ -1000,9 +1006,11 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.sk_part = skp;  // split over one workgroup per CU where the upper tiles are fewer
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr, bool x3) {  // Qm = a I + b S + c S S
+  auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr, int split,
+                  const float* pre = nullptr) {  // Qm = a I + b S + c S S (S scaled by pre inside the product)
     GemmF32Args g = gemm((int)r, (int)r, (int)r);
-    g.split_bf16 = x3;
+    g.split = split;
+    g.pre_a = g.pre_b = pre;
     g.batch = (int)P;
     g.A = S; g.sAm = r; g.sAk = 1; g.sAb = rr;
     g.B = S; g.sBk = r; g.sBn = 1; g.sBb = rr;
@@ -1014,9 +1022,11 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   };
   // Xo = s X Qm, or with Yin: Xo = Yin - lr s X Qm (the LMO's last product
   // and Eq. 7's argument U - lr D in one launch)
-  auto apply = [&](const float* X, float* Xo, const float* sptr, bool x3, const float* Yin = nullptr) {
+  auto apply = [&](const float* X, float* Xo, const float* sptr, int split, const float* Yin = nullptr,
+                   const float* pre = nullptr) {  // (pre: X's factor inside the product)
     GemmF32Args g = gemm((int)d, (int)r, (int)r);
-    g.split_bf16 = x3;
+    g.split = split;
+    g.pre_a = pre;
     g.batch = (int)P;
     g.A = X; g.sAm = r; g.sAk = 1; g.sAb = n;
     g.B = Qm; g.sBk = r; g.sBn = 1; g.sBb = rr;
@@ -1057,34 +1067,35 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   LAUNCH("stiefel:fro_scale", launch_fro_scale(partial, nblk, (int)P, 1e-7f, 1.0f / 1048576.0f, scale, scale2, s));
 
   // Eq. 6: D = PE(M / (||M|| + eps)), products in split-bf16 (the direction
-  // carries about 3e-5 relative error; the retraction below stays fp32)
+  // carries about 3e-5 relative error; the retraction below keeps fp32's)
   const float* Xin = M;
   float* bufs[2] = {X0, X1};
   int cur = 0;
   for (int i = 0; i < lmo_steps; ++i) {
     const double a = kLmoCoef[i][0], b = kLmoCoef[i][1], cc = kLmoCoef[i][2];
     const bool first = i == 0, last = i == lmo_steps - 1;
-    LAUNCH("stiefel:lmo_gram", gram(Xin, first ? scale2 : nullptr, true));
-    LAUNCH("stiefel:lmo_poly", poly(a, b, cc, nullptr, nullptr, true));
+    LAUNCH("stiefel:lmo_gram", gram(Xin, first ? scale2 : nullptr, GEMM_SPLIT_BF16));
+    LAUNCH("stiefel:lmo_poly", poly(a, b, cc, nullptr, nullptr, GEMM_SPLIT_BF16));
     float* Xo = bufs[cur];
     // the last product writes Y = U - lr D directly (D itself is not kept)
-    LAUNCH("stiefel:lmo_apply", apply(Xin, Xo, first ? scale : nullptr, true, last ? U : nullptr));
+    LAUNCH("stiefel:lmo_apply", apply(Xin, Xo, first ? scale : nullptr, GEMM_SPLIT_BF16, last ? U : nullptr));
     Xin = Xo;
     cur ^= 1;
   }
   float* Y = (float*)Xin;
   // Eq. 7: U = PE(Y / nu), nu^2 = max row sum |Y^T Y|
-  LAUNCH("stiefel:gram", gram(Y, nullptr, false));
+  LAUNCH("stiefel:gram", gram(Y, nullptr, GEMM_SPLIT_NONE));
   // (the momentum's norm partials are consumed by now; their buffer takes the row maxima)
-  LAUNCH("stiefel:inf_norm_scales", launch_inf_norm_scales(S, (int)P, (int)r, partial, inv_nu, inv_nu2, inv_nu4, s));
+  LAUNCH("stiefel:inf_norm_scales", launch_inf_norm_scales(S, (int)P, (int)r, partial, inv_nu, inv_nu2, s));
   Xin = Y;
   for (int i = 0; i < retract_steps; ++i) {
     const double a = kRetractCoef[i][0], b = kRetractCoef[i][1], cc = kRetractCoef[i][2];
     const bool first = i == 0;
-    if (!first) LAUNCH("stiefel:gram", gram(Xin, nullptr, false));
-    LAUNCH("stiefel:poly", poly(a, b, cc, first ? inv_nu4 : nullptr, first ? inv_nu2 : nullptr, false));
+    if (!first) LAUNCH("stiefel:gram", gram(Xin, nullptr, GEMM_SPLIT_F16));
+    // the first step: Qm = a I + b S / nu^2 + c (S / nu^2)^2 and Y Qm / nu
+    LAUNCH("stiefel:poly", poly(a, b, cc, nullptr, first ? inv_nu2 : nullptr, GEMM_SPLIT_F16, first ? inv_nu2 : nullptr));
     float* Xo = (i == retract_steps - 1) ? U : bufs[cur];
-    LAUNCH("stiefel:apply", apply(Xin, Xo, first ? inv_nu : nullptr, false));
+    LAUNCH("stiefel:apply", apply(Xin, Xo, nullptr, GEMM_SPLIT_F16, nullptr, first ? inv_nu : nullptr));
     Xin = Xo;
     cur ^= 1;
   }

@@ -119,3 +119,20 @@ def test_step_at_shape_limits(P, d, r):
     print(P, d, r, "U rel err", e_u, "M rel err", e_m, "dU rel err", du, "orth", _orth_err(Un))
     assert e_u <= 1e-5 and e_m <= 1e-5 and du <= DU_TOL
     assert _orth_err(Un) <= 1e-5
+
+
+def test_step_far_off_the_manifold():
+    """U scaled by 4096 (entries above 1000, Y^T Y above 1e7): the
+    retraction's 16-bit split products see Y and Y^T Y only after their
+    1/nu and 1/nu^2 factors, so nothing overflows; U_new matches the oracle
+    and is orthonormal."""
+    st = synth.stiefel_inputs(None, seed=77, P=2, d=256, r=64, gscale=1.0, lr=1e-2, beta=0.95, steps=1)
+    U = (st["U"] * 4096.0).astype(np.float32)
+    G, M = st["G"], st["M"]
+    Un, Mn = _gpu_step(U, G, M, st["lr"], st["beta"])
+    Ur, Mr = spel.stiefel_step_batched(U, G, M, st["lr"], st["beta"], mode="pe")
+    e_u, e_m = rel_fro(Un, Ur), rel_fro(Mn, Mr)
+    print("scaled U: U rel err", e_u, "M rel err", e_m, "orth", _orth_err(Un))
+    assert np.isfinite(Un).all()
+    assert e_u <= 1e-5 and e_m <= 1e-5
+    assert _orth_err(Un) <= 1e-5
