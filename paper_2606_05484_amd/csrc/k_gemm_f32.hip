@@ -204,6 +204,55 @@ __device__ __forceinline__ void sk_run(const GemmF32Args& g, F&& products, int t
   }
 }
 
+// The epilogue of the aligned kernels for one wave's 64 x 64 block of tile
+// (tbm, tbn): C = alpha acc + beta Cin, plus diag where m == n, and the
+// mirrored element of an off-diagonal tile of a symmetric product.  Cin is
+// read in full before the first store: C may alias Cin as far as the
+// compiler knows, which would otherwise hold every load behind the store
+// before it.
+template <typename TO>
+__device__ __forceinline__ void gv_epilogue(const GemmF32Args& g, const f32x16_t (&acc)[2][2], int b, int tbm,
+                                            int tbn, int lane, int wm, int wn) {
+  const int m0 = tbm * GV_BM + wm * 64, n0 = tbn * GV_BN + wn * 64;
+  const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
+  const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
+  const bool has_cin = g.Cin && beta != 0.f;
+  float cin[2][2][16];
+  if (has_cin) {
+    const float* Cin = g.Cin + b * g.sCinb;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0 + i * 32 + acc_row(e, lane), n = n0 + j * 32 + (lane & 31);
+          cin[i][j][e] = (m < g.M && n < g.N) ? Cin[m * g.sCinm + n * g.sCinn] : 0.f;
+        }
+  }
+  TO* C = (TO*)g.C + b * g.sCb;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = m0 + i * 32 + acc_row(e, lane), n = n0 + j * 32 + (lane & 31);
+        if (m < g.M && n < g.N) {
+          float v = alpha * acc[i][j][e];
+          if (has_cin) v += beta * cin[i][j][e];
+          if (m == n) v += g.diag;
+          if constexpr (sizeof(TO) == 4) {
+            C[m * g.sCm + n * g.sCn] = v;
+            if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = v;
+          } else {
+            C[m * g.sCm + n * g.sCn] = (TO)f2bf(v);
+            if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = (TO)f2bf(v);
+          }
+        }
+      }
+}
+
 // Operand loads are raw buffer loads (out-of-range offsets read zero) into
 // registers that are converted to fp32 only when the stage is written to LDS,
 // so nothing waits for the loads before the products of the current stage.
@@ -355,35 +404,9 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
   }
   int tbm, tbn, b;
   gv_tile(g, tbm, tbn, b);
-  const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
   f32x16_t acc[2][2];
   products(b, tbm, tbn, 0, nk, acc);
-
-  const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
-  const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
-  const float* Cin = g.Cin ? g.Cin + b * g.sCinb : nullptr;
-  TO* C = (TO*)g.C + b * g.sCb;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        int m = m0 + wm * 64 + i * 32 + acc_row(e, lane);
-        int n = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (m < g.M && n < g.N) {
-          float v = alpha * acc[i][j][e];
-          if (Cin && beta != 0.f) v += beta * Cin[m * g.sCinm + n * g.sCinn];
-          if (m == n) v += g.diag;
-          if constexpr (sizeof(TO) == 4) {
-            C[m * g.sCm + n * g.sCn] = v;
-            if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = v;
-          } else {
-            C[m * g.sCm + n * g.sCn] = (TO)f2bf(v);
-            if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = (TO)f2bf(v);
-          }
-        }
-      }
+  gv_epilogue<TO>(g, acc, b, tbm, tbn, lane, wm, wn);
 }
 
 // Split variants of the aligned fp32 GEMM (fp32 operands and output): every
@@ -569,30 +592,9 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
   }
   int tbm, tbn, b;
   gv_tile(g, tbm, tbn, b);
-  const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
   f32x16_t acc[2][2];
   products(b, tbm, tbn, 0, nk, acc);
-
-  const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
-  const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
-  const float* Cin = g.Cin ? g.Cin + b * g.sCinb : nullptr;
-  float* C = (float*)g.C + b * g.sCb;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        int m = m0 + wm * 64 + i * 32 + acc_row(e, lane);
-        int n = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (m < g.M && n < g.N) {
-          float v = alpha * acc[i][j][e];
-          if (Cin && beta != 0.f) v += beta * Cin[m * g.sCinm + n * g.sCinn];
-          if (m == n) v += g.diag;
-          C[m * g.sCm + n * g.sCn] = v;
-          if (g.sym_upper && tbm != tbn) C[n * g.sCm + m * g.sCn] = v;
-        }
-      }
+  gv_epilogue<float>(g, acc, b, tbm, tbn, lane, wm, wn);
 }
 
 // The stream-K fix-up: one single-wave workgroup per (tile, wave quarter)
