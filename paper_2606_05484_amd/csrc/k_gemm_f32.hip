@@ -159,7 +159,7 @@ __device__ __forceinline__ void gv_tile(const GemmF32Args& g, int& bm, int& bn, 
 
 // Stream-K split of a symmetric product (sym_upper with a partial
 // workspace): the (tile, k-stage) units, tile after tile (batch entries
-// outermost), are dealt out in equal runs of U to one workgroup per CU, the
+// outermost), are dealt out in equal runs of U to two workgroups per CU, the
 // runs of each XCD contiguous so that its workgroups share operands in its
 // L2.  A run covers the end of one tile and the start of the next; each
 // (tile, workgroup) piece of accumulators goes to its own fp32 slot, and
@@ -441,7 +441,7 @@ constexpr int GX_LD = GV_BK + 8;  // bf16 per row of a [row][k] tile
 constexpr int GX_CPR = GV_BM / 8;  // 16-byte chunks per k of a [k][row] tile
 
 template <bool AK, bool F16>
-__global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
+__global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_gemm_x3(GemmF32Args g) {
   // [row][k] tiles (k-contiguous A) or [k][row] tiles (the rest), per buffer and piece
   constexpr int A_ELEMS = AK ? GV_BM * GX_LD : GV_BK * GV_BM;
   __shared__ __attribute__((aligned(16))) bf16_t Ah[2][A_ELEMS];
@@ -459,11 +459,13 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
               (AK ? (int64_t)(g.M - 1) * g.sAm + g.K : (int64_t)(g.K - 1) * g.sAk + g.M) * 4);
   const __amdgpu_buffer_rsrc_t rB = gv_rsrc((const float*)g.B + b * g.sBb, ((int64_t)(g.K - 1) * g.sBk + g.N) * 4);
   typedef Raw4<float>::type raw_t;
-  raw_t ra[4], rb[4];
+  // two register sets: the loads of stages it + 1 and it + 2 are in flight
+  // while stage it is multiplied
+  raw_t ra0[4], rb0[4], ra1[4], rb1[4];
   // B (and an m-contiguous A): thread t loads rows 4 (t % 32) + 0..3 at
   // k = 4 (t / 32) + 0..3, one 16-byte piece per k; a k-contiguous A: row
   // t / 2, k = 16 (t % 2) + 0..15
-  auto load = [&](int k0) {
+  auto load = [&](int k0, raw_t (&ra)[4], raw_t (&rb)[4]) {
     const int kb = k0 + 4 * (tid >> 5), c = 4 * (tid & 31);
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
@@ -512,7 +514,7 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
       *(uint2*)(Lo + off) = make_uint2(l0, l1);
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, const raw_t (&ra)[4], const raw_t (&rb)[4]) {
     const int kk = 4 * (tid >> 5), c = 4 * (tid & 31);
     put_kmajor(Bh[buf], Bl[buf], rb, c, kk, sb);
     if constexpr (!AK) {
@@ -539,12 +541,12 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
 
-  load(ks0 * GV_BK);
-  store(0);
-  __syncthreads();
-  for (int it = ks0; it < ks1; ++it) {
+  // stage it: request stage it + 2 into (la, lb), multiply the LDS buffer of
+  // stage it, write stage it + 1 from (sa, sb) into the other buffer (last
+  // read in stage it - 1, before the barrier that ended it)
+  auto stage = [&](int it, raw_t (&la)[4], raw_t (&lb)[4], const raw_t (&sa_)[4], const raw_t (&sb_)[4]) {
     const int buf = (it - ks0) & 1;
-    if (it + 1 < ks1) load((it + 1) * GV_BK);
+    if (it + 2 < ks1) load((it + 2) * GV_BK, la, lb);
 #pragma unroll
     for (int ks = 0; ks < GV_BK / 16; ++ks) {
       u32x4 f[8];  // ah0 ah1 al0 al1 bh0 bh1 bl0 bl1
@@ -574,9 +576,16 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_x3(GemmF32Args g) {
           acc[i][j] = mma(f[i], f[4 + j], acc[i][j]);
         }
     }
-    // the other buffer was last read in the previous stage, before the barrier
-    if (it + 1 < ks1) store(buf ^ 1);
+    if (it + 1 < ks1) store(buf ^ 1, sa_, sb_);
     __syncthreads();
+  };
+  load(ks0 * GV_BK, ra0, rb0);
+  if (ks0 + 1 < ks1) load((ks0 + 1) * GV_BK, ra1, rb1);
+  store(0, ra0, rb0);
+  __syncthreads();
+  for (int it = ks0; it < ks1; it += 2) {
+    stage(it, ra0, rb0, ra1, rb1);
+    if (it + 1 < ks1) stage(it + 1, ra1, rb1, ra0, rb0);
   }
   if constexpr (F16) {
 #pragma unroll

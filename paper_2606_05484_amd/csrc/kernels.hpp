@@ -53,7 +53,7 @@ struct GemmF32Args {
   int sym_upper;   // C = A B known symmetric (B = A^T, M == N, no Cin): only tiles on or above the
                    // diagonal are computed, each off-diagonal one also written mirrored (aligned case)
   float* sk_part;  // sym_upper, fp32 operands and output: with this workspace (gemm_f32_sk_bytes)
-                   // the tiles' K ranges are split evenly over one workgroup per CU (stream-K) and
+                   // the tiles' K ranges are split evenly over two workgroups per CU (stream-K) and
                    // a second launch sums each tile's pieces in K order
 };
 hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStream_t s);
@@ -65,7 +65,7 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
 struct SkPlan {
   int T, nk, U, maxp, nwg;
 };
-constexpr int SK_WORKGROUPS = 256;  // one per compute unit of an MI355X
+constexpr int SK_WORKGROUPS = 512;  // two per compute unit of an MI355X
 __host__ __device__ inline SkPlan gemm_f32_sk_plan(int M, int K, int batch) {
   SkPlan p;
   const int ntm = (M + 127) / 128;

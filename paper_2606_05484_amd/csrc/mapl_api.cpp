@@ -123,8 +123,8 @@ struct Carve {
 };
 
 // The Stiefel step's Gram products X^T X ([r, r] upper tiles over K = d)
-// take the stream-K split where they have fewer tiles than the chip has CUs
-// and K is long enough for the split to pay for its fix-up launch.
+// take the stream-K split where they have fewer tiles than two per CU and K
+// is long enough for the split to pay for its fix-up launch.
 bool gram_stream_k(int P, int d, int r) {
   const SkPlan p = gemm_f32_sk_plan(r, d, P);
   return p.T < SK_WORKGROUPS && p.nk >= 16;
@@ -1003,7 +1003,7 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.B = X; g.sBk = r; g.sBn = 1; g.sBb = n;
     g.C = S; g.sCm = r; g.sCn = 1; g.sCb = rr;
     g.alpha_ptr = aptr;
-    g.sk_part = skp;  // split over one workgroup per CU where the upper tiles are fewer
+    g.sk_part = skp;  // split over two workgroups per CU where the upper tiles are fewer
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
   auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr, int split,
