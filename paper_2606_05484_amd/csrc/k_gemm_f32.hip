@@ -606,26 +606,29 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
   gv_epilogue<float>(g, acc, b, tbm, tbn, lane, wm, wn);
 }
 
-// The stream-K fix-up: one single-wave workgroup per (tile, wave quarter)
-// sums that quarter's pieces in piece (= K) order and applies the epilogue
-// of the one-launch kernels (scaling, diagonal); an off-diagonal tile's
-// mirror is written through a 64 x 64 LDS transpose, in whole rows.
-__global__ __launch_bounds__(64) void k_gemm_sk_fix(GemmF32Args g) {
+// The stream-K fix-up: one workgroup per (tile, wave quarter), one wave per
+// 32 x 32 block of the quarter, sums the pieces in piece (= K) order and
+// applies the epilogue of the one-launch kernels (scaling, diagonal); an
+// off-diagonal tile's mirror is written through a 64 x 64 LDS transpose, in
+// whole rows.
+__global__ __launch_bounds__(256) void k_gemm_sk_fix(GemmF32Args g) {
   __shared__ float L[64][65];
   const SkPlan p = gemm_f32_sk_plan(g.M, g.K, g.batch);
-  const int t = blockIdx.x >> 2, wave = blockIdx.x & 3, lane = threadIdx.x;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int t = blockIdx.x >> 2, wave = blockIdx.x & 3;
+  const int lane = threadIdx.x & 63, blk = threadIdx.x >> 6;  // blk = (i, j) block of the quarter
+  const int wm = wave >> 1, wn = wave & 1, i = blk >> 1, j = blk & 1;
   const int pf = (int)(((int64_t)t * p.nk) / p.U), pl = (int)(((int64_t)(t + 1) * p.nk - 1) / p.U);
-  const float* slot = g.sk_part + (int64_t)t * p.maxp * (128 * 128) + 64 * wave + lane;
-  float v[64];
+  // a piece holds element e of block (i, j) of quarter w, lane l, at ((2i + j) 16 + e) 256 + 64 w + l
+  const float* slot = g.sk_part + (int64_t)t * p.maxp * (128 * 128) + blk * 16 * 256 + 64 * wave + lane;
+  float v[16];
 #pragma unroll
-  for (int q = 0; q < 64; ++q) v[q] = slot[q * 256];
+  for (int e = 0; e < 16; ++e) v[e] = slot[e * 256];
   for (int pc = 1; pc <= pl - pf; ++pc) {
-    float w[64];
+    float w[16];
 #pragma unroll
-    for (int q = 0; q < 64; ++q) w[q] = slot[(int64_t)pc * (128 * 128) + q * 256];
+    for (int e = 0; e < 16; ++e) w[e] = slot[(int64_t)pc * (128 * 128) + e * 256];
 #pragma unroll
-    for (int q = 0; q < 64; ++q) v[q] += w[q];
+    for (int e = 0; e < 16; ++e) v[e] += w[e];
   }
   int b, bm, bn;
   sk_tile(t, g.M, b, bm, bn);
@@ -633,21 +636,17 @@ __global__ __launch_bounds__(64) void k_gemm_sk_fix(GemmF32Args g) {
   const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
   float* C = (float*)g.C + b * g.sCb;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int mm = i * 32 + acc_row(e, lane), nn = j * 32 + (lane & 31);
-        float x = alpha * v[(i * 2 + j) * 16 + e];
-        if (mb + mm == nb + nn) x += g.diag;
-        if (mb + mm < g.M && nb + nn < g.N) C[(mb + mm) * g.sCm + (nb + nn) * g.sCn] = x;
-        L[mm][nn] = x;
-      }
+  for (int e = 0; e < 16; ++e) {
+    const int mm = i * 32 + acc_row(e, lane), nn = j * 32 + (lane & 31);
+    float x = alpha * v[e];
+    if (mb + mm == nb + nn) x += g.diag;
+    if (mb + mm < g.M && nb + nn < g.N) C[(mb + mm) * g.sCm + (nb + nn) * g.sCn] = x;
+    L[mm][nn] = x;
+  }
   if (bm == bn) return;  // a diagonal tile has no mirror (uniform over the workgroup)
   __syncthreads();
-  // mirror: C[nb + nn][mb + lane] = L[lane][nn], one 64-float row per step
-  for (int nn = 0; nn < 64; ++nn)
+  // mirror: C[nb + nn][mb + lane] = L[lane][nn], one 64-float row per wave and step
+  for (int nn = blk; nn < 64; nn += 4)
     if (nb + nn < g.N && mb + lane < g.M) C[(nb + nn) * g.sCm + (mb + lane) * g.sCn] = L[lane][nn];
 }
 
@@ -682,7 +681,7 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
                                    : dim3(ntm, (g.N + GV_BN - 1) / GV_BN, g.batch);
   auto sk_fix = [&]() {
     if (!g.sk_part) return hipGetLastError();
-    hipLaunchKernelGGL(k_gemm_sk_fix, dim3(4 * gemm_f32_sk_plan(g.M, g.K, g.batch).T), dim3(64), 0, s, g);
+    hipLaunchKernelGGL(k_gemm_sk_fix, dim3(4 * gemm_f32_sk_plan(g.M, g.K, g.batch).T), dim3(256), 0, s, g);
     return hipGetLastError();
   };
   if (g.split && (vm < 0 || ta || tb || to)) return hipErrorInvalidValue;
