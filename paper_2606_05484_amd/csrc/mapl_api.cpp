@@ -380,6 +380,7 @@ extern "C" size_t mapl_workspace_bytes(const mapl_codec_desc* desc, int call, in
     c.take((size_t)P * 2048 * 4);    // partial sums of M^2 and G^2
     c.take((size_t)P * 8 * 4);       // scalars
     if (gram_stream_k((int)P, (int)d, (int)r)) c.take(gemm_f32_sk_bytes((int)r, (int)d, (int)P));  // Gram pieces
+    for (int i = 0; i < 4; ++i) c.take((size_t)P * r * r * 4);  // retraction: Q', S Q, two products of Q's
     return c.off;
   }
   if (call < MAPL_CALL_ENCODE || call > MAPL_CALL_ENCODE_BWD) {
@@ -983,17 +984,17 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   float* skp = gram_stream_k((int)P, (int)d, (int)r)
                    ? at<float>(ws, c.take(gemm_f32_sk_bytes((int)r, (int)d, (int)P)))
                    : nullptr;
+  float* Q2 = at<float>(ws, c.take((size_t)P * r * r * 4));
+  float* Tm = at<float>(ws, c.take((size_t)P * r * r * 4));
+  float* Pq[2] = {at<float>(ws, c.take((size_t)P * r * r * 4)), at<float>(ws, c.take((size_t)P * r * r * 4))};
   float* scale = sc, *scale2 = sc + P, *inv_nu = sc + 2 * P, *inv_nu2 = sc + 3 * P;
   const int64_t n = d * r, rr = r * r;
 
   // split: the products from 16-bit pieces (hi.hi + hi.lo + lo.hi) on the
   // 16-bit matrix units.  GEMM_SPLIT_BF16 (about 2^-15 relative per term,
   // any exponent) carries the LMO's direction; GEMM_SPLIT_F16 (fp32's
-  // accuracy, |operands| < 255) the retraction, whose iterates have
-  // spectral norm at most about 1.03: X0 = Y / nu has norm <= 1 (its first
-  // step takes Y and S = Y^T Y scaled by 1/nu and 1/nu^2 inside the split)
-  // and each PolarExpress quintic maps [0, 1.03] into [0, 1.03], so every
-  // entry of X, S = X^T X and a + b S + c S^2 stays below 5.
+  // accuracy, |operands| < 255) the retraction, whose operands are bounded
+  // by construction (see there).
   auto gram = [&](const float* X, const float* aptr, int split) {  // S = X^T X (times aptr)
     GemmF32Args g = gemm((int)r, (int)r, (int)d);
     g.split = split;
@@ -1007,15 +1008,15 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
   auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr, int split,
-                  const float* pre = nullptr) {  // Qm = a I + b S + c S S (S scaled by pre inside the product)
-    GemmF32Args g = gemm((int)r, (int)r, (int)r);
+                  const float* pre = nullptr, float* Qo = nullptr) {  // Qo (Qm) = a I + b S + c S S
+    GemmF32Args g = gemm((int)r, (int)r, (int)r);                      // (S scaled by pre inside the product)
     g.split = split;
     g.pre_a = g.pre_b = pre;
     g.batch = (int)P;
     g.A = S; g.sAm = r; g.sAk = 1; g.sAb = rr;
     g.B = S; g.sBk = r; g.sBn = 1; g.sBb = rr;
     g.Cin = S; g.sCinm = r; g.sCinn = 1; g.sCinb = rr;
-    g.C = Qm; g.sCm = r; g.sCn = 1; g.sCb = rr;
+    g.C = Qo ? Qo : Qm; g.sCm = r; g.sCn = 1; g.sCb = rr;
     g.alpha = (float)cc; g.beta = (float)b; g.diag = (float)a;
     g.alpha_ptr = aptr; g.beta_ptr = bptr;
     return launch_gemm_f32(g, 0, 0, 0, s);
@@ -1023,19 +1024,32 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   // Xo = s X Qm, or with Yin: Xo = Yin - lr s X Qm (the LMO's last product
   // and Eq. 7's argument U - lr D in one launch)
   auto apply = [&](const float* X, float* Xo, const float* sptr, int split, const float* Yin = nullptr,
-                   const float* pre = nullptr) {  // (pre: X's factor inside the product)
+                   const float* pre = nullptr, const float* Bm = nullptr) {  // (pre: X's factor inside the product)
     GemmF32Args g = gemm((int)d, (int)r, (int)r);
     g.split = split;
     g.pre_a = pre;
     g.batch = (int)P;
     g.A = X; g.sAm = r; g.sAk = 1; g.sAb = n;
-    g.B = Qm; g.sBk = r; g.sBn = 1; g.sBb = rr;
+    g.B = Bm ? Bm : Qm; g.sBk = r; g.sBn = 1; g.sBb = rr;
     g.C = Xo; g.sCm = r; g.sCn = 1; g.sCb = n;
     g.alpha_ptr = sptr;
     if (Yin) {
       g.Cin = Yin; g.sCinm = r; g.sCinn = 1; g.sCinb = n; g.beta = 1.f;
       g.alpha = -lr;
     }
+    return launch_gemm_f32(g, 0, 0, 0, s);
+  };
+  // Co = (A scaled by pre inside) B for r x r factors, fp16 split; sym: the
+  // product is symmetric (upper tiles computed, mirrored)
+  auto rmul = [&](float* Co, const float* Am, const float* Bm, const float* pre, bool sym) {
+    GemmF32Args g = gemm((int)r, (int)r, (int)r);
+    g.split = GEMM_SPLIT_F16;
+    g.pre_a = pre;
+    g.sym_upper = sym ? 1 : 0;
+    g.batch = (int)P;
+    g.A = Am; g.sAm = r; g.sAk = 1; g.sAb = rr;
+    g.B = Bm; g.sBk = r; g.sBn = 1; g.sBb = rr;
+    g.C = Co; g.sCm = r; g.sCn = 1; g.sCb = rr;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
 
@@ -1087,17 +1101,54 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   LAUNCH("stiefel:gram", gram(Y, nullptr, GEMM_SPLIT_NONE));
   // (the momentum's norm partials are consumed by now; their buffer takes the row maxima)
   LAUNCH("stiefel:inf_norm_scales", launch_inf_norm_scales(S, (int)P, (int)r, partial, inv_nu, inv_nu2, s));
-  Xin = Y;
-  for (int i = 0; i < retract_steps; ++i) {
-    const double a = kRetractCoef[i][0], b = kRetractCoef[i][1], cc = kRetractCoef[i][2];
-    const bool first = i == 0;
-    if (!first) LAUNCH("stiefel:gram", gram(Xin, nullptr, GEMM_SPLIT_F16));
-    // the first step: Qm = a I + b S / nu^2 + c (S / nu^2)^2 and Y Qm / nu
-    LAUNCH("stiefel:poly", poly(a, b, cc, nullptr, first ? inv_nu2 : nullptr, GEMM_SPLIT_F16, first ? inv_nu2 : nullptr));
-    float* Xo = (i == retract_steps - 1) ? U : bufs[cur];
-    LAUNCH("stiefel:apply", apply(Xin, Xo, nullptr, GEMM_SPLIT_F16, nullptr, first ? inv_nu : nullptr));
-    Xin = Xo;
+  // The retraction's iterates X_i = X_0 Q_0 ... Q_{i-1} (X_0 = Y / nu) are
+  // carried in the r x r space: S_i = X_i^T X_i, Q_i = a I + b S_i + c S_i^2,
+  // S_{i+1} = Q_i (S_i Q_i) and P_{i+1} = P_i Q_i, then X_j = X_i P_j: the
+  // same iterates, with r^3 products in place of the d r^2 Gram and apply
+  // products of every step (the Q_i are polynomials in S_i and commute with
+  // it).  Every operand of the fp16 split stays bounded whatever the input:
+  // S_0 / nu^2 and X_0 have spectral norm <= 1, the schedule's quintics map
+  // [0, 1] and then [0, 1.03] into [0, 1.03] (so S_i, S_i Q_i and Q_i stay
+  // below 5), and each quintic p has p(x) <= a x there, so the eigenvalues
+  // p(...)(sigma) / sigma of a product of Q's stay below the product of
+  // their a's.  The steps therefore run in segments whose a's multiply to at
+  // most kSegGrowth (all seven of the paper's schedule: 116); a longer
+  // schedule applies P to X at a segment's end and starts the next from
+  // that X's Gram product.
+  constexpr double kSegGrowth = 200.0;  // < 255, the fp16 split's operand bound
+  const float* Xseg = Y;
+  for (int i = 0; i < retract_steps;) {
+    int j = i;
+    for (double growth = 1.0; j < retract_steps && growth * kRetractCoef[j][0] <= kSegGrowth; ++j)
+      growth *= kRetractCoef[j][0];
+    if (j == i) return fail(MAPL_E_UNSUPPORTED, "stiefel: retraction coefficient above the split bound");
+    if (i > 0) LAUNCH("stiefel:gram", gram(Xseg, nullptr, GEMM_SPLIT_F16));  // S_i = X_i^T X_i
+    const float* Pprev = nullptr;
+    int pq = 0;
+    for (int k = i; k < j; ++k) {
+      const double a = kRetractCoef[k][0], b = kRetractCoef[k][1], cc = kRetractCoef[k][2];
+      const bool first = k == 0;  // S_0 = Y^T Y, scaled by 1/nu^2 inside
+      float* Q = (k & 1) ? Q2 : Qm;
+      LAUNCH("stiefel:poly", poly(a, b, cc, nullptr, first ? inv_nu2 : nullptr, GEMM_SPLIT_F16,
+                                  first ? inv_nu2 : nullptr, Q));
+      if (k == i) {
+        Pprev = Q;
+      } else {
+        LAUNCH("stiefel:ret_p", rmul(Pq[pq], Pprev, Q, nullptr, false));  // P_{k+1} = P_k Q_k
+        Pprev = Pq[pq];
+        pq ^= 1;
+      }
+      if (k + 1 < j) {
+        LAUNCH("stiefel:ret_sq", rmul(Tm, S, Q, first ? inv_nu2 : nullptr, false));  // S_k Q_k
+        LAUNCH("stiefel:ret_s", rmul(S, Q, Tm, nullptr, true));                       // S_{k+1}
+      }
+    }
+    // X_j = X_i P_j (X_0 = Y / nu)
+    float* Xo = j == retract_steps ? U : bufs[cur];
+    LAUNCH("stiefel:apply", apply(Xseg, Xo, nullptr, GEMM_SPLIT_F16, nullptr, i == 0 ? inv_nu : nullptr, Pprev));
+    Xseg = Xo;
     cur ^= 1;
+    i = j;
   }
   return MAPL_OK;
 }
