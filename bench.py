@@ -557,21 +557,39 @@ def spel_step_timing(torch, mapl, synth, P, dd, rr, reps):
     return time_steps(torch, run, 2, reps)
 
 
+# Segments of the r x r PolarExpress iteration at the 5 / 7 schedule the
+# bench runs (consecutive steps whose linear coefficients multiply to at
+# most 200): the LMO in 3 + 2 steps, the retraction in one segment of 7.
+SPEL_SEGMENTS = {"lmo": (3, 2), "retraction": (7,)}
+
+
+def spel_flop_split(P, dd, rr):
+    """(fp32-MFMA flops, split-product flops) of one SPEL step as the library
+    computes it: Eq. 4's two products and the Gram product of Y on the fp32
+    matrix units; per PolarExpress segment of n steps a Gram product of its
+    start (the LMO's first: of M), n polynomials, n - 1 updates
+    S <- Q (S Q), n - 1 products of Q's and one d x r x r product forming X.
+    Every product counted in full (the symmetric ones compute half)."""
+    big, small = 2 * dd * rr * rr, 2 * rr ** 3
+    f32 = 2 * big + big  # U^T G, G - U sym(S), Y^T Y
+    split = 0
+    for name, segs in SPEL_SEGMENTS.items():
+        for k, n in enumerate(segs):
+            gram = 0 if (name == "retraction" and k == 0) else big  # Y^T Y is the fp32 one
+            split += gram + n * small + (n - 1) * 2 * small + (n - 1) * small + big
+    return P * f32, P * split
+
+
 def spel_flops(P, dd, rr):
-    it = 4 * dd * rr * rr + 2 * rr ** 3
-    return P * (4 * dd * rr * rr + 12 * it)
+    return sum(spel_flop_split(P, dd, rr))
 
 
 def spel_roofline_s(P, dd, rr):
-    """Eq. 4's two products and the retraction's first Gram product (the one
-    that fixes nu) on the fp32 matrix units; every other product as a split
-    product (three 16-bit products per flop: bf16 pieces in the 5 LMO steps,
-    fp16 pieces in the 7 retraction steps) on the 16-bit matrix units, whose
-    dense fp16 and bf16 peaks are equal."""
-    it = 4 * dd * rr * rr + 2 * rr ** 3
-    f32 = 4 * dd * rr * rr + 2 * dd * rr * rr
-    split = 12 * it - 2 * dd * rr * rr
-    return P * f32 / PEAK_F32 + P * split * 3 / PEAK_BF16
+    """The fp32 products at the fp32 matrix peak; the split products as three
+    fp16 products per flop at the 16-bit matrix peak (fp16 and bf16 dense
+    peaks are equal)."""
+    f32, split = spel_flop_split(P, dd, rr)
+    return f32 / PEAK_F32 + split * 3 / PEAK_BF16
 
 
 def main():

@@ -409,25 +409,19 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
   gv_epilogue<TO>(g, acc, b, tbm, tbn, lane, wm, wn);
 }
 
-// Split variants of the aligned fp32 GEMM (fp32 operands and output): every
-// operand element x is held as two 16-bit pieces hi + lo, and each product
-// is taken as hi.hi + hi.lo + lo.hi on the 16-bit matrix units (fp32
-// accumulation), dropping lo.lo, at five times the fp32 MFMA rate:
-//  - F16 = false: hi = bf16(x), lo = bf16(x - hi) (round to nearest even;
-//    x - hi - lo is below 2^-16 |x|): about 2^-15 relative error per
-//    product term, over fp32's whole exponent range;
-//  - F16 = true: the split of Ootomo and Yokota (2022) on fp16 pieces, with
-//    a power-of-two prescale instead of their scaled low piece:
-//    y = 2^8 x, hi = fp16(y), lo = fp16(y - hi) (both round to nearest
-//    even, subnormals kept), products on v_mfma_f32_32x32x16_f16 and the
-//    sums scaled by 2^-16 (exact).  An operand may carry a per-batch factor
-//    (pre_a, pre_b) taken into the prescale, so the product is of the
-//    scaled operands.  hi + lo holds y to 22 bits where lo is
-//    normal (|x| >= 2^-11) and to an absolute 2^-33 below that, so each
-//    product term carries about 2^-21 relative error: fp32's accuracy for
-//    the sums over K of a few thousand.  The (scaled) operands must satisfy
-//    |x| < 255 (hi stays finite); callers use it only where a norm bound
-//    holds.
+// Split variant of the aligned fp32 GEMM (fp32 operands and output): the
+// split of Ootomo and Yokota (2022) on fp16 pieces, with a power-of-two
+// prescale instead of their scaled low piece.  Every operand element x is
+// held as y = 2^8 x, hi = fp16(y), lo = fp16(y - hi) (both round to nearest
+// even, subnormals kept), each product taken as hi.hi + hi.lo + lo.hi on
+// v_mfma_f32_32x32x16_f16 (fp32 accumulation, lo.lo dropped) and the sums
+// scaled by 2^-16 (exact), at five times the fp32 MFMA rate.  An operand may
+// carry a per-batch factor (pre_a, pre_b) taken into the prescale, so the
+// product is of the scaled operands.  hi + lo holds y to 22 bits where lo is
+// normal (|x| >= 2^-11) and to an absolute 2^-33 below that, so each product
+// term carries about 2^-21 relative error: fp32's accuracy for the sums over
+// K of a few thousand.  The (scaled) operands must satisfy |x| < 255 (hi
+// stays finite); callers use it only where a norm bound holds.
 // Same tiling as k_gemm_f32v (128 x 128, K staged 32 at a time, 16-byte
 // loads into registers one stage ahead, two LDS buffers).  Hi and lo pieces
 // live apart in LDS, each operand in the layout its loads give:
@@ -437,10 +431,10 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
 //  - B and an m-contiguous A as [k][row] (k-major, 128 rows = 16 chunks per
 //    k, chunk-swizzled by wg_sw), written 8 bytes per lane along the row and
 //    read with transposing LDS reads (tr_frag).
-constexpr int GX_LD = GV_BK + 8;  // bf16 per row of a [row][k] tile
+constexpr int GX_LD = GV_BK + 8;  // 16-bit pieces per row of a [row][k] tile
 constexpr int GX_CPR = GV_BM / 8;  // 16-byte chunks per k of a [k][row] tile
 
-template <bool AK, bool F16>
+template <bool AK>
 __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_gemm_x3(GemmF32Args g) {
   // [row][k] tiles (k-contiguous A) or [k][row] tiles (the rest), per buffer and piece
   constexpr int A_ELEMS = AK ? GV_BM * GX_LD : GV_BK * GV_BM;
@@ -483,24 +477,16 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
     }
   };
   // the fp16 split's prescale: 2^8 times the operand's factor for this batch entry
-  const float sa = F16 ? 256.f * (g.pre_a ? g.pre_a[b] : 1.f) : 1.f;
-  const float sb = F16 ? 256.f * (g.pre_b ? g.pre_b[b] : 1.f) : 1.f;
+  const float sa = 256.f * (g.pre_a ? g.pre_a[b] : 1.f);
+  const float sb = 256.f * (g.pre_b ? g.pre_b[b] : 1.f);
   // hi and lo pieces of two floats, packed
   auto split2 = [](float x, float y, uint32_t& hi, uint32_t& lo, float sc) {
-    if constexpr (F16) {
-      const f32x2_t v = (f32x2_t){x, y} * sc;
-      const f16x2_t h = __builtin_convertvector(v, f16x2_t);
-      hi = __builtin_bit_cast(uint32_t, h);
-      lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(v - __builtin_convertvector(h, f32x2_t), f16x2_t));
-    } else {
-      hi = pack_bf2(x, y);
-      lo = pack_bf2(x - __uint_as_float(hi << 16), y - __uint_as_float(hi & 0xFFFF0000u));
-    }
+    const f32x2_t v = (f32x2_t){x, y} * sc;
+    const f16x2_t h = __builtin_convertvector(v, f16x2_t);
+    hi = __builtin_bit_cast(uint32_t, h);
+    lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(v - __builtin_convertvector(h, f32x2_t), f16x2_t));
   };
-  auto mma = [](const u32x4& a, const u32x4& b, f32x16_t c) {
-    if constexpr (F16) return mfma32x32x16h(as_uint4(a), as_uint4(b), c);
-    else return mfma32x32x16(as_uint4(a), as_uint4(b), c);
-  };
+  auto mma = [](const u32x4& a, const u32x4& b, f32x16_t c) { return mfma32x32x16h(as_uint4(a), as_uint4(b), c); };
   // 4 consecutive rows at 4 consecutive k (v[h]: k = h) into a [k][row] tile
   auto put_kmajor = [&](bf16_t* H, bf16_t* Lo, const raw_t (&v)[4], int row0, int kk, float sc) {
 #pragma unroll
@@ -587,12 +573,10 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
     stage(it, ra0, rb0, ra1, rb1);
     if (it + 1 < ks1) stage(it + 1, ra1, rb1, ra0, rb0);
   }
-  if constexpr (F16) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] *= 1.f / 65536.f;
-  }
+    for (int j = 0; j < 2; ++j) acc[i][j] *= 1.f / 65536.f;
   };
 
   if (g.sk_part) {
@@ -685,12 +669,9 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
     return hipGetLastError();
   };
   if (g.split && (vm < 0 || ta || tb || to)) return hipErrorInvalidValue;
-  if (g.split == GEMM_SPLIT_BF16 || g.split == GEMM_SPLIT_F16) {
-    const bool h = g.split == GEMM_SPLIT_F16;
-    if (vm && h) hipLaunchKernelGGL((k_gemm_x3<true, true>), vgrid, dim3(GF_THREADS), 0, s, g);
-    else if (vm) hipLaunchKernelGGL((k_gemm_x3<true, false>), vgrid, dim3(GF_THREADS), 0, s, g);
-    else if (h) hipLaunchKernelGGL((k_gemm_x3<false, true>), vgrid, dim3(GF_THREADS), 0, s, g);
-    else hipLaunchKernelGGL((k_gemm_x3<false, false>), vgrid, dim3(GF_THREADS), 0, s, g);
+  if (g.split == GEMM_SPLIT_F16) {
+    if (vm) hipLaunchKernelGGL((k_gemm_x3<true>), vgrid, dim3(GF_THREADS), 0, s, g);
+    else hipLaunchKernelGGL((k_gemm_x3<false>), vgrid, dim3(GF_THREADS), 0, s, g);
     const hipError_t e = hipGetLastError();
     return e != hipSuccess ? e : sk_fix();
   }

@@ -143,11 +143,11 @@ __global__ void k_momentum(float* __restrict__ M, const float* __restrict__ gR, 
   }
 }
 
-// LMO normalisation of Eq. 6: scale = 1 / (||M||_F + eps), scale2 = scale^2;
-// both 0 (so the LMO returns D = 0) when ||M||_F <= zero_rel ||G||_F: a
-// momentum below the fp32 resolution of the gradient carries no direction.
+// LMO normalisation of Eq. 6: scale = 1 / (||M||_F + eps), or 0 (so the LMO
+// returns D = 0) when ||M||_F <= zero_rel ||G||_F: a momentum below the fp32
+// resolution of the gradient carries no direction.
 __global__ void k_fro_scale(const float* __restrict__ partial, int nblk, int P, float eps, float zero_rel,
-                            float* scale, float* scale2) {
+                            float* scale) {
   const int p = blockIdx.x, lane = threadIdx.x;
   float s = 0.f, sg = 0.f;
   for (int i = lane; i < nblk; i += 64) {
@@ -160,7 +160,6 @@ __global__ void k_fro_scale(const float* __restrict__ partial, int nblk, int P, 
     const float nm = sqrtf(s);
     const float sc = nm <= zero_rel * sqrtf(sg) ? 0.f : 1.f / (nm + eps);
     scale[p] = sc;
-    scale2[p] = sc * sc;
   }
 }
 
@@ -279,8 +278,8 @@ hipError_t launch_momentum(float* M, const float* gR, const float* G, int64_t n,
 }
 
 hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float zero_rel, float* scale,
-                            float* scale2, hipStream_t s) {
-  hipLaunchKernelGGL(k_fro_scale, dim3(P), dim3(64), 0, s, partial, nblk, P, eps, zero_rel, scale, scale2);
+                            hipStream_t s) {
+  hipLaunchKernelGGL(k_fro_scale, dim3(P), dim3(64), 0, s, partial, nblk, P, eps, zero_rel, scale);
   return hipGetLastError();
 }
 

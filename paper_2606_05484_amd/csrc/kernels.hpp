@@ -36,7 +36,7 @@ bool gemm_tn_gathers(const TnArgs& g);
 // ---------------------------------------------------------------- fp32 GEMM
 // C[b](m,n) = alpha_b sum_k A[b](m,k) B[b](k,n) + beta_b Cin[b](m,n)
 // element types: 0 = fp32, 1 = bf16 (A, B, C); Cin is fp32 (may be null).
-enum { GEMM_SPLIT_NONE = 0, GEMM_SPLIT_BF16 = 1, GEMM_SPLIT_F16 = 2 };
+enum { GEMM_SPLIT_NONE = 0, GEMM_SPLIT_F16 = 1 };
 struct GemmF32Args {
   const void* A; int64_t sAm, sAk, sAb;
   const void* B; int64_t sBk, sBn, sBb;
@@ -46,8 +46,8 @@ struct GemmF32Args {
   float alpha, beta;
   const float* alpha_ptr; const float* beta_ptr;
   float diag;  // added to every element with m == n after the scaling
-  int split;  // fp32 operands and output, aligned: GEMM_SPLIT_BF16 or GEMM_SPLIT_F16 takes the products
-             // as hi.hi + hi.lo + lo.hi of 16-bit pieces (GEMM_SPLIT_F16: |operands| < 255)
+  int split;  // fp32 operands and output, aligned: GEMM_SPLIT_F16 takes the products as
+             // hi.hi + hi.lo + lo.hi of fp16 pieces of 2^8 x (|operands| < 255)
   const float* pre_a; const float* pre_b;  // GEMM_SPLIT_F16 only: per-batch factors of A and B
                                            // (null: 1), applied before the split
   int sym_upper;   // C = A B known symmetric (B = A^T, M == N, no Cin): only tiles on or above the
@@ -232,10 +232,10 @@ hipError_t launch_symmetrize(float* S, int P, int r, hipStream_t s);
 // partial sums of M^2 -> partial[p][nblk], of G^2 -> partial[P + p][nblk].
 hipError_t launch_momentum(float* M, const float* gR, const float* G, int64_t n, int P, float beta, float* partial,
                            int nblk, hipStream_t s);
-// scale[p] = 1/(||M_p|| + eps), scale2[p] = scale^2; both 0 when
-// ||M_p|| <= zero_rel ||G_p|| (norms from launch_momentum's partials).
+// scale[p] = 1/(||M_p|| + eps), or 0 when ||M_p|| <= zero_rel ||G_p||
+// (norms from launch_momentum's partials).
 hipError_t launch_fro_scale(const float* partial, int nblk, int P, float eps, float zero_rel, float* scale,
-                            float* scale2, hipStream_t s);
+                            hipStream_t s);
 // For S [P][r][r]: nu2 = max_i sum_j |S_ij|; inv_nu = 1/sqrt(nu2), inv_nu2 = 1/nu2;
 // part: P * ceil(r / 16) floats of scratch.
 hipError_t launch_inf_norm_scales(const float* S, int P, int r, float* part, float* inv_nu, float* inv_nu2,

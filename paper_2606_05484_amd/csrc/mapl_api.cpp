@@ -987,52 +987,50 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   float* Q2 = at<float>(ws, c.take((size_t)P * r * r * 4));
   float* Tm = at<float>(ws, c.take((size_t)P * r * r * 4));
   float* Pq[2] = {at<float>(ws, c.take((size_t)P * r * r * 4)), at<float>(ws, c.take((size_t)P * r * r * 4))};
-  float* scale = sc, *scale2 = sc + P, *inv_nu = sc + 2 * P, *inv_nu2 = sc + 3 * P;
+  float* scale = sc, *inv_nu = sc + P, *inv_nu2 = sc + 2 * P;
   const int64_t n = d * r, rr = r * r;
 
-  // split: the products from 16-bit pieces (hi.hi + hi.lo + lo.hi) on the
-  // 16-bit matrix units.  GEMM_SPLIT_BF16 (about 2^-15 relative per term,
-  // any exponent) carries the LMO's direction; GEMM_SPLIT_F16 (fp32's
-  // accuracy, |operands| < 255) the retraction, whose operands are bounded
-  // by construction (see there).
-  auto gram = [&](const float* X, const float* aptr, int split) {  // S = X^T X (times aptr)
+  // split: GEMM_SPLIT_F16 takes the products from fp16 pieces (hi.hi +
+  // hi.lo + lo.hi) on the 16-bit matrix units, with fp32's accuracy for
+  // operands below 255 (PolarExpress below keeps them there); Eq. 4 and the
+  // Gram product of Y (any norm) run on the fp32 matrix units.
+  // S = X^T X (X scaled by pre inside the split)
+  auto gram = [&](const float* X, int split, const float* pre) {
     GemmF32Args g = gemm((int)r, (int)r, (int)d);
     g.split = split;
+    g.pre_a = g.pre_b = pre;
     g.sym_upper = 1;  // X^T X: the tiles above the diagonal, mirrored
     g.batch = (int)P;
     g.A = X; g.sAm = 1; g.sAk = r; g.sAb = n;
     g.B = X; g.sBk = r; g.sBn = 1; g.sBb = n;
     g.C = S; g.sCm = r; g.sCn = 1; g.sCb = rr;
-    g.alpha_ptr = aptr;
     g.sk_part = skp;  // split over two workgroups per CU where the upper tiles are fewer
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  auto poly = [&](double a, double b, double cc, const float* aptr, const float* bptr, int split,
-                  const float* pre = nullptr, float* Qo = nullptr) {  // Qo (Qm) = a I + b S + c S S
-    GemmF32Args g = gemm((int)r, (int)r, (int)r);                      // (S scaled by pre inside the product)
-    g.split = split;
-    g.pre_a = g.pre_b = pre;
+  // Qo = a I + b S' + c S' S' with S' = sp S (sp: a per-projector factor, or none)
+  auto poly = [&](double a, double b, double cc, const float* sp, float* Qo) {
+    GemmF32Args g = gemm((int)r, (int)r, (int)r);
+    g.split = GEMM_SPLIT_F16;
+    g.pre_a = g.pre_b = sp;
     g.batch = (int)P;
     g.A = S; g.sAm = r; g.sAk = 1; g.sAb = rr;
     g.B = S; g.sBk = r; g.sBn = 1; g.sBb = rr;
     g.Cin = S; g.sCinm = r; g.sCinn = 1; g.sCinb = rr;
-    g.C = Qo ? Qo : Qm; g.sCm = r; g.sCn = 1; g.sCb = rr;
+    g.C = Qo; g.sCm = r; g.sCn = 1; g.sCb = rr;
     g.alpha = (float)cc; g.beta = (float)b; g.diag = (float)a;
-    g.alpha_ptr = aptr; g.beta_ptr = bptr;
+    g.beta_ptr = sp;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  // Xo = s X Qm, or with Yin: Xo = Yin - lr s X Qm (the LMO's last product
-  // and Eq. 7's argument U - lr D in one launch)
-  auto apply = [&](const float* X, float* Xo, const float* sptr, int split, const float* Yin = nullptr,
-                   const float* pre = nullptr, const float* Bm = nullptr) {  // (pre: X's factor inside the product)
+  // Xo = X' Bm with X' = pre X, or with Yin: Xo = Yin - lr X' Bm (the LMO's
+  // last product and Eq. 7's argument U - lr D in one launch)
+  auto apply = [&](const float* X, const float* pre, const float* Bm, float* Xo, const float* Yin) {
     GemmF32Args g = gemm((int)d, (int)r, (int)r);
-    g.split = split;
+    g.split = GEMM_SPLIT_F16;
     g.pre_a = pre;
     g.batch = (int)P;
     g.A = X; g.sAm = r; g.sAk = 1; g.sAb = n;
-    g.B = Bm ? Bm : Qm; g.sBk = r; g.sBn = 1; g.sBb = rr;
+    g.B = Bm; g.sBk = r; g.sBn = 1; g.sBb = rr;
     g.C = Xo; g.sCm = r; g.sCn = 1; g.sCb = n;
-    g.alpha_ptr = sptr;
     if (Yin) {
       g.Cin = Yin; g.sCinm = r; g.sCinn = 1; g.sCinb = n; g.beta = 1.f;
       g.alpha = -lr;
@@ -1078,78 +1076,75 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   int nblk = (int)((n + 255) / 256);
   if (nblk > 1024) nblk = 1024;
   LAUNCH("stiefel:momentum", launch_momentum(M, X0, G, n, (int)P, beta, partial, nblk, s));
-  LAUNCH("stiefel:fro_scale", launch_fro_scale(partial, nblk, (int)P, 1e-7f, 1.0f / 1048576.0f, scale, scale2, s));
+  LAUNCH("stiefel:fro_scale", launch_fro_scale(partial, nblk, (int)P, 1e-7f, 1.0f / 1048576.0f, scale, s));
 
-  // Eq. 6: D = PE(M / (||M|| + eps)), products in split-bf16 (the direction
-  // carries about 3e-5 relative error; the retraction below keeps fp32's)
-  const float* Xin = M;
+  // PolarExpress (Eqs. 6 and 7) with the iterates carried in the r x r
+  // space: for X_i = X_0 Q_0 ... Q_{i-1}, S_i = X_i^T X_i,
+  // Q_i = a I + b S_i + c S_i^2, S_{i+1} = Q_i (S_i Q_i) and
+  // P_{i+1} = P_i Q_i, and X_j = X_i P_j -- the same iterates, with r^3
+  // products in place of each step's d r^2 Gram and apply products (the Q_i
+  // are polynomials in S_i and commute with it).  Every product runs in the
+  // fp16 split, whose operands must stay below 255: X_0 has spectral norm
+  // <= 1 (M / (||M||_F + eps), Y / nu), both schedules keep the singular
+  // values below 2.1 (so X, S, S Q and Q stay below 9), and each quintic p
+  // has |p(x)| <= a x on the values it meets, so the eigenvalues
+  // p(...)(sigma) / sigma of a product of Q's stay below the product of
+  // their a's.  The steps run in segments whose a's multiply to at most
+  // kSegGrowth; at a segment's end X_j = X_i P_j is formed and the next
+  // segment starts from its Gram product.  On entry S holds X_0^T X_0
+  // divided by spre (the first step's products scale it by spre inside, null:
+  // 1); X_0 is Xs scaled by xpre inside its one product.  X_K, or
+  // Yin - lr X_K, goes to out (null: the X buffer not read last), and
+  // *written names the buffer.
+  constexpr double kSegGrowth = 200.0;  // < 255, the fp16 split's operand bound
   float* bufs[2] = {X0, X1};
-  int cur = 0;
-  for (int i = 0; i < lmo_steps; ++i) {
-    const double a = kLmoCoef[i][0], b = kLmoCoef[i][1], cc = kLmoCoef[i][2];
-    const bool first = i == 0, last = i == lmo_steps - 1;
-    LAUNCH("stiefel:lmo_gram", gram(Xin, first ? scale2 : nullptr, GEMM_SPLIT_BF16));
-    LAUNCH("stiefel:lmo_poly", poly(a, b, cc, nullptr, nullptr, GEMM_SPLIT_BF16));
-    float* Xo = bufs[cur];
-    // the last product writes Y = U - lr D directly (D itself is not kept)
-    LAUNCH("stiefel:lmo_apply", apply(Xin, Xo, first ? scale : nullptr, GEMM_SPLIT_BF16, last ? U : nullptr));
-    Xin = Xo;
-    cur ^= 1;
-  }
-  float* Y = (float*)Xin;
-  // Eq. 7: U = PE(Y / nu), nu^2 = max row sum |Y^T Y|
-  LAUNCH("stiefel:gram", gram(Y, nullptr, GEMM_SPLIT_NONE));
+  auto other = [&](const float* p) { return p == bufs[0] ? bufs[1] : bufs[0]; };
+  auto polar_rr = [&](const double (*coef)[3], int steps, const float* Xs, const float* xpre, const float* spre,
+                      float* out, const float* Yin, float** written) -> int {
+    const float* Xseg = Xs;
+    for (int i = 0; i < steps;) {
+      int j = i;
+      for (double growth = 1.0; j < steps && growth * coef[j][0] <= kSegGrowth; ++j) growth *= coef[j][0];
+      if (j == i) return fail(MAPL_E_UNSUPPORTED, "stiefel: PolarExpress coefficient above the split bound");
+      if (i > 0) LAUNCH("stiefel:pe_gram", gram(Xseg, GEMM_SPLIT_F16, nullptr));  // S_i = X_i^T X_i
+      const float* Pprev = nullptr;
+      int pq = 0;
+      for (int k = i; k < j; ++k) {
+        const double a = coef[k][0], b = coef[k][1], cc = coef[k][2];
+        const float* sp = k == 0 ? spre : nullptr;
+        float* Q = (k & 1) ? Q2 : Qm;
+        LAUNCH("stiefel:pe_poly", poly(a, b, cc, sp, Q));
+        if (k == i) {
+          Pprev = Q;
+        } else {
+          LAUNCH("stiefel:pe_p", rmul(Pq[pq], Pprev, Q, nullptr, false));  // P_{k+1} = P_k Q_k
+          Pprev = Pq[pq];
+          pq ^= 1;
+        }
+        if (k + 1 < j) {
+          LAUNCH("stiefel:pe_sq", rmul(Tm, S, Q, sp, false));  // S_k Q_k
+          LAUNCH("stiefel:pe_s", rmul(S, Q, Tm, nullptr, true));  // S_{k+1} (symmetric)
+        }
+      }
+      float* Xo = j == steps && out ? out : other(Xseg);
+      LAUNCH("stiefel:pe_apply", apply(Xseg, i == 0 ? xpre : nullptr, Pprev, Xo, j == steps ? Yin : nullptr));
+      Xseg = Xo;
+      i = j;
+    }
+    if (written) *written = (float*)Xseg;
+    return MAPL_OK;
+  };
+
+  // Eq. 6: D = PE(M / (||M||_F + eps)); the last product writes Y = U - lr D
+  // (D itself is not kept)
+  LAUNCH("stiefel:lmo_gram", gram(M, GEMM_SPLIT_F16, scale));
+  float* Y = nullptr;
+  if ((st = polar_rr(kLmoCoef, lmo_steps, M, scale, nullptr, nullptr, U, &Y))) return st;
+  // Eq. 7: U = PE(Y / nu), nu^2 = max row sum |Y^T Y|: Y^T Y in fp32 (it fixes nu)
+  LAUNCH("stiefel:gram", gram(Y, GEMM_SPLIT_NONE, nullptr));
   // (the momentum's norm partials are consumed by now; their buffer takes the row maxima)
   LAUNCH("stiefel:inf_norm_scales", launch_inf_norm_scales(S, (int)P, (int)r, partial, inv_nu, inv_nu2, s));
-  // The retraction's iterates X_i = X_0 Q_0 ... Q_{i-1} (X_0 = Y / nu) are
-  // carried in the r x r space: S_i = X_i^T X_i, Q_i = a I + b S_i + c S_i^2,
-  // S_{i+1} = Q_i (S_i Q_i) and P_{i+1} = P_i Q_i, then X_j = X_i P_j: the
-  // same iterates, with r^3 products in place of the d r^2 Gram and apply
-  // products of every step (the Q_i are polynomials in S_i and commute with
-  // it).  Every operand of the fp16 split stays bounded whatever the input:
-  // S_0 / nu^2 and X_0 have spectral norm <= 1, the schedule's quintics map
-  // [0, 1] and then [0, 1.03] into [0, 1.03] (so S_i, S_i Q_i and Q_i stay
-  // below 5), and each quintic p has p(x) <= a x there, so the eigenvalues
-  // p(...)(sigma) / sigma of a product of Q's stay below the product of
-  // their a's.  The steps therefore run in segments whose a's multiply to at
-  // most kSegGrowth (all seven of the paper's schedule: 116); a longer
-  // schedule applies P to X at a segment's end and starts the next from
-  // that X's Gram product.
-  constexpr double kSegGrowth = 200.0;  // < 255, the fp16 split's operand bound
-  const float* Xseg = Y;
-  for (int i = 0; i < retract_steps;) {
-    int j = i;
-    for (double growth = 1.0; j < retract_steps && growth * kRetractCoef[j][0] <= kSegGrowth; ++j)
-      growth *= kRetractCoef[j][0];
-    if (j == i) return fail(MAPL_E_UNSUPPORTED, "stiefel: retraction coefficient above the split bound");
-    if (i > 0) LAUNCH("stiefel:gram", gram(Xseg, nullptr, GEMM_SPLIT_F16));  // S_i = X_i^T X_i
-    const float* Pprev = nullptr;
-    int pq = 0;
-    for (int k = i; k < j; ++k) {
-      const double a = kRetractCoef[k][0], b = kRetractCoef[k][1], cc = kRetractCoef[k][2];
-      const bool first = k == 0;  // S_0 = Y^T Y, scaled by 1/nu^2 inside
-      float* Q = (k & 1) ? Q2 : Qm;
-      LAUNCH("stiefel:poly", poly(a, b, cc, nullptr, first ? inv_nu2 : nullptr, GEMM_SPLIT_F16,
-                                  first ? inv_nu2 : nullptr, Q));
-      if (k == i) {
-        Pprev = Q;
-      } else {
-        LAUNCH("stiefel:ret_p", rmul(Pq[pq], Pprev, Q, nullptr, false));  // P_{k+1} = P_k Q_k
-        Pprev = Pq[pq];
-        pq ^= 1;
-      }
-      if (k + 1 < j) {
-        LAUNCH("stiefel:ret_sq", rmul(Tm, S, Q, first ? inv_nu2 : nullptr, false));  // S_k Q_k
-        LAUNCH("stiefel:ret_s", rmul(S, Q, Tm, nullptr, true));                       // S_{k+1}
-      }
-    }
-    // X_j = X_i P_j (X_0 = Y / nu)
-    float* Xo = j == retract_steps ? U : bufs[cur];
-    LAUNCH("stiefel:apply", apply(Xseg, Xo, nullptr, GEMM_SPLIT_F16, nullptr, i == 0 ? inv_nu : nullptr, Pprev));
-    Xseg = Xo;
-    cur ^= 1;
-    i = j;
-  }
+  if ((st = polar_rr(kRetractCoef, retract_steps, Y, inv_nu, inv_nu2, U, nullptr, nullptr))) return st;
   return MAPL_OK;
 }
 
