@@ -214,6 +214,9 @@ template <typename TO>
 __device__ __forceinline__ void gv_epilogue(const GemmF32Args& g, const f32x16_t (&acc)[2][2], int b, int tbm,
                                             int tbn, int lane, int wm, int wn) {
   const int m0 = tbm * GV_BM + wm * 64, n0 = tbn * GV_BN + wn * 64;
+  const bool second = g.A2 && b >= g.bsplit;  // the second product of a paired launch
+  void* const Cbase = second ? g.C2 : g.C;
+  if (second) b -= g.bsplit;
   const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
   const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
   const bool has_cin = g.Cin && beta != 0.f;
@@ -230,7 +233,7 @@ __device__ __forceinline__ void gv_epilogue(const GemmF32Args& g, const f32x16_t
           cin[i][j][e] = (m < g.M && n < g.N) ? Cin[m * g.sCinm + n * g.sCinn] : 0.f;
         }
   }
-  TO* C = (TO*)g.C + b * g.sCb;
+  TO* C = (TO*)Cbase + b * g.sCb;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -448,10 +451,13 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
   // the products of tile (tbm, tbn) of batch entry b over k-stages [ks0, ks1)
   auto products = [&](int b, int tbm, int tbn, int ks0, int ks1, f32x16_t (&acc)[2][2]) {
   const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
+  // a paired launch's second product: A2 and entry b - bsplit of the rest
+  const bool second = g.A2 && b >= g.bsplit;
+  const int e = second ? b - g.bsplit : b;
   const __amdgpu_buffer_rsrc_t rA =
-      gv_rsrc((const float*)g.A + b * g.sAb,
+      gv_rsrc((const float*)(second ? g.A2 : g.A) + e * g.sAb,
               (AK ? (int64_t)(g.M - 1) * g.sAm + g.K : (int64_t)(g.K - 1) * g.sAk + g.M) * 4);
-  const __amdgpu_buffer_rsrc_t rB = gv_rsrc((const float*)g.B + b * g.sBb, ((int64_t)(g.K - 1) * g.sBk + g.N) * 4);
+  const __amdgpu_buffer_rsrc_t rB = gv_rsrc((const float*)g.B + e * g.sBb, ((int64_t)(g.K - 1) * g.sBk + g.N) * 4);
   typedef Raw4<float>::type raw_t;
   // two register sets: the loads of stages it + 1 and it + 2 are in flight
   // while stage it is multiplied
@@ -477,8 +483,8 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
     }
   };
   // the fp16 split's prescale: 2^8 times the operand's factor for this batch entry
-  const float sa = 256.f * (g.pre_a ? g.pre_a[b] : 1.f);
-  const float sb = 256.f * (g.pre_b ? g.pre_b[b] : 1.f);
+  const float sa = 256.f * (g.pre_a ? g.pre_a[e] : 1.f);
+  const float sb = 256.f * (g.pre_b ? g.pre_b[e] : 1.f);
   // hi and lo pieces of two floats, packed
   auto split2 = [](float x, float y, uint32_t& hi, uint32_t& lo, float sc) {
     const f32x2_t v = (f32x2_t){x, y} * sc;
@@ -658,6 +664,8 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
   if (g.sym_upper && (vm < 0 || g.M != g.N || g.Cin)) return hipErrorInvalidValue;
   if (g.split < 0 || g.split > GEMM_SPLIT_F16) return hipErrorInvalidValue;
   if ((g.pre_a || g.pre_b) && g.split != GEMM_SPLIT_F16) return hipErrorInvalidValue;
+  if (g.A2 && (g.split != GEMM_SPLIT_F16 || !g.C2 || g.sk_part || g.bsplit <= 0 || g.bsplit >= g.batch))
+    return hipErrorInvalidValue;
   if (g.sk_part && !(g.sym_upper && ta == 0 && tb == 0 && to == 0)) return hipErrorInvalidValue;
   const int ntm = (g.M + GV_BM - 1) / GV_BM;
   const dim3 vgrid = g.sk_part      ? dim3(gemm_f32_sk_plan(g.M, g.K, g.batch).nwg)

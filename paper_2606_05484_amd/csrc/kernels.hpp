@@ -50,6 +50,10 @@ struct GemmF32Args {
              // hi.hi + hi.lo + lo.hi of fp16 pieces of 2^8 x (|operands| < 255)
   const float* pre_a; const float* pre_b;  // GEMM_SPLIT_F16 only: per-batch factors of A and B
                                            // (null: 1), applied before the split
+  const void* A2; void* C2; int bsplit;   // GEMM_SPLIT_F16 only, optional: batch entries b >= bsplit
+                                           // multiply A2 and write C2 (their entry b - bsplit), with
+                                           // B, Cin and the per-batch factors of entry b - bsplit: two
+                                           // products that share B in one launch
   int sym_upper;   // C = A B known symmetric (B = A^T, M == N, no Cin): only tiles on or above the
                    // diagonal are computed, each off-diagonal one also written mirrored (aligned case)
   float* sk_part;  // sym_upper, fp32 operands and output: with this workspace (gemm_f32_sk_bytes)

@@ -1051,6 +1051,18 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
 
+  // C1 = A1 Bm and C2 = A2 Bm in one launch (two r x r products sharing Bm)
+  auto rmul2 = [&](float* C1, const float* A1, float* C2o, const float* A2m, const float* Bm) {
+    GemmF32Args g = gemm((int)r, (int)r, (int)r);
+    g.split = GEMM_SPLIT_F16;
+    g.batch = 2 * (int)P;
+    g.bsplit = (int)P;
+    g.A = A1; g.A2 = A2m; g.sAm = r; g.sAk = 1; g.sAb = rr;
+    g.B = Bm; g.sBk = r; g.sBn = 1; g.sBb = rr;
+    g.C = C1; g.C2 = C2o; g.sCm = r; g.sCn = 1; g.sCb = rr;
+    return launch_gemm_f32(g, 0, 0, 0, s);
+  };
+
   // Eq. 4: S = U^T G, sym, g_R = G - U sym(S)  -> X0
   {
     GemmF32Args g = gemm((int)r, (int)r, (int)d);
@@ -1114,17 +1126,20 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
         const float* sp = k == 0 ? spre : nullptr;
         float* Q = (k & 1) ? Q2 : Qm;
         LAUNCH("stiefel:pe_poly", poly(a, b, cc, sp, Q));
-        if (k == i) {
-          Pprev = Q;
-        } else {
-          LAUNCH("stiefel:pe_p", rmul(Pq[pq], Pprev, Q, nullptr, false));  // P_{k+1} = P_k Q_k
+        const bool pprod = k > i, supd = k + 1 < j;  // P_{k+1} = P_k Q_k; S_{k+1} = Q_k (S_k Q_k)
+        if (pprod && supd)  // S_k Q_k and P_k Q_k share Q_k: one launch (sp is null past step 0)
+          LAUNCH("stiefel:pe_sq_p", rmul2(Tm, S, Pq[pq], Pprev, Q));
+        else if (pprod)
+          LAUNCH("stiefel:pe_p", rmul(Pq[pq], Pprev, Q, nullptr, false));
+        else if (supd)
+          LAUNCH("stiefel:pe_sq", rmul(Tm, S, Q, sp, false));
+        if (pprod) {
           Pprev = Pq[pq];
           pq ^= 1;
+        } else {
+          Pprev = Q;  // P_{i+1} = Q_i
         }
-        if (k + 1 < j) {
-          LAUNCH("stiefel:pe_sq", rmul(Tm, S, Q, sp, false));  // S_k Q_k
-          LAUNCH("stiefel:pe_s", rmul(S, Q, Tm, nullptr, true));  // S_{k+1} (symmetric)
-        }
+        if (supd) LAUNCH("stiefel:pe_s", rmul(S, Q, Tm, nullptr, true));  // S_{k+1} (symmetric)
       }
       float* Xo = j == steps && out ? out : other(Xseg);
       LAUNCH("stiefel:pe_apply", apply(Xseg, i == 0 ? xpre : nullptr, Pprev, Xo, j == steps ? Yin : nullptr));
