@@ -130,8 +130,9 @@ constexpr int GV_BM = 128, GV_BN = 128, GV_BK = 32;
 // read once from HBM instead of once per XCD).  Otherwise the grid's
 // (x, y, z).  With sym_upper the tiles are those on or above the diagonal of
 // an nt x nt tile grid, row by row.
+template <int BT = GV_BM>
 __device__ __forceinline__ void gv_tile(const GemmF32Args& g, int& bm, int& bn, int& b) {
-  const int ntm = (g.M + 127) / 128, ntn = (g.N + 127) / 128;
+  const int ntm = (g.M + BT - 1) / BT, ntn = (g.N + BT - 1) / BT;
   const int T = g.sym_upper ? ntm * (ntm + 1) / 2 : ntm * ntn;
   int t;
   if (g.batch % 8 == 0) {
@@ -204,29 +205,30 @@ __device__ __forceinline__ void sk_run(const GemmF32Args& g, F&& products, int t
   }
 }
 
-// The epilogue of the aligned kernels for one wave's 64 x 64 block of tile
-// (tbm, tbn): C = alpha acc + beta Cin, plus diag where m == n, and the
-// mirrored element of an off-diagonal tile of a symmetric product.  Cin is
+// The epilogue of the aligned kernels for one wave's 32F x 32F block of
+// tile (tbm, tbn) (tiles of 64F x 64F, 2 x 2 waves): C = alpha acc +
+// beta Cin, plus diag where m == n, and the mirrored element of an
+// off-diagonal tile of a symmetric product.  Cin is
 // read in full before the first store: C may alias Cin as far as the
 // compiler knows, which would otherwise hold every load behind the store
 // before it.
-template <typename TO>
-__device__ __forceinline__ void gv_epilogue(const GemmF32Args& g, const f32x16_t (&acc)[2][2], int b, int tbm,
+template <typename TO, int F = 2>
+__device__ __forceinline__ void gv_epilogue(const GemmF32Args& g, const f32x16_t (&acc)[F][F], int b, int tbm,
                                             int tbn, int lane, int wm, int wn) {
-  const int m0 = tbm * GV_BM + wm * 64, n0 = tbn * GV_BN + wn * 64;
+  const int m0 = (tbm * 2 + wm) * 32 * F, n0 = (tbn * 2 + wn) * 32 * F;
   const bool second = g.A2 && b >= g.bsplit;  // the second product of a paired launch
   void* const Cbase = second ? g.C2 : g.C;
   if (second) b -= g.bsplit;
   const float alpha = g.alpha * (g.alpha_ptr ? g.alpha_ptr[b] : 1.f);
   const float beta = g.beta * (g.beta_ptr ? g.beta_ptr[b] : 1.f);
   const bool has_cin = g.Cin && beta != 0.f;
-  float cin[2][2][16];
+  float cin[F][F][16];
   if (has_cin) {
     const float* Cin = g.Cin + b * g.sCinb;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < F; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < F; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int m = m0 + i * 32 + acc_row(e, lane), n = n0 + j * 32 + (lane & 31);
@@ -235,9 +237,9 @@ __device__ __forceinline__ void gv_epilogue(const GemmF32Args& g, const f32x16_t
   }
   TO* C = (TO*)Cbase + b * g.sCb;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < F; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < F; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int m = m0 + i * 32 + acc_row(e, lane), n = n0 + j * 32 + (lane & 31);
@@ -435,22 +437,29 @@ __global__ __launch_bounds__(GF_THREADS) void k_gemm_f32v(GemmF32Args g) {
 //    k, chunk-swizzled by wg_sw), written 8 bytes per lane along the row and
 //    read with transposing LDS reads (tr_frag).
 constexpr int GX_LD = GV_BK + 8;  // 16-bit pieces per row of a [row][k] tile
-constexpr int GX_CPR = GV_BM / 8;  // 16-byte chunks per k of a [k][row] tile
+constexpr int X3_SMALL_BELOW = 512;  // 128-tile workgroups under which the split kernel takes 64 x 64 tiles
 
-template <bool AK>
-__global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_gemm_x3(GemmF32Args g) {
+template <bool AK, int BT>
+__global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(256 / BT, 256 / BT))) void k_gemm_x3(
+    GemmF32Args g) {
+  static_assert(BT == 128 || BT == 64, "tiles of 128 x 128 or 64 x 64");
+  constexpr int F = BT / 64;        // 32 x 32 blocks per wave and dimension (wave tile BT/2 square)
+  constexpr int CPR = BT / 8;       // 16-byte chunks per k of a [k][row] tile
+  constexpr int KPT = 4 * BT / 128; // k per thread of a [k][row] operand's stage (4 column quads each)
+  constexpr int TPR = 256 / BT;     // threads per row of a k-contiguous A's stage
+  constexpr int KQ = BT / 32;       // 4-float loads per thread and stage of a k-contiguous A
   // [row][k] tiles (k-contiguous A) or [k][row] tiles (the rest), per buffer and piece
-  constexpr int A_ELEMS = AK ? GV_BM * GX_LD : GV_BK * GV_BM;
+  constexpr int A_ELEMS = AK ? BT * GX_LD : GV_BK * BT;
   __shared__ __attribute__((aligned(16))) bf16_t Ah[2][A_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t Al[2][A_ELEMS];
-  __shared__ __attribute__((aligned(16))) bf16_t Bh[2][GV_BK * GV_BN];
-  __shared__ __attribute__((aligned(16))) bf16_t Bl[2][GV_BK * GV_BN];
+  __shared__ __attribute__((aligned(16))) bf16_t Bh[2][GV_BK * BT];
+  __shared__ __attribute__((aligned(16))) bf16_t Bl[2][GV_BK * BT];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, 64 x 64 each
+  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, BT/2 x BT/2 each
   const int nk = (g.K + GV_BK - 1) / GV_BK;
   // the products of tile (tbm, tbn) of batch entry b over k-stages [ks0, ks1)
-  auto products = [&](int b, int tbm, int tbn, int ks0, int ks1, f32x16_t (&acc)[2][2]) {
-  const int m0 = tbm * GV_BM, n0 = tbn * GV_BN;
+  auto products = [&](int b, int tbm, int tbn, int ks0, int ks1, f32x16_t (&acc)[F][F]) {
+  const int m0 = tbm * BT, n0 = tbn * BT;
   // a paired launch's second product: A2 and entry b - bsplit of the rest
   const bool second = g.A2 && b >= g.bsplit;
   const int e = second ? b - g.bsplit : b;
@@ -462,22 +471,22 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
   // two register sets: the loads of stages it + 1 and it + 2 are in flight
   // while stage it is multiplied
   raw_t ra0[4], rb0[4], ra1[4], rb1[4];
-  // B (and an m-contiguous A): thread t loads rows 4 (t % 32) + 0..3 at
-  // k = 4 (t / 32) + 0..3, one 16-byte piece per k; a k-contiguous A: row
-  // t / 2, k = 16 (t % 2) + 0..15
+  // B (and an m-contiguous A): thread t loads rows 4 (t % (BT/4)) + 0..3 at
+  // k = KPT (t / (BT/4)) + 0..KPT-1, one 16-byte piece per k; a
+  // k-contiguous A: row t / TPR, k = 4 KQ (t % TPR) + 0..4 KQ-1
   auto load = [&](int k0, raw_t (&ra)[4], raw_t (&rb)[4]) {
-    const int kb = k0 + 4 * (tid >> 5), c = 4 * (tid & 31);
+    const int kb = k0 + KPT * (tid / (BT / 4)), c = 4 * (tid % (BT / 4));
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
+    for (int h = 0; h < KPT; ++h) {
       const int k = kb + h;
       rb[h] = Raw4<float>::load(rB, (k < g.K && n0 + c < g.N) ? (uint32_t)(((int64_t)k * g.sBk + n0 + c) * 4) : GV_OOB);
       if constexpr (!AK)
         ra[h] = Raw4<float>::load(rA, (k < g.K && m0 + c < g.M) ? (uint32_t)(((int64_t)k * g.sAk + m0 + c) * 4) : GV_OOB);
     }
     if constexpr (AK) {
-      const int m = m0 + (tid >> 1), k = k0 + 16 * (tid & 1);
+      const int m = m0 + tid / TPR, k = k0 + 4 * KQ * (tid % TPR);
 #pragma unroll
-      for (int h = 0; h < 4; ++h)
+      for (int h = 0; h < KQ; ++h)
         ra[h] = Raw4<float>::load(rA, (m < g.M && k + 4 * h < g.K) ? (uint32_t)(((int64_t)m * g.sAm + k + 4 * h) * 4)
                                                                     : GV_OOB);
     }
@@ -493,12 +502,12 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
     lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(v - __builtin_convertvector(h, f32x2_t), f16x2_t));
   };
   auto mma = [](const u32x4& a, const u32x4& b, f32x16_t c) { return mfma32x32x16h(as_uint4(a), as_uint4(b), c); };
-  // 4 consecutive rows at 4 consecutive k (v[h]: k = h) into a [k][row] tile
+  // 4 consecutive rows at KPT consecutive k (v[h]: k = h) into a [k][row] tile
   auto put_kmajor = [&](bf16_t* H, bf16_t* Lo, const raw_t (&v)[4], int row0, int kk, float sc) {
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
+    for (int h = 0; h < KPT; ++h) {
       const int k = kk + h;
-      const int off = k * GX_CPR * 8 + (((row0 >> 3) ^ wg_sw(k, GX_CPR)) << 3) + (row0 & 7);
+      const int off = k * CPR * 8 + (((row0 >> 3) ^ wg_sw(k, CPR)) << 3) + (row0 & 7);
       uint32_t h0, l0, h1, l1;
       split2(__uint_as_float(v[h][0]), __uint_as_float(v[h][1]), h0, l0, sc);
       split2(__uint_as_float(v[h][2]), __uint_as_float(v[h][3]), h1, l1, sc);
@@ -507,31 +516,32 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
     }
   };
   auto store = [&](int buf, const raw_t (&ra)[4], const raw_t (&rb)[4]) {
-    const int kk = 4 * (tid >> 5), c = 4 * (tid & 31);
+    const int kk = KPT * (tid / (BT / 4)), c = 4 * (tid % (BT / 4));
     put_kmajor(Bh[buf], Bl[buf], rb, c, kk, sb);
     if constexpr (!AK) {
       put_kmajor(Ah[buf], Al[buf], ra, c, kk, sa);
     } else {
-      const int m = tid >> 1, k = 16 * (tid & 1);
-      uint32_t hv[8], lv[8];
+      const int m = tid / TPR, k = 4 * KQ * (tid % TPR);
+      uint32_t hv[2 * KQ], lv[2 * KQ];
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
+      for (int h = 0; h < KQ; ++h) {
         split2(__uint_as_float(ra[h][0]), __uint_as_float(ra[h][1]), hv[2 * h], lv[2 * h], sa);
         split2(__uint_as_float(ra[h][2]), __uint_as_float(ra[h][3]), hv[2 * h + 1], lv[2 * h + 1], sa);
       }
       bf16_t* H = Ah[buf] + m * GX_LD + k;
       bf16_t* Lo = Al[buf] + m * GX_LD + k;
-      *(uint4*)H = make_uint4(hv[0], hv[1], hv[2], hv[3]);
-      *(uint4*)(H + 8) = make_uint4(hv[4], hv[5], hv[6], hv[7]);
-      *(uint4*)Lo = make_uint4(lv[0], lv[1], lv[2], lv[3]);
-      *(uint4*)(Lo + 8) = make_uint4(lv[4], lv[5], lv[6], lv[7]);
+#pragma unroll
+      for (int q = 0; q < KQ / 2; ++q) {
+        *(uint4*)(H + 8 * q) = make_uint4(hv[4 * q], hv[4 * q + 1], hv[4 * q + 2], hv[4 * q + 3]);
+        *(uint4*)(Lo + 8 * q) = make_uint4(lv[4 * q], lv[4 * q + 1], lv[4 * q + 2], lv[4 * q + 3]);
+      }
     }
   };
 
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < F; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+    for (int j = 0; j < F; ++j) acc[i][j] = f32x16_t{};
 
   // stage it: request stage it + 2 into (la, lb), multiply the LDS buffer of
   // stage it, write stage it + 1 from (sa, sb) into the other buffer (last
@@ -541,31 +551,31 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
     if (it + 2 < ks1) load((it + 2) * GV_BK, la, lb);
 #pragma unroll
     for (int ks = 0; ks < GV_BK / 16; ++ks) {
-      u32x4 f[8];  // ah0 ah1 al0 al1 bh0 bh1 bl0 bl1
+      u32x4 f[4 * F];  // a hi [F], a lo [F], b hi [F], b lo [F]
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < F; ++i) {
         if constexpr (AK) {
-          const int row = wm * 64 + i * 32 + (lane & 31), kc = 16 * ks + 8 * (lane >> 5);
+          const int row = wm * 32 * F + i * 32 + (lane & 31), kc = 16 * ks + 8 * (lane >> 5);
           f[i] = *(const u32x4*)(Ah[buf] + row * GX_LD + kc);
-          f[2 + i] = *(const u32x4*)(Al[buf] + row * GX_LD + kc);
+          f[F + i] = *(const u32x4*)(Al[buf] + row * GX_LD + kc);
         } else {
-          f[i] = tr_frag(Ah[buf], GX_CPR, 16 * ks, wm * 64 + i * 32, lane);
-          f[2 + i] = tr_frag(Al[buf], GX_CPR, 16 * ks, wm * 64 + i * 32, lane);
+          f[i] = tr_frag(Ah[buf], CPR, 16 * ks, wm * 32 * F + i * 32, lane);
+          f[F + i] = tr_frag(Al[buf], CPR, 16 * ks, wm * 32 * F + i * 32, lane);
         }
       }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        f[4 + j] = tr_frag(Bh[buf], GX_CPR, 16 * ks, wn * 64 + j * 32, lane);
-        f[6 + j] = tr_frag(Bl[buf], GX_CPR, 16 * ks, wn * 64 + j * 32, lane);
+      for (int j = 0; j < F; ++j) {
+        f[2 * F + j] = tr_frag(Bh[buf], CPR, 16 * ks, wn * 32 * F + j * 32, lane);
+        f[3 * F + j] = tr_frag(Bl[buf], CPR, 16 * ks, wn * 32 * F + j * 32, lane);
       }
       lds_wait(f);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < F; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          acc[i][j] = mma(f[2 + i], f[4 + j], acc[i][j]);
-          acc[i][j] = mma(f[i], f[6 + j], acc[i][j]);
-          acc[i][j] = mma(f[i], f[4 + j], acc[i][j]);
+        for (int j = 0; j < F; ++j) {
+          acc[i][j] = mma(f[F + i], f[2 * F + j], acc[i][j]);
+          acc[i][j] = mma(f[i], f[3 * F + j], acc[i][j]);
+          acc[i][j] = mma(f[i], f[2 * F + j], acc[i][j]);
         }
     }
     if (it + 1 < ks1) store(buf ^ 1, sa_, sb_);
@@ -580,20 +590,22 @@ __global__ __launch_bounds__(GF_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2
     if (it + 1 < ks1) stage(it + 1, ra1, rb1, ra0, rb0);
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < F; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] *= 1.f / 65536.f;
+    for (int j = 0; j < F; ++j) acc[i][j] *= 1.f / 65536.f;
   };
 
-  if (g.sk_part) {
-    sk_run(g, products, tid);
-    return;
+  if constexpr (BT == GV_BM) {
+    if (g.sk_part) {
+      sk_run(g, products, tid);
+      return;
+    }
   }
   int tbm, tbn, b;
-  gv_tile(g, tbm, tbn, b);
-  f32x16_t acc[2][2];
+  gv_tile<BT>(g, tbm, tbn, b);
+  f32x16_t acc[F][F];
   products(b, tbm, tbn, 0, nk, acc);
-  gv_epilogue<float>(g, acc, b, tbm, tbn, lane, wm, wn);
+  gv_epilogue<float, F>(g, acc, b, tbm, tbn, lane, wm, wn);
 }
 
 // The stream-K fix-up: one workgroup per (tile, wave quarter), one wave per
@@ -678,8 +690,21 @@ hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStre
   };
   if (g.split && (vm < 0 || ta || tb || to)) return hipErrorInvalidValue;
   if (g.split == GEMM_SPLIT_F16) {
-    if (vm) hipLaunchKernelGGL((k_gemm_x3<true>), vgrid, dim3(GF_THREADS), 0, s, g);
-    else hipLaunchKernelGGL((k_gemm_x3<false>), vgrid, dim3(GF_THREADS), 0, s, g);
+    // 64 x 64 tiles where 128 x 128 ones would give fewer than X3_SMALL_BELOW
+    // workgroups: such launches are bound by one workgroup's latency, and
+    // four times the workgroups hide it better than the larger tiles' fewer
+    // LDS bytes per product help
+    const int ntn = (g.N + GV_BN - 1) / GV_BN;
+    const int64_t t128 = (int64_t)(g.sym_upper ? ntm * (ntm + 1) / 2 : ntm * ntn) * g.batch;
+    if (!g.sk_part && t128 < X3_SMALL_BELOW) {
+      const int m64 = (g.M + 63) / 64, n64 = (g.N + 63) / 64;
+      const dim3 grid64 = g.sym_upper ? dim3(m64 * (m64 + 1) / 2, 1, g.batch) : dim3(m64, n64, g.batch);
+      if (vm) hipLaunchKernelGGL((k_gemm_x3<true, 64>), grid64, dim3(GF_THREADS), 0, s, g);
+      else hipLaunchKernelGGL((k_gemm_x3<false, 64>), grid64, dim3(GF_THREADS), 0, s, g);
+      return hipGetLastError();
+    }
+    if (vm) hipLaunchKernelGGL((k_gemm_x3<true, GV_BM>), vgrid, dim3(GF_THREADS), 0, s, g);
+    else hipLaunchKernelGGL((k_gemm_x3<false, GV_BM>), vgrid, dim3(GF_THREADS), 0, s, g);
     const hipError_t e = hipGetLastError();
     return e != hipSuccess ? e : sk_fix();
   }
