@@ -207,10 +207,12 @@ int mapl_encode_bwd(const mapl_codec_desc* desc, const void* dZ, const void* X,
  *         |Y^T Y| (an upper bound of sigma_max(Y)^2)                (Eq. 7)
  * PolarExpress step: X <- a X + X (b S + c S^2), S = X^T X, with the greedy
  * minimax odd-quintic schedule designed for singular values in [1e-3, 1]
- * (LMO) and [0.5, 1] (retraction).  Every product is fp32 except those of
- * the LMO's iterations, which multiply split-bf16 operands (each fp32 value
- * as bf16 hi + bf16 lo, three products, fp32 accumulation: about 3e-5
- * relative error in the direction D; the retraction and U stay fp32).
+ * (LMO) and [0.5, 1] (retraction).  Eq. 4 and Y^T Y are fp32 products; the
+ * PolarExpress iterates are computed as X_0 times a product of the steps'
+ * r x r polynomials, whose products multiply fp16 pieces of fp32 values
+ * (hi + lo of 2^8 x, three products, fp32 accumulation: fp32's accuracy;
+ * every operand is bounded by construction, for any U, G and M).  The
+ * workspace (mapl_workspace_bytes, MAPL_CALL_STIEFEL) holds the iterates.
  * Requirements: 1 <= P, 32 <= r <= d,
  * r multiple of 32, d multiple of 32, r <= 1024, 1 <= lmo_steps,
  * retract_steps <= 16.  The retraction is accurate while lr*||D||_2 <= 1/3. */
