@@ -138,15 +138,26 @@ def test_step_far_off_the_manifold():
     assert _orth_err(Un) <= 1e-5
 
 
-def test_long_retraction_schedule():
-    """Twelve retraction steps: more than one segment of the r x r iteration
-    (the a's of a segment multiply to at most 200), so the retraction applies
-    its product of Q's to X, takes that X's Gram product and goes on."""
+def test_long_schedules():
+    """Eight LMO and twelve retraction steps: more than one segment of the
+    r x r iteration in both (the a's of a segment multiply to at most 200),
+    so each forms X from its product of Q's at a segment's end, takes that
+    X's Gram product and goes on."""
     st = synth.stiefel_inputs(None, seed=81, P=2, d=512, r=128, gscale=1.0, lr=1e-2, beta=0.95, steps=1)
     U, G, M = st["U"], st["G"], st["M"]
-    Un, Mn = _gpu_step(U, G, M, st["lr"], st["beta"], lmo=5, ret=12)
-    Ur, Mr = spel.stiefel_step_batched(U, G, M, st["lr"], st["beta"], mode="pe", lmo_steps=5, retract_steps=12)
+    Un, Mn = _gpu_step(U, G, M, st["lr"], st["beta"], lmo=8, ret=12)
+    Ur, Mr = spel.stiefel_step_batched(U, G, M, st["lr"], st["beta"], mode="pe", lmo_steps=8, retract_steps=12)
     e_u, e_m, du = rel_fro(Un, Ur), rel_fro(Mn, Mr), rel_fro(Un - U, Ur - U)
-    print("12 retraction steps: U rel err", e_u, "M rel err", e_m, "dU rel err", du, "orth", _orth_err(Un))
+    print("8 LMO + 12 retraction steps: U rel err", e_u, "M rel err", e_m, "dU rel err", du, "orth", _orth_err(Un))
     assert e_u <= 1e-5 and e_m <= 1e-5 and du <= DU_TOL
     assert _orth_err(Un) <= 1e-5
+
+
+def test_step_is_reproducible():
+    """Two calls on the same state give bitwise equal U and M: every
+    reduction (the stream-K fix-up included) runs in a fixed order."""
+    st = synth.stiefel_inputs("c5")
+    U, G, M = st["U"], st["G"], st["M"]
+    a = _gpu_step(U, G, M, st["lr"], st["beta"])
+    b = _gpu_step(U, G, M, st["lr"], st["beta"])
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
