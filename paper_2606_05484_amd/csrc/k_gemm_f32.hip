@@ -673,7 +673,8 @@ int gemm_f32_vec_mode(const GemmF32Args& g, int ta, int tb) {
 hipError_t launch_gemm_f32(const GemmF32Args& g, int ta, int tb, int to, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0 || g.batch <= 0) return hipSuccess;
   const int vm = gemm_f32_vec_mode(g, ta, tb);
-  if (g.sym_upper && (vm < 0 || g.M != g.N || g.Cin)) return hipErrorInvalidValue;
+  if (g.sym_upper && (vm < 0 || g.M != g.N)) return hipErrorInvalidValue;
+  if (g.sk_part && g.Cin) return hipErrorInvalidValue;  // the fix-up applies no Cin
   if (g.split < 0 || g.split > GEMM_SPLIT_F16) return hipErrorInvalidValue;
   if ((g.pre_a || g.pre_b) && g.split != GEMM_SPLIT_F16) return hipErrorInvalidValue;
   if (g.A2 && (g.split != GEMM_SPLIT_F16 || !g.C2 || g.sk_part || g.bsplit <= 0 || g.bsplit >= g.batch))

@@ -54,8 +54,9 @@ struct GemmF32Args {
                                            // multiply A2 and write C2 (their entry b - bsplit), with
                                            // B, Cin and the per-batch factors of entry b - bsplit: two
                                            // products that share B in one launch
-  int sym_upper;   // C = A B known symmetric (B = A^T, M == N, no Cin): only tiles on or above the
-                   // diagonal are computed, each off-diagonal one also written mirrored (aligned case)
+  int sym_upper;   // C = A B known symmetric (M == N; Cin, if any, symmetric too): only tiles on or
+                   // above the diagonal are computed, each off-diagonal one also written mirrored
+                   // (aligned case)
   float* sk_part;  // sym_upper, fp32 operands and output: with this workspace (gemm_f32_sk_bytes)
                    // the tiles' K ranges are split evenly over two workgroups per CU (stream-K) and
                    // a second launch sums each tile's pieces in K order

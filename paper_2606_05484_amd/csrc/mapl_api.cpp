@@ -1007,10 +1007,12 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.sk_part = skp;  // split over two workgroups per CU where the upper tiles are fewer
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  // Qo = a I + b S' + c S' S' with S' = sp S (sp: a per-projector factor, or none)
+  // Qo = a I + b S' + c S' S' with S' = sp S (sp: a per-projector factor, or
+  // none); symmetric, like every r x r product of the iteration below
   auto poly = [&](double a, double b, double cc, const float* sp, float* Qo) {
     GemmF32Args g = gemm((int)r, (int)r, (int)r);
     g.split = GEMM_SPLIT_F16;
+    g.sym_upper = 1;
     g.pre_a = g.pre_b = sp;
     g.batch = (int)P;
     g.A = S; g.sAm = r; g.sAk = 1; g.sAb = rr;
@@ -1051,10 +1053,11 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
 
-  // C1 = A1 Bm and C2 = A2 Bm in one launch (two r x r products sharing Bm)
+  // C1 = A1 Bm and C2 = A2 Bm in one launch (two symmetric r x r products sharing Bm)
   auto rmul2 = [&](float* C1, const float* A1, float* C2o, const float* A2m, const float* Bm) {
     GemmF32Args g = gemm((int)r, (int)r, (int)r);
     g.split = GEMM_SPLIT_F16;
+    g.sym_upper = 1;
     g.batch = 2 * (int)P;
     g.bsplit = (int)P;
     g.A = A1; g.A2 = A2m; g.sAm = r; g.sAk = 1; g.sAb = rr;
@@ -1127,12 +1130,15 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
         float* Q = (k & 1) ? Q2 : Qm;
         LAUNCH("stiefel:pe_poly", poly(a, b, cc, sp, Q));
         const bool pprod = k > i, supd = k + 1 < j;  // P_{k+1} = P_k Q_k; S_{k+1} = Q_k (S_k Q_k)
+        // S_k, Q_k and P_k are polynomials in the segment's first S, so they
+        // commute and every product here is symmetric: each computes the
+        // tiles on and above the diagonal and mirrors them
         if (pprod && supd)  // S_k Q_k and P_k Q_k share Q_k: one launch (sp is null past step 0)
           LAUNCH("stiefel:pe_sq_p", rmul2(Tm, S, Pq[pq], Pprev, Q));
         else if (pprod)
-          LAUNCH("stiefel:pe_p", rmul(Pq[pq], Pprev, Q, nullptr, false));
+          LAUNCH("stiefel:pe_p", rmul(Pq[pq], Pprev, Q, nullptr, true));
         else if (supd)
-          LAUNCH("stiefel:pe_sq", rmul(Tm, S, Q, sp, false));
+          LAUNCH("stiefel:pe_sq", rmul(Tm, S, Q, sp, true));
         if (pprod) {
           Pprev = Pq[pq];
           pq ^= 1;
