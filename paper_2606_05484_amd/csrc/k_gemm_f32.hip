@@ -1,9 +1,11 @@
-// Batched strided GEMM on the fp32 matrix units (v_mfma_f32_32x32x2_f32):
+// Batched strided GEMM with fp32 results:
 //   C[b](m,n) = alpha_b * sum_k A[b](m,k) B[b](k,n) + beta_b * Cin[b](m,n)
-// with alpha_b = alpha * (alpha_ptr ? alpha_ptr[b] : 1), likewise beta.
-// Operands may be fp32 or bf16 (widened exactly to fp32 in LDS); any
-// element strides, so transposed operands need no copies.  This kernel
-// carries every product of the Stiefel step and the fp32 codec path.
+// with alpha_b = alpha * (alpha_ptr ? alpha_ptr[b] : 1), likewise beta, on
+// the fp32 matrix units (v_mfma_f32_32x32x2_f32) or, for fp32 operands with
+// GEMM_SPLIT_F16, as products of fp16 pieces on the 16-bit matrix units
+// (k_gemm_x3).  Operands may be fp32 or bf16 (widened exactly to fp32 in
+// LDS); any element strides, so transposed operands need no copies.  These
+// kernels carry every product of the Stiefel step and the fp32 codec path.
 #include "common.hpp"
 #include "kernels.hpp"
 
