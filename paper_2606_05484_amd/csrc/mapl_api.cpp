@@ -1007,8 +1007,9 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.sk_part = skp;  // split over two workgroups per CU where the upper tiles are fewer
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  // Qo = a I + b S' + c S' S' with S' = sp S (sp: a per-projector factor, or
-  // none); symmetric, like every r x r product of the iteration below
+  // Qo = (a I + b S' + c S' S') / a with S' = sp S (sp: a per-projector
+  // factor, or none); symmetric, like every r x r product of the iteration
+  // below
   auto poly = [&](double a, double b, double cc, const float* sp, float* Qo) {
     GemmF32Args g = gemm((int)r, (int)r, (int)r);
     g.split = GEMM_SPLIT_F16;
@@ -1019,13 +1020,13 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.B = S; g.sBk = r; g.sBn = 1; g.sBb = rr;
     g.Cin = S; g.sCinm = r; g.sCinn = 1; g.sCinb = rr;
     g.C = Qo; g.sCm = r; g.sCn = 1; g.sCb = rr;
-    g.alpha = (float)cc; g.beta = (float)b; g.diag = (float)a;
+    g.alpha = (float)(cc / a); g.beta = (float)(b / a); g.diag = 1.f;
     g.beta_ptr = sp;
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
-  // Xo = X' Bm with X' = pre X, or with Yin: Xo = Yin - lr X' Bm (the LMO's
-  // last product and Eq. 7's argument U - lr D in one launch)
-  auto apply = [&](const float* X, const float* pre, const float* Bm, float* Xo, const float* Yin) {
+  // Xo = alpha X' Bm with X' = pre X, or with Yin: Xo = Yin - lr alpha X' Bm
+  // (the LMO's last product and Eq. 7's argument U - lr D in one launch)
+  auto apply = [&](const float* X, const float* pre, const float* Bm, float* Xo, const float* Yin, double alpha) {
     GemmF32Args g = gemm((int)d, (int)r, (int)r);
     g.split = GEMM_SPLIT_F16;
     g.pre_a = pre;
@@ -1033,17 +1034,19 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     g.A = X; g.sAm = r; g.sAk = 1; g.sAb = n;
     g.B = Bm; g.sBk = r; g.sBn = 1; g.sBb = rr;
     g.C = Xo; g.sCm = r; g.sCn = 1; g.sCb = n;
+    g.alpha = (float)alpha;
     if (Yin) {
       g.Cin = Yin; g.sCinm = r; g.sCinn = 1; g.sCinb = n; g.beta = 1.f;
-      g.alpha = -lr;
+      g.alpha = (float)(-lr * alpha);
     }
     return launch_gemm_f32(g, 0, 0, 0, s);
   };
   // Co = (A scaled by pre inside) B for r x r factors, fp16 split; sym: the
   // product is symmetric (upper tiles computed, mirrored)
-  auto rmul = [&](float* Co, const float* Am, const float* Bm, const float* pre, bool sym) {
+  auto rmul = [&](float* Co, const float* Am, const float* Bm, const float* pre, bool sym, double alpha = 1.0) {
     GemmF32Args g = gemm((int)r, (int)r, (int)r);
     g.split = GEMM_SPLIT_F16;
+    g.alpha = (float)alpha;
     g.pre_a = pre;
     g.sym_upper = sym ? 1 : 0;
     g.batch = (int)P;
@@ -1099,19 +1102,22 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
   // P_{i+1} = P_i Q_i, and X_j = X_i P_j -- the same iterates, with r^3
   // products in place of each step's d r^2 Gram and apply products (the Q_i
   // are polynomials in S_i and commute with it).  Every product runs in the
-  // fp16 split, whose operands must stay below 255: X_0 has spectral norm
-  // <= 1 (M / (||M||_F + eps), Y / nu), both schedules keep the singular
-  // values below 2.1 (so X, S, S Q and Q stay below 9), and each quintic p
-  // has |p(x)| <= a x on the values it meets, so the eigenvalues
-  // p(...)(sigma) / sigma of a product of Q's stay below the product of
-  // their a's.  The steps run in segments whose a's multiply to at most
-  // kSegGrowth; at a segment's end X_j = X_i P_j is formed and the next
-  // segment starts from its Gram product.  On entry S holds X_0^T X_0
-  // divided by spre (the first step's products scale it by spre inside, null:
-  // 1); X_0 is Xs scaled by xpre inside its one product.  X_K, or
-  // Yin - lr X_K, goes to out (null: the X buffer not read last), and
-  // *written names the buffer.
-  constexpr double kSegGrowth = 200.0;  // < 255, the fp16 split's operand bound
+  // fp16 split, whose operands must stay below 255, and the factors carry
+  // Q~_i = Q_i / a_i, P~ = Q~_i ... Q~_{j-1}, with S_{i+1} = a_i^2 Q~_i (S_i Q~_i)
+  // and X_j = (a_i ... a_{j-1}) X_i P~: X_0 has spectral norm <= 1
+  // (M / (||M||_F + eps), Y / nu), both schedules keep every singular value
+  // below 2.1 (so X, S and S Q~ stay below 5), and each quintic p has
+  // |p(x)| <= a x on the values it meets, so Q~ and P~ have eigenvalues in
+  // [-1, 1].  A segment runs while its a's multiply to at most kSegGrowth,
+  // which keeps P~'s entries for the unit singular values above 2^-11 (the
+  // fp16 split's full-precision range; the paper's schedules, 5 and 7
+  // steps, are one segment each: 1043 and 116); a longer schedule forms
+  // X_j = X_i P_j at a segment's end and starts the next from X_j's Gram
+  // product.  On entry S holds X_0^T X_0 divided by spre (the first step's
+  // products scale it by spre inside, null: 1); X_0 is Xs scaled by xpre
+  // inside its one product.  X_K, or Yin - lr X_K, goes to out (null: the X
+  // buffer not read last), and *written names the buffer.
+  constexpr double kSegGrowth = 2048.0;
   float* bufs[2] = {X0, X1};
   auto other = [&](const float* p) { return p == bufs[0] ? bufs[1] : bufs[0]; };
   auto polar_rr = [&](const double (*coef)[3], int steps, const float* Xs, const float* xpre, const float* spre,
@@ -1119,8 +1125,8 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
     const float* Xseg = Xs;
     for (int i = 0; i < steps;) {
       int j = i;
-      for (double growth = 1.0; j < steps && growth * coef[j][0] <= kSegGrowth; ++j) growth *= coef[j][0];
-      if (j == i) return fail(MAPL_E_UNSUPPORTED, "stiefel: PolarExpress coefficient above the split bound");
+      double growth = 1.0;
+      for (; j < steps && (j == i || growth * coef[j][0] <= kSegGrowth); ++j) growth *= coef[j][0];
       if (i > 0) LAUNCH("stiefel:pe_gram", gram(Xseg, GEMM_SPLIT_F16, nullptr));  // S_i = X_i^T X_i
       const float* Pprev = nullptr;
       int pq = 0;
@@ -1128,12 +1134,12 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
         const double a = coef[k][0], b = coef[k][1], cc = coef[k][2];
         const float* sp = k == 0 ? spre : nullptr;
         float* Q = (k & 1) ? Q2 : Qm;
-        LAUNCH("stiefel:pe_poly", poly(a, b, cc, sp, Q));
-        const bool pprod = k > i, supd = k + 1 < j;  // P_{k+1} = P_k Q_k; S_{k+1} = Q_k (S_k Q_k)
-        // S_k, Q_k and P_k are polynomials in the segment's first S, so they
+        LAUNCH("stiefel:pe_poly", poly(a, b, cc, sp, Q));  // Q~_k
+        const bool pprod = k > i, supd = k + 1 < j;  // P~ <- P~ Q~_k; S_{k+1} = a^2 Q~_k (S_k Q~_k)
+        // S_k, Q~_k and P~ are polynomials in the segment's first S, so they
         // commute and every product here is symmetric: each computes the
         // tiles on and above the diagonal and mirrors them
-        if (pprod && supd)  // S_k Q_k and P_k Q_k share Q_k: one launch (sp is null past step 0)
+        if (pprod && supd)  // S_k Q~_k and P~ Q~_k share Q~_k: one launch (sp is null past step 0)
           LAUNCH("stiefel:pe_sq_p", rmul2(Tm, S, Pq[pq], Pprev, Q));
         else if (pprod)
           LAUNCH("stiefel:pe_p", rmul(Pq[pq], Pprev, Q, nullptr, true));
@@ -1143,12 +1149,13 @@ extern "C" int mapl_stiefel_step(int64_t P, int64_t d, int64_t r, float* U, cons
           Pprev = Pq[pq];
           pq ^= 1;
         } else {
-          Pprev = Q;  // P_{i+1} = Q_i
+          Pprev = Q;  // P~ = Q~_i
         }
-        if (supd) LAUNCH("stiefel:pe_s", rmul(S, Q, Tm, nullptr, true));  // S_{k+1} (symmetric)
+        if (supd) LAUNCH("stiefel:pe_s", rmul(S, Q, Tm, nullptr, true, a * a));  // S_{k+1} (symmetric)
       }
       float* Xo = j == steps && out ? out : other(Xseg);
-      LAUNCH("stiefel:pe_apply", apply(Xseg, i == 0 ? xpre : nullptr, Pprev, Xo, j == steps ? Yin : nullptr));
+      LAUNCH("stiefel:pe_apply",
+             apply(Xseg, i == 0 ? xpre : nullptr, Pprev, Xo, j == steps ? Yin : nullptr, growth));
       Xseg = Xo;
       i = j;
     }
