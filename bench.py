@@ -559,8 +559,8 @@ def spel_step_timing(torch, mapl, synth, P, dd, rr, reps):
 
 # Segments of the r x r PolarExpress iteration at the 5 / 7 schedule the
 # bench runs (consecutive steps whose linear coefficients multiply to at
-# most 200): the LMO in 3 + 2 steps, the retraction in one segment of 7.
-SPEL_SEGMENTS = {"lmo": (3, 2), "retraction": (7,)}
+# most 2048): one segment each.
+SPEL_SEGMENTS = {"lmo": (5,), "retraction": (7,)}
 
 
 def spel_flop_split(P, dd, rr):
